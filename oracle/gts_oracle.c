@@ -1,0 +1,408 @@
+/*
+ * gts_oracle.c — plain, serial CPU oracle of the tile-graph simulation
+ * backend of GTSim (arXiv 2607.11262, Sec. 5).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load or call this code.  It shares no
+ * code, header, table or constant generator with the HIP library; the only
+ * things both sides agree on are interface formats (the 32-word hardware
+ * record, the edge encoding, the class numbers), each restated here.
+ *
+ * Method.  A serial event-driven list scheduler over one binary heap keyed
+ * (cycle, phase, id), exactly the rules below, one simulation per call.
+ * Where the paper fixes a behaviour the rule cites it; where it is silent the
+ * reading used is the one listed in DESIGN.md ("Readings").
+ *
+ *  R2  Resources (Sec. 5.2 compute: tensor cores, CUDA cores, SFUs; memory:
+ *      TMA/LSU front end, L2, DRAM).  TENSOR/ALU/SFU nodes occupy the
+ *      per-subpartition lanes of their SM named by their warps (lane of warp
+ *      w = w mod n_subpart; Sec. 2.2 subpartitions, Sec. 5.3 warp-group
+ *      issue across subpartitions).  SMEM nodes occupy the SM's shared-memory
+ *      pipe.  GLOAD/GSTORE nodes occupy the SM's global-memory engine, then
+ *      the chip-wide L2 server (or DRAM server when the op's MISS flag is
+ *      set).  SYNC nodes occupy nothing.
+ *  R3  Durations, integer cycles, rates in Q16.16, cdiv(a,b) = ceil(a/b):
+ *        compute on k distinct lanes:
+ *            occ = max(1, cdiv(work*65536*n_subpart, k*rate)), latency lat
+ *        SMEM: occ = max(1, cdiv(work*65536, rate_smem)), latency lat_smem
+ *        GMEM engine: occ_e = max(1, cdiv(work*65536, rate_gmem))
+ *        L2/DRAM:     occ_m = max(1, cdiv(work*65536, rate_srv)), lat_srv
+ *        SYNC: finish = start + max(1, lat_sync)
+ *  R4  Every server is FIFO and non-preemptive with one "available" cycle;
+ *      reserving at s for occ cycles sets it to s + occ.  A multi-lane node
+ *      starts at max(ready, avail of each of its lanes) and advances them all.
+ *      finish = start + occ + lat for compute and SMEM nodes (Sec. 5.2: each
+ *      resource = latency, width, sustained throughput; latency overlaps the
+ *      next node's occupancy).
+ *  R6  One step per distinct event cycle t, in this phase order:
+ *        1. CTA_RETIRE events at t free their SM slot;
+ *        2. dispatch (Sec. 5.1 TB scheduler): pending CTAs in index order,
+ *           each to the SM with the most free slots (ties: lowest SM id);
+ *           a CTA of kernel k may go only once every CTA of kernels < k has
+ *           retired; launch = t + cta_launch_lat (+ kernel_launch_lat for the
+ *           CTAs dispatched in the step in which their kernel first
+ *           dispatches); every node of the CTA whose in-edges are all
+ *           released becomes ready at max(its release cycle, launch);
+ *        3. NODE_READY events at t in increasing node id: issue;
+ *           a GLOAD/GSTORE reserves its engine at s = max(t, avail) (its
+ *           start), releases its ORDER edges and raises MEM_ARRIVE at s;
+ *        4. MEM_ARRIVE events at t in increasing node id: m = max(t, avail
+ *           of its L2/DRAM server), server avail = m + occ_m,
+ *           finish = max(s + occ_e, m + occ_m) + lat_srv.
+ *  R8  Release (Sec. 5.1/5.3: order edges at issue, data edges at
+ *      completion): ORDER at start + 1, DATA and SYNC at finish (ORDER too
+ *      under ORDER_AT_FINISH).  A node is ready when every in-edge has been
+ *      released, at the latest release cycle (and not before its CTA's
+ *      launch); if its CTA is not yet dispatched it waits for dispatch.
+ *  R9  Residency per kernel: slots = min(max_cta_per_sm,
+ *      smem_per_sm / smem_per_cta, max_warps_per_sm / warps_per_cta); a zero
+ *      makes the simulation INFEASIBLE.  A CTA retires at the largest finish
+ *      of its nodes (Sec. 5.1 / 5.3: a TB completes when all its nodes have
+ *      finished; its SM resources are then released).
+ *  R10 makespan = max finish; any cycle above 0xFFFFFFFE is OVERFLOW.
+ *  R11 digest = sum over v of mix64(((start<<32)|finish) ^ mix64(v+1)),
+ *      mod 2^64, mix64 = the SplitMix64 finaliser (Steele, Lea, Flood 2014).
+ *  R12 NO_CONTENTION: servers never delay (start = ready, m = s).
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---- interface formats (restated, not shared) ---------------------------- */
+enum { K_TENSOR = 0, K_ALU = 1, K_SFU = 2, K_SMEM = 3, K_GLOAD = 4, K_GSTORE = 5, K_SYNC = 6 };
+enum { E_DATA = 0, E_ORDER = 1, E_SYNC = 2 };
+/* hardware record: 32 u32 words */
+enum {
+  HW_NSM = 0, HW_NSUB = 1, HW_MAXCTA = 2, HW_MAXWARPS = 3, HW_SMEM = 4,
+  HW_RATE = 5,  /* +0 tensor +1 alu +2 sfu +3 smem +4 gmem +5 l2 +6 dram */
+  HW_LAT = 12,  /* +0 tensor +1 alu +2 sfu +3 smem +4 l2 +5 dram +6 sync */
+  HW_CTALAT = 19, HW_KLAT = 20
+};
+enum { F_NODES = 1, F_DIGEST = 2, F_NOCONT = 4, F_ORDER_FIN = 8 };
+enum { ST_OK = 0, ST_INFEASIBLE = 1, ST_OVERFLOW = 2, ST_DEADLOCK = 3 };
+
+#define MAXCYC 0xFFFFFFFEull
+#define EV_RETIRE 0ull
+#define EV_READY 1ull
+#define EV_MEM 2ull
+
+static uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+static uint64_t cdiv(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+static uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+/* ---- binary min-heap of 64-bit keys (cycle << 32 | phase << 30 | id) ----- */
+typedef struct { uint64_t *a; size_t n; } heap_t;
+
+static void heap_push(heap_t *h, uint64_t key) {
+  size_t i = h->n++;
+  while (i > 0) {
+    size_t p = (i - 1) / 2;
+    if (h->a[p] <= key) break;
+    h->a[i] = h->a[p];
+    i = p;
+  }
+  h->a[i] = key;
+}
+
+static uint64_t heap_pop(heap_t *h) {
+  uint64_t top = h->a[0];
+  uint64_t last = h->a[--h->n];
+  size_t i = 0;
+  for (;;) {
+    size_t l = 2 * i + 1, r = l + 1, m = i;
+    uint64_t mv = last;
+    if (l < h->n && h->a[l] < mv) { m = l; mv = h->a[l]; }
+    if (r < h->n && h->a[r] < mv) { m = r; mv = h->a[r]; }
+    if (m == i) break;
+    h->a[i] = h->a[m];
+    i = m;
+  }
+  if (h->n) h->a[i] = last;
+  return top;
+}
+
+static uint64_t mkkey(uint64_t t, uint64_t phase, uint64_t id) {
+  return (t << 32) | (phase << 30) | id;
+}
+
+/* ---- one simulation ------------------------------------------------------- */
+typedef struct {
+  /* graph */
+  uint32_t N, C, K, P;
+  const uint8_t *op_cls, *op_flags;
+  const uint32_t *op_work, *op_warps;
+  const uint16_t *node_op;
+  const uint32_t *succ_ptr, *succ, *cta_node_begin, *kernel_cta_begin;
+  const uint16_t *kernel_warps;
+  const uint32_t *kernel_smem;
+  /* hw */
+  uint32_t nsm, nsub, flags;
+  const uint32_t *hw;
+  /* derived per op */
+  uint64_t *occ, *occm, *lat; uint32_t *lanes; int *to_dram;
+  uint64_t *slots;
+  /* per node */
+  uint32_t *indeg, *cnt, *node_cta, *acc, *st, *fin;
+  /* per CTA */
+  int64_t *cta_sm; uint32_t *cta_launch, *cta_left, *cta_maxfin, *cta_kernel;
+  /* per SM */
+  uint64_t *resident, *lane_av, *smem_av, *eng_av;
+  uint64_t l2_av, dram_av;
+  /* control */
+  heap_t heap;
+  uint32_t next_cta; uint64_t retired;
+  int64_t *kstart;
+  int overflow;
+  uint64_t nfinished;
+} sim_t;
+
+static void release_edge(sim_t *S, uint32_t w, uint64_t r) {
+  if (r > S->acc[w]) S->acc[w] = (uint32_t)r;
+  S->cnt[w]++;
+  if (S->cnt[w] == S->indeg[w]) {
+    uint32_t c = S->node_cta[w];
+    if (S->cta_sm[c] >= 0)
+      heap_push(&S->heap, mkkey(max64(S->acc[w], S->cta_launch[c]), EV_READY, w));
+  }
+}
+
+/* release the out-edges of v whose release cycle is decided now:
+ * which = 0: ORDER edges at start+1; which = 1: DATA/SYNC edges at finish
+ * (and ORDER edges too when ORDER_AT_FINISH). */
+static void release_out(sim_t *S, uint32_t v, int which, uint64_t cyc) {
+  int order_at_fin = (S->flags & F_ORDER_FIN) != 0;
+  for (uint32_t e = S->succ_ptr[v]; e < S->succ_ptr[v + 1]; e++) {
+    uint32_t w = S->succ[e] & 0x3FFFFFFFu;
+    uint32_t kind = S->succ[e] >> 30;
+    int is_order_now = (kind == E_ORDER) && !order_at_fin;
+    if (which == 0 && is_order_now) release_edge(S, w, cyc);
+    if (which == 1 && !is_order_now) release_edge(S, w, cyc);
+  }
+}
+
+/* record v's (start, finish) and do the CTA bookkeeping */
+static int complete(sim_t *S, uint32_t v, uint64_t start, uint64_t finish) {
+  if (finish > MAXCYC) { S->overflow = 1; return 0; }
+  S->st[v] = (uint32_t)start;
+  S->fin[v] = (uint32_t)finish;
+  S->nfinished++;
+  uint32_t c = S->node_cta[v];
+  if (finish > S->cta_maxfin[c]) S->cta_maxfin[c] = (uint32_t)finish;
+  if (--S->cta_left[c] == 0) heap_push(&S->heap, mkkey(S->cta_maxfin[c], EV_RETIRE, c));
+  return 1;
+}
+
+static void dispatch(sim_t *S, uint64_t t) {
+  while (S->next_cta < S->C) {
+    uint32_t c = S->next_cta;
+    uint32_t k = S->cta_kernel[c];
+    if (S->retired < S->kernel_cta_begin[k]) break;   /* previous kernel still running */
+    int64_t best = -1; uint64_t bestfree = 0;
+    for (uint32_t m = 0; m < S->nsm; m++) {
+      uint64_t fr = S->slots[k] - S->resident[m];
+      if (fr > bestfree) { bestfree = fr; best = m; }
+    }
+    if (best < 0) break;                                 /* every SM full */
+    if (S->kstart[k] < 0) S->kstart[k] = (int64_t)t;
+    uint64_t launch = t + S->hw[HW_CTALAT];
+    if ((uint64_t)S->kstart[k] == t) launch += S->hw[HW_KLAT];
+    if (launch > MAXCYC) { S->overflow = 1; return; }
+    S->cta_sm[c] = best;
+    S->cta_launch[c] = (uint32_t)launch;
+    S->resident[best]++;
+    for (uint32_t v = S->cta_node_begin[c]; v < S->cta_node_begin[c + 1]; v++)
+      if (S->cnt[v] == S->indeg[v])
+        heap_push(&S->heap, mkkey(max64(S->acc[v], launch), EV_READY, v));
+    S->next_cta++;
+  }
+}
+
+static void issue(sim_t *S, uint32_t v, uint64_t t) {
+  uint32_t p = S->node_op[v];
+  uint32_t c = S->node_cta[v];
+  uint64_t sm = (uint64_t)S->cta_sm[c];
+  int nocont = (S->flags & F_NOCONT) != 0;
+  uint32_t cls = S->op_cls[p];
+  if (cls == K_TENSOR || cls == K_ALU || cls == K_SFU) {
+    uint64_t s = t;
+    uint64_t *lanes = S->lane_av + sm * S->nsub;
+    if (!nocont)
+      for (uint32_t l = 0; l < S->nsub; l++)
+        if (S->lanes[p] >> l & 1) s = max64(s, lanes[l]);
+    for (uint32_t l = 0; l < S->nsub; l++)
+      if (S->lanes[p] >> l & 1) lanes[l] = s + S->occ[p];
+    if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;
+    release_out(S, v, 0, s + 1);
+    release_out(S, v, 1, S->fin[v]);
+  } else if (cls == K_SMEM) {
+    uint64_t s = nocont ? t : max64(t, S->smem_av[sm]);
+    S->smem_av[sm] = s + S->occ[p];
+    if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;
+    release_out(S, v, 0, s + 1);
+    release_out(S, v, 1, S->fin[v]);
+  } else if (cls == K_SYNC) {
+    if (!complete(S, v, t, t + S->lat[p])) return;
+    release_out(S, v, 0, t + 1);
+    release_out(S, v, 1, S->fin[v]);
+  } else { /* GLOAD / GSTORE: engine now, global server at MEM_ARRIVE */
+    uint64_t s = nocont ? t : max64(t, S->eng_av[sm]);
+    if (s + S->occ[p] > MAXCYC) { S->overflow = 1; return; }
+    S->eng_av[sm] = s + S->occ[p];
+    S->st[v] = (uint32_t)s;
+    release_out(S, v, 0, s + 1);
+    heap_push(&S->heap, mkkey(s, EV_MEM, v));
+  }
+}
+
+static void mem_arrive(sim_t *S, uint32_t v, uint64_t t) {
+  uint32_t p = S->node_op[v];
+  uint64_t *av = S->to_dram[p] ? &S->dram_av : &S->l2_av;
+  uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);
+  *av = m + S->occm[p];
+  uint64_t s = S->st[v];
+  uint64_t f = max64(s + S->occ[p], m + S->occm[p]) + S->lat[p];
+  if (!complete(S, v, s, f)) return;
+  release_out(S, v, 1, f);
+}
+
+#define ALLOC(ptr, n) do { size_t cnt_ = (size_t)(n); (ptr) = calloc(cnt_ ? cnt_ : 1, sizeof(*(ptr))); if (!(ptr)) goto oom; } while (0)
+
+int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t n_kernels,
+                  uint32_t n_ops, const uint8_t *op_cls, const uint8_t *op_flags,
+                  const uint32_t *op_work, const uint32_t *op_warps, const uint16_t *node_op,
+                  const uint32_t *succ_ptr, const uint32_t *succ, const uint32_t *cta_node_begin,
+                  const uint32_t *kernel_cta_begin, const uint16_t *kernel_warps,
+                  const uint32_t *kernel_smem, const uint32_t *hw, uint32_t flags,
+                  uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
+                  uint64_t *out_digest, uint32_t *out_cta) {
+  (void)n_edges;
+  if (!hw || !out_makespan || !out_status) return -1;
+  sim_t S;
+  memset(&S, 0, sizeof S);
+  S.N = n_nodes; S.C = n_ctas; S.K = n_kernels; S.P = n_ops;
+  S.op_cls = op_cls; S.op_flags = op_flags; S.op_work = op_work; S.op_warps = op_warps;
+  S.node_op = node_op; S.succ_ptr = succ_ptr; S.succ = succ;
+  S.cta_node_begin = cta_node_begin; S.kernel_cta_begin = kernel_cta_begin;
+  S.kernel_warps = kernel_warps; S.kernel_smem = kernel_smem;
+  S.hw = hw; S.nsm = hw[HW_NSM]; S.nsub = hw[HW_NSUB]; S.flags = flags;
+  int rc = 0;
+
+  /* R9 residency per kernel */
+  ALLOC(S.slots, S.K);
+  int infeasible = 0;
+  for (uint32_t k = 0; k < S.K; k++) {
+    uint64_t s = hw[HW_MAXCTA];
+    if (kernel_smem[k]) s = s < hw[HW_SMEM] / kernel_smem[k] ? s : hw[HW_SMEM] / kernel_smem[k];
+    uint64_t wl = hw[HW_MAXWARPS] / kernel_warps[k];
+    s = s < wl ? s : wl;
+    S.slots[k] = s;
+    if (s == 0) infeasible = 1;
+  }
+  if (infeasible) {
+    *out_status = ST_INFEASIBLE; *out_makespan = 0xFFFFFFFFu;
+    if (out_digest) *out_digest = 0;
+    free(S.slots);
+    return 0;
+  }
+
+  /* R3 durations per op */
+  ALLOC(S.occ, S.P); ALLOC(S.occm, S.P); ALLOC(S.lat, S.P); ALLOC(S.lanes, S.P); ALLOC(S.to_dram, S.P);
+  for (uint32_t p = 0; p < S.P; p++) {
+    uint64_t w = op_work[p];
+    uint32_t cls = op_cls[p];
+    if (cls == K_TENSOR || cls == K_ALU || cls == K_SFU) {
+      uint32_t lanes = 0;
+      for (uint32_t wp = 0; wp < 32; wp++)
+        if (op_warps[p] >> wp & 1) lanes |= 1u << (wp % S.nsub);
+      uint64_t k = (uint64_t)__builtin_popcount(lanes);
+      S.lanes[p] = lanes;
+      S.occ[p] = max64(1, cdiv(w * 65536ull * S.nsub, k * hw[HW_RATE + cls]));
+      S.lat[p] = hw[HW_LAT + cls];
+    } else if (cls == K_SMEM) {
+      S.occ[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + 3]));
+      S.lat[p] = hw[HW_LAT + 3];
+    } else if (cls == K_SYNC) {
+      S.lat[p] = max64(1, hw[HW_LAT + 6]);
+    } else {
+      int dram = (op_flags[p] & 1) != 0;
+      S.to_dram[p] = dram;
+      S.occ[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + 4]));
+      S.occm[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + (dram ? 6 : 5)]));
+      S.lat[p] = hw[HW_LAT + (dram ? 5 : 4)];
+    }
+  }
+
+  /* per node / per CTA / per SM state */
+  ALLOC(S.indeg, S.N); ALLOC(S.cnt, S.N); ALLOC(S.node_cta, S.N); ALLOC(S.acc, S.N);
+  ALLOC(S.st, S.N); ALLOC(S.fin, S.N);
+  for (uint32_t e = 0; e < succ_ptr[S.N]; e++) S.indeg[succ[e] & 0x3FFFFFFFu]++;
+  ALLOC(S.cta_sm, S.C); ALLOC(S.cta_launch, S.C); ALLOC(S.cta_left, S.C);
+  ALLOC(S.cta_maxfin, S.C); ALLOC(S.cta_kernel, S.C);
+  for (uint32_t k = 0; k < S.K; k++)
+    for (uint32_t c = kernel_cta_begin[k]; c < kernel_cta_begin[k + 1]; c++) S.cta_kernel[c] = k;
+  for (uint32_t c = 0; c < S.C; c++) {
+    S.cta_sm[c] = -1;
+    S.cta_left[c] = cta_node_begin[c + 1] - cta_node_begin[c];
+    for (uint32_t v = cta_node_begin[c]; v < cta_node_begin[c + 1]; v++) S.node_cta[v] = c;
+  }
+  ALLOC(S.resident, S.nsm); ALLOC(S.lane_av, (uint64_t)S.nsm * S.nsub);
+  ALLOC(S.smem_av, S.nsm); ALLOC(S.eng_av, S.nsm);
+  ALLOC(S.kstart, S.K);
+  for (uint32_t k = 0; k < S.K; k++) S.kstart[k] = -1;
+  ALLOC(S.heap.a, (uint64_t)S.N + S.C);
+
+  /* R6 event loop */
+  dispatch(&S, 0);
+  while (S.heap.n && !S.overflow) {
+    uint64_t t = S.heap.a[0] >> 32;
+    int any_retire = 0;
+    while (S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_RETIRE) {
+      uint32_t c = (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu);
+      S.resident[S.cta_sm[c]]--;
+      S.retired++;
+      any_retire = 1;
+    }
+    if (any_retire) dispatch(&S, t);
+    while (!S.overflow && S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_READY)
+      issue(&S, (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu), t);
+    while (!S.overflow && S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_MEM)
+      mem_arrive(&S, (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu), t);
+  }
+
+  if (S.overflow) {
+    *out_status = ST_OVERFLOW; *out_makespan = 0xFFFFFFFFu;
+    if (out_digest) *out_digest = 0;
+  } else if (S.nfinished != S.N) {
+    *out_status = ST_DEADLOCK; *out_makespan = 0xFFFFFFFFu;
+    if (out_digest) *out_digest = 0;
+  } else {
+    uint64_t mk = 0, dg = 0;
+    for (uint32_t v = 0; v < S.N; v++) {
+      if (S.fin[v] > mk) mk = S.fin[v];
+      dg += mix64((((uint64_t)S.st[v] << 32) | S.fin[v]) ^ mix64((uint64_t)v + 1));
+    }
+    *out_status = ST_OK; *out_makespan = (uint32_t)mk;
+    if (out_digest) *out_digest = dg;
+  }
+  if (out_cycles)
+    for (uint32_t v = 0; v < S.N; v++) { out_cycles[2 * (uint64_t)v] = S.st[v]; out_cycles[2 * (uint64_t)v + 1] = S.fin[v]; }
+  if (out_cta)
+    for (uint32_t c = 0; c < S.C; c++) {
+      out_cta[2 * (uint64_t)c] = (uint32_t)S.cta_sm[c];
+      out_cta[2 * (uint64_t)c + 1] = S.cta_launch[c];
+    }
+  goto done;
+oom:
+  rc = -2;
+done:
+  free(S.slots); free(S.occ); free(S.occm); free(S.lat); free(S.lanes); free(S.to_dram);
+  free(S.indeg); free(S.cnt); free(S.node_cta); free(S.acc); free(S.st); free(S.fin);
+  free(S.cta_sm); free(S.cta_launch); free(S.cta_left); free(S.cta_maxfin); free(S.cta_kernel);
+  free(S.resident); free(S.lane_av); free(S.smem_av); free(S.eng_av); free(S.kstart); free(S.heap.a);
+  return rc;
+}

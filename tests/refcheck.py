@@ -1,0 +1,241 @@
+"""Independent checks of simulation results (test helpers).
+
+These re-state the timing rules in a different form from the event-driven
+oracle, so that a slip in the oracle (a dropped latency, a wrong phase
+order, a wrong lane, a wrong tie-break) shows up as a mismatch:
+
+* ``verify_schedule`` takes a finished schedule (per-node start/finish and
+  per-CTA SM/launch) and checks that it is the fixed point of the rules
+  written as equations: every node's start equals max(ready, server
+  availability) with each server's users taken in FIFO order of
+  (ready cycle, node id), every finish equals start + the node's duration,
+  every ready cycle equals the latest release over its in-edges (order edges
+  at source start + 1, data/sync edges at source finish), and the CTA
+  dispatch sequence re-simulated from the CTAs' retire cycles matches.
+  Because each quantity depends only on strictly earlier ones the rules
+  have exactly one fixed point, so passing means the schedule is the one
+  the rules define.
+* ``asap_bruteforce`` enumerates every path of a tiny DAG to get the
+  uncontended (as-soon-as-possible) start of each node: the longest path
+  with order edges weighing 1 and data/sync edges the source's duration.
+* ``durations`` computes each op's occupancy / latency from the hardware
+  record by the integer formulas (ceil division, Q16.16 rates).
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+from paper_2607_11262_amd.gen import hw as H
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, ORDER, SFU, SMEM, SYNC, SYNC_EDGE, TENSOR,
+                                             GraphBuilder)
+
+MAXCYC = 0xFFFFFFFE
+CLASS = {"TENSOR": TENSOR, "ALU": ALU, "SFU": SFU, "SMEM": SMEM, "GLOAD": GLOAD, "GSTORE": GSTORE, "SYNC": SYNC}
+KIND = {"D": DATA, "O": ORDER, "S": SYNC_EDGE}
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_schedules.json")
+
+
+def cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def durations(g, rec):
+    """Per op: dict(kind, lanes, occ, occ_m, lat, dram)."""
+    nsub = H.get(rec, "n_subpart")
+    rates = [H.get(rec, f) for f in ("rate_tensor", "rate_alu", "rate_sfu", "rate_smem", "rate_gmem", "rate_l2",
+                                       "rate_dram")]
+    lats = [H.get(rec, f) for f in ("lat_tensor", "lat_alu", "lat_sfu", "lat_smem", "lat_l2", "lat_dram",
+                                      "lat_sync")]
+    out = []
+    for p in range(g.n_ops):
+        cls, work, warps, miss = int(g.op_cls[p]), int(g.op_work[p]), int(g.op_warps[p]), int(g.op_flags[p]) & 1
+        if cls in (TENSOR, ALU, SFU):
+            lanes = sorted({w % nsub for w in range(32) if warps >> w & 1})
+            occ = max(1, cdiv(work * 65536 * nsub, len(lanes) * rates[cls]))
+            out.append(dict(kind="compute", lanes=lanes, occ=occ, lat=lats[cls]))
+        elif cls == SMEM:
+            out.append(dict(kind="smem", occ=max(1, cdiv(work * 65536, rates[3])), lat=lats[3]))
+        elif cls == SYNC:
+            out.append(dict(kind="sync", lat=max(1, lats[6])))
+        else:
+            out.append(dict(kind="gmem", occ=max(1, cdiv(work * 65536, rates[4])),
+                            occ_m=max(1, cdiv(work * 65536, rates[6] if miss else rates[5])),
+                            lat=lats[5] if miss else lats[4], dram=bool(miss)))
+    return out
+
+
+def node_duration(d) -> int:
+    """Uncontended start-to-finish length of a node."""
+    if d["kind"] in ("compute", "smem"):
+        return d["occ"] + d["lat"]
+    if d["kind"] == "sync":
+        return d["lat"]
+    return max(d["occ"], d["occ_m"]) + d["lat"]
+
+
+def slots_per_kernel(g, rec):
+    out = []
+    for k in range(g.n_kernels):
+        s = H.get(rec, "max_cta_per_sm")
+        if int(g.kernel_smem[k]):
+            s = min(s, H.get(rec, "smem_per_sm") // int(g.kernel_smem[k]))
+        s = min(s, H.get(rec, "max_warps_per_sm") // int(g.kernel_warps[k]))
+        out.append(s)
+    return out
+
+
+def verify_schedule(g, rec, flags, cycles, cta):
+    """Raise AssertionError unless (cycles, cta) is the schedule the rules
+    define for graph g on hardware record rec.  cycles [N,2], cta [C,2]."""
+    N, C = g.n_nodes, g.n_ctas
+    nocont = bool(flags & 4)
+    order_fin = bool(flags & 8)
+    dur = durations(g, rec)
+    st = cycles[:, 0].astype(np.int64)
+    fi = cycles[:, 1].astype(np.int64)
+    node_cta = g.node_cta()
+    cta_sm = cta[:, 0].astype(np.int64)
+    launch = cta[:, 1].astype(np.int64)
+    # ready cycle of every node from its in-edges' release cycles
+    ready = launch[node_cta].copy()
+    src, dst, kind = g.sources(), g.targets(), g.kinds()
+    rel = np.where((kind == ORDER) & (not order_fin), st[src] + 1, fi[src])
+    np.maximum.at(ready, dst, rel)
+    ops = g.node_op.astype(np.int64)
+    nsub = H.get(rec, "n_subpart")
+    order = np.lexsort((np.arange(N), ready))  # FIFO (ready, id)
+    lane_av, smem_av, eng_av = {}, {}, {}
+    gstart = {}
+    for v in order:
+        d = dur[ops[v]]
+        sm = int(cta_sm[node_cta[v]])
+        r = int(ready[v])
+        if d["kind"] == "compute":
+            s = r if nocont else max([r] + [lane_av.get((sm, l), 0) for l in d["lanes"]])
+            for l in d["lanes"]:
+                lane_av[(sm, l)] = s + d["occ"]
+            assert st[v] == s and fi[v] == s + d["occ"] + d["lat"], f"compute node {v}: {st[v], fi[v]} != {s}"
+        elif d["kind"] == "smem":
+            s = r if nocont else max(r, smem_av.get(sm, 0))
+            smem_av[sm] = s + d["occ"]
+            assert st[v] == s and fi[v] == s + d["occ"] + d["lat"], f"smem node {v}"
+        elif d["kind"] == "sync":
+            assert st[v] == r and fi[v] == r + d["lat"], f"sync node {v}"
+        else:
+            s = r if nocont else max(r, eng_av.get(sm, 0))
+            eng_av[sm] = s + d["occ"]
+            assert st[v] == s, f"gmem node {v} start {st[v]} != {s}"
+            gstart[v] = s
+    # global L2 / DRAM servers in FIFO order of (arrival = engine start, id)
+    av = {False: 0, True: 0}
+    for v in sorted(gstart, key=lambda x: (gstart[x], x)):
+        d = dur[ops[v]]
+        s = gstart[v]
+        m = s if nocont else max(s, av[d["dram"]])
+        av[d["dram"]] = m + d["occ_m"]
+        assert fi[v] == max(s + d["occ"], m + d["occ_m"]) + d["lat"], f"gmem node {v} finish"
+    # CTA dispatch re-simulated from retire cycles
+    exp_sm, exp_launch = dispatch_from_retires(g, rec, fi)
+    assert np.array_equal(exp_sm, cta_sm), "CTA -> SM mapping"
+    assert np.array_equal(exp_launch, launch), "CTA launch cycles"
+
+
+def dispatch_from_retires(g, rec, finish):
+    """CTA (sm, launch) implied by each CTA's retire cycle (max finish of its
+    nodes): in-order dispatch at t = 0 and at each retire cycle, to the SM
+    with the most free slots (lowest id on ties), kernels in sequence."""
+    C, K = g.n_ctas, g.n_kernels
+    node_cta = g.node_cta()
+    retire = np.zeros(C, dtype=np.int64)
+    np.maximum.at(retire, node_cta, finish.astype(np.int64))
+    cta_kernel = g.cta_kernel()
+    slots = slots_per_kernel(g, rec)
+    nsm = H.get(rec, "n_sm")
+    kb = g.kernel_cta_begin.astype(np.int64)
+    resident = [0] * nsm
+    sm_of = np.full(C, -1, dtype=np.int64)
+    launch = np.zeros(C, dtype=np.int64)
+    kstart = {}
+    nxt, retired = 0, 0
+    pending = []  # (retire cycle, cta) of dispatched CTAs
+
+    def dispatch(t):
+        nonlocal nxt
+        while nxt < C:
+            k = int(cta_kernel[nxt])
+            if retired < kb[k]:
+                return
+            free = [slots[k] - resident[m] for m in range(nsm)]
+            best = max(range(nsm), key=lambda m: (free[m], -m))
+            if free[best] <= 0:
+                return
+            kstart.setdefault(k, t)
+            la = t + H.get(rec, "cta_launch_lat") + (H.get(rec, "kernel_launch_lat") if kstart[k] == t else 0)
+            sm_of[nxt], launch[nxt] = best, la
+            resident[best] += 1
+            pending.append((int(retire[nxt]), nxt))
+            nxt += 1
+
+    dispatch(0)
+    while pending:
+        pending.sort()
+        t = pending[0][0]
+        while pending and pending[0][0] == t:
+            _, c = pending.pop(0)
+            resident[sm_of[c]] -= 1
+            retired += 1
+        dispatch(t)
+    return sm_of, launch
+
+
+def asap_bruteforce(g, rec, flags=0):
+    """Uncontended starts by enumerating every path (tiny single-kernel graphs
+    whose CTAs all launch in the first dispatch step)."""
+    dur = durations(g, rec)
+    ops = g.node_op.astype(np.int64)
+    N = g.n_nodes
+    launch0 = H.get(rec, "cta_launch_lat") + H.get(rec, "kernel_launch_lat")
+    preds = [[] for _ in range(N)]
+    for u, v, k in zip(g.sources(), g.targets(), g.kinds()):
+        w = 1 if (k == ORDER and not (flags & 8)) else node_duration(dur[ops[u]])
+        preds[int(v)].append((int(u), w))
+    best = [None] * N
+
+    def paths_to(v):  # all path weights ending at v, by explicit enumeration
+        if not preds[v]:
+            return [launch0]
+        out = [launch0]
+        for u, w in preds[v]:
+            out += [x + w for x in paths_to(u)]
+        return out
+
+    for v in range(N):
+        best[v] = max(paths_to(v))
+    starts = np.array(best, dtype=np.int64)
+    finishes = starts + np.array([node_duration(dur[ops[v]]) for v in range(N)], dtype=np.int64)
+    return starts, finishes
+
+
+def load_golden():
+    with open(GOLDEN) as f:
+        doc = json.load(f)
+    cases = {c["name"]: c for c in doc["cases"]}
+    out = []
+    for c in doc["cases"]:
+        src = cases[c["same_graph_as"]] if "same_graph_as" in c else c
+        b = GraphBuilder()
+        for k in src["kernels"]:
+            b.kernel(k["warps"], k["smem"])
+            for cta in k["ctas"]:
+                b.cta()
+                for cls, work, warps, miss in cta:
+                    b.node(CLASS[cls], work, warps, 1 if miss else 0)
+        for u, v, kd in src["edges"]:
+            b.edge(u, v, KIND[kd])
+        g = b.build(c["name"])
+        rec = H.toy(**c["hw"])
+        out.append((c, g, rec))
+    return out

@@ -1,0 +1,112 @@
+"""The oracle's pins have teeth: each plausible mistake, planted in a copy
+of the oracle source on the CPU, is caught by at least one pin (hand
+schedules, closed forms, brute-force longest paths, the equation-form
+schedule verifier).  Nothing here touches a GPU."""
+import functools
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import refcheck
+from paper_2607_11262_amd.gen import hw as H
+from paper_2607_11262_amd.gen import workloads as W
+from paper_2607_11262_amd.gen.rng import SplitMix64
+
+# (name, original text, replacement, replace all occurrences?)
+MUTANTS = [
+    ("drop_compute_latency", "if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SMEM)",
+     "if (!complete(S, v, s, s + S->occ[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SMEM)", False),
+    ("order_release_at_start", "release_out(S, v, 0, s + 1);", "release_out(S, v, 0, s);", True),
+    ("memory_phase_before_issue", "#define EV_RETIRE 0ull\n#define EV_READY 1ull\n#define EV_MEM 2ull",
+     "#define EV_RETIRE 1ull\n#define EV_READY 2ull\n#define EV_MEM 0ull", False),
+    ("lane_is_warp_div_nsub", "lanes |= 1u << (wp % S.nsub)", "lanes |= 1u << (wp / S.nsub % S.nsub)", False),
+    ("dispatch_tie_highest_sm", "if (fr > bestfree) { bestfree = fr; best = m; }",
+     "if (fr >= bestfree && fr > 0) { bestfree = fr; best = m; }", False),
+    ("no_kernel_launch_latency", "launch += S->hw[HW_KLAT];", ";", False),
+    ("misses_served_by_l2", "S.to_dram[p] = dram;", "S.to_dram[p] = 0;", False),
+    ("gmem_finish_ignores_engine", "max64(s + S->occ[p], m + S->occm[p])", "(m + S->occm[p])", False),
+    ("ready_ignores_launch", "mkkey(max64(S->acc[w], S->cta_launch[c]), EV_READY, w)", "mkkey(S->acc[w], EV_READY, w)",
+     False),
+    ("retire_at_last_finish", "if (finish > S->cta_maxfin[c]) S->cta_maxfin[c] = (uint32_t)finish;",
+     "S->cta_maxfin[c] = (uint32_t)finish;", False),
+    ("order_at_finish_flag_ignored", "int is_order_now = (kind == E_ORDER) && !order_at_fin;",
+     "int is_order_now = (kind == E_ORDER);", False),
+    ("sync_edges_release_at_issue", "int is_order_now = (kind == E_ORDER) && !order_at_fin;",
+     "int is_order_now = (kind != E_DATA) && !order_at_fin;", False),
+    ("occupancy_floor", "static uint64_t cdiv(uint64_t a, uint64_t b) { return (a + b - 1) / b; }",
+     "static uint64_t cdiv(uint64_t a, uint64_t b) { return a / b; }", False),
+    ("no_contention_ignored_on_l2_dram", "uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);",
+     "uint64_t m = max64(t, *av);", False),
+    ("residency_ignores_warps", "s = s < wl ? s : wl;", ";", False),
+    ("residency_ignores_smem", "if (kernel_smem[k]) s =", "if (0) s =", False),
+    ("multi_lane_uses_first_lane", "if (S->lanes[p] >> l & 1) s = max64(s, lanes[l]);",
+     "if (S->lanes[p] >> l & 1) { s = max64(s, lanes[l]); break; }", False),
+    ("smem_latency_dropped", "if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)",
+     "if (!complete(S, v, s, s + S->occ[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)", False),
+    ("sync_node_zero_latency_allowed", "S.lat[p] = max64(1, hw[HW_LAT + 6]);", "S.lat[p] = hw[HW_LAT + 6];", False),
+    ("cta_launch_latency_dropped", "uint64_t launch = t + S->hw[HW_CTALAT];", "uint64_t launch = t;", False),
+]
+
+
+@functools.lru_cache(maxsize=None)
+def _variant(name, tmpdir):
+    src = oracle.source_text()
+    for n, a, b, every in MUTANTS:
+        if n == name:
+            assert a in src, f"mutation anchor of {name} not found"
+            src = src.replace(a, b) if every else src.replace(a, b, 1)
+    path = os.path.join(tmpdir, f"libgts_oracle_{name}.so")
+    oracle.build_variant(src, path)
+    return path
+
+
+def _checks(lib):
+    """Yields nothing; raises AssertionError at the first pin a variant breaks."""
+    for case, g, rec in refcheck.load_golden():
+        r = oracle.simulate(g, rec, case["flags"], want_cta=True, lib_path=lib)
+        exp = case["expect"]
+        assert (r.status, r.makespan) == (exp["status"], exp["makespan"]), case["name"]
+        if "cycles" in exp:
+            assert r.cycles.tolist() == exp["cycles"], case["name"]
+        if "cta" in exp:
+            assert r.cta.tolist() == exp["cta"], case["name"]
+    for seed in range(40):
+        rng = SplitMix64(seed, 14)
+        g = W.random_graph(rng, n_nodes_max=rng.choice([6, 20, 60]), n_kernels_max=3, ctas_max=4)
+        rec = H.sample_random(rng)
+        flags = rng.choice([0, 0, 0, 4, 8])
+        r = oracle.simulate(g, rec, flags, want_cta=True, lib_path=lib)
+        if min(refcheck.slots_per_kernel(g, rec)) == 0:
+            assert r.status == 1
+            continue
+        assert r.status == 0
+        refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+    for seed in range(40):
+        rng = SplitMix64(seed, 13)
+        g = W.random_graph(rng, n_nodes_max=12, n_kernels_max=1, ctas_max=3)
+        rec = H.sample_random(rng)
+        rec[H.FIELDS["n_sm"]] = g.n_ctas
+        rec[H.FIELDS["max_cta_per_sm"]] = 1
+        rec[H.FIELDS["max_warps_per_sm"]] = 64
+        rec[H.FIELDS["smem_per_sm"]] = 1 << 20
+        r = oracle.simulate(g, rec, 4, lib_path=lib)
+        if r.status == 0:
+            s, f = refcheck.asap_bruteforce(g, rec, 4)
+            assert r.cycles[:, 0].tolist() == s.tolist() and r.cycles[:, 1].tolist() == f.tolist()
+
+
+def test_unmutated_source_passes(tmp_path_factory):
+    d = str(tmp_path_factory.mktemp("mut"))
+    path = os.path.join(d, "libgts_oracle_plain.so")
+    oracle.build_variant(oracle.source_text(), path)
+    _checks(path)
+
+
+@pytest.mark.parametrize("name", [m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, tmp_path_factory):
+    d = str(tmp_path_factory.mktemp("mut"))
+    lib = _variant(name, d)
+    with pytest.raises(AssertionError):
+        _checks(lib)

@@ -1,0 +1,223 @@
+"""Pins of the CPU oracle to things other than itself (no GPU).
+
+* hand-computed schedules (tests/golden/hand_schedules.json, each citing the
+  passage whose rule it exercises);
+* closed forms: a dependency chain finishes at the sum of its node
+  durations; independent nodes on one FIFO server finish at prefix sums of
+  their occupancies plus the latency;
+* brute force: with servers switched off, every start equals the longest
+  path found by enumerating all paths of a tiny DAG;
+* the schedule verifier (tests/refcheck.py), an equation-form statement of
+  the rules, on random graphs and machines and on small workload graphs;
+* invariants: contention never makes a node start earlier than in the
+  uncontended schedule; the makespan bounds every server's total occupancy;
+  batches are order-independent.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import refcheck
+from paper_2607_11262_amd.gen import hw as H
+from paper_2607_11262_amd.gen import workloads as W
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, SFU, SMEM, SYNC, TENSOR, GraphBuilder,
+                                             empty_graph, validate)
+from paper_2607_11262_amd.gen.rng import SplitMix64
+
+GOLDEN = refcheck.load_golden()
+
+
+@pytest.mark.parametrize("case,g,rec", GOLDEN, ids=[c["name"] for c, _, _ in GOLDEN])
+def test_hand_schedule(case, g, rec):
+    validate(g)
+    r = oracle.simulate(g, rec, case["flags"], want_cta=True)
+    exp = case["expect"]
+    assert r.status == exp["status"]
+    assert r.makespan == exp["makespan"]
+    if "cycles" in exp:
+        assert r.cycles.tolist() == exp["cycles"]
+    if "cta" in exp:
+        assert r.cta.tolist() == exp["cta"]
+    if r.status == 0:
+        refcheck.verify_schedule(g, rec, case["flags"], r.cycles, r.cta)
+
+
+def test_empty_graph():
+    r = oracle.simulate(empty_graph(), H.toy())
+    assert (r.status, r.makespan, r.digest) == (0, 0, 0)
+
+
+def _chain(classes, works, warps=0xF):
+    b = GraphBuilder()
+    b.kernel(4, 1024)
+    b.cta()
+    ids = [b.node(c, w, warps, flags) for c, w, flags in zip(classes, works, [i % 2 for i in range(len(classes))])]
+    for u, v in zip(ids[:-1], ids[1:]):
+        b.edge(u, v, DATA)
+    return b.build("chain")
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_closed_form_chain(seed):
+    """A DATA chain never waits on a server (each predecessor's occupancy
+    ends before its finish), so the makespan is launch + the sum of the
+    per-node durations."""
+    rng = SplitMix64(seed, 11)
+    rec = H.sample_random(rng)
+    n = rng.randint(1, 30)
+    cls = [rng.choice([TENSOR, ALU, SFU, SMEM, GLOAD, GSTORE, SYNC]) for _ in range(n)]
+    works = [rng.randint(0, 100000) for _ in range(n)]
+    g = _chain(cls, works)
+    r = oracle.simulate(g, rec)
+    dur = refcheck.durations(g, rec)
+    expect = H.get(rec, "cta_launch_lat") + H.get(rec, "kernel_launch_lat")
+    expect += sum(refcheck.node_duration(dur[int(p)]) for p in g.node_op)
+    if r.status == 0:
+        assert r.makespan == expect
+    else:
+        assert expect > 0xFFFFFFFE
+
+
+@pytest.mark.parametrize("cls", [TENSOR, ALU, SFU, SMEM])
+@pytest.mark.parametrize("seed", range(5))
+def test_closed_form_one_server(cls, seed):
+    """n independent nodes on one FIFO server, all ready at cycle 0, finish
+    at the prefix sums of their occupancies plus the latency (id order)."""
+    rng = SplitMix64(seed, 12)
+    rec = H.toy()
+    n = rng.randint(1, 40)
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    b.cta()
+    works = [rng.randint(0, 20000) for _ in range(n)]
+    for w in works:
+        b.node(cls, w, 0xF)
+    g = b.build()
+    r = oracle.simulate(g, rec)
+    dur = refcheck.durations(g, rec)
+    occ = [dur[int(p)]["occ"] for p in g.node_op]
+    lat = dur[int(g.node_op[0])]["lat"]
+    pref = np.cumsum(occ)
+    assert r.cycles[:, 1].tolist() == (pref + lat).tolist()
+    assert r.cycles[:, 0].tolist() == (pref - np.array(occ)).tolist()
+
+
+def _bruteforce_graph(rng):
+    """Tiny single-kernel graphs whose CTAs all fit at once."""
+    return W.random_graph(rng, n_nodes_max=12, n_kernels_max=1, ctas_max=3)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_no_contention_is_longest_path(seed):
+    rng = SplitMix64(seed, 13)
+    g = _bruteforce_graph(rng)
+    validate(g)
+    rec = H.sample_random(rng)
+    rec[H.FIELDS["n_sm"]] = g.n_ctas  # every CTA resident from the first step
+    rec[H.FIELDS["max_cta_per_sm"]] = 1
+    rec[H.FIELDS["max_warps_per_sm"]] = 64
+    rec[H.FIELDS["smem_per_sm"]] = 1 << 20
+    for flags in (4, 4 | 8):
+        r = oracle.simulate(g, rec, flags)
+        if r.status != 0:
+            continue
+        s, f = refcheck.asap_bruteforce(g, rec, flags)
+        assert r.cycles[:, 0].tolist() == s.tolist()
+        assert r.cycles[:, 1].tolist() == f.tolist()
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_verifier_random(seed):
+    rng = SplitMix64(seed, 14)
+    g = W.random_graph(rng, n_nodes_max=rng.choice([6, 20, 60]), n_kernels_max=3, ctas_max=4)
+    validate(g)
+    rec = H.sample_random(rng)
+    flags = rng.choice([0, 0, 0, 4, 8])
+    r = oracle.simulate(g, rec, flags, want_cta=True)
+    if r.status == 1:
+        assert min(refcheck.slots_per_kernel(g, rec)) == 0
+        return
+    assert min(refcheck.slots_per_kernel(g, rec)) > 0
+    assert r.status == 0
+    refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+    assert r.makespan == int(r.cycles[:, 1].max()) if g.n_nodes else 0
+
+
+def _small_workloads():
+    return [
+        ("gemm_256", W.gemm(256, 256, 256, 64, 64, 32, 2), H.preset("A100")),
+        ("gemm_512_s3", W.gemm(512, 256, 512, 128, 64, 64, 3), H.preset("H100", n_sm=7)),
+        ("gemm_perwarp", W.gemm(256, 128, 256, 64, 64, 32, 3, per_warp=True), H.preset("H100", n_sm=3)),
+        ("fa_small", W.flash_attention(1, 2, 512, 128, 128, 64), H.preset("H100", n_sm=5)),
+        ("fa_causal", W.flash_attention(1, 2, 512, 128, 128, 64, causal=True), H.preset("H100", n_sm=5)),
+        ("decode_small", W.splitkv_decode(batch=3, kv_min=64, kv_max=1500, seed=7), H.preset("H100", n_sm=6)),
+        ("decoder_tiny", W.decoder_layer(tokens=128, hidden=256, heads=4, kv_heads=2, ffn=512, d=64),
+         H.preset("H100", n_sm=9)),
+    ]
+
+
+@pytest.mark.parametrize("name,g,rec", _small_workloads(), ids=[n for n, _, _ in _small_workloads()])
+def test_verifier_workloads(name, g, rec):
+    validate(g)
+    for flags in (0, 4):
+        r = oracle.simulate(g, rec, flags, want_cta=True)
+        assert r.status == 0
+        refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_invariants(seed):
+    """Contention only delays (per node, vs. the uncontended schedule) and the
+    makespan is at least each server's total occupancy (I6, I7)."""
+    rng = SplitMix64(seed, 15)
+    g = W.random_graph(rng, n_nodes_max=40, n_kernels_max=1, ctas_max=2)
+    rec = H.sample_random(rng)
+    rec[H.FIELDS["n_sm"]] = g.n_ctas
+    rec[H.FIELDS["max_cta_per_sm"]] = 1
+    rec[H.FIELDS["max_warps_per_sm"]] = 64
+    rec[H.FIELDS["smem_per_sm"]] = 1 << 20
+    a = oracle.simulate(g, rec, 0, want_cta=True)
+    b = oracle.simulate(g, rec, 4)
+    if a.status != 0:
+        return
+    assert np.all(a.cycles[:, 0] >= b.cycles[:, 0])
+    assert np.all(a.cycles[:, 1] >= b.cycles[:, 1])
+    dur = refcheck.durations(g, rec)
+    tot = {}
+    node_cta = g.node_cta()
+    for v in range(g.n_nodes):
+        d = dur[int(g.node_op[v])]
+        sm = int(a.cta[node_cta[v], 0])
+        if d["kind"] == "compute":
+            for lane in d["lanes"]:
+                tot[("lane", sm, lane)] = tot.get(("lane", sm, lane), 0) + d["occ"]
+        elif d["kind"] == "smem":
+            tot[("smem", sm)] = tot.get(("smem", sm), 0) + d["occ"]
+        elif d["kind"] == "gmem":
+            tot[("eng", sm)] = tot.get(("eng", sm), 0) + d["occ"]
+            tot[("glob", d["dram"])] = tot.get(("glob", d["dram"]), 0) + d["occ_m"]
+    assert a.makespan >= max(tot.values(), default=0)
+
+
+def test_batch_order_independent():
+    g = W.gemm(256, 256, 512, 64, 128, 32, 3)
+    hws = H.sample_h100_sweep(99, 12)
+    mk, st, dg, cyc = oracle.simulate_batch(g, hws, want_nodes=True, threads=4)
+    perm = np.arange(12)[::-1]
+    mk2, st2, dg2, cyc2 = oracle.simulate_batch(g, hws[perm], want_nodes=True, threads=1)
+    assert np.array_equal(mk[perm], mk2) and np.array_equal(dg[perm], dg2) and np.array_equal(cyc[perm], cyc2)
+
+
+def test_digest_matches_definition():
+    """R11: digest = sum_v mix64(((start << 32) | finish) ^ mix64(v + 1))."""
+    def mix64(z):
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & (2**64 - 1)
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & (2**64 - 1)
+        return z ^ (z >> 31)
+
+    g = W.gemm(256, 256, 256, 128, 128, 32, 2)
+    r = oracle.simulate(g, H.preset("A100"))
+    d = 0
+    for v, (s, f) in enumerate(r.cycles.tolist()):
+        d = (d + mix64(((s << 32) | f) ^ mix64(v + 1))) % 2**64
+    assert d == r.digest
