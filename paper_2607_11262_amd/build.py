@@ -1,0 +1,46 @@
+"""Build libgts.so in-tree with hipcc for gfx950.
+
+    python -m paper_2607_11262_amd.build
+
+Compiles every source each time it is called (the build check must see
+compile errors even when a library is already present)."""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+OUT = os.path.join(PKG, "libgts.so")
+BUILD = os.path.join(ROOT, "_build")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = os.environ.get("GTS_OFFLOAD_ARCH", "gfx950")
+
+# Packed FP32 instructions are kept out of generated code (-packed-fp32-ops).
+DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
+                "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
+
+
+def _run(cmd):
+    print("+", " ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+
+
+def build(verbose: bool = True) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    sim_o = os.path.join(BUILD, "gts_sim.o")
+    host_o = os.path.join(BUILD, "gts_host.o")
+    _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, "gts_sim.hip"), "-o", sim_o])
+    _run([HIPCC, *HOST_FLAGS, "-x", "c++", "-c", os.path.join(CSRC, "gts_host.cpp"), "-o", host_o])
+    tmp = OUT + f".tmp{os.getpid()}"
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", "-o", tmp, sim_o, host_o])
+    os.replace(tmp, OUT)
+    return OUT
+
+
+if __name__ == "__main__":
+    build()
+    sys.exit(0)

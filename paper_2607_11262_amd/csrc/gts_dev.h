@@ -1,0 +1,95 @@
+// gts_dev.h — device image and scratch layouts shared by the host library
+// (gts_host.cpp) and the simulation kernels (gts_sim.hip).  Internal to
+// libgts.so; the public ABI is include/gts.h.
+#pragma once
+#include <stdint.h>
+
+namespace gts {
+
+constexpr uint32_t kImageMagic = 0x47545331u;  // "GTS1"
+constexpr uint32_t kMaxCycle = 0xFFFFFFFEu;     // largest representable finish
+constexpr uint32_t kAlign = 256;
+
+// Graph property bits (computed at upload).
+constexpr uint32_t kGraphSinksAreMemory = 1u;   // every node without an intra-CTA
+                                                // successor is a GLOAD/GSTORE
+constexpr uint32_t kGraphCrossFromMemory = 2u;  // every cross-CTA edge has a
+                                                // GLOAD/GSTORE source, DATA/SYNC kind
+
+struct ImageHeader {            // at offset 0 of the device image
+  uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
+  uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots;
+  uint32_t max_cta_nodes, max_outdeg, pad0, pad1;
+};
+
+struct OpDev {                  // one distinct operation descriptor
+  uint8_t cls, flags;
+  uint16_t pad;
+  uint32_t work, warps, pad2;
+};
+
+struct NodeDev {                // 16 B, one per node
+  uint32_t op_indeg;            // op id (low 16) | in-degree (high 16)
+  uint32_t cta;
+  uint32_t succ_begin, succ_end;
+};
+
+struct CtaDev {                 // 16 B, one per CTA
+  uint32_t node_begin, node_count;
+  uint32_t root_begin, root_count;  // nodes without intra-CTA in-edges
+};
+
+struct KernelDev {              // 16 B, one per kernel
+  uint32_t cta_begin, cta_end, warps, smem;
+};
+
+// Device-side view passed to kernels by value.
+struct Image {
+  const OpDev* ops;
+  const NodeDev* nodes;
+  const uint32_t* succ;
+  const CtaDev* ctas;
+  const KernelDev* kernels;
+  const uint32_t* roots;
+  uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props;
+};
+
+// Hardware record word indices (gts_hw_params field order).
+enum : uint32_t {
+  HW_NSM = 0, HW_NSUB = 1, HW_MAXCTA = 2, HW_MAXWARPS = 3, HW_SMEM = 4,
+  HW_RATE = 5, HW_LAT = 12, HW_CTALAT = 19, HW_KLAT = 20, HW_WORDS = 32
+};
+enum : uint32_t { R_TENSOR = 0, R_ALU, R_SFU, R_SMEM, R_GMEM, R_L2, R_DRAM };
+enum : uint32_t { L_TENSOR = 0, L_ALU, L_SFU, L_SMEM, L_L2, L_DRAM, L_SYNC };
+enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC };
+enum : uint32_t { EDGE_DATA = 0, EDGE_ORDER = 1, EDGE_SYNC = 2 };
+
+// Per-simulation scratch regions (byte offsets within one simulation's slice).
+struct SimLayout {
+  uint64_t off_state;   // u64 per node: acc (low 32) | released in-edges (high 32)
+  uint64_t off_cta;     // CtaState per CTA
+  uint64_t off_pend;    // pending events: u64 key + u32 aux per entry
+  uint64_t off_optab;   // per-op duration table when it does not fit LDS
+  uint64_t pend_cap;
+  uint64_t stride;      // bytes per simulation (multiple of kAlign)
+};
+
+struct CtaState {
+  uint32_t sm, launch, left, maxfin;
+};
+
+struct Launch {
+  Image img;
+  const uint32_t* hw;          // [B][32]
+  uint8_t* sims;               // B slices of layout.stride bytes
+  SimLayout layout;
+  uint32_t* out_cycles;        // [B][N][2] or null
+  uint32_t* out_makespan;
+  int32_t* out_status;
+  uint64_t* out_digest;        // or null
+  uint32_t B, flags;
+  uint32_t lds_optab;          // op table held in LDS (else in scratch)
+  uint32_t lds_words_servers;  // words of per-SM server state reserved in LDS
+};
+
+}  // namespace gts

