@@ -1,0 +1,192 @@
+#!/usr/bin/env python3
+"""Throughput of the batched tile-graph simulation on one MI355X.
+
+Workload: the GEMM design sweep -- 64 seeded GEMM tile graphs (M, N, K in
+{1,2,4,8}K; CTA tiles {64,128,256}^2 x {32,64}; 2-4 pipeline stages; 4 warps)
+each simulated under 4096 seeded H100-based hardware configurations (SMs
+64-192, DRAM 1.5-8 TB/s, shared memory 96-256 KiB, tensor rate 0.5-4x).
+One step = one graph of the sweep against its 4096 configurations
+(digest + makespan + status per simulation), step i using sweep graph i mod
+64.  Graph images and hardware records are resident in HBM before timing.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Prints one JSON line: simulated tile-nodes per second (value), simulations
+per second, the roofline of the simulation kernel (algorithmic bytes per
+launch / mean launch time from HIP events, against 8 TB/s HBM) and the CPU
+oracle timed on a bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+B_PER_GRAPH = 4096
+
+
+def alg_bytes_per_sim(g) -> int:
+    """Bytes one simulation must read from the graph (16-byte node record per
+    node, 4 bytes per edge) plus its 16 bytes of per-simulation output."""
+    return 16 * g.n_nodes + 4 * g.n_edges + 16
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=16)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mem-budget-gb", type=float, default=96.0, help="device scratch budget per launch")
+    ap.add_argument("--graphs", type=str, default="", help="comma-separated sweep graph indices (default: step order)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); simulations are independent, "
+              "so a multi-GPU run would shard the batch (see DESIGN.md).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2607_11262_amd import api
+    from paper_2607_11262_amd.gen import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    api.lib()  # fails loudly if libgts.so is missing
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    params = W.sweep_params()
+    if args.graphs:
+        order = [int(x) for x in args.graphs.split(",")]
+    else:
+        order = list(range(64))
+    step_graphs = [order[i % len(order)] for i in range(args.steps)]
+    warm_graphs = [order[i % len(order)] for i in range(args.warmup)]
+    needed = sorted(set(step_graphs) | set(warm_graphs))
+
+    flags = api.OUT_DIGEST
+    t_gen = time.time()
+    prepared = {}
+    host_graphs = {}
+    budget = int(args.mem_budget_gb * (1 << 30))
+    max_scratch = 0
+    for gi in needed:
+        g = W.sweep_graph(params[gi])
+        hw = W.config_hw(2, B=B_PER_GRAPH, index=gi)
+        dg = api.upload(g)
+        hs = api.upload_hw(hw)
+        per_sim = api.scratch_bytes(dg, 1, flags) - api.scratch_bytes(dg, 0, flags)
+        chunk = max(1, min(B_PER_GRAPH, budget // max(per_sim, 1)))
+        max_scratch = max(max_scratch, api.scratch_bytes(dg, chunk, flags))
+        outs = api.alloc_outputs(dg, B_PER_GRAPH, flags, dev)
+        prepared[gi] = (dg, hs, chunk, outs, g.n_nodes, alg_bytes_per_sim(g))
+        host_graphs[gi] = (g, hw)
+        print(f"[bench] graph {gi} {params[gi]} N={g.n_nodes} E={g.n_edges} chunk={chunk}", file=sys.stderr,
+              flush=True)
+    t_gen = time.time() - t_gen
+    scratch = torch.empty(max_scratch, dtype=torch.uint8, device=dev)
+    launches = []  # (start event, end event, algorithmic bytes, node-sims)
+
+    def step(gi, record):
+        dg, hs, chunk, (cyc, mk, st, dgst), n, abps = prepared[gi]
+        for first in range(0, B_PER_GRAPH, chunk):
+            b = min(chunk, B_PER_GRAPH - first)
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            api.simulate_hwset_into(dg, hs, first, b, flags, None, mk[first:first + b], st[first:first + b],
+                                    dgst[first:first + b], scratch, stream)
+            if record:
+                e1.record(stream)
+                launches.append((e0, e1, abps * b, n * b))
+
+    for gi in warm_graphs:
+        step(gi, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for gi in step_graphs:
+        step(gi, True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+
+    node_sims = sum(prepared[gi][4] * B_PER_GRAPH for gi in step_graphs)
+    sims = B_PER_GRAPH * len(step_graphs)
+    durs = np.array([a.elapsed_time(b) * 1e-3 for a, b, _, _ in launches])
+    abytes = np.array([x for _, _, x, _ in launches], dtype=np.float64)
+    # dominant kernel: the simulation kernel (the only kernel in the step)
+    achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
+    statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
+
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        gi = step_graphs[0]
+        g, hw = host_graphs[gi]
+        threads = min(16, len(os.sched_getaffinity(0)))
+        mk_gpu = prepared[gi][3][1].cpu().numpy().view(np.uint32)
+        st_gpu = prepared[gi][3][2].cpu().numpy()
+        dg_gpu = prepared[gi][3][3].cpu().numpy().view(np.uint64)
+        done, checked, bad = 0, 0, 0
+        c0 = time.perf_counter()
+        while time.perf_counter() - c0 < args.cpu_seconds and done < B_PER_GRAPH:
+            idx = list(range(done, min(done + threads, B_PER_GRAPH)))
+            omk, ost, odg, _ = oracle.simulate_batch(g, hw[idx], flags, want_nodes=False, threads=threads)
+            for j, b in enumerate(idx):
+                checked += 1
+                bad += int(not (omk[j] == mk_gpu[b] and ost[j] == st_gpu[b] and odg[j] == dg_gpu[b]))
+            done = idx[-1] + 1
+        csec = time.perf_counter() - c0
+        cpu = {"value": g.n_nodes * done / csec, "unit": "simulated tile-nodes/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"sweep graph {gi} {params[gi]} ({g.n_nodes} nodes) x its first {done} hw configs, "
+                         f"{threads} threads, {csec:.1f} s"}
+        parity = {"checked_sims": checked, "mismatches": bad}
+
+    out = {
+        "metric": "simulated tile-nodes/sec (batched) + simulations/sec; % of HBM roofline",
+        "value": node_sims / elapsed,
+        "unit": "simulated tile-nodes/s",
+        "n_gpus": 1,
+        "steps": len(step_graphs),
+        "warmup": len(warm_graphs),
+        "ms_per_step": elapsed / len(step_graphs) * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": "gemm_design_sweep", "graphs": step_graphs, "sims_per_graph": B_PER_GRAPH,
+                   "outputs": "makespan+status+digest", "parallelism": "one wavefront per simulation"},
+        "simulations_per_s": sims / elapsed,
+        "node_sims": node_sims,
+        "infeasible_sims": int((statuses == 1).sum()),
+        "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "gts_sim_wave", "launches": len(launches),
+                     "mean_launch_ms": float(durs.mean() * 1e3)},
+        "cpu_baseline": cpu,
+        "parity_sample": parity,
+        "setup_s": t_gen,
+    }
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -202,6 +202,30 @@ int gts_simulate_batch(const gts_graph *g, const gts_hw_params *hw_host, uint32_
                        uint64_t *out_digest, void *scratch, uint64_t scratch_bytes,
                        uint32_t flags, void *hip_stream);
 
+/* ---- device-resident hardware sets ---------------------------------------- */
+typedef struct gts_hwset gts_hwset;  /* opaque handle to uploaded hw records */
+
+/* Bytes of device memory gts_hwset_upload needs for B records. */
+int gts_hwset_device_bytes(uint32_t B, uint64_t *bytes);
+
+/* Validates hw_host[0..B) (GTS_E_HW names the first bad record), copies the
+ * records into the caller's device buffer dev_buf (>= gts_hwset_device_bytes)
+ * on hip_stream and waits for the copy.  *out receives a handle that refers
+ * to (does not own) dev_buf and remembers the largest n_sm / n_subpart. */
+int gts_hwset_upload(const gts_hw_params *hw_host, uint32_t B, void *dev_buf, uint64_t dev_bytes,
+                     void *hip_stream, gts_hwset **out);
+
+/* Frees the handle (not the caller's buffer).  NULL is accepted. */
+int gts_hwset_release(gts_hwset *hw);
+
+/* As gts_simulate_batch, for the B records hw[first .. first + B) of an
+ * uploaded set (already in device memory: no host copy is made).  Output
+ * row b belongs to record first + b.  Scratch: gts_scratch_bytes(g, B, ...). */
+int gts_simulate_hwset(const gts_graph *g, const gts_hwset *hw, uint32_t first, uint32_t B,
+                       uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
+                       uint64_t *out_digest, void *scratch, uint64_t scratch_bytes,
+                       uint32_t flags, void *hip_stream);
+
 /* Checks one hardware record on the host (GTS_OK or GTS_E_HW). */
 int gts_hw_validate(const gts_hw_params *hw);
 

@@ -28,7 +28,8 @@ SIM_OK, SIM_INFEASIBLE, SIM_OVERFLOW, SIM_DEADLOCK = 0, 1, 2, 3
 OUT_NODES, OUT_DIGEST, NO_CONTENTION, ORDER_AT_FINISH = 1, 2, 4, 8
 
 EXPORTS = ("gts_graph_validate", "gts_graph_device_bytes", "gts_graph_upload", "gts_graph_release", "gts_graph_sizes",
-           "gts_scratch_bytes", "gts_simulate_batch", "gts_hw_validate", "gts_strerror", "gts_last_error")
+           "gts_scratch_bytes", "gts_simulate_batch", "gts_hwset_device_bytes", "gts_hwset_upload",
+           "gts_hwset_release", "gts_simulate_hwset", "gts_hw_validate", "gts_strerror", "gts_last_error")
 
 
 class GtsError(RuntimeError):
@@ -66,6 +67,10 @@ def lib():
         L.gts_scratch_bytes.argtypes = [vp, u32, u32, u64p]
         L.gts_simulate_batch.argtypes = [vp, vp, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
         L.gts_hw_validate.argtypes = [vp]
+        L.gts_hwset_device_bytes.argtypes = [u32, u64p]
+        L.gts_hwset_upload.argtypes = [vp, u32, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
+        L.gts_hwset_release.argtypes = [vp]
+        L.gts_simulate_hwset.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
         L.gts_strerror.argtypes = [ctypes.c_int]
         L.gts_strerror.restype = ctypes.c_char_p
         L.gts_last_error.restype = ctypes.c_char_p
@@ -199,6 +204,42 @@ def simulate(g: Graph, hw, flags: int = OUT_NODES | OUT_DIGEST, stream=None, scr
     cyc, mk, st, dg = alloc_outputs(g, B, flags, g.image.device)
     simulate_into(g, hw, flags, cyc, mk, st, dg, scratch, stream)
     return Result(cyc, mk, st, dg)
+
+
+class HwSet:
+    """Hardware records resident in device memory (gts_hwset_upload)."""
+
+    def __init__(self, buf, handle, B):
+        self.buf, self.handle, self.B = buf, handle, B
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.gts_hwset_release(self.handle)
+            self.handle = None
+
+
+def upload_hw(hw, stream=None, device="cuda") -> HwSet:
+    import torch
+    hw = np.ascontiguousarray(hw, dtype=np.uint32).reshape(-1, 32)
+    B = hw.shape[0]
+    n = ctypes.c_uint64(0)
+    _check(lib().gts_hwset_device_bytes(B, ctypes.byref(n)), "gts_hwset_device_bytes")
+    buf = torch.empty(max(int(n.value), 1), dtype=torch.uint8, device=device)
+    handle = ctypes.c_void_p()
+    _check(lib().gts_hwset_upload(hw.ctypes.data, B, ctypes.c_void_p(buf.data_ptr()), buf.numel(), _stream(stream),
+                                  ctypes.byref(handle)), "gts_hwset_upload")
+    return HwSet(buf, handle, B)
+
+
+def simulate_hwset_into(g: Graph, hs: HwSet, first: int, B: int, flags, cyc, mk, st, dg, scratch, stream=None):
+    """Enqueue records [first, first + B) of a resident set; outputs row b is
+    record first + b (pass tensor views offset accordingly)."""
+    _check(lib().gts_simulate_hwset(g.handle, hs.handle, first, B,
+                                    ctypes.c_void_p(cyc.data_ptr() if cyc is not None else 0),
+                                    ctypes.c_void_p(mk.data_ptr()), ctypes.c_void_p(st.data_ptr()),
+                                    ctypes.c_void_p(dg.data_ptr() if dg is not None else 0),
+                                    ctypes.c_void_p(scratch.data_ptr()), scratch.numel(), flags, _stream(stream)),
+           "gts_simulate_hwset")
 
 
 def to_numpy(res: Result):

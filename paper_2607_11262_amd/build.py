@@ -21,6 +21,7 @@ ARCH = os.environ.get("GTS_OFFLOAD_ARCH", "gfx950")
 # Packed FP32 instructions are kept out of generated code (-packed-fp32-ops).
 DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
                 "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
+KERNELS = ("gts_sim.hip", "gts_window.hip")
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 
 
@@ -31,12 +32,15 @@ def _run(cmd):
 
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    sim_o = os.path.join(BUILD, "gts_sim.o")
+    objs = []
+    for src in KERNELS:
+        o = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", o])
+        objs.append(o)
     host_o = os.path.join(BUILD, "gts_host.o")
-    _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, "gts_sim.hip"), "-o", sim_o])
     _run([HIPCC, *HOST_FLAGS, "-x", "c++", "-c", os.path.join(CSRC, "gts_host.cpp"), "-o", host_o])
     tmp = OUT + f".tmp{os.getpid()}"
-    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", "-o", tmp, sim_o, host_o])
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", "-o", tmp, *objs, host_o])
     os.replace(tmp, OUT)
     return OUT
 

@@ -62,7 +62,11 @@ enum : uint32_t {
 enum : uint32_t { R_TENSOR = 0, R_ALU, R_SFU, R_SMEM, R_GMEM, R_L2, R_DRAM };
 enum : uint32_t { L_TENSOR = 0, L_ALU, L_SFU, L_SMEM, L_L2, L_DRAM, L_SYNC };
 enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC };
-enum : uint32_t { EDGE_DATA = 0, EDGE_ORDER = 1, EDGE_SYNC = 2 };
+// Device-image edge encoding: target | bits << 30.  DATA and SYNC edges time
+// identically (released at the source's finish) and share bit pattern 0;
+// bit 30 marks an ORDER edge (released at the source's start + 1), bit 31 an
+// edge into another CTA.
+constexpr uint32_t kDevOrder = 1u, kDevCross = 2u;
 
 // Per-simulation scratch regions (byte offsets within one simulation's slice).
 struct SimLayout {
@@ -70,6 +74,8 @@ struct SimLayout {
   uint64_t off_cta;     // CtaState per CTA
   uint64_t off_pend;    // pending events: u64 key + u32 aux per entry
   uint64_t off_optab;   // per-op duration table when it does not fit LDS
+  uint64_t off_rq;      // windowed kernel: [kQueueReady][n_sm] u64 ready / retire keys
+  uint64_t off_mq;      // windowed kernel: [kQueueMem][n_sm] u64 memory-arrival keys
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };
@@ -77,6 +83,12 @@ struct SimLayout {
 struct CtaState {
   uint32_t sm, launch, left, maxfin;
 };
+
+// Per-SM event queues of the windowed kernel (entries per SM).
+constexpr uint32_t kQueueReady = 64;   // ready nodes and CTA retirements
+constexpr uint32_t kQueueMem = 256;    // memory arrivals (FIFO ring)
+constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
+constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
 
 struct Launch {
   Image img;
@@ -90,6 +102,10 @@ struct Launch {
   uint32_t B, flags;
   uint32_t lds_optab;          // op table held in LDS (else in scratch)
   uint32_t lds_words_servers;  // words of per-SM server state reserved in LDS
+  uint32_t retry_only;         // general kernel: run only simulations marked kStatusRetry
+  uint32_t max_nsm;            // largest n_sm of the batch
+  uint32_t max_nsub;           // largest n_subpart of the batch
+  uint32_t memcap;             // windowed kernel: memory arrivals per window held in LDS
 };
 
 }  // namespace gts

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -16,12 +17,18 @@
 
 namespace gts {
 hipError_t launch_sim(const Launch& L, uint32_t lds_bytes, hipStream_t stream);
+hipError_t launch_window(const Launch& L, uint32_t lds_bytes, hipStream_t stream);
 }
 
 struct gts_graph {
   gts::Image img;
   uint64_t bytes;
   uint32_t max_cta_nodes, max_outdeg;
+};
+
+struct gts_hwset {
+  const uint32_t* dev;  // [B][32] in the caller's device buffer
+  uint32_t B, max_nsm, max_nsub;
 };
 
 namespace {
@@ -208,7 +215,13 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
   off = align_up(off + s.pend_cap * 12, gts::kAlign);
   s.off_optab = off;
   off = align_up(off + (uint64_t)P * 16, gts::kAlign);
-  s.stride = off;
+  // The windowed kernel's per-SM queues overlay the general kernel's pending
+  // list (a simulation the windowed kernel hands back is restarted from
+  // scratch by the general kernel).
+  s.off_rq = s.off_pend;
+  s.off_mq = align_up(s.off_rq + 8ull * gts::kQueueReady * GTS_MAX_SM, gts::kAlign);
+  const uint64_t mq_end = align_up(s.off_mq + 8ull * gts::kQueueMem * GTS_MAX_SM, gts::kAlign);
+  s.stride = std::max(off, mq_end) + gts::kStatsBytes;
   return s;
 }
 
@@ -227,6 +240,79 @@ int check_hw(const gts_hw_params* hw, uint32_t index) {
     return fail(GTS_E_HW, "hw[%u] launch latency exceeds 2^30", index);
   for (int i = 0; i < 11; ++i)
     if (hw->reserved[i]) return fail(GTS_E_HW, "hw[%u].reserved[%d] is not zero", index, i);
+  return GTS_OK;
+}
+
+uint64_t sim_scratch_bytes(const gts_graph* g, uint32_t B) {
+  return (uint64_t)B * sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops).stride;
+}
+
+int check_sim_args(const gts_graph* g, uint32_t B, const uint32_t* out_cycles, const uint32_t* out_makespan,
+                   const int32_t* out_status, const uint64_t* out_digest, uint32_t flags) {
+  if (!g) return fail(GTS_E_ARG, "graph handle is NULL");
+  if (flags & ~GTS_FLAGS_ALL) return fail(GTS_E_ARG, "unknown flags 0x%x", flags);
+  if (B == 0) return GTS_OK;
+  if (!out_makespan || !out_status) return fail(GTS_E_ARG, "out_makespan and out_status are required");
+  if ((flags & GTS_OUT_NODES) && !out_cycles && g->img.n_nodes)
+    return fail(GTS_E_ARG, "GTS_OUT_NODES without out_cycles");
+  if ((flags & GTS_OUT_DIGEST) && !out_digest) return fail(GTS_E_ARG, "GTS_OUT_DIGEST without out_digest");
+  return GTS_OK;
+}
+
+// Enqueue the simulation for B records at hw_dev (device, validated).  Graphs
+// whose CTAs end in memory nodes and whose cross-CTA edges leave memory
+// nodes go to the windowed kernel first; simulations it cannot finish within
+// its queue capacities (and every other graph) run on the general kernel.
+int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_nsm, uint32_t max_nsub,
+           uint32_t* out_cycles, uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, uint8_t* sims,
+           uint32_t flags, hipStream_t st) {
+  constexpr uint32_t kLdsBudget = 64 * 1024;
+  const uint32_t server_bytes = 4u * (max_nsm * (max_nsub + 2) + max_nsm);
+  const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
+  const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
+  const uint32_t lds_general = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
+  gts::Launch L;
+  L.img = g->img;
+  L.hw = hw_dev;
+  L.sims = sims;
+  L.layout = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
+  L.out_cycles = (flags & GTS_OUT_NODES) ? out_cycles : nullptr;
+  L.out_makespan = out_makespan;
+  L.out_status = out_status;
+  L.out_digest = (flags & GTS_OUT_DIGEST) ? out_digest : nullptr;
+  L.B = B;
+  L.flags = flags;
+  L.lds_optab = lds_optab ? 1u : 0u;
+  L.lds_words_servers = server_bytes / 4;
+  L.retry_only = 0;
+  L.max_nsm = max_nsm;
+  L.max_nsub = max_nsub;
+  L.memcap = 0;
+
+  const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory;
+  const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
+  bool windowed = (g->img.props & need_props) == need_props && g->img.n_nodes > 0 &&
+                  !(force && std::strcmp(force, "general") == 0);
+  uint32_t lds_window = 0;
+  if (windowed) {
+    constexpr uint32_t kWindowBudget = 48 * 1024;
+    const uint64_t fixed = optab_bytes + 4ull * (max_nsm * (max_nsub + 2) + 4ull * max_nsm + 2);
+    uint32_t cap = 2048;
+    while (cap > 256 && fixed + 12ull * cap > kWindowBudget) cap >>= 1;
+    windowed = fixed + 12ull * cap <= kLdsBudget;
+    L.memcap = cap;
+    lds_window = (uint32_t)(fixed + 12ull * cap + 8);
+  }
+  // GTS_KERNEL=window (diagnostics): no general-kernel pass, so simulations
+  // the windowed kernel hands back keep their internal retry status.
+  const bool window_only = windowed && force && std::strcmp(force, "window") == 0;
+  hipError_t e = hipSuccess;
+  if (windowed) {
+    e = gts::launch_window(L, lds_window, st);
+    L.retry_only = 1;
+  }
+  if (e == hipSuccess && !window_only) e = gts::launch_sim(L, lds_general, st);
+  if (e != hipSuccess) return fail(GTS_E_HIP, "kernel launch: %s", hipGetErrorString(e));
   return GTS_OK;
 }
 
@@ -322,7 +408,18 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     nodes[v].succ_begin = h->succ_ptr[v];
     nodes[v].succ_end = h->succ_ptr[v + 1];
   }
-  if (h->n_edges) std::memcpy(img.data() + L.succ, h->succ, (size_t)h->n_edges * 4);
+  {
+    // DATA and SYNC share one pattern; mark ORDER and cross-CTA edges.
+    auto* succ = reinterpret_cast<uint32_t*>(img.data() + L.succ);
+    for (uint32_t u = 0; u < h->n_nodes; ++u)
+      for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
+        const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
+        const uint32_t kind = h->succ[e] >> GTS_EDGE_KIND_SHIFT;
+        const uint32_t bits = (kind == GTS_EDGE_ORDER ? gts::kDevOrder : 0u) |
+                              (d.node_cta[u] != d.node_cta[v] ? gts::kDevCross : 0u);
+        succ[e] = v | (bits << GTS_EDGE_KIND_SHIFT);
+      }
+  }
   auto* ctas = reinterpret_cast<gts::CtaDev*>(img.data() + L.ctas);
   for (uint32_t c = 0; c < h->n_ctas; ++c) {
     ctas[c].node_begin = h->cta_node_begin[c];
@@ -387,8 +484,7 @@ int gts_scratch_bytes(const gts_graph* g, uint32_t B, uint32_t flags, uint64_t* 
   g_last_error.clear();
   if (!g || !bytes) return fail(GTS_E_ARG, "graph handle or bytes is NULL");
   if (flags & ~GTS_FLAGS_ALL) return fail(GTS_E_ARG, "unknown flags 0x%x", flags);
-  const gts::SimLayout s = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
-  *bytes = hw_area_bytes(B) + (uint64_t)B * s.stride;
+  *bytes = hw_area_bytes(B) + sim_scratch_bytes(g, B);
   return GTS_OK;
 }
 
@@ -396,14 +492,42 @@ int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_
                        uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, void* scratch,
                        uint64_t scratch_bytes, uint32_t flags, void* hip_stream) {
   g_last_error.clear();
-  if (!g) return fail(GTS_E_ARG, "graph handle is NULL");
-  if (flags & ~GTS_FLAGS_ALL) return fail(GTS_E_ARG, "unknown flags 0x%x", flags);
-  if (B == 0) return GTS_OK;
+  int rc = check_sim_args(g, B, out_cycles, out_makespan, out_status, out_digest, flags);
+  if (rc || B == 0) return rc;
   if (!hw_host) return fail(GTS_E_ARG, "hw_host is NULL");
-  if (!out_makespan || !out_status) return fail(GTS_E_ARG, "out_makespan and out_status are required");
-  if ((flags & GTS_OUT_NODES) && !out_cycles && g->img.n_nodes)
-    return fail(GTS_E_ARG, "GTS_OUT_NODES without out_cycles");
-  if ((flags & GTS_OUT_DIGEST) && !out_digest) return fail(GTS_E_ARG, "GTS_OUT_DIGEST without out_digest");
+  uint32_t max_nsm = 0, max_nsub = 0;
+  for (uint32_t b = 0; b < B; ++b) {
+    rc = check_hw(&hw_host[b], b);
+    if (rc) return rc;
+    max_nsm = std::max(max_nsm, hw_host[b].n_sm);
+    max_nsub = std::max(max_nsub, hw_host[b].n_subpart);
+  }
+  const uint64_t need = hw_area_bytes(B) + sim_scratch_bytes(g, B);
+  if (!scratch) return fail(GTS_E_ARG, "scratch is NULL");
+  if (scratch_bytes < need)
+    return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
+                (unsigned long long)scratch_bytes);
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  uint8_t* base = static_cast<uint8_t*>(scratch);
+  hipError_t e = hipMemcpyAsync(base, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return fail(GTS_E_HIP, "hw upload: %s", hipGetErrorString(e));
+  return launch(g, reinterpret_cast<const uint32_t*>(base), B, max_nsm, max_nsub, out_cycles, out_makespan,
+                out_status, out_digest, base + hw_area_bytes(B), flags, st);
+}
+
+int gts_hwset_device_bytes(uint32_t B, uint64_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(GTS_E_ARG, "bytes is NULL");
+  *bytes = hw_area_bytes(B);
+  return GTS_OK;
+}
+
+int gts_hwset_upload(const gts_hw_params* hw_host, uint32_t B, void* dev_buf, uint64_t dev_bytes, void* hip_stream,
+                     gts_hwset** out) {
+  g_last_error.clear();
+  if (!out) return fail(GTS_E_ARG, "out is NULL");
+  *out = nullptr;
+  if (B && !hw_host) return fail(GTS_E_ARG, "hw_host is NULL");
   uint32_t max_nsm = 0, max_nsub = 0;
   for (uint32_t b = 0; b < B; ++b) {
     int rc = check_hw(&hw_host[b], b);
@@ -411,40 +535,48 @@ int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_
     max_nsm = std::max(max_nsm, hw_host[b].n_sm);
     max_nsub = std::max(max_nsub, hw_host[b].n_subpart);
   }
-  const gts::SimLayout s = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
-  const uint64_t need = hw_area_bytes(B) + (uint64_t)B * s.stride;
+  if (B && !dev_buf) return fail(GTS_E_ARG, "dev_buf is NULL");
+  if (dev_bytes < (uint64_t)B * sizeof(gts_hw_params))
+    return fail(GTS_E_SCRATCH, "hw set needs %llu bytes, got %llu",
+                (unsigned long long)((uint64_t)B * sizeof(gts_hw_params)), (unsigned long long)dev_bytes);
+  if (B) {
+    hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = hipMemcpyAsync(dev_buf, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail(GTS_E_HIP, "hw set upload: %s", hipGetErrorString(e));
+  }
+  gts_hwset* h = new (std::nothrow) gts_hwset;
+  if (!h) return fail(GTS_E_ARG, "out of host memory");
+  h->dev = static_cast<const uint32_t*>(dev_buf);
+  h->B = B;
+  h->max_nsm = max_nsm;
+  h->max_nsub = max_nsub;
+  *out = h;
+  return GTS_OK;
+}
+
+int gts_hwset_release(gts_hwset* hw) {
+  delete hw;
+  return GTS_OK;
+}
+
+int gts_simulate_hwset(const gts_graph* g, const gts_hwset* hw, uint32_t first, uint32_t B, uint32_t* out_cycles,
+                       uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, void* scratch,
+                       uint64_t scratch_bytes, uint32_t flags, void* hip_stream) {
+  g_last_error.clear();
+  int rc = check_sim_args(g, B, out_cycles, out_makespan, out_status, out_digest, flags);
+  if (rc || B == 0) return rc;
+  if (!hw) return fail(GTS_E_ARG, "hw set handle is NULL");
+  if ((uint64_t)first + B > hw->B)
+    return fail(GTS_E_ARG, "records %u..%u exceed the set of %u", first, first + B, hw->B);
+  const uint64_t need = sim_scratch_bytes(g, B);
   if (!scratch) return fail(GTS_E_ARG, "scratch is NULL");
   if (scratch_bytes < need)
     return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
                 (unsigned long long)scratch_bytes);
-
-  constexpr uint32_t kLdsBudget = 64 * 1024;
-  const uint32_t server_bytes = 4u * (max_nsm * (max_nsub + 2) + max_nsm);
-  const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
-  const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
-  const uint32_t lds_bytes = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
-
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  uint8_t* base = static_cast<uint8_t*>(scratch);
-  hipError_t e = hipMemcpyAsync(base, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
-  if (e != hipSuccess) return fail(GTS_E_HIP, "hw upload: %s", hipGetErrorString(e));
-
-  gts::Launch L;
-  L.img = g->img;
-  L.hw = reinterpret_cast<const uint32_t*>(base);
-  L.sims = base + hw_area_bytes(B);
-  L.layout = s;
-  L.out_cycles = (flags & GTS_OUT_NODES) ? out_cycles : nullptr;
-  L.out_makespan = out_makespan;
-  L.out_status = out_status;
-  L.out_digest = (flags & GTS_OUT_DIGEST) ? out_digest : nullptr;
-  L.B = B;
-  L.flags = flags;
-  L.lds_optab = lds_optab ? 1u : 0u;
-  L.lds_words_servers = server_bytes / 4;
-  e = gts::launch_sim(L, lds_bytes, st);
-  if (e != hipSuccess) return fail(GTS_E_HIP, "kernel launch: %s", hipGetErrorString(e));
-  return GTS_OK;
+  return launch(g, hw->dev + (uint64_t)first * gts::HW_WORDS, B, hw->max_nsm, hw->max_nsub, out_cycles,
+                out_makespan, out_status, out_digest, static_cast<uint8_t*>(scratch), flags,
+                reinterpret_cast<hipStream_t>(hip_stream));
 }
 
 }  // extern "C"
