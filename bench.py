@@ -42,12 +42,14 @@ def alg_bytes_per_sim(g) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=16)
+    ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mem-budget-gb", type=float, default=96.0, help="device scratch budget per launch")
     ap.add_argument("--graphs", type=str, default="", help="comma-separated sweep graph indices (default: step order)")
+    ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
+                    help="only run a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -63,8 +65,17 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
-    api.lib()  # fails loudly if libgts.so is missing
     torch.cuda.set_device(0)
+    if args.calibrate_copy_gib > 0:
+        n = int(args.calibrate_copy_gib * (1 << 30))
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read": n, "bytes_written": n, "launches": 3}))
+        return 0
+    api.lib()  # fails loudly if libgts.so is missing
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
 
@@ -124,7 +135,10 @@ def main() -> int:
     t1 = time.perf_counter()
     elapsed = t1 - t0
 
-    node_sims = sum(prepared[gi][4] * B_PER_GRAPH for gi in step_graphs)
+    # simulated nodes count only feasible simulations (an infeasible one
+    # stops after the residency check); simulations/s counts all of them
+    ok_per_graph = {gi: int((prepared[gi][3][2] == 0).sum().item()) for gi in set(step_graphs)}
+    node_sims = sum(prepared[gi][4] * ok_per_graph[gi] for gi in step_graphs)
     sims = B_PER_GRAPH * len(step_graphs)
     durs = np.array([a.elapsed_time(b) * 1e-3 for a, b, _, _ in launches])
     abytes = np.array([x for _, _, x, _ in launches], dtype=np.float64)
@@ -135,27 +149,33 @@ def main() -> int:
     cpu = None
     parity = None
     if not args.no_cpu_baseline:
+        # the oracle on a bounded sample of the same sweep: batches of
+        # `threads` configurations, cycling through the timed graphs, each
+        # result also checked against the GPU's
         import oracle
-        gi = step_graphs[0]
-        g, hw = host_graphs[gi]
         threads = min(16, len(os.sched_getaffinity(0)))
-        mk_gpu = prepared[gi][3][1].cpu().numpy().view(np.uint32)
-        st_gpu = prepared[gi][3][2].cpu().numpy()
-        dg_gpu = prepared[gi][3][3].cpu().numpy().view(np.uint64)
-        done, checked, bad = 0, 0, 0
+        checked, bad, nodes_done = 0, 0, 0
+        used = []
         c0 = time.perf_counter()
-        while time.perf_counter() - c0 < args.cpu_seconds and done < B_PER_GRAPH:
-            idx = list(range(done, min(done + threads, B_PER_GRAPH)))
+        k = 0
+        while time.perf_counter() - c0 < args.cpu_seconds and (k // len(step_graphs) + 1) * threads <= B_PER_GRAPH:
+            gi = step_graphs[k % len(step_graphs)]
+            first = (k // len(step_graphs)) * threads
+            k += 1
+            g, hw = host_graphs[gi]
+            idx = list(range(first, min(first + threads, B_PER_GRAPH)))
+            mk_gpu = prepared[gi][3][1][idx].cpu().numpy().view(np.uint32)
+            st_gpu = prepared[gi][3][2][idx].cpu().numpy()
+            dg_gpu = prepared[gi][3][3][idx].cpu().numpy().view(np.uint64)
             omk, ost, odg, _ = oracle.simulate_batch(g, hw[idx], flags, want_nodes=False, threads=threads)
-            for j, b in enumerate(idx):
-                checked += 1
-                bad += int(not (omk[j] == mk_gpu[b] and ost[j] == st_gpu[b] and odg[j] == dg_gpu[b]))
-            done = idx[-1] + 1
+            checked += len(idx)
+            bad += int(np.sum((omk != mk_gpu) | (ost != st_gpu) | (odg != dg_gpu)))
+            nodes_done += g.n_nodes * int(np.sum(ost == 0))
+            used.append(gi)
         csec = time.perf_counter() - c0
-        cpu = {"value": g.n_nodes * done / csec, "unit": "simulated tile-nodes/s", "cores": threads,
-               "kind": "oracle",
-               "sample": f"sweep graph {gi} {params[gi]} ({g.n_nodes} nodes) x its first {done} hw configs, "
-                         f"{threads} threads, {csec:.1f} s"}
+        cpu = {"value": nodes_done / csec, "unit": "simulated tile-nodes/s", "cores": threads, "kind": "oracle",
+               "sample": f"{checked} simulations ({len(set(used))} sweep graphs, {threads} configurations each, "
+                         f"cycling in step order), {threads} threads, {csec:.1f} s"}
         parity = {"checked_sims": checked, "mismatches": bad}
 
     out = {
@@ -178,7 +198,7 @@ def main() -> int:
         "infeasible_sims": int((statuses == 1).sum()),
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "gts_sim_wave", "launches": len(launches),
+                     "kernel": "gts_sim_window", "launches": len(launches),
                      "mean_launch_ms": float(durs.mean() * 1e3)},
         "cpu_baseline": cpu,
         "parity_sample": parity,
