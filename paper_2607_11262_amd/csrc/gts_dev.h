@@ -2,6 +2,7 @@
 // (gts_host.cpp) and the simulation kernels (gts_sim.hip).  Internal to
 // libgts.so; the public ABI is include/gts.h.
 #pragma once
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace gts {
@@ -18,8 +19,8 @@ constexpr uint32_t kGraphCrossFromMemory = 2u;  // every cross-CTA edge has a
 
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
-  uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots;
-  uint32_t max_cta_nodes, max_outdeg, pad0, pad1;
+  uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots, off_indeg;
+  uint32_t max_cta_nodes, max_outdeg;
 };
 
 struct OpDev {                  // one distinct operation descriptor
@@ -28,16 +29,20 @@ struct OpDev {                  // one distinct operation descriptor
   uint32_t work, warps, pad2;
 };
 
-struct NodeDev {                // 16 B, one per node
+constexpr uint32_t kInlineSucc = 4;
+struct NodeDev {                // 32 B, one per node
   uint32_t op_indeg;            // op id (low 16) | in-degree (high 16)
   uint32_t cta;
-  uint32_t succ_begin, succ_end;
+  uint32_t succ_begin, succ_end;   // all successors in succ[]
+  uint32_t succ[kInlineSucc];      // copies of the first four successors
 };
 
 struct CtaDev {                 // 16 B, one per CTA
   uint32_t node_begin, node_count;
-  uint32_t root_begin, root_count;  // nodes without intra-CTA in-edges
+  uint32_t root_begin, root_count;  // nodes without intra-CTA in-edges; bit 31 of
+                                    // root_count: the CTA receives cross-CTA edges
 };
+constexpr uint32_t kCtaShared = 0x80000000u;
 
 struct KernelDev {              // 16 B, one per kernel
   uint32_t cta_begin, cta_end, warps, smem;
@@ -51,6 +56,7 @@ struct Image {
   const CtaDev* ctas;
   const KernelDev* kernels;
   const uint32_t* roots;
+  const uint16_t* indeg;        // in-degree per node
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props;
 };
 
@@ -65,8 +71,9 @@ enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC 
 // Device-image edge encoding: target | bits << 30.  DATA and SYNC edges time
 // identically (released at the source's finish) and share bit pattern 0;
 // bit 30 marks an ORDER edge (released at the source's start + 1), bit 31 an
-// edge into another CTA.
-constexpr uint32_t kDevOrder = 1u, kDevCross = 2u;
+// edge into a "shared" node (one with an in-edge from another CTA), whose
+// state is updated with atomics by the windowed kernel.
+constexpr uint32_t kDevOrder = 1u, kDevShared = 2u;
 
 // Per-simulation scratch regions (byte offsets within one simulation's slice).
 struct SimLayout {
@@ -74,8 +81,9 @@ struct SimLayout {
   uint64_t off_cta;     // CtaState per CTA
   uint64_t off_pend;    // pending events: u64 key + u32 aux per entry
   uint64_t off_optab;   // per-op duration table when it does not fit LDS
-  uint64_t off_rq;      // windowed kernel: [kQueueReady][n_sm] u64 ready / retire keys
-  uint64_t off_mq;      // windowed kernel: [kQueueMem][n_sm] u64 memory-arrival keys
+  uint64_t off_rq;      // windowed kernel: [kQueueReady][n_sm] u64 ready keys (spill)
+  uint64_t off_mq;      // windowed kernel: [kQueueMem][n_sm] u64 arrival keys + [kQueueMem][n_sm] u32 op (spill)
+  uint64_t off_ret;     // windowed kernel: pending retirements beyond the LDS part (u64 each)
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };
@@ -84,9 +92,13 @@ struct CtaState {
   uint32_t sm, launch, left, maxfin;
 };
 
-// Per-SM event queues of the windowed kernel (entries per SM).
-constexpr uint32_t kQueueReady = 64;   // ready nodes and CTA retirements
-constexpr uint32_t kQueueMem = 256;    // memory arrivals (FIFO ring)
+// Windowed kernel: per-SM queues (entries per SM beyond the LDS part spill
+// to per-simulation scratch) and per-window limits.
+constexpr uint32_t kQueueReady = 64;   // ready nodes per SM (LDS part + spill)
+constexpr uint32_t kQueueMem = 256;    // memory-arrival FIFO spill ring per SM
+constexpr uint32_t kRetireLds = 256;   // pending CTA retirements held in LDS ...
+constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
+constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
 
@@ -106,6 +118,51 @@ struct Launch {
   uint32_t max_nsm;            // largest n_sm of the batch
   uint32_t max_nsub;           // largest n_subpart of the batch
   uint32_t memcap;             // windowed kernel: memory arrivals per window held in LDS
+  uint32_t ql;                 // windowed kernel: ready entries per SM held in LDS
+  uint32_t qml;                // windowed kernel: memory-arrival entries per SM held in LDS
 };
+
+// LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
+// even words).  NS / NSUB: largest n_sm / n_subpart of the batch.
+struct WinLds {
+  uint32_t optab, srv, resident, rq_cnt, rq_l, mq_lh, mq_nl, mq_gh, mq_ng, mq_lk, mq_la;
+  uint32_t ret_cnt, ret_min, ret_l, misc, dstart, dcnt, bucket, w_key0, w_aux0, s_key, s_slot, w_fin, total;
+};
+__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t ql, uint32_t qml,
+                                           uint32_t memcap) {
+  WinLds L;
+  uint32_t o = 0;
+  auto take = [&o](uint32_t words, bool wide) {
+    if (wide) o = (o + 1u) & ~1u;
+    const uint32_t r = o;
+    o += words;
+    return r;
+  };
+  L.optab = take(4u * P, true);
+  L.srv = take(NS * (NSUB + 2u), false);
+  L.resident = take(NS, false);
+  L.rq_cnt = take(NS, false);
+  L.rq_l = take(2u * ql * NS, true);
+  L.mq_lh = take(NS, false);
+  L.mq_nl = take(NS, false);
+  L.mq_gh = take(NS, false);
+  L.mq_ng = take(NS, false);
+  L.mq_lk = take(2u * qml * NS, true);
+  L.mq_la = take(qml * NS, false);
+  L.ret_cnt = take(1, false);
+  L.ret_min = take(1, false);
+  L.ret_l = take(2u * kRetireLds, true);
+  L.misc = take(8, false);
+  L.dstart = take(NS, false);
+  L.dcnt = take(NS, false);
+  L.bucket = take(kWindowMax, false);
+  L.w_key0 = take(2u * memcap, true);
+  L.w_aux0 = take(memcap, false);
+  L.s_key = take(2u * memcap, true);
+  L.s_slot = take(memcap, false);
+  L.w_fin = take(memcap, false);
+  L.total = o;
+  return L;
+}
 
 }  // namespace gts

@@ -53,6 +53,7 @@ bool is_memory(uint8_t c) { return c == gts::C_GLOAD || c == gts::C_GSTORE; }
 // Everything the image needs that is derived from a valid host graph.
 struct Derived {
   std::vector<uint32_t> indeg, node_cta, roots, root_begin, root_count;
+  std::vector<uint8_t> shared;  // node has an in-edge from another CTA
   uint32_t props = 0, max_cta_nodes = 0, max_outdeg = 0;
 };
 
@@ -172,6 +173,12 @@ int check_graph(const gts_graph_host* h, Derived* d) {
     }
     d->root_count[c] = (uint32_t)d->roots.size() - d->root_begin[c];
   }
+  d->shared.assign(N, 0);
+  for (uint32_t u = 0; u < N; ++u)
+    for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
+      const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
+      if (node_cta[u] != node_cta[v]) d->shared[v] = 1;
+    }
   d->indeg.swap(indeg);
   d->node_cta.swap(node_cta);
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u);
@@ -181,7 +188,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
 }
 
 struct ImageLayout {
-  uint64_t ops, nodes, succ, ctas, kernels, roots, total;
+  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, total;
 };
 
 ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
@@ -199,6 +206,8 @@ ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
   off = align_up(off + (uint64_t)h->n_kernels * sizeof(gts::KernelDev), gts::kAlign);
   L.roots = off;
   off = align_up(off + n_roots * 4, gts::kAlign);
+  L.indeg = off;
+  off = align_up(off + (uint64_t)h->n_nodes * 2, gts::kAlign);
   L.total = off;
   return L;
 }
@@ -220,8 +229,9 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
   // scratch by the general kernel).
   s.off_rq = s.off_pend;
   s.off_mq = align_up(s.off_rq + 8ull * gts::kQueueReady * GTS_MAX_SM, gts::kAlign);
-  const uint64_t mq_end = align_up(s.off_mq + 8ull * gts::kQueueMem * GTS_MAX_SM, gts::kAlign);
-  s.stride = std::max(off, mq_end) + gts::kStatsBytes;
+  s.off_ret = align_up(s.off_mq + 12ull * gts::kQueueMem * GTS_MAX_SM, gts::kAlign);
+  const uint64_t ret_end = align_up(s.off_ret + 8ull * (gts::kRetireCap - gts::kRetireLds), gts::kAlign);
+  s.stride = std::max(off, ret_end) + gts::kStatsBytes;
   return s;
 }
 
@@ -288,6 +298,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.max_nsm = max_nsm;
   L.max_nsub = max_nsub;
   L.memcap = 0;
+  L.ql = L.qml = 0;
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
@@ -295,13 +306,18 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
   if (windowed) {
+    // LDS per simulation: fixed tables plus ql / qml queue entries per SM
+    // (halved until the layout fits the budget) and the window buffers.
     constexpr uint32_t kWindowBudget = 48 * 1024;
-    const uint64_t fixed = optab_bytes + 4ull * (max_nsm * (max_nsub + 2) + 4ull * max_nsm + 2);
-    uint32_t cap = 2048;
-    while (cap > 256 && fixed + 12ull * cap > kWindowBudget) cap >>= 1;
-    windowed = fixed + 12ull * cap <= kLdsBudget;
-    L.memcap = cap;
-    lds_window = (uint32_t)(fixed + 12ull * cap + 8);
+    L.memcap = std::max<uint32_t>(256u, max_nsm);
+    uint32_t q = 16;
+    auto bytes = [&](uint32_t qq) {
+      return 4ull * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qq, qq, L.memcap).total;
+    };
+    while (q > 2 && bytes(q) > kWindowBudget) q >>= 1;
+    L.ql = L.qml = q;
+    windowed = bytes(q) <= kLdsBudget;
+    lds_window = (uint32_t)bytes(q);
   }
   // GTS_KERNEL=window (diagnostics): no general-kernel pass, so simulations
   // the windowed kernel hands back keep their internal retry status.
@@ -392,6 +408,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   hdr->off_ctas = L.ctas;
   hdr->off_kernels = L.kernels;
   hdr->off_roots = L.roots;
+  hdr->off_indeg = L.indeg;
   hdr->max_cta_nodes = d.max_cta_nodes;
   hdr->max_outdeg = d.max_outdeg;
   auto* ops = reinterpret_cast<gts::OpDev*>(img.data() + L.ops);
@@ -402,30 +419,34 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     ops[p].warps = h->op_warps[p];
   }
   auto* nodes = reinterpret_cast<gts::NodeDev*>(img.data() + L.nodes);
-  for (uint32_t v = 0; v < h->n_nodes; ++v) {
-    nodes[v].op_indeg = (uint32_t)h->node_op[v] | (d.indeg[v] << 16);
-    nodes[v].cta = d.node_cta[v];
-    nodes[v].succ_begin = h->succ_ptr[v];
-    nodes[v].succ_end = h->succ_ptr[v + 1];
-  }
-  {
-    // DATA and SYNC share one pattern; mark ORDER and cross-CTA edges.
-    auto* succ = reinterpret_cast<uint32_t*>(img.data() + L.succ);
-    for (uint32_t u = 0; u < h->n_nodes; ++u)
-      for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
-        const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
-        const uint32_t kind = h->succ[e] >> GTS_EDGE_KIND_SHIFT;
-        const uint32_t bits = (kind == GTS_EDGE_ORDER ? gts::kDevOrder : 0u) |
-                              (d.node_cta[u] != d.node_cta[v] ? gts::kDevCross : 0u);
-        succ[e] = v | (bits << GTS_EDGE_KIND_SHIFT);
-      }
+  auto* succ_dev = reinterpret_cast<uint32_t*>(img.data() + L.succ);
+  auto* indeg16 = reinterpret_cast<uint16_t*>(img.data() + L.indeg);
+  // DATA and SYNC share one pattern; mark ORDER edges and edges into
+  // shared nodes; the first four successors are also copied into the node.
+  for (uint32_t u = 0; u < h->n_nodes; ++u) {
+    for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
+      const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
+      const uint32_t kind = h->succ[e] >> GTS_EDGE_KIND_SHIFT;
+      const uint32_t bits = (kind == GTS_EDGE_ORDER ? gts::kDevOrder : 0u) | (d.shared[v] ? gts::kDevShared : 0u);
+      succ_dev[e] = v | (bits << GTS_EDGE_KIND_SHIFT);
+    }
+    gts::NodeDev& n = nodes[u];
+    n.op_indeg = (uint32_t)h->node_op[u] | (d.indeg[u] << 16);
+    n.cta = d.node_cta[u];
+    n.succ_begin = h->succ_ptr[u];
+    n.succ_end = h->succ_ptr[u + 1];
+    for (uint32_t k = 0; k < gts::kInlineSucc; ++k)
+      n.succ[k] = n.succ_begin + k < n.succ_end ? succ_dev[n.succ_begin + k] : 0u;
+    indeg16[u] = (uint16_t)d.indeg[u];
   }
   auto* ctas = reinterpret_cast<gts::CtaDev*>(img.data() + L.ctas);
   for (uint32_t c = 0; c < h->n_ctas; ++c) {
     ctas[c].node_begin = h->cta_node_begin[c];
     ctas[c].node_count = h->cta_node_begin[c + 1] - h->cta_node_begin[c];
     ctas[c].root_begin = d.root_begin[c];
-    ctas[c].root_count = d.root_count[c];
+    bool shared = false;
+    for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1] && !shared; ++v) shared = d.shared[v] != 0;
+    ctas[c].root_count = d.root_count[c] | (shared ? gts::kCtaShared : 0u);
   }
   auto* ks = reinterpret_cast<gts::KernelDev*>(img.data() + L.kernels);
   for (uint32_t k = 0; k < h->n_kernels; ++k) {
@@ -450,6 +471,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.ctas = reinterpret_cast<const gts::CtaDev*>(base + L.ctas);
   g->img.kernels = reinterpret_cast<const gts::KernelDev*>(base + L.kernels);
   g->img.roots = reinterpret_cast<const uint32_t*>(base + L.roots);
+  g->img.indeg = reinterpret_cast<const uint16_t*>(base + L.indeg);
   g->img.n_nodes = h->n_nodes;
   g->img.n_edges = h->n_edges;
   g->img.n_ctas = h->n_ctas;

@@ -175,11 +175,12 @@ struct Sim {
         resident[sm] += 1;
       }
       ++next_cta;
-      for (uint32_t r0 = 0; r0 < cd.root_count; r0 += 64) {
+      const uint32_t nroots = cd.root_count & ~kCtaShared;
+      for (uint32_t r0 = 0; r0 < nroots; r0 += 64) {
         const uint32_t ri = r0 + lane;
         bool ready = false;
         uint64_t key = 0;
-        if (ri < cd.root_count) {
+        if (ri < nroots) {
           const uint32_t v = G.roots[cd.root_begin + ri];
           const uint64_t s = pld(&state[v]);
           const uint32_t indeg = G.nodes[v].op_indeg >> 16;
