@@ -16,6 +16,8 @@ constexpr uint32_t kGraphSinksAreMemory = 1u;   // every node without an intra-C
                                                 // successor is a GLOAD/GSTORE
 constexpr uint32_t kGraphCrossFromMemory = 2u;  // every cross-CTA edge has a
                                                 // GLOAD/GSTORE source, DATA/SYNC kind
+constexpr uint32_t kGraphSmallOutdeg = 4u;      // every out-degree is below 0xFFFF
+constexpr uint32_t kGraphHasShared = 8u;        // some CTA receives cross-CTA edges
 
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
@@ -29,18 +31,22 @@ struct OpDev {                  // one distinct operation descriptor
   uint32_t work, warps, pad2;
 };
 
-constexpr uint32_t kInlineSucc = 4;
-struct NodeDev {                // 32 B, one per node
-  uint32_t op_indeg;            // op id (low 16) | in-degree (high 16)
+constexpr uint32_t kInlineSucc = 3;
+struct NodeDev {                // 32 B, one per node and a sentinel after the last
+  uint32_t op_nsucc;            // op id (low 16) | out-degree (high 16, 0xFFFF if larger)
   uint32_t cta;
-  uint32_t succ_begin, succ_end;   // all successors in succ[]
-  uint32_t succ[kInlineSucc];      // copies of the first four successors
+  uint32_t succ_begin;          // successors: succ[succ_begin, next record's succ_begin)
+  uint32_t succ[kInlineSucc];   // copies of the first three successors
+  uint16_t sindeg[kInlineSucc]; // and their in-degrees
+  uint16_t pad;
 };
 
-struct CtaDev {                 // 16 B, one per CTA
+constexpr uint32_t kInlineRoots = 4;
+struct CtaDev {                 // 32 B, one per CTA
   uint32_t node_begin, node_count;
   uint32_t root_begin, root_count;  // nodes without intra-CTA in-edges; bit 31 of
                                     // root_count: the CTA receives cross-CTA edges
+  uint32_t root[kInlineRoots];      // copies of the first four roots
 };
 constexpr uint32_t kCtaShared = 0x80000000u;
 
@@ -81,9 +87,9 @@ struct SimLayout {
   uint64_t off_cta;     // CtaState per CTA
   uint64_t off_pend;    // pending events: u64 key + u32 aux per entry
   uint64_t off_optab;   // per-op duration table when it does not fit LDS
-  uint64_t off_rq;      // windowed kernel: [kQueueReady][n_sm] u64 ready keys (spill)
-  uint64_t off_mq;      // windowed kernel: [kQueueMem][n_sm] u64 arrival keys + [kQueueMem][n_sm] u32 op (spill)
-  uint64_t off_ret;     // windowed kernel: pending retirements beyond the LDS part (u64 each)
+  uint64_t off_rp;      // windowed kernel: ready pools beyond LDS, [kPoolSpill][64] u64
+  uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
+  uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };
@@ -92,12 +98,13 @@ struct CtaState {
   uint32_t sm, launch, left, maxfin;
 };
 
-// Windowed kernel: per-SM queues (entries per SM beyond the LDS part spill
-// to per-simulation scratch) and per-window limits.
-constexpr uint32_t kQueueReady = 64;   // ready nodes per SM (LDS part + spill)
-constexpr uint32_t kQueueMem = 256;    // memory-arrival FIFO spill ring per SM
+// Windowed kernel limits.
+constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs per lane)
+constexpr uint32_t kPoolSpill = 48;    // ready entries per lane beyond the LDS pool
+constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
 constexpr uint32_t kRetireLds = 256;   // pending CTA retirements held in LDS ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
+constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
@@ -117,19 +124,17 @@ struct Launch {
   uint32_t retry_only;         // general kernel: run only simulations marked kStatusRetry
   uint32_t max_nsm;            // largest n_sm of the batch
   uint32_t max_nsub;           // largest n_subpart of the batch
-  uint32_t memcap;             // windowed kernel: memory arrivals per window held in LDS
-  uint32_t ql;                 // windowed kernel: ready entries per SM held in LDS
-  uint32_t qml;                // windowed kernel: memory-arrival entries per SM held in LDS
+  uint32_t qp;                 // windowed kernel: ready-pool entries per lane held in LDS
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
-// even words).  NS / NSUB: largest n_sm / n_subpart of the batch.
+// even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: ready
+// entries per lane.
 struct WinLds {
-  uint32_t optab, srv, resident, rq_cnt, rq_l, mq_lh, mq_nl, mq_gh, mq_ng, mq_lk, mq_la;
-  uint32_t ret_cnt, ret_min, ret_l, misc, dstart, dcnt, bucket, w_key0, w_aux0, s_key, s_slot, w_fin, total;
+  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, rp_cnt, rp, ret_cnt, ret_min, ret_l, w_key, w_aux, w_fin;
+  uint32_t total;
 };
-__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t ql, uint32_t qml,
-                                           uint32_t memcap) {
+__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t QP) {
   WinLds L;
   uint32_t o = 0;
   auto take = [&o](uint32_t words, bool wide) {
@@ -141,26 +146,17 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB
   L.optab = take(4u * P, true);
   L.srv = take(NS * (NSUB + 2u), false);
   L.resident = take(NS, false);
-  L.rq_cnt = take(NS, false);
-  L.rq_l = take(2u * ql * NS, true);
-  L.mq_lh = take(NS, false);
-  L.mq_nl = take(NS, false);
-  L.mq_gh = take(NS, false);
-  L.mq_ng = take(NS, false);
-  L.mq_lk = take(2u * qml * NS, true);
-  L.mq_la = take(qml * NS, false);
+  L.mq_head = take(NS, false);
+  L.mq_pos = take(NS, false);
+  L.dsc = take(NS, false);
+  L.rp_cnt = take(64, false);
+  L.rp = take(2u * 64u * QP, true);
   L.ret_cnt = take(1, false);
   L.ret_min = take(1, false);
   L.ret_l = take(2u * kRetireLds, true);
-  L.misc = take(8, false);
-  L.dstart = take(NS, false);
-  L.dcnt = take(NS, false);
-  L.bucket = take(kWindowMax, false);
-  L.w_key0 = take(2u * memcap, true);
-  L.w_aux0 = take(memcap, false);
-  L.s_key = take(2u * memcap, true);
-  L.s_slot = take(memcap, false);
-  L.w_fin = take(memcap, false);
+  L.w_key = take(2u * kWinCap, true);
+  L.w_aux = take(kWinCap, false);
+  L.w_fin = take(kWinCap, false);
   L.total = o;
   return L;
 }

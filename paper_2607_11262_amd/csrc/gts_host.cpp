@@ -181,7 +181,10 @@ int check_graph(const gts_graph_host* h, Derived* d) {
     }
   d->indeg.swap(indeg);
   d->node_cta.swap(node_cta);
-  d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u);
+  bool any_shared = false;
+  for (uint32_t v = 0; v < N && !any_shared; ++v) any_shared = d->shared[v] != 0;
+  d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
+             (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   return GTS_OK;
@@ -197,7 +200,7 @@ ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
   L.ops = off;
   off = align_up(off + (uint64_t)h->n_ops * sizeof(gts::OpDev), gts::kAlign);
   L.nodes = off;
-  off = align_up(off + (uint64_t)h->n_nodes * sizeof(gts::NodeDev), gts::kAlign);
+  off = align_up(off + ((uint64_t)h->n_nodes + 1) * sizeof(gts::NodeDev), gts::kAlign);
   L.succ = off;
   off = align_up(off + (uint64_t)h->n_edges * 4, gts::kAlign);
   L.ctas = off;
@@ -227,9 +230,9 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
   // The windowed kernel's per-SM queues overlay the general kernel's pending
   // list (a simulation the windowed kernel hands back is restarted from
   // scratch by the general kernel).
-  s.off_rq = s.off_pend;
-  s.off_mq = align_up(s.off_rq + 8ull * gts::kQueueReady * GTS_MAX_SM, gts::kAlign);
-  s.off_ret = align_up(s.off_mq + 12ull * gts::kQueueMem * GTS_MAX_SM, gts::kAlign);
+  s.off_rp = s.off_pend;
+  s.off_mq = align_up(s.off_rp + 8ull * gts::kPoolSpill * 64, gts::kAlign);
+  s.off_ret = align_up(s.off_mq + 12ull * gts::kRing * gts::kWinMaxSm, gts::kAlign);
   const uint64_t ret_end = align_up(s.off_ret + 8ull * (gts::kRetireCap - gts::kRetireLds), gts::kAlign);
   s.stride = std::max(off, ret_end) + gts::kStatsBytes;
   return s;
@@ -297,27 +300,25 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.retry_only = 0;
   L.max_nsm = max_nsm;
   L.max_nsub = max_nsub;
-  L.memcap = 0;
-  L.ql = L.qml = 0;
+  L.qp = 0;
 
-  const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory;
+  const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
-  bool windowed = (g->img.props & need_props) == need_props && g->img.n_nodes > 0 &&
+  bool windowed = (g->img.props & need_props) == need_props && g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
   if (windowed) {
-    // LDS per simulation: fixed tables plus ql / qml queue entries per SM
-    // (halved until the layout fits the budget) and the window buffers.
-    constexpr uint32_t kWindowBudget = 48 * 1024;
-    L.memcap = std::max<uint32_t>(256u, max_nsm);
-    uint32_t q = 16;
-    auto bytes = [&](uint32_t qq) {
-      return 4ull * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qq, qq, L.memcap).total;
-    };
-    while (q > 2 && bytes(q) > kWindowBudget) q >>= 1;
-    L.ql = L.qml = q;
-    windowed = bytes(q) <= kLdsBudget;
-    lds_window = (uint32_t)bytes(q);
+    // LDS per simulation: fixed tables plus qp ready entries per lane; take
+    // the largest qp in [8, 16] that keeps the most simulations per CU.
+    constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 8;
+    auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qp).total; };
+    auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
+    uint32_t qp = 16;
+    for (uint32_t q = 15; q >= 8; --q)
+      if (per_cu(q) > per_cu(qp)) qp = q;
+    L.qp = qp;
+    windowed = bytes(qp) <= kLdsBudget;
+    lds_window = bytes(qp);
   }
   // GTS_KERNEL=window (diagnostics): no general-kernel pass, so simulations
   // the windowed kernel hands back keep their internal retry status.
@@ -422,7 +423,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   auto* succ_dev = reinterpret_cast<uint32_t*>(img.data() + L.succ);
   auto* indeg16 = reinterpret_cast<uint16_t*>(img.data() + L.indeg);
   // DATA and SYNC share one pattern; mark ORDER edges and edges into
-  // shared nodes; the first four successors are also copied into the node.
+  // shared nodes; the first three successors and their in-degrees are also
+  // copied into the node record.
   for (uint32_t u = 0; u < h->n_nodes; ++u) {
     for (uint32_t e = h->succ_ptr[u]; e < h->succ_ptr[u + 1]; ++e) {
       const uint32_t v = h->succ[e] & GTS_EDGE_TARGET_MASK;
@@ -431,14 +433,17 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
       succ_dev[e] = v | (bits << GTS_EDGE_KIND_SHIFT);
     }
     gts::NodeDev& n = nodes[u];
-    n.op_indeg = (uint32_t)h->node_op[u] | (d.indeg[u] << 16);
+    const uint32_t deg = h->succ_ptr[u + 1] - h->succ_ptr[u];
+    n.op_nsucc = (uint32_t)h->node_op[u] | (std::min<uint32_t>(deg, 0xFFFFu) << 16);
     n.cta = d.node_cta[u];
     n.succ_begin = h->succ_ptr[u];
-    n.succ_end = h->succ_ptr[u + 1];
-    for (uint32_t k = 0; k < gts::kInlineSucc; ++k)
-      n.succ[k] = n.succ_begin + k < n.succ_end ? succ_dev[n.succ_begin + k] : 0u;
+    for (uint32_t k = 0; k < gts::kInlineSucc; ++k) {
+      n.succ[k] = k < deg ? succ_dev[n.succ_begin + k] : 0u;
+      n.sindeg[k] = k < deg ? (uint16_t)d.indeg[h->succ[n.succ_begin + k] & GTS_EDGE_TARGET_MASK] : (uint16_t)0;
+    }
     indeg16[u] = (uint16_t)d.indeg[u];
   }
+  nodes[h->n_nodes].succ_begin = h->n_edges;  // sentinel: end of the last node's successors
   auto* ctas = reinterpret_cast<gts::CtaDev*>(img.data() + L.ctas);
   for (uint32_t c = 0; c < h->n_ctas; ++c) {
     ctas[c].node_begin = h->cta_node_begin[c];
@@ -447,6 +452,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     bool shared = false;
     for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1] && !shared; ++v) shared = d.shared[v] != 0;
     ctas[c].root_count = d.root_count[c] | (shared ? gts::kCtaShared : 0u);
+    for (uint32_t r = 0; r < gts::kInlineRoots; ++r)
+      ctas[c].root[r] = r < d.root_count[c] ? d.roots[d.root_begin[c] + r] : 0u;
   }
   auto* ks = reinterpret_cast<gts::KernelDev*>(img.data() + L.kernels);
   for (uint32_t k = 0; k < h->n_kernels; ++k) {

@@ -78,11 +78,13 @@ struct Sim {
 
   // Release the out-edges of a node selected by `which`: 0 = ORDER edges
   // released at issue, 1 = every other edge, released at completion.
-  __device__ void release(const NodeDev& rec, uint32_t which, uint64_t r, uint32_t src_cta, uint32_t src_sm) {
+  __device__ void release(uint32_t v, const NodeDev& rec, uint32_t which, uint64_t r, uint32_t src_cta,
+                          uint32_t src_sm) {
     const bool ofin = (flags & GTS_ORDER_AT_FINISH) != 0;
-    for (uint32_t e0 = rec.succ_begin; e0 < rec.succ_end; e0 += 64) {
+    const uint32_t succ_end = G.nodes[v + 1].succ_begin;
+    for (uint32_t e0 = rec.succ_begin; e0 < succ_end; e0 += 64) {
       const uint32_t e = e0 + lane;
-      const bool active = e < rec.succ_end;
+      const bool active = e < succ_end;
       const uint32_t ent = active ? G.succ[e] : 0u;
       const uint32_t kind = ent >> GTS_EDGE_KIND_SHIFT;
       const uint32_t w = ent & GTS_EDGE_TARGET_MASK;
@@ -93,16 +95,17 @@ struct Sim {
       uint32_t aux = 0;
       if (sel) {
         const uint64_t s = pld(&state[w]);
-        const NodeDev nr = G.nodes[w];
+        const uint32_t nr_cta = G.nodes[w].cta;
+        const uint32_t nr_indeg = G.indeg[w];
         uint32_t acc = (uint32_t)s;
         const uint32_t cnt = (uint32_t)(s >> 32) + 1;
         acc = r > acc ? (uint32_t)r : acc;
         pst(&state[w], ((uint64_t)cnt << 32) | acc);
-        if (cnt == (nr.op_indeg >> 16) && nr.cta < next_cta) {
+        if (cnt == nr_indeg && nr_cta < next_cta) {
           uint32_t launch = 0, sm = src_sm;
-          if (nr.cta != src_cta) {
-            launch = pld(&cst[nr.cta].launch);
-            sm = pld(&cst[nr.cta].sm);
+          if (nr_cta != src_cta) {
+            launch = pld(&cst[nr_cta].launch);
+            sm = pld(&cst[nr_cta].sm);
           }
           ready = true;
           key = mkkey(acc > launch ? acc : launch, kEvReady, w);
@@ -183,7 +186,7 @@ struct Sim {
         if (ri < nroots) {
           const uint32_t v = G.roots[cd.root_begin + ri];
           const uint64_t s = pld(&state[v]);
-          const uint32_t indeg = G.nodes[v].op_indeg >> 16;
+          const uint32_t indeg = G.indeg[v];
           if ((uint32_t)(s >> 32) == indeg) {
             const uint32_t acc = (uint32_t)s;
             ready = true;
@@ -198,7 +201,7 @@ struct Sim {
 
   __device__ void issue(uint32_t v, uint32_t t, uint32_t sm) {
     const NodeDev rec = G.nodes[v];
-    const uint4 od = optab[rec.op_indeg & 0xFFFFu];
+    const uint4 od = optab[rec.op_nsucc & 0xFFFFu];
     const uint32_t cls = od.w & 7u;
     const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
     uint32_t* S = srv + sm * sstride;
@@ -215,21 +218,21 @@ struct Sim {
       const uint64_t f = s + od.x + od.z;
       if (!complete(v, rec, s, f, sm)) return;
       if (lane < nsub && ((lanes >> lane) & 1u)) S[lane] = (uint32_t)(s + od.x);
-      release(rec, 0, s + 1, rec.cta, sm);
-      release(rec, 1, f, rec.cta, sm);
+      release(v, rec, 0, s + 1, rec.cta, sm);
+      release(v, rec, 1, f, rec.cta, sm);
     } else if (cls == C_SMEM) {
       const uint32_t a = S[nsub];
       const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
       const uint64_t f = s + od.x + od.z;
       if (!complete(v, rec, s, f, sm)) return;
       if (lane == 0) S[nsub] = (uint32_t)(s + od.x);
-      release(rec, 0, s + 1, rec.cta, sm);
-      release(rec, 1, f, rec.cta, sm);
+      release(v, rec, 0, s + 1, rec.cta, sm);
+      release(v, rec, 1, f, rec.cta, sm);
     } else if (cls == C_SYNC) {
       const uint64_t f = (uint64_t)t + od.z;
       if (!complete(v, rec, t, f, sm)) return;
-      release(rec, 0, (uint64_t)t + 1, rec.cta, sm);
-      release(rec, 1, f, rec.cta, sm);
+      release(v, rec, 0, (uint64_t)t + 1, rec.cta, sm);
+      release(v, rec, 1, f, rec.cta, sm);
     } else {
       const uint32_t a = S[nsub + 1];
       const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
@@ -238,14 +241,14 @@ struct Sim {
         return;
       }
       if (lane == 0) S[nsub + 1] = (uint32_t)(s + od.x);
-      release(rec, 0, s + 1, rec.cta, sm);
+      release(v, rec, 0, s + 1, rec.cta, sm);
       push_one(mkkey(s, kEvMem, v), sm);
     }
   }
 
   __device__ void mem_arrive(uint32_t v, uint32_t t, uint32_t sm) {
     const NodeDev rec = G.nodes[v];
-    const uint4 od = optab[rec.op_indeg & 0xFFFFu];
+    const uint4 od = optab[rec.op_nsucc & 0xFFFFu];
     const bool dram = (od.w >> 3) & 1u;
     const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
     const uint64_t av = dram ? dram_av : l2_av;
@@ -258,7 +261,7 @@ struct Sim {
     const uint64_t e = (uint64_t)t + od.x;
     const uint64_t f = (e > mend ? e : mend) + od.z;
     if (!complete(v, rec, t, f, sm)) return;
-    release(rec, 1, f, rec.cta, sm);
+    release(v, rec, 1, f, rec.cta, sm);
   }
 };
 
