@@ -100,7 +100,7 @@ struct CtaState {
 
 // Windowed kernel limits.
 constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs per lane)
-constexpr uint32_t kPoolSpill = 48;    // ready entries per lane beyond the LDS pool
+constexpr uint32_t kPoolSpill = 240;   // ready entries per lane beyond the LDS pool
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
 constexpr uint32_t kRetireLds = 256;   // pending CTA retirements held in LDS ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)

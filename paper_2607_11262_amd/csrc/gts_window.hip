@@ -230,6 +230,46 @@ struct WSim {
     const uint32_t n = rp_cnt[l];
     return n < QP + kPoolSpill ? n : QP + kPoolSpill;
   }
+  // Smallest pool entry of each SM slot (with its index): the LDS part, then
+  // the spill eight entries per round trip.
+  __device__ __forceinline__ static void consider(uint64_t k, uint32_t i, uint64_t (&best)[NB], uint32_t (&bi)[NB]) {
+    const uint32_t j = (uint32_t)(k >> 30) & 3u;
+#pragma unroll
+    for (uint32_t jj = 0; jj < NB; ++jj)
+      if (j == jj && k < best[jj]) {
+        best[jj] = k;
+        bi[jj] = i;
+      }
+  }
+  __device__ __forceinline__ void pool_scan(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
+    const uint32_t nl = n < QP ? n : QP;
+    for (uint32_t i = 0; i < nl; ++i) consider(rp[i * 64u + lane], i, best, bi);
+    for (uint32_t i0 = QP; i0 < n; i0 += 8) {
+      uint64_t kk[8];
+#pragma unroll
+      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? rp_g[(i0 + q - QP) * 64u + lane] : kNoKey;
+#pragma unroll
+      for (uint32_t q = 0; q < 8; ++q)
+        if (i0 + q < n) consider(kk[q], i0 + q, best, bi);
+    }
+  }
+  // Smallest cycle in the lane's pool (kNoKey if empty).
+  __device__ __forceinline__ uint64_t pool_min(uint32_t n) const {
+    uint64_t m = kNoKey;
+    const uint32_t nl = n < QP ? n : QP;
+    for (uint32_t i = 0; i < nl; ++i) {
+      const uint64_t k = rp[i * 64u + lane] >> 32;
+      m = k < m ? k : m;
+    }
+    for (uint32_t i0 = QP; i0 < n; i0 += 8) {
+      uint64_t kk[8];
+#pragma unroll
+      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? rp_g[(i0 + q - QP) * 64u + lane] >> 32 : kNoKey;
+#pragma unroll
+      for (uint32_t q = 0; q < 8; ++q) m = kk[q] < m ? kk[q] : m;
+    }
+    return m;
+  }
   __device__ __forceinline__ void rq_push(uint32_t s, uint32_t cyc, uint32_t v) {
     const uint32_t l = s & 63u;
     const uint32_t slot = atomicAdd(&rp_cnt[l], 1u);
@@ -436,18 +476,7 @@ struct WSim {
       best[j] = kNoKey;
       bi[j] = 0;
     }
-    if (!bad) {
-      for (uint32_t i = 0; i < n; ++i) {
-        const uint64_t k = rp_get(lane, i);
-        const uint32_t j = (uint32_t)(k >> 30) & 3u;
-#pragma unroll
-        for (uint32_t jj = 0; jj < NB; ++jj)
-          if (j == jj && k < best[jj]) {
-            best[jj] = k;
-            bi[jj] = i;
-          }
-      }
-    }
+    if (!bad) pool_scan(n, best, bi);
     bool ok[NB];
     uint32_t taken = 0;
 #pragma unroll
@@ -853,11 +882,7 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_window(Launch L) {
     // T: lower bound of the earliest pending event
     uint64_t tmin = kNoKey;
     {
-      const uint32_t n = S.rp_n(lane);
-      for (uint32_t i = 0; i < n; ++i) {
-        const uint64_t k = S.rp_get(lane, i) >> 32;
-        tmin = k < tmin ? k : tmin;
-      }
+      tmin = S.pool_min(S.rp_n(lane));
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;

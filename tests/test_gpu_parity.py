@@ -200,3 +200,57 @@ def test_digest_only_mode_matches(torch_cuda):
     a = run_gpu(torch_cuda, g, hws, ALL)
     b = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
     assert np.array_equal(a[1], b[1]) and np.array_equal(a[3], b[3]) and np.array_equal(a[2], b[2])
+
+
+def test_config2_bench_launch(torch_cuda):
+    """The bench's launch shape: one sweep graph against its 4096 resident
+    hardware records in one launch (digest outputs), sampled against the
+    oracle; per-node cycles on two of the records."""
+    ps = W.sweep_params()
+    for gi in (0, 7):
+        g = W.sweep_graph(ps[gi])
+        hws = W.config_hw(2, B=4096, index=gi)
+        note(f"config 2 bench launch graph {gi} N={g.n_nodes} B=4096")
+        dg = api.upload(g)
+        hs = api.upload_hw(hws)
+        flags = api.OUT_DIGEST
+        scratch = torch_cuda.empty(api.scratch_bytes(dg, 4096, flags), dtype=torch_cuda.uint8, device="cuda")
+        cyc, mk, st, dgst = api.alloc_outputs(dg, 4096, flags)
+        api.simulate_hwset_into(dg, hs, 0, 4096, flags, None, mk, st, dgst, scratch)
+        torch_cuda.cuda.synchronize()
+        gpu = (None, mk.cpu().numpy().view(np.uint32), st.cpu().numpy(), dgst.cpu().numpy().view(np.uint64))
+        compare(g, hws, flags, gpu, sims=list(range(0, 4096, 128)) + [4095], nodes=False)
+        sub = hws[[1, 4094]]
+        compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
+
+
+def test_config3_full(torch_cuda):
+    """FlashAttention forward, 2.6M nodes, all 256 records in one launch."""
+    g = W.config_graph(3)
+    hws = W.config_hw(3)
+    note(f"config 3 N={g.n_nodes} B={hws.shape[0]}")
+    gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
+    compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 16))
+    sub = hws[[3, 128, 255]]
+    compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
+
+
+def test_config4_digest_all(torch_cuda):
+    """Split-KV decode: every one of the 1024 records, digest and makespan."""
+    g = W.config_graph(4)
+    hws = W.config_hw(4)
+    note(f"config 4 N={g.n_nodes} B={hws.shape[0]} (all)")
+    gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
+    compare(g, hws, api.OUT_DIGEST, gpu, threads=16)
+
+
+def test_config5_full(torch_cuda):
+    """Decoder layer, 20.5M nodes over nine kernels, all 64 records in one
+    launch; per-node cycles on two records."""
+    g = W.config_graph(5)
+    hws = W.config_hw(5)
+    note(f"config 5 N={g.n_nodes} B={hws.shape[0]}")
+    gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
+    compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 8))
+    sub = hws[[5, 63]]
+    compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
