@@ -57,7 +57,6 @@ namespace {
 
 constexpr uint64_t kNoKey = ~0ull;
 constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u, kBadWindow = 16u;
-constexpr uint32_t NB = kWinMaxSm / 64;  // SMs per lane
 constexpr uint32_t GQ = 3;               // ring entries loaded per SM and window
 
 // Node state: latest release cycle (low word) | released in-edges (high word).
@@ -176,6 +175,7 @@ __device__ __forceinline__ bool needs_slow(const Rec r) {
 }
 
 // Loaded ring entries with cycle below X.
+template <uint32_t NB>
 __device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], uint64_t X) {
   uint32_t c = 0;
 #pragma unroll
@@ -185,6 +185,9 @@ __device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], uin
   return c;
 }
 
+// One simulation on one wavefront; NB = SMs per lane (ceil(n_sm / 64) of the
+// largest hardware record of the batch).
+template <uint32_t NB>
 struct WSim {
   Image G;
   const uint32_t* hw;
@@ -768,13 +771,13 @@ struct WSim {
   }
 };
 
-}  // namespace
 
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window(Launch L) {
+template <uint32_t NB>
+__device__ __forceinline__ void window_body(const Launch& L) {
   const uint32_t b = blockIdx.x;
   if (b >= L.B) return;
   extern __shared__ uint32_t lds[];
-  WSim S;
+  WSim<NB> S;
   S.G = L.img;
   S.hw = L.hw + (uint64_t)b * HW_WORDS;
   S.b = b;
@@ -946,11 +949,11 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_window(Launch L) {
       const uint32_t R = dp;
       if (R) {
         if (R <= 64)
-          S.sort_keys<1>(R);
+          S.template sort_keys<1>(R);
         else if (R <= 128)
-          S.sort_keys<2>(R);
+          S.template sort_keys<2>(R);
         else
-          S.sort_keys<4>(R);
+          S.template sort_keys<4>(R);
         bool stop = false;
         for (uint32_t i = 0; i < R && !stop;) {
           const uint64_t r = uni64(S.w_key[i] >> 32);
@@ -1064,11 +1067,11 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_window(Launch L) {
     const uint64_t c4 = __builtin_amdgcn_s_memtime();
     if (M) {
       if (M <= 64)
-        S.memory_phase<1>(M);
+        S.template memory_phase<1>(M);
       else if (M <= 128)
-        S.memory_phase<2>(M);
+        S.template memory_phase<2>(M);
       else
-        S.memory_phase<4>(M);
+        S.template memory_phase<4>(M);
     }
     wsync();
     const uint64_t c5 = __builtin_amdgcn_s_memtime();
@@ -1129,9 +1132,24 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_window(Launch L) {
   }
 }
 
+}  // namespace
+
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window1(Launch L) { window_body<1>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window2(Launch L) { window_body<2>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window3(Launch L) { window_body<3>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window4(Launch L) { window_body<4>(L); }
+
 hipError_t launch_window(const Launch& L, uint32_t lds_bytes, hipStream_t stream) {
   if (L.B == 0) return hipSuccess;
-  hipLaunchKernelGGL(gts_sim_window, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  const uint32_t nb = (L.max_nsm + 63) / 64;
+  if (nb <= 1)
+    hipLaunchKernelGGL(gts_sim_window1, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  else if (nb == 2)
+    hipLaunchKernelGGL(gts_sim_window2, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  else if (nb == 3)
+    hipLaunchKernelGGL(gts_sim_window3, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  else
+    hipLaunchKernelGGL(gts_sim_window4, dim3(L.B), dim3(64), lds_bytes, stream, L);
   return hipGetLastError();
 }
 
