@@ -131,7 +131,7 @@ struct Launch {
 // even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: ready
 // entries per lane.
 struct WinLds {
-  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, rp_cnt, rp, ret_cnt, ret_min, ret_l, w_key, w_aux, w_fin;
+  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, rp_cnt, rp, ret_cnt, ret_min, ret_l, w_key, w_aux, w_fin, stage;
   uint32_t total;
 };
 __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t QP) {
@@ -157,6 +157,7 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB
   L.w_key = take(2u * kWinCap, true);
   L.w_aux = take(kWinCap, false);
   L.w_fin = take(kWinCap, false);
+  L.stage = take(kWinCap, false);
   L.total = o;
   return L;
 }

@@ -200,7 +200,7 @@ struct WSim {
   uint32_t *ret_cnt, *ret_min;
   uint64_t* ret_l;
   uint64_t* w_key;
-  uint32_t *w_aux, *w_fin;
+  uint32_t *w_aux, *w_fin, *stage;
   // scratch
   uint64_t* state;
   CtaState* cst;
@@ -246,7 +246,14 @@ struct WSim {
   }
   __device__ __forceinline__ void pool_scan(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
     const uint32_t nl = n < QP ? n : QP;
-    for (uint32_t i = 0; i < nl; ++i) consider(rp[i * 64u + lane], i, best, bi);
+    for (uint32_t i0 = 0; i0 < nl; i0 += 4) {  // four LDS reads in flight
+      uint64_t kk[4];
+#pragma unroll
+      for (uint32_t q = 0; q < 4; ++q) kk[q] = rp[(i0 + q < QP ? i0 + q : QP - 1) * 64u + lane];
+#pragma unroll
+      for (uint32_t q = 0; q < 4; ++q)
+        if (i0 + q < nl) consider(kk[q], i0 + q, best, bi);
+    }
     for (uint32_t i0 = QP; i0 < n; i0 += 8) {
       uint64_t kk[8];
 #pragma unroll
@@ -260,9 +267,13 @@ struct WSim {
   __device__ __forceinline__ uint64_t pool_min(uint32_t n) const {
     uint64_t m = kNoKey;
     const uint32_t nl = n < QP ? n : QP;
-    for (uint32_t i = 0; i < nl; ++i) {
-      const uint64_t k = rp[i * 64u + lane] >> 32;
-      m = k < m ? k : m;
+    for (uint32_t i0 = 0; i0 < nl; i0 += 4) {
+      uint64_t kk[4];
+#pragma unroll
+      for (uint32_t q = 0; q < 4; ++q) kk[q] = rp[(i0 + q < QP ? i0 + q : QP - 1) * 64u + lane] >> 32;
+#pragma unroll
+      for (uint32_t q = 0; q < 4; ++q)
+        if (i0 + q < nl) m = kk[q] < m ? kk[q] : m;
     }
     for (uint32_t i0 = QP; i0 < n; i0 += 8) {
       uint64_t kk[8];
@@ -468,9 +479,11 @@ struct WSim {
     }
   }
 
-  // ---- local phase: the smallest ready node below H of each of this lane's
-  // SMs, one record load and one batch of state loads for all of them.
-  __device__ __forceinline__ bool local_batch(uint64_t H) {
+  // ---- local phase step: each lane takes the smallest ready entry below H of
+  // each of its SMs (at most one node per SM per step, so the nodes of one
+  // step touch disjoint servers, CTAs and node states); the taken nodes are
+  // packed into w_key / w_aux and issued W per lane.
+  __device__ __forceinline__ bool local_step(uint64_t H) {
     uint32_t n = rp_n(lane);
     uint64_t best[NB];
     uint32_t bi[NB];
@@ -480,14 +493,23 @@ struct WSim {
       bi[j] = 0;
     }
     if (!bad) pool_scan(n, best, bi);
-    bool ok[NB];
-    uint32_t taken = 0;
+    uint32_t taken = 0, cnt = 0;
 #pragma unroll
     for (uint32_t j = 0; j < NB; ++j) {
-      ok[j] = best[j] != kNoKey && (best[j] >> 32) < H;
-      taken |= ok[j] ? 1u << j : 0u;
+      const bool ok = best[j] != kNoKey && (best[j] >> 32) < H;
+      taken |= ok ? 1u << j : 0u;
+      cnt += ok;
     }
-    if (!__ballot(taken != 0)) return false;
+    uint32_t p = wave_excl_scan_u32(cnt, lane);
+    const uint32_t E = uni(__shfl(p + cnt, 63, 64));
+    if (E == 0) return false;
+#pragma unroll
+    for (uint32_t j = 0; j < NB; ++j)
+      if ((taken >> j) & 1u) {
+        w_key[p] = best[j];
+        w_aux[p] = lane + 64u * j;
+        ++p;
+      }
     // remove the taken entries, highest index first
 #pragma unroll
     for (uint32_t rep = 0; rep < NB; ++rep) {
@@ -505,20 +527,39 @@ struct WSim {
       }
     }
     rp_cnt[lane] = n;
-    uint32_t ev_t[NB], ev_v[NB], ev_s[NB];
-    Rec rec[NB];
+    wsync();
+    if (E <= 64) {
+      issue_events<1>(0, E);
+    } else {
+      issue_events<2>(0, E < 128u ? E : 128u);
+      if (E > 128) issue_events<2>(128, E);
+    }
+    return true;
+  }
+
+  // Issue the packed nodes [i0, E) of w_key (cycle << 32 | slot << 30 |
+  // node) / w_aux (SM), node i on lane (i - i0) mod 64: one record load and
+  // one batch of state loads for all of them.
+  template <uint32_t W>
+  __device__ __forceinline__ void issue_events(uint32_t i0, uint32_t E) {
+    uint32_t ev_t[W], ev_v[W], ev_s[W];
+    bool ok[W];
+    Rec rec[W];
 #pragma unroll
-    for (uint32_t j = 0; j < NB; ++j) {
-      ev_t[j] = (uint32_t)(best[j] >> 32);
-      ev_v[j] = (uint32_t)best[j] & GTS_EDGE_TARGET_MASK;
-      ev_s[j] = lane + 64u * j;
-      rec[j] = load_rec(G.nodes, ok[j] ? ev_v[j] : 0u);
+    for (uint32_t w = 0; w < W; ++w) {
+      const uint32_t i = i0 + w * 64u + lane;
+      ok[w] = i < E;
+      const uint64_t key = ok[w] ? w_key[i] : 0ull;
+      ev_t[w] = (uint32_t)(key >> 32);
+      ev_v[w] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
+      ev_s[w] = ok[w] ? w_aux[i] : 0u;
+      rec[w] = load_rec(G.nodes, ev_v[w]);
     }
     // timing on the SM's servers
-    uint64_t rel_i[NB], rel_f[NB];
-    bool is_mem[NB];
+    uint64_t rel_i[W], rel_f[W];
+    bool is_mem[W];
 #pragma unroll
-    for (uint32_t j = 0; j < NB; ++j) {
+    for (uint32_t j = 0; j < W; ++j) {
       is_mem[j] = false;
       rel_i[j] = rel_f[j] = 0;
       if (ok[j]) {
@@ -561,11 +602,11 @@ struct WSim {
       }
     }
     // successor states (inline, unshared) and CTA state, loads in flight together
-    uint64_t sv[NB][kInlineSucc];
-    uint4 cs[NB];
-    bool sel[NB][kInlineSucc];
+    uint64_t sv[W][kInlineSucc];
+    uint4 cs[W];
+    bool sel[W][kInlineSucc];
 #pragma unroll
-    for (uint32_t j = 0; j < NB; ++j) {
+    for (uint32_t j = 0; j < W; ++j) {
       const uint32_t nout = ok[j] ? rec[j].nsucc() : 0u;
 #pragma unroll
       for (uint32_t k = 0; k < kInlineSucc; ++k) {
@@ -582,7 +623,7 @@ struct WSim {
       if (ok[j] && !is_mem[j]) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
     }
 #pragma unroll
-    for (uint32_t j = 0; j < NB; ++j) {
+    for (uint32_t j = 0; j < W; ++j) {
 #pragma unroll
       for (uint32_t k = 0; k < kInlineSucc; ++k) {
         if (sel[j][k]) {
@@ -605,7 +646,6 @@ struct WSim {
         ++st_local;
       }
     }
-    return true;
   }
 
   // ---- memory phase, E arrivals per lane: sort w_key[0, M) by (cycle, id),
@@ -628,7 +668,7 @@ struct WSim {
     for (uint32_t r = 0; r < E; ++r) {
       od[r] = make_uint4(0, 0, 0, 0);
       if (k[r] != kNoKey) {
-        od[r] = optab[w_aux[p[r]]];
+        od[r] = optab[w_aux[p[r]] & 0xFFFFu];
         const Compose g{(int64_t)(k[r] >> 32), (int64_t)od[r].y};
         if ((od[r].w >> 3) & 1u)
           fdr = compose(fdr, g);
@@ -678,9 +718,10 @@ struct WSim {
     complete_arrivals();
   }
 
-  // Completion by the owner lane, one arrival of each of its SMs per round
-  // (arrivals of different SMs touch different CTAs and nodes; shared nodes
-  // use atomics).
+  // Completion of the window's arrivals in rounds: round r takes the r-th
+  // arrival of every SM (arrivals of different SMs touch different CTAs and
+  // nodes; shared nodes use atomics), packs their slots into stage[] and
+  // completes them W per lane.
   __device__ __forceinline__ void complete_arrivals() {
     uint32_t rounds = 0;
 #pragma unroll
@@ -688,65 +729,92 @@ struct WSim {
       const uint32_t s = lane + 64u * j;
       if (j < nslot && s < nsm) rounds = (dsc[s] >> 16) > rounds ? (dsc[s] >> 16) : rounds;
     }
+    rounds = uni(wave_max_u64(rounds));
     for (uint32_t r = 0; r < rounds; ++r) {
-      Rec rec[NB];
-      uint32_t vv[NB], ss[NB], ff[NB], tt[NB];
-      bool ok[NB];
+      uint32_t cnt = 0;
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;
-        const uint32_t d = j < nslot && s < nsm ? dsc[s] : 0u;
-        ok[j] = r < (d >> 16);
-        ss[j] = s;
-        const uint32_t slot = (d & 0xFFFFu) + r;
-        const uint64_t key = ok[j] ? w_key[slot] : 0ull;
-        vv[j] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
-        tt[j] = (uint32_t)(key >> 32);
-        ff[j] = ok[j] ? w_fin[slot] : 0u;
-        rec[j] = load_rec(G.nodes, vv[j]);
+        if (j < nslot && s < nsm) cnt += r < (dsc[s] >> 16);
       }
-      uint64_t sv[NB][kInlineSucc];
-      bool sel[NB][kInlineSucc];
-      uint4 cs[NB];
+      uint32_t p = wave_excl_scan_u32(cnt, lane);
+      const uint32_t E = uni(__shfl(p + cnt, 63, 64));
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
-        const uint32_t nout = ok[j] ? rec[j].nsucc() : 0u;
-#pragma unroll
-        for (uint32_t k = 0; k < kInlineSucc; ++k) {
-          sel[j][k] = false;
-          sv[j][k] = 0;
-          if (k < nout) {
-            const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
-            const bool at_issue = (bits & kDevOrder) && !ofin;
-            sel[j][k] = !(bits & kDevShared) && !at_issue;
-            if (sel[j][k]) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
-          }
-        }
-        cs[j] = make_uint4(0, 0, 0, 0);
-        if (ok[j]) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
+        const uint32_t s = lane + 64u * j;
+        if (j < nslot && s < nsm && r < (dsc[s] >> 16)) stage[p++] = (dsc[s] & 0xFFFFu) + r;
       }
+      wsync();
+      if (E <= 64) {
+        complete_events<1>(0, E);
+      } else {
+        complete_events<2>(0, E < 128u ? E : 128u);
+        if (E > 128) complete_events<2>(128, E);
+      }
+      wsync();
+    }
+  }
+
+  // Complete the packed arrivals stage[i0, E) (slots of w_key / w_aux /
+  // w_fin), arrival i on lane (i - i0) mod 64.
+  template <uint32_t W>
+  __device__ __forceinline__ void complete_events(uint32_t i0, uint32_t E) {
+    Rec rec[W];
+    uint32_t vv[W], ss[W], ff[W], tt[W];
+    bool ok[W];
 #pragma unroll
-      for (uint32_t j = 0; j < NB; ++j) {
-        const uint32_t f = ff[j];
+    for (uint32_t j = 0; j < W; ++j) {
+      const uint32_t i = i0 + j * 64u + lane;
+      ok[j] = i < E;
+      const uint32_t slot = ok[j] ? stage[i] : 0u;
+      const uint64_t key = ok[j] ? w_key[slot] : 0ull;
+      vv[j] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
+      tt[j] = (uint32_t)(key >> 32);
+      ff[j] = ok[j] ? w_fin[slot] : 0u;
+      ss[j] = ok[j] ? w_aux[slot] >> 16 : 0u;
+      rec[j] = load_rec(G.nodes, vv[j]);
+    }
+    uint64_t sv[W][kInlineSucc];
+    bool sel[W][kInlineSucc];
+    uint4 cs[W];
 #pragma unroll
-        for (uint32_t k = 0; k < kInlineSucc; ++k) {
-          if (sel[j][k]) {
-            const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
-            const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
-            uint32_t acc = (uint32_t)sv[j][k];
-            acc = f > acc ? f : acc;
-            state[w] = ((uint64_t)cnt << 32) | acc;
-            if (cnt == rec[j].sindeg(k)) rq_push(ss[j], acc, w);
-          }
+    for (uint32_t j = 0; j < W; ++j) {
+      const uint32_t nout = ok[j] ? rec[j].nsucc() : 0u;
+#pragma unroll
+      for (uint32_t k = 0; k < kInlineSucc; ++k) {
+        sel[j][k] = false;
+        sv[j][k] = 0;
+        if (k < nout) {
+          const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
+          const bool at_issue = (bits & kDevOrder) && !ofin;
+          sel[j][k] = !(bits & kDevShared) && !at_issue;
+          if (sel[j][k]) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
         }
-        if (ok[j]) {
-          record(vv[j], tt[j], f);
-          const uint32_t left = cs[j].z - 1u;
-          const uint32_t mf = f > cs[j].w ? f : cs[j].w;
-          *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(left, mf);
-          if (left == 0) ret_push(mf, ss[j]);  // the CTA retires at its largest finish
-          if (needs_slow(rec[j])) release_slow(rec[j], 1u, 0, f, ss[j]);
+      }
+      cs[j] = make_uint4(0, 0, 0, 0);
+      if (ok[j]) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < W; ++j) {
+      const uint32_t f = ff[j];
+#pragma unroll
+      for (uint32_t k = 0; k < kInlineSucc; ++k) {
+        if (sel[j][k]) {
+          const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
+          const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
+          uint32_t acc = (uint32_t)sv[j][k];
+          acc = f > acc ? f : acc;
+          state[w] = ((uint64_t)cnt << 32) | acc;
+          if (cnt == rec[j].sindeg(k)) rq_push(ss[j], acc, w);
         }
+      }
+      if (ok[j]) {
+        record(vv[j], tt[j], f);
+        const uint32_t left = cs[j].z - 1u;
+        const uint32_t mf = f > cs[j].w ? f : cs[j].w;
+        *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(left, mf);
+        if (left == 0) ret_push(mf, ss[j]);  // the CTA retires at its largest finish
+        if (needs_slow(rec[j])) release_slow(rec[j], 1u, 0, f, ss[j]);
       }
     }
   }
@@ -812,6 +880,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.w_key = reinterpret_cast<uint64_t*>(lds + W.w_key);
   S.w_aux = lds + W.w_aux;
   S.w_fin = lds + W.w_fin;
+  S.stage = lds + W.stage;
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
 
   bool infeasible = false;
@@ -976,7 +1045,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     // Local phase.
     for (;;) {
       ++S.st_iters;
-      if (!S.local_batch(H0)) break;
+      if (!S.local_step(H0)) break;
     }
     wsync();
     const uint64_t c3 = __builtin_amdgcn_s_memtime();
@@ -1041,7 +1110,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
             for (uint32_t q = 0; q < GQ; ++q) {
               if (ehi[j][q] < H) {
                 S.w_key[p + d] = ((uint64_t)ehi[j][q] << 32) | elo[j][q];
-                S.w_aux[p + d] = eop[j][q];
+                S.w_aux[p + d] = eop[j][q] | (s << 16);
                 ++d;
               }
             }
