@@ -46,7 +46,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mem-budget-gb", type=float, default=96.0, help="device scratch budget per launch")
+    ap.add_argument("--mem-budget-gb", type=float, default=160.0, help="device scratch budget per launch")
     ap.add_argument("--graphs", type=str, default="", help="comma-separated sweep graph indices (default: step order)")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
                     help="only run a plain device-to-device copy of this many GiB (HBM counter calibration)")
@@ -100,7 +100,11 @@ def main() -> int:
         dg = api.upload(g)
         hs = api.upload_hw(hw)
         per_sim = api.scratch_bytes(dg, 1, flags) - api.scratch_bytes(dg, 0, flags)
-        chunk = max(1, min(B_PER_GRAPH, budget // max(per_sim, 1)))
+        # launches of equal size (a short tail launch would cost a whole
+        # simulation's latency for a few waves)
+        most = max(1, min(B_PER_GRAPH, budget // max(per_sim, 1)))
+        n_launch = -(-B_PER_GRAPH // most)
+        chunk = -(-B_PER_GRAPH // n_launch)
         max_scratch = max(max_scratch, api.scratch_bytes(dg, chunk, flags))
         outs = api.alloc_outputs(dg, B_PER_GRAPH, flags, dev)
         prepared[gi] = (dg, hs, chunk, outs, g.n_nodes, alg_bytes_per_sim(g))

@@ -87,7 +87,7 @@ struct SimLayout {
   uint64_t off_cta;     // CtaState per CTA
   uint64_t off_pend;    // pending events: u64 key + u32 aux per entry
   uint64_t off_optab;   // per-op duration table when it does not fit LDS
-  uint64_t off_rp;      // windowed kernel: ready pools beyond LDS, [kPoolSpill][64] u64
+  uint64_t off_rp;      // windowed kernel: later ready entries beyond LDS, [kPoolSpill][64] u64
   uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
   uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
   uint64_t pend_cap;
@@ -100,12 +100,14 @@ struct CtaState {
 
 // Windowed kernel limits.
 constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs per lane)
-constexpr uint32_t kPoolSpill = 240;   // ready entries per lane beyond the LDS pool
+constexpr uint32_t kNear = 8;          // ready entries per lane due in the current window (LDS)
+constexpr uint32_t kPoolSpill = 240;   // later ready entries per lane beyond the LDS part
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
 constexpr uint32_t kRetireLds = 256;   // pending CTA retirements held in LDS ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
 constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
+static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
 
@@ -124,14 +126,15 @@ struct Launch {
   uint32_t retry_only;         // general kernel: run only simulations marked kStatusRetry
   uint32_t max_nsm;            // largest n_sm of the batch
   uint32_t max_nsub;           // largest n_subpart of the batch
-  uint32_t qp;                 // windowed kernel: ready-pool entries per lane held in LDS
+  uint32_t qp;                 // windowed kernel: later ready entries per lane held in LDS
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
-// even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: ready
-// entries per lane.
+// even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: later
+// ready entries per lane held in LDS.
 struct WinLds {
-  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, rp_cnt, rp, ret_cnt, ret_min, ret_l, w_key, w_aux, w_fin, stage;
+  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
+  uint32_t w_key, w_aux, w_fin, stage;
   uint32_t total;
 };
 __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t QP) {
@@ -148,16 +151,22 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB
   L.resident = take(NS, false);
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
-  L.dsc = take(NS, false);
-  L.rp_cnt = take(64, false);
-  L.rp = take(2u * 64u * QP, true);
+  L.nr_cnt = take(64, false);
+  L.fr_cnt = take(64, false);
+  L.fr_min = take(64, false);
+  L.fr_hot = take(64, false);
+  L.nr = take(2u * 64u * kNear, true);
+  // the memory phase's split (per SM) and packed slots share the near lists,
+  // which are empty from the end of a local phase to the next window start
+  L.dsc = L.nr;
+  L.stage = L.nr + kWinMaxSm;
+  L.fr = take(2u * 64u * QP, true);
   L.ret_cnt = take(1, false);
   L.ret_min = take(1, false);
   L.ret_l = take(2u * kRetireLds, true);
   L.w_key = take(2u * kWinCap, true);
   L.w_aux = take(kWinCap, false);
   L.w_fin = take(kWinCap, false);
-  L.stage = take(kWinCap, false);
   L.total = o;
   return L;
 }

@@ -191,12 +191,12 @@ template <uint32_t NB>
 struct WSim {
   Image G;
   const uint32_t* hw;
-  uint32_t b, lane, flags, nsm, nsub, sstride, nslot, QP;
+  uint32_t b, lane, flags, nsm, nsub, sstride, nslot, QF;
   bool nocont, ofin;
   // LDS
   uint4* optab;
-  uint32_t *srv, *resident, *mq_head, *mq_pos, *dsc, *rp_cnt;
-  uint64_t* rp;
+  uint32_t *srv, *resident, *mq_head, *mq_pos, *dsc, *nr_cnt, *fr_cnt, *fr_min, *fr_hot;
+  uint64_t *nr, *fr;
   uint32_t *ret_cnt, *ret_min;
   uint64_t* ret_l;
   uint64_t* w_key;
@@ -204,13 +204,13 @@ struct WSim {
   // scratch
   uint64_t* state;
   CtaState* cst;
-  uint64_t* rp_g;
+  uint64_t* fr_g;
   uint32_t* mq_g;
   uint64_t* ret_g;
   uint32_t* out_cycles;
   // uniform control
   uint32_t next_cta, retired, cur_k, k_begin, k_end, kstart_k, kstart_t, kstart_valid;
-  uint64_t slots, l2_av, dram_av, Lm;
+  uint64_t slots, l2_av, dram_av, Lm, Hnear;
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
@@ -218,23 +218,52 @@ struct WSim {
   uint32_t st_maxrq, st_maxmq, st_maxret;
   uint64_t tm0, tm1, tm2, tm3, tm4;
 
-  // ---- ready pool of lane l: entries (cycle << 32 | SM slot << 30 | node),
-  // SM slot = SM / 64; [0, QP) in LDS, [QP, QP + kPoolSpill) in scratch.
-  __device__ __forceinline__ uint64_t rp_get(uint32_t l, uint32_t i) const {
-    return i < QP ? rp[i * 64u + l] : rp_g[(i - QP) * 64u + l];
+  // ---- ready nodes of lane l's SMs, entries (cycle << 32 | SM slot << 30 |
+  // node) with SM slot = SM / 64, in two lists: "near" holds only entries
+  // below the current window end (kNear per lane, LDS), "far" the rest ([0,
+  // QF) in LDS, [QF, QF + kPoolSpill) in scratch) with a lower bound of its
+  // cycles in fr_min.  At each window start the far entries below the window
+  // end move to near; fr_hot marks a far list that still holds such entries
+  // (near was full), which the local phase then scans as well.
+  __device__ __forceinline__ uint64_t fr_get(uint32_t l, uint32_t i) const {
+    return i < QF ? fr[i * 64u + l] : fr_g[(i - QF) * 64u + l];
   }
-  __device__ __forceinline__ void rp_set(uint32_t l, uint32_t i, uint64_t k) {
-    if (i < QP)
-      rp[i * 64u + l] = k;
+  __device__ __forceinline__ void fr_set(uint32_t l, uint32_t i, uint64_t k) {
+    if (i < QF)
+      fr[i * 64u + l] = k;
     else
-      rp_g[(i - QP) * 64u + l] = k;
+      fr_g[(i - QF) * 64u + l] = k;
   }
-  __device__ __forceinline__ uint32_t rp_n(uint32_t l) const {
-    const uint32_t n = rp_cnt[l];
-    return n < QP + kPoolSpill ? n : QP + kPoolSpill;
+  __device__ __forceinline__ uint32_t fr_n(uint32_t l) const {
+    const uint32_t n = fr_cnt[l];
+    return n < QF + kPoolSpill ? n : QF + kPoolSpill;
   }
-  // Smallest pool entry of each SM slot (with its index): the LDS part, then
-  // the spill eight entries per round trip.
+  __device__ __forceinline__ void far_push(uint32_t l, uint64_t key) {
+    const uint32_t slot = atomicAdd(&fr_cnt[l], 1u);
+    st_maxrq = slot + 1 > st_maxrq ? slot + 1 : st_maxrq;
+    if (slot < QF + kPoolSpill) {
+      fr_set(l, slot, key);
+      atomicMin(&fr_min[l], (uint32_t)(key >> 32));
+    } else {
+      bad |= kBadReady;
+    }
+  }
+  __device__ __forceinline__ void rq_push(uint32_t s, uint32_t cyc, uint32_t v) {
+    const uint32_t l = s & 63u;
+    const uint64_t key = ((uint64_t)cyc << 32) | ((uint64_t)(s >> 6) << 30) | v;
+    if (cyc < Hnear) {
+      const uint32_t slot = atomicAdd(&nr_cnt[l], 1u);
+      if (slot < kNear) {
+        nr[slot * 64u + l] = key;
+        return;
+      }
+      atomicSub(&nr_cnt[l], 1u);
+      fr_hot[l] = 1u;
+    }
+    far_push(l, key);
+  }
+
+  // Smallest entry of each SM slot with its index (far indices carry bit 31).
   __device__ __forceinline__ static void consider(uint64_t k, uint32_t i, uint64_t (&best)[NB], uint32_t (&bi)[NB]) {
     const uint32_t j = (uint32_t)(k >> 30) & 3u;
 #pragma unroll
@@ -244,54 +273,48 @@ struct WSim {
         bi[jj] = i;
       }
   }
-  __device__ __forceinline__ void pool_scan(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
-    const uint32_t nl = n < QP ? n : QP;
-    for (uint32_t i0 = 0; i0 < nl; i0 += 4) {  // four LDS reads in flight
-      uint64_t kk[4];
-#pragma unroll
-      for (uint32_t q = 0; q < 4; ++q) kk[q] = rp[(i0 + q < QP ? i0 + q : QP - 1) * 64u + lane];
-#pragma unroll
-      for (uint32_t q = 0; q < 4; ++q)
-        if (i0 + q < nl) consider(kk[q], i0 + q, best, bi);
-    }
-    for (uint32_t i0 = QP; i0 < n; i0 += 8) {
+  __device__ __forceinline__ void scan_far(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
+    for (uint32_t i0 = 0; i0 < n; i0 += 8) {
       uint64_t kk[8];
 #pragma unroll
-      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? rp_g[(i0 + q - QP) * 64u + lane] : kNoKey;
+      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? fr_get(lane, i0 + q) : kNoKey;
 #pragma unroll
       for (uint32_t q = 0; q < 8; ++q)
-        if (i0 + q < n) consider(kk[q], i0 + q, best, bi);
+        if (i0 + q < n) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
     }
   }
-  // Smallest cycle in the lane's pool (kNoKey if empty).
-  __device__ __forceinline__ uint64_t pool_min(uint32_t n) const {
-    uint64_t m = kNoKey;
-    const uint32_t nl = n < QP ? n : QP;
-    for (uint32_t i0 = 0; i0 < nl; i0 += 4) {
-      uint64_t kk[4];
+
+  // Window start: move this lane's far entries below H to near.
+  __device__ __forceinline__ void pool_rebuild(uint64_t H) {
+    uint32_t hot = 0;
+    if (fr_min[lane] < H) {
+      const uint32_t n = fr_n(lane);
+      uint32_t nn = nr_cnt[lane], kp = 0, mn = 0xFFFFFFFFu;
+      for (uint32_t i0 = 0; i0 < n; i0 += 8) {  // in place: writes stay below the reads
+        uint64_t kk[8];
 #pragma unroll
-      for (uint32_t q = 0; q < 4; ++q) kk[q] = rp[(i0 + q < QP ? i0 + q : QP - 1) * 64u + lane] >> 32;
+        for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? fr_get(lane, i0 + q) : kNoKey;
 #pragma unroll
-      for (uint32_t q = 0; q < 4; ++q)
-        if (i0 + q < nl) m = kk[q] < m ? kk[q] : m;
+        for (uint32_t q = 0; q < 8; ++q) {
+          if (i0 + q < n) {
+            const uint32_t cyc = (uint32_t)(kk[q] >> 32);
+            if (cyc < H && nn < kNear) {
+              nr[nn * 64u + lane] = kk[q];
+              ++nn;
+            } else {
+              hot |= cyc < H;
+              fr_set(lane, kp, kk[q]);
+              ++kp;
+              mn = cyc < mn ? cyc : mn;
+            }
+          }
+        }
+      }
+      fr_cnt[lane] = kp;
+      fr_min[lane] = mn;
+      nr_cnt[lane] = nn;
     }
-    for (uint32_t i0 = QP; i0 < n; i0 += 8) {
-      uint64_t kk[8];
-#pragma unroll
-      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? rp_g[(i0 + q - QP) * 64u + lane] >> 32 : kNoKey;
-#pragma unroll
-      for (uint32_t q = 0; q < 8; ++q) m = kk[q] < m ? kk[q] : m;
-    }
-    return m;
-  }
-  __device__ __forceinline__ void rq_push(uint32_t s, uint32_t cyc, uint32_t v) {
-    const uint32_t l = s & 63u;
-    const uint32_t slot = atomicAdd(&rp_cnt[l], 1u);
-    st_maxrq = slot + 1 > st_maxrq ? slot + 1 : st_maxrq;
-    if (slot < QP + kPoolSpill)
-      rp_set(l, slot, ((uint64_t)cyc << 32) | ((uint64_t)(s >> 6) << 30) | v);
-    else
-      bad |= kBadReady;
+    fr_hot[lane] = hot;
   }
 
   // ---- per-SM memory-arrival FIFO (strictly increasing cycles): a ring of
@@ -484,7 +507,10 @@ struct WSim {
   // step touch disjoint servers, CTAs and node states); the taken nodes are
   // packed into w_key / w_aux and issued W per lane.
   __device__ __forceinline__ bool local_step(uint64_t H) {
-    uint32_t n = rp_n(lane);
+    uint32_t nn = nr_cnt[lane];
+    nn = nn < kNear ? nn : kNear;
+    const bool hot = fr_hot[lane] != 0;
+    uint32_t fn = hot ? fr_n(lane) : 0u;
     uint64_t best[NB];
     uint32_t bi[NB];
 #pragma unroll
@@ -492,7 +518,17 @@ struct WSim {
       best[j] = kNoKey;
       bi[j] = 0;
     }
-    if (!bad) pool_scan(n, best, bi);
+    if (!bad) {
+      for (uint32_t i0 = 0; i0 < nn; i0 += 4) {  // four LDS reads in flight
+        uint64_t kk[4];
+#pragma unroll
+        for (uint32_t q = 0; q < 4; ++q) kk[q] = nr[(i0 + q < kNear ? i0 + q : kNear - 1) * 64u + lane];
+#pragma unroll
+        for (uint32_t q = 0; q < 4; ++q)
+          if (i0 + q < nn) consider(kk[q], i0 + q, best, bi);
+      }
+      if (hot) scan_far(fn, best, bi);
+    }
     uint32_t taken = 0, cnt = 0;
 #pragma unroll
     for (uint32_t j = 0; j < NB; ++j) {
@@ -510,7 +546,7 @@ struct WSim {
         w_aux[p] = lane + 64u * j;
         ++p;
       }
-    // remove the taken entries, highest index first
+    // remove the taken entries, highest index first (far ones first)
 #pragma unroll
     for (uint32_t rep = 0; rep < NB; ++rep) {
       uint32_t sel = NB, mx = 0;
@@ -522,11 +558,18 @@ struct WSim {
         }
       if (sel != NB) {
         taken &= ~(1u << sel);
-        if (mx != n - 1) rp_set(lane, mx, rp_get(lane, n - 1));
-        --n;
+        if (mx & 0x80000000u) {
+          const uint32_t i = mx & 0x7FFFFFFFu;
+          if (i != fn - 1) fr_set(lane, i, fr_get(lane, fn - 1));
+          --fn;
+        } else {
+          if (mx != nn - 1) nr[mx * 64u + lane] = nr[(nn - 1) * 64u + lane];
+          --nn;
+        }
       }
     }
-    rp_cnt[lane] = n;
+    nr_cnt[lane] = nn;
+    if (hot) fr_cnt[lane] = fn;
     wsync();
     if (E <= 64) {
       issue_events<1>(0, E);
@@ -857,12 +900,12 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.nsub = S.hw[HW_NSUB];
   S.sstride = S.nsub + 2;
   S.nslot = (S.nsm + 63) / 64;
-  S.QP = L.qp;
+  S.QF = L.qp;
   const uint32_t lane = S.lane;
   uint8_t* sim = L.sims + (uint64_t)b * L.layout.stride;
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
-  S.rp_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_rp);
+  S.fr_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_rp);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
   S.ret_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_ret);
   const WinLds W = win_lds(S.G.n_ops, L.max_nsm, L.max_nsub, L.qp);
@@ -872,8 +915,12 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.mq_head = lds + W.mq_head;
   S.mq_pos = lds + W.mq_pos;
   S.dsc = lds + W.dsc;
-  S.rp_cnt = lds + W.rp_cnt;
-  S.rp = reinterpret_cast<uint64_t*>(lds + W.rp);
+  S.nr_cnt = lds + W.nr_cnt;
+  S.fr_cnt = lds + W.fr_cnt;
+  S.fr_min = lds + W.fr_min;
+  S.fr_hot = lds + W.fr_hot;
+  S.nr = reinterpret_cast<uint64_t*>(lds + W.nr);
+  S.fr = reinterpret_cast<uint64_t*>(lds + W.fr);
   S.ret_cnt = lds + W.ret_cnt;
   S.ret_min = lds + W.ret_min;
   S.ret_l = reinterpret_cast<uint64_t*>(lds + W.ret_l);
@@ -913,9 +960,12 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     S.resident[i] = 0;
     S.mq_head[i] = 0xFFFFFFFFu;
     S.mq_pos[i] = 0;
-    S.dsc[i] = 0;
   }
-  S.rp_cnt[lane] = 0;
+  S.nr_cnt[lane] = 0;
+  S.fr_cnt[lane] = 0;
+  S.fr_min[lane] = 0xFFFFFFFFu;
+  S.fr_hot[lane] = 0;
+  S.Hnear = 0;
   if (lane == 0) {
     *S.ret_cnt = 0;
     *S.ret_min = 0xFFFFFFFFu;
@@ -954,7 +1004,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     // T: lower bound of the earliest pending event
     uint64_t tmin = kNoKey;
     {
-      tmin = S.pool_min(S.rp_n(lane));
+      const uint32_t fm = S.fr_min[lane];  // near is empty between windows
+      tmin = fm == 0xFFFFFFFFu ? kNoKey : fm;  // 0xFFFFFFFF: empty (cycles stop at kMaxCycle)
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;
@@ -1043,10 +1094,14 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     const uint64_t c2 = __builtin_amdgcn_s_memtime();
 
     // Local phase.
+    S.pool_rebuild(H0);
+    wsync();
+    S.Hnear = H0;
     for (;;) {
       ++S.st_iters;
       if (!S.local_step(H0)) break;
     }
+    S.Hnear = 0;
     wsync();
     const uint64_t c3 = __builtin_amdgcn_s_memtime();
     if (__ballot(S.bad != 0)) break;
