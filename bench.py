@@ -19,8 +19,10 @@ oracle timed on a bounded sample of the same workload on this host.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -37,6 +39,34 @@ def alg_bytes_per_sim(g) -> int:
     """Bytes one simulation must read from the graph (16-byte node record per
     node, 4 bytes per edge) plus its 16 bytes of per-simulation output."""
     return 16 * g.n_nodes + 4 * g.n_edges + 16
+
+
+PROFILE = os.path.join(ROOT, "profiles", "gts_sim_window_gemm_design_sweep.md")
+KERNEL_SOURCES = ("gts_window.hip", "gts_common.h", "gts_dev.h")
+
+
+def recorded_traffic(n_launch: int):
+    """HBM bytes per launch of the simulation kernel, from the committed
+    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE summed over the
+    timed launches, scaled by the same counters on a plain copy), or None
+    when that summary was taken on other kernel sources or other launches."""
+    try:
+        text = open(PROFILE).read()
+    except OSError:
+        return None
+    m = re.search(r"traffic-record: sha256=(\w+) launches=(\d+) fetch_kib=(\d+) write_kib=(\d+) "
+                  r"fetch_factor=([\d.]+) write_factor=([\d.]+)", text)
+    if not m:
+        return None
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_11262_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    if m.group(1) != h.hexdigest() or int(m.group(2)) != n_launch:
+        return None
+    fetch = int(m.group(3)) * 1024 * float(m.group(5))
+    write = int(m.group(4)) * 1024 * float(m.group(6))
+    return (fetch + write) / n_launch
 
 
 def main() -> int:
@@ -148,6 +178,7 @@ def main() -> int:
     abytes = np.array([x for _, _, x, _ in launches], dtype=np.float64)
     # dominant kernel: the simulation kernel (the only kernel in the step)
     achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
+    traffic = recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
     cpu = None
@@ -201,7 +232,8 @@ def main() -> int:
         "node_sims": node_sims,
         "infeasible_sims": int((statuses == 1).sum()),
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_over_algorithmic": (traffic / float(abytes.mean())) if traffic else None,
                      "kernel": "gts_sim_window", "launches": len(launches),
                      "mean_launch_ms": float(durs.mean() * 1e3)},
         "cpu_baseline": cpu,
