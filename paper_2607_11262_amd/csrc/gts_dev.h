@@ -18,6 +18,8 @@ constexpr uint32_t kGraphCrossFromMemory = 2u;  // every cross-CTA edge has a
                                                 // GLOAD/GSTORE source, DATA/SYNC kind
 constexpr uint32_t kGraphSmallOutdeg = 4u;      // every out-degree is below 0xFFFF
 constexpr uint32_t kGraphHasShared = 8u;        // some CTA receives cross-CTA edges
+constexpr uint32_t kGraphComputeFeedsData = 16u;  // every non-memory node has a DATA or
+                                                  // SYNC out-edge inside its CTA
 
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
@@ -41,12 +43,13 @@ struct NodeDev {                // 32 B, one per node and a sentinel after the l
   uint16_t pad;
 };
 
-constexpr uint32_t kInlineRoots = 4;
+constexpr uint32_t kInlineRoots = 3;
 struct CtaDev {                 // 32 B, one per CTA
   uint32_t node_begin, node_count;
   uint32_t root_begin, root_count;  // nodes without intra-CTA in-edges; bit 31 of
                                     // root_count: the CTA receives cross-CTA edges
-  uint32_t root[kInlineRoots];      // copies of the first four roots
+  uint32_t mem_count;               // GLOAD / GSTORE nodes
+  uint32_t root[kInlineRoots];      // copies of the first three roots
 };
 constexpr uint32_t kCtaShared = 0x80000000u;
 

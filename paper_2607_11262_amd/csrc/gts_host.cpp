@@ -161,7 +161,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   d->root_begin.assign(C, 0);
   d->root_count.assign(C, 0);
   d->roots.clear();
-  bool sinks_memory = true;
+  bool sinks_memory = true, compute_feeds_data = true;
   for (uint32_t c = 0; c < C; ++c) {
     d->root_begin[c] = (uint32_t)d->roots.size();
     for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1]; ++v) {
@@ -170,6 +170,11 @@ int check_graph(const gts_graph_host* h, Derived* d) {
       for (uint32_t e = h->succ_ptr[v]; e < h->succ_ptr[v + 1] && !has_intra_succ; ++e)
         has_intra_succ = node_cta[h->succ[e] & GTS_EDGE_TARGET_MASK] == c;
       if (!has_intra_succ && !is_memory(h->op_cls[h->node_op[v]])) sinks_memory = false;
+      bool feeds = is_memory(h->op_cls[h->node_op[v]]);
+      for (uint32_t e = h->succ_ptr[v]; e < h->succ_ptr[v + 1] && !feeds; ++e)
+        feeds = node_cta[h->succ[e] & GTS_EDGE_TARGET_MASK] == c &&
+                (h->succ[e] >> GTS_EDGE_KIND_SHIFT) != GTS_EDGE_ORDER;
+      if (!feeds) compute_feeds_data = false;
     }
     d->root_count[c] = (uint32_t)d->roots.size() - d->root_begin[c];
   }
@@ -184,7 +189,8 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   bool any_shared = false;
   for (uint32_t v = 0; v < N && !any_shared; ++v) any_shared = d->shared[v] != 0;
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
-             (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u);
+             (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
+             (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   return GTS_OK;
@@ -456,6 +462,9 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     bool shared = false;
     for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1] && !shared; ++v) shared = d.shared[v] != 0;
     ctas[c].root_count = d.root_count[c] | (shared ? gts::kCtaShared : 0u);
+    uint32_t mem = 0;
+    for (uint32_t v = h->cta_node_begin[c]; v < h->cta_node_begin[c + 1]; ++v) mem += is_memory(h->op_cls[h->node_op[v]]);
+    ctas[c].mem_count = mem;
     for (uint32_t r = 0; r < gts::kInlineRoots; ++r)
       ctas[c].root[r] = r < d.root_count[c] ? d.roots[d.root_begin[c] + r] : 0u;
   }

@@ -193,6 +193,7 @@ struct WSim {
   const uint32_t* hw;
   uint32_t b, lane, flags, nsm, nsub, sstride, nslot, QF;
   bool nocont, ofin;
+  bool mem_only;  // CTA bookkeeping on memory nodes only (compute nodes always feed a later memory node)
   // LDS
   uint4* optab;
   uint32_t *srv, *resident, *mq_head, *mq_pos, *dsc, *nr_cnt, *fr_cnt, *fr_min, *fr_hot;
@@ -411,12 +412,12 @@ struct WSim {
       if (bits & kDevShared) {
         release_shared(w, r, rec.cta(), s);
       } else {
-        const uint64_t sv = state[w];
         const uint32_t ind = G.indeg[w];
+        const uint64_t sv = ind != 1 ? state[w] : 0ull;
         const uint32_t cnt = (uint32_t)(sv >> 32) + 1u;
         uint32_t acc = (uint32_t)sv;
         acc = r > acc ? (uint32_t)r : acc;
-        state[w] = ((uint64_t)cnt << 32) | acc;
+        if (ind != 1) state[w] = ((uint64_t)cnt << 32) | acc;
         if (cnt == ind) rq_push(s, acc, w);
       }
     }
@@ -472,8 +473,8 @@ struct WSim {
       if (lane < k) {
         const uint4* p = reinterpret_cast<const uint4*>(G.ctas + c);
         c0 = p[0];  // node_begin, node_count, root_begin, root_count
-        c1 = p[1];  // first four roots
-        *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, c0.y, 0u);
+        c1 = p[1];  // memory nodes, first three roots
+        *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
       }
       // zero the node state of unshared CTAs (shared ones were zeroed at start)
       for (uint32_t j = 0; j < k; ++j) {
@@ -485,7 +486,7 @@ struct WSim {
         const bool shared = (c0.w & kCtaShared) != 0;
         const uint32_t nroots = c0.w & ~kCtaShared;
         for (uint32_t r = 0; r < nroots; ++r) {
-          const uint32_t v = r == 0 ? c1.x : r == 1 ? c1.y : r == 2 ? c1.z : r == 3 ? c1.w : G.roots[c0.z + r];
+          const uint32_t v = r == 0 ? c1.y : r == 1 ? c1.z : r == 2 ? c1.w : G.roots[c0.z + r];
           if (!shared) {  // no in-edges at all
             rq_push(mysm, (uint32_t)launch, v);
           } else {
@@ -659,11 +660,12 @@ struct WSim {
           const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
           const bool at_issue = (bits & kDevOrder) && !ofin;
           sel[j][k] = !(bits & kDevShared) && (at_issue || !is_mem[j]);
-          if (sel[j][k]) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
+          // a node with one in-edge needs no state: this release readies it
+          if (sel[j][k] && rec[j].sindeg(k) != 1) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
         }
       }
       cs[j] = make_uint4(0, 0, 0, 0);
-      if (ok[j] && !is_mem[j]) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
+      if (ok[j] && !is_mem[j] && !mem_only) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
     }
 #pragma unroll
     for (uint32_t j = 0; j < W; ++j) {
@@ -676,12 +678,12 @@ struct WSim {
           const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
           uint32_t acc = (uint32_t)sv[j][k];
           acc = r > acc ? (uint32_t)r : acc;
-          state[w] = ((uint64_t)cnt << 32) | acc;
+          if (rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
           if (cnt == rec[j].sindeg(k)) rq_push(ev_s[j], acc, w);
         }
       }
       if (ok[j]) {
-        if (!is_mem[j]) {  // a compute node never completes its CTA
+        if (!is_mem[j] && !mem_only) {  // a compute node never completes its CTA
           const uint32_t mf = (uint32_t)rel_f[j] > cs[j].w ? (uint32_t)rel_f[j] : cs[j].w;
           *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(cs[j].z - 1u, mf);
         }
@@ -831,7 +833,7 @@ struct WSim {
           const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
           const bool at_issue = (bits & kDevOrder) && !ofin;
           sel[j][k] = !(bits & kDevShared) && !at_issue;
-          if (sel[j][k]) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
+          if (sel[j][k] && rec[j].sindeg(k) != 1) sv[j][k] = state[rec[j].succ(k) & GTS_EDGE_TARGET_MASK];
         }
       }
       cs[j] = make_uint4(0, 0, 0, 0);
@@ -847,7 +849,7 @@ struct WSim {
           const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
           uint32_t acc = (uint32_t)sv[j][k];
           acc = f > acc ? f : acc;
-          state[w] = ((uint64_t)cnt << 32) | acc;
+          if (rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
           if (cnt == rec[j].sindeg(k)) rq_push(ss[j], acc, w);
         }
       }
@@ -896,6 +898,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.flags = L.flags;
   S.nocont = (L.flags & GTS_NO_CONTENTION) != 0;
   S.ofin = (L.flags & GTS_ORDER_AT_FINISH) != 0;
+  S.mem_only = (L.img.props & kGraphComputeFeedsData) != 0;
   S.nsm = S.hw[HW_NSM];
   S.nsub = S.hw[HW_NSUB];
   S.sstride = S.nsub + 2;
