@@ -103,12 +103,12 @@ struct CtaState {
 
 // Windowed kernel limits.
 constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs per lane)
-constexpr uint32_t kNear = 8;          // ready entries per lane due in the current window (LDS)
+constexpr uint32_t kNear = 4;          // ready entries per lane due in the current window (LDS)
 constexpr uint32_t kPoolSpill = 240;   // later ready entries per lane beyond the LDS part
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
-constexpr uint32_t kRetireLds = 256;   // pending CTA retirements held in LDS ...
+constexpr uint32_t kRetireLds = 128;   // pending CTA retirements held in LDS ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
-constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
+constexpr uint32_t kWinCap = 128;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
@@ -136,7 +136,7 @@ struct Launch {
 // even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: later
 // ready entries per lane held in LDS.
 struct WinLds {
-  uint32_t optab, srv, resident, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
+  uint32_t optab, srv, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
   uint32_t w_key, w_aux, w_fin, stage;
   uint32_t total;
 };
@@ -151,7 +151,6 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB
   };
   L.optab = take(4u * P, true);
   L.srv = take(NS * (NSUB + 2u), false);
-  L.resident = take(NS, false);
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
   L.nr_cnt = take(64, false);

@@ -318,11 +318,13 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // A large batch wants eight simulations per CU (the register limit); a
     // small one fewer, so it takes the largest qp that still gives each
     // simulation a wave slot (fewer entries spill to scratch).
-    constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 8, kCus = 256, kMaxQp = 160;
+    constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kCus = 256, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qp).total; };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
-    const uint32_t want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (B + kCus - 1) / kCus));
-    constexpr uint32_t kMinQp = 4;
+    uint32_t want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (B + kCus - 1) / kCus));
+    if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU
+      want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (uint32_t)std::strtoul(w, nullptr, 10)));
+    constexpr uint32_t kMinQp = 2;
     uint32_t qp = kMinQp;
     for (uint32_t q = kMinQp + 1; q <= kMaxQp; ++q)
       if (bytes(q) <= kLdsBudget && per_cu(q) >= std::min(want, per_cu(kMinQp))) qp = q;

@@ -16,7 +16,7 @@
 //       out-edges (all inside the same CTA); memory nodes reserve the SM's
 //       engine and queue an arrival at their engine start;
 //   memory phase: the arrivals with cycle < H from all SMs are sorted by
-//       (cycle, node id) in registers (bitonic network across the wave),
+//       (cycle, node id) (each counts the smaller keys, read by LDS broadcast),
 //       served by the chip-wide L2 and DRAM FIFO servers through a max-plus
 //       prefix scan, and completed by the lane that owns their SM (CTA
 //       bookkeeping, release of out-edges).
@@ -56,7 +56,7 @@ namespace gts {
 namespace {
 
 constexpr uint64_t kNoKey = ~0ull;
-constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u, kBadWindow = 16u;
+constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u;
 constexpr uint32_t GQ = 3;               // ring entries loaded per SM and window
 
 // Node state: latest release cycle (low word) | released in-edges (high word).
@@ -75,74 +75,94 @@ __device__ __forceinline__ void wsync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return uni(x);
+// Cross-lane steps by DPP (VALU lane shifts inside rows of 16 and row
+// broadcasts) rather than LDS-crossbar shuffles: row_shr:n gives lane l the
+// value of lane l - n of its row (lanes without one keep `old`); row_bcast:15
+// / :31 give rows 1, 3 / rows 2, 3 lane 15 / lane 31 (other rows keep `old`).
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+template <int ctrl, int row_mask = 0xF>
+__device__ __forceinline__ uint32_t dpp(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, ctrl, row_mask, 0xF, false);
+}
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
 }
 
-__device__ __forceinline__ uint32_t wave_excl_scan_u32(uint32_t x, uint32_t lane) {
-  uint32_t inc = x;
-#pragma unroll
-  for (uint32_t d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(inc, d, 64);
-    if (lane >= d) inc += y;
-  }
-  return inc - x;
+__device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t x) {
+  x += dpp<kRowShr1>(0u, x);
+  x += dpp<kRowShr2>(0u, x);
+  x += dpp<kRowShr4>(0u, x);
+  x += dpp<kRowShr8>(0u, x);
+  x += dpp<kRowBcast15, 0xA>(0u, x);
+  x += dpp<kRowBcast31, 0xC>(0u, x);
+  return x;
 }
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) { return lane_u32(wave_incl_sum_u32(x), 63); }
+__device__ __forceinline__ uint32_t wave_excl_scan_u32(uint32_t x) { return wave_incl_sum_u32(x) - x; }
+
+// Wave-wide min / max of a u64 (uniform result): row reductions by DPP, then
+// the four row results.
+template <bool kMax>
+__device__ __forceinline__ uint64_t wave_ext_u64(uint64_t x) {
+  uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
+  const uint32_t id = kMax ? 0u : ~0u;
+#define GTS_EXT_STEP(C)                                              \
+  {                                                                  \
+    const uint32_t plo = dpp<C>(id, lo), phi = dpp<C>(id, hi);       \
+    const bool less = phi < hi || (phi == hi && plo < lo);           \
+    if (kMax ? (!less && (phi != hi || plo != lo)) : less) {         \
+      lo = plo;                                                      \
+      hi = phi;                                                      \
+    }                                                                \
+  }
+  GTS_EXT_STEP(kRowShr1)
+  GTS_EXT_STEP(kRowShr2)
+  GTS_EXT_STEP(kRowShr4)
+  GTS_EXT_STEP(kRowShr8)
+#undef GTS_EXT_STEP
+  uint64_t r = kMax ? 0ull : ~0ull;
+#pragma unroll
+  for (int l = 15; l < 64; l += 16) {
+    const uint64_t v = ((uint64_t)lane_u32(hi, l) << 32) | lane_u32(lo, l);
+    r = kMax ? (v > r ? v : r) : (v < r ? v : r);
+  }
+  return r;
+}
+__device__ __forceinline__ uint64_t wmin64(uint64_t x) { return wave_ext_u64<false>(x); }
+__device__ __forceinline__ uint64_t wmax64(uint64_t x) { return wave_ext_u64<true>(x); }
 
 struct Compose {  // f(x) = max(x, a) + o on int64
   int64_t a, o;
 };
+constexpr int64_t kNegCycle = -(int64_t(1) << 62);  // below every cycle: max(x, kNegCycle) = x
 __device__ __forceinline__ Compose compose(Compose f, Compose g) {  // g after f
   const int64_t ga = g.a - f.o;
   return Compose{f.a > ga ? f.a : ga, f.o + g.o};
 }
-__device__ __forceinline__ Compose shfl_up_c(Compose c, uint32_t d) {
-  return Compose{__shfl_up(c.a, d, 64), __shfl_up(c.o, d, 64)};
+template <int ctrl, int row_mask = 0xF>
+__device__ __forceinline__ Compose dpp_c(Compose c) {  // lanes without a source get the identity
+  const uint64_t a = (uint64_t)c.a, o = (uint64_t)c.o, na = (uint64_t)kNegCycle;
+  const uint32_t alo = dpp<ctrl, row_mask>((uint32_t)na, (uint32_t)a);
+  const uint32_t ahi = dpp<ctrl, row_mask>((uint32_t)(na >> 32), (uint32_t)(a >> 32));
+  const uint32_t olo = dpp<ctrl, row_mask>(0u, (uint32_t)o);
+  const uint32_t ohi = dpp<ctrl, row_mask>(0u, (uint32_t)(o >> 32));
+  return Compose{(int64_t)(((uint64_t)ahi << 32) | alo), (int64_t)(((uint64_t)ohi << 32) | olo)};
 }
-
-// Bitonic sort, ascending, of 64*E keys with payloads held E per lane (element
-// lane*E + r in k[r]).  Equal keys are allowed (each keeps its payload).
-template <uint32_t E>
-__device__ __forceinline__ void bitonic(uint64_t (&k)[E], uint32_t (&p)[E], uint32_t lane) {
-#pragma unroll
-  for (uint32_t size = 2; size <= 64 * E; size <<= 1) {
-#pragma unroll
-    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-      if (stride < E) {
-#pragma unroll
-        for (uint32_t r = 0; r < E; ++r) {
-          if ((r & stride) == 0) {
-            const uint32_t q = r | stride;
-            const bool asc = ((lane * E + r) & size) == 0;
-            if (asc ? k[r] > k[q] : k[r] < k[q]) {
-              const uint64_t tk = k[r];
-              k[r] = k[q];
-              k[q] = tk;
-              const uint32_t tp = p[r];
-              p[r] = p[q];
-              p[q] = tp;
-            }
-          }
-        }
-      } else {
-        const uint32_t d = stride / E;
-        const bool lower = (lane & d) == 0;
-#pragma unroll
-        for (uint32_t r = 0; r < E; ++r) {
-          const uint64_t ok = __shfl_xor(k[r], d, 64);
-          const uint32_t op = __shfl_xor(p[r], d, 64);
-          const bool asc = ((lane * E + r) & size) == 0;
-          const bool take = (lower == asc) ? ok < k[r] : ok > k[r];
-          if (take) {
-            k[r] = ok;
-            p[r] = op;
-          }
-        }
-      }
-    }
-  }
+// Inclusive scan of compositions across the wave (lane 0 first).
+__device__ __forceinline__ Compose wave_incl_compose(Compose c) {
+  c = compose(dpp_c<kRowShr1>(c), c);
+  c = compose(dpp_c<kRowShr2>(c), c);
+  c = compose(dpp_c<kRowShr4>(c), c);
+  c = compose(dpp_c<kRowShr8>(c), c);
+  c = compose(dpp_c<kRowBcast15, 0xA>(c), c);
+  c = compose(dpp_c<kRowBcast31, 0xC>(c), c);
+  return c;
+}
+__device__ __forceinline__ Compose lane_c(Compose c, int l) {
+  const uint64_t a = (uint64_t)c.a, o = (uint64_t)c.o;
+  return Compose{(int64_t)(((uint64_t)lane_u32((uint32_t)(a >> 32), l) << 32) | lane_u32((uint32_t)a, l)),
+                 (int64_t)(((uint64_t)lane_u32((uint32_t)(o >> 32), l) << 32) | lane_u32((uint32_t)o, l))};
 }
 
 // A node record held in registers: a = {op | out-degree << 16, cta,
@@ -174,14 +194,15 @@ __device__ __forceinline__ bool needs_slow(const Rec r) {
   return sh;
 }
 
-// Loaded ring entries with cycle below X.
+// Loaded ring entries whose key (cycle << 32 | kind << 30 | node) is below K.
 template <uint32_t NB>
-__device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], uint64_t X) {
+__device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], const uint32_t (&elo)[NB][GQ],
+                                              uint64_t K) {
   uint32_t c = 0;
 #pragma unroll
   for (uint32_t j = 0; j < NB; ++j)
 #pragma unroll
-    for (uint32_t q = 0; q < GQ; ++q) c += ehi[j][q] < X;
+    for (uint32_t q = 0; q < GQ; ++q) c += (((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K;
   return c;
 }
 
@@ -196,7 +217,9 @@ struct WSim {
   bool mem_only;  // CTA bookkeeping on memory nodes only (compute nodes always feed a later memory node)
   // LDS
   uint4* optab;
-  uint32_t *srv, *resident, *mq_head, *mq_pos, *dsc, *nr_cnt, *fr_cnt, *fr_min, *fr_hot;
+  // mq_pos[s]: SM s's ring head (bits 0-7) and entry count (bits 8-15), and
+  // its resident CTAs (bits 16-31)
+  uint32_t *srv, *mq_head, *mq_pos, *dsc, *nr_cnt, *fr_cnt, *fr_min, *fr_hot;
   uint64_t *nr, *fr;
   uint32_t *ret_cnt, *ret_min;
   uint64_t* ret_l;
@@ -324,7 +347,7 @@ struct WSim {
   // lane only.
   __device__ __forceinline__ void mq_push(uint32_t s, uint64_t key, uint32_t op) {
     const uint32_t pos = mq_pos[s];
-    const uint32_t h = pos & 0xFFu, c = pos >> 8;
+    const uint32_t h = pos & 0xFFu, c = (pos >> 8) & 0xFFu;
     if (c >= kRing) {
       bad |= kBadMemQ;
       return;
@@ -334,7 +357,7 @@ struct WSim {
     e[1] = (uint32_t)(key >> 32);
     e[2] = op;
     if (c == 0) mq_head[s] = (uint32_t)(key >> 32);
-    mq_pos[s] = h | ((c + 1) << 8);
+    mq_pos[s] = (pos & 0xFFFF0000u) | h | ((c + 1) << 8);
     st_maxmq = c + 1 > st_maxmq ? c + 1 : st_maxmq;
   }
 
@@ -445,15 +468,15 @@ struct WSim {
       while (k < lim) {
         uint64_t best = 0;
         for (uint32_t m = lane; m < nsm; m += 64) {
-          const uint64_t fr = slots - resident[m];
+          const uint64_t fr = slots - (mq_pos[m] >> 16);
           const uint64_t key = (fr << 32) | (0xFFFFFFFFu - m);
           best = key > best ? key : best;
         }
-        best = uni64(wave_max_u64(best));
+        best = wmax64(best);
         if ((best >> 32) == 0) break;  // every SM is full
         const uint32_t sm = 0xFFFFFFFFu - (uint32_t)best;
         if (lane == k) mysm = sm;
-        if (lane == (sm & 63u)) resident[sm] += 1;
+        if (lane == (sm & 63u)) mq_pos[sm] += 1u << 16;
         wsync();
         ++k;
       }
@@ -537,15 +560,23 @@ struct WSim {
       taken |= ok ? 1u << j : 0u;
       cnt += ok;
     }
-    uint32_t p = wave_excl_scan_u32(cnt, lane);
-    const uint32_t E = uni(__shfl(p + cnt, 63, 64));
-    if (E == 0) return false;
+    const uint32_t incl = wave_incl_sum_u32(cnt);
+    const uint32_t total = lane_u32(incl, 63);
+    if (total == 0) return false;
+    // at most kWinCap nodes per step (SMs do not interact inside a window, so
+    // the others simply wait for the next step)
+    const uint32_t E = total < kWinCap ? total : kWinCap;
+    uint32_t p = incl - cnt;
 #pragma unroll
     for (uint32_t j = 0; j < NB; ++j)
       if ((taken >> j) & 1u) {
-        w_key[p] = best[j];
-        w_aux[p] = lane + 64u * j;
-        ++p;
+        if (p < kWinCap) {
+          w_key[p] = best[j];
+          w_aux[p] = lane + 64u * j;
+          ++p;
+        } else {
+          taken &= ~(1u << j);
+        }
       }
     // remove the taken entries, highest index first (far ones first)
 #pragma unroll
@@ -693,21 +724,53 @@ struct WSim {
     }
   }
 
+  // ---- rank sort of w_key[0, M) (M <= 64 E): stage[rank] = slot, where a
+  // key's rank counts the smaller keys (and, with ties, the equal keys in
+  // lower slots).  Every lane reads each key by an LDS broadcast.
+  template <uint32_t E>
+  __device__ __forceinline__ void rank_sort(uint32_t M, bool ties) {
+    uint64_t k[E];
+    uint32_t rk[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      const uint32_t i = r * 64u + lane;
+      k[r] = i < M ? w_key[i] : kNoKey;
+      rk[r] = 0;
+    }
+    for (uint32_t i0 = 0; i0 < M; i0 += 16) {
+      uint64_t kk[16];
+#pragma unroll
+      for (uint32_t q = 0; q < 16; ++q) kk[q] = w_key[i0 + q < M ? i0 + q : M - 1];
+#pragma unroll
+      for (uint32_t q = 0; q < 16; ++q)
+#pragma unroll
+        for (uint32_t r = 0; r < E; ++r) {
+          const uint32_t i = r * 64u + lane;
+          const bool before = kk[q] < k[r] || (ties && kk[q] == k[r] && i0 + q < i);
+          rk[r] += (i0 + q < M && before) ? 1u : 0u;
+        }
+    }
+    wsync();
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r)
+      if (r * 64u + lane < M) stage[rk[r]] = r * 64u + lane;
+    wsync();
+  }
+
   // ---- memory phase, E arrivals per lane: sort w_key[0, M) by (cycle, id),
   // serve them in that order, then complete them on their SMs' lanes.
   template <uint32_t E>
   __device__ __forceinline__ void memory_phase(uint32_t M) {
-    constexpr int64_t kNeg = -(int64_t(1) << 62);
+    rank_sort<E>(M, false);  // arrival keys are distinct
     uint64_t k[E];
     uint32_t p[E];
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
-      const uint32_t i = lane * E + r;
-      k[r] = i < M ? w_key[i] : kNoKey;
-      p[r] = i;
+      const uint32_t pos = lane * E + r;
+      p[r] = pos < M ? stage[pos] : 0u;
+      k[r] = pos < M ? w_key[p[r]] : kNoKey;
     }
-    bitonic<E>(k, p, lane);
-    Compose fl2{kNeg, 0}, fdr{kNeg, 0};
+    Compose fl2{kNegCycle, 0}, fdr{kNegCycle, 0};
     uint4 od[E];
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
@@ -721,19 +784,11 @@ struct WSim {
           fl2 = compose(fl2, g);
       }
     }
-    Compose il2 = fl2, idr = fdr;
-#pragma unroll
-    for (uint32_t d = 1; d < 64; d <<= 1) {
-      const Compose pl2 = shfl_up_c(il2, d), pdr = shfl_up_c(idr, d);
-      if (lane >= d) {
-        il2 = compose(pl2, il2);
-        idr = compose(pdr, idr);
-      }
-    }
-    Compose el2 = shfl_up_c(il2, 1), edr = shfl_up_c(idr, 1);
-    if (lane == 0) el2 = edr = Compose{kNeg, 0};
-    const Compose tl2{__shfl(il2.a, 63, 64), __shfl(il2.o, 63, 64)};
-    const Compose tdr{__shfl(idr.a, 63, 64), __shfl(idr.o, 63, 64)};
+    const Compose il2 = wave_incl_compose(fl2), idr = wave_incl_compose(fdr);
+    Compose el2 = Compose{__shfl_up(il2.a, 1, 64), __shfl_up(il2.o, 1, 64)};
+    Compose edr = Compose{__shfl_up(idr.a, 1, 64), __shfl_up(idr.o, 1, 64)};
+    if (lane == 0) el2 = edr = Compose{kNegCycle, 0};
+    const Compose tl2 = lane_c(il2, 63), tdr = lane_c(idr, 63);
     int64_t xl2 = ((int64_t)l2_av > el2.a ? (int64_t)l2_av : el2.a) + el2.o;
     int64_t xdr = ((int64_t)dram_av > edr.a ? (int64_t)dram_av : edr.a) + edr.o;
     if (!nocont) {
@@ -774,7 +829,7 @@ struct WSim {
       const uint32_t s = lane + 64u * j;
       if (j < nslot && s < nsm) rounds = (dsc[s] >> 16) > rounds ? (dsc[s] >> 16) : rounds;
     }
-    rounds = uni(wave_max_u64(rounds));
+    rounds = (uint32_t)wmax64(rounds);
     for (uint32_t r = 0; r < rounds; ++r) {
       uint32_t cnt = 0;
 #pragma unroll
@@ -782,8 +837,9 @@ struct WSim {
         const uint32_t s = lane + 64u * j;
         if (j < nslot && s < nsm) cnt += r < (dsc[s] >> 16);
       }
-      uint32_t p = wave_excl_scan_u32(cnt, lane);
-      const uint32_t E = uni(__shfl(p + cnt, 63, 64));
+      const uint32_t incl = wave_incl_sum_u32(cnt);
+      const uint32_t E = lane_u32(incl, 63);
+      uint32_t p = incl - cnt;
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;
@@ -864,24 +920,6 @@ struct WSim {
     }
   }
 
-  // ---- sort the R retirements in w_key[0, R) by cycle, in place.
-  template <uint32_t E>
-  __device__ __forceinline__ void sort_keys(uint32_t R) {
-    uint64_t k[E];
-    uint32_t p[E];
-#pragma unroll
-    for (uint32_t r = 0; r < E; ++r) {
-      const uint32_t i = lane * E + r;
-      k[r] = i < R ? w_key[i] : kNoKey;
-      p[r] = 0;
-    }
-    bitonic<E>(k, p, lane);
-    wsync();
-#pragma unroll
-    for (uint32_t r = 0; r < E; ++r)
-      if (lane * E + r < R) w_key[lane * E + r] = k[r];
-    wsync();
-  }
 };
 
 
@@ -914,7 +952,6 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   const WinLds W = win_lds(S.G.n_ops, L.max_nsm, L.max_nsub, L.qp);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.srv = lds + W.srv;
-  S.resident = lds + W.resident;
   S.mq_head = lds + W.mq_head;
   S.mq_pos = lds + W.mq_pos;
   S.dsc = lds + W.dsc;
@@ -956,11 +993,10 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       lm = d < lm ? d : lm;
     }
   }
-  lm = uni64(wave_min_u64(lm));
+  lm = wmin64(lm);
   S.Lm = lm < kWindowMax ? lm : kWindowMax;
   for (uint32_t i = lane; i < S.nsm * S.sstride; i += 64) S.srv[i] = 0;
   for (uint32_t i = lane; i < S.nsm; i += 64) {
-    S.resident[i] = 0;
     S.mq_head[i] = 0xFFFFFFFFu;
     S.mq_pos[i] = 0;
   }
@@ -1012,7 +1048,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;
-        if (j < S.nslot && s < S.nsm && (S.mq_pos[s] >> 8)) {
+        if (j < S.nslot && s < S.nsm && ((S.mq_pos[s] >> 8) & 0xFFu)) {
           const uint64_t k = S.mq_head[s];
           tmin = k < tmin ? k : tmin;
         }
@@ -1020,7 +1056,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     }
     const uint32_t rmin = uni(*S.ret_min);
     if (uni(*S.ret_cnt)) tmin = rmin < tmin ? rmin : tmin;
-    const uint64_t T = uni64(wave_min_u64(tmin));
+    const uint64_t T = wmin64(tmin);
     if (T == kNoKey) break;
     uint64_t H0 = T + S.Lm;
     H0 = H0 < 0xFFFFFFFFull ? H0 : 0xFFFFFFFFull;  // cycles never exceed kMaxCycle
@@ -1042,9 +1078,9 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         }
         H0 = lo;
         D = wave_sum_u32(S.count_ret(H0, n));
-        if (D > kWinCap) S.bad |= kBadWindow;
       }
-      if (__ballot(S.bad != 0)) break;
+      // more than kWinCap at cycle T alone: released together without a sort
+      const bool single = D > kWinCap;
       // compact in place, 64 entries at a time: due ones to w_key, the rest
       // to the front of the list
       uint32_t dp = 0, kp = 0, kmin = 0xFFFFFFFFu;
@@ -1054,7 +1090,12 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         const bool due = i < n && (k >> 32) < H0;
         const bool keep = i < n && !due;
         const uint64_t bd = __ballot(due), bk = __ballot(keep);
-        if (due) S.w_key[dp + lanes_below(bd, lane)] = k;
+        if (due) {
+          if (single)
+            atomicSub(&S.mq_pos[(uint32_t)k], 1u << 16);
+          else
+            S.w_key[dp + lanes_below(bd, lane)] = k;
+        }
         if (keep) {
           S.ret_set(kp + lanes_below(bk, lane), k);
           kmin = (uint32_t)(k >> 32) < kmin ? (uint32_t)(k >> 32) : kmin;
@@ -1062,27 +1103,35 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         dp += (uint32_t)__popcll(bd);
         kp += (uint32_t)__popcll(bk);
       }
-      kmin = (uint32_t)uni64(wave_min_u64(kmin));
+      kmin = (uint32_t)wmin64(kmin);
       wsync();
       if (lane == 0) {
         *S.ret_cnt = kp;
         *S.ret_min = kmin;
       }
       wsync();
-      const uint32_t R = dp;
+      const uint32_t R = single ? 0u : dp;
+      if (single) {
+        wsync();
+        S.retired += dp;
+        S.st_retires += dp;
+        S.dispatch((uint32_t)T);
+        wsync();
+        if (__ballot(S.bad != 0)) break;
+      }
       if (R) {
         if (R <= 64)
-          S.template sort_keys<1>(R);
+          S.template rank_sort<1>(R, true);
         else if (R <= 128)
-          S.template sort_keys<2>(R);
+          S.template rank_sort<2>(R, true);
         else
-          S.template sort_keys<4>(R);
+          S.template rank_sort<4>(R, true);
         bool stop = false;
-        for (uint32_t i = 0; i < R && !stop;) {
-          const uint64_t r = uni64(S.w_key[i] >> 32);
+        for (uint32_t i = 0; i < R && !stop;) {  // retirement i in cycle order is w_key[stage[i]]
+          const uint64_t r = uni64(S.w_key[S.stage[i]] >> 32);
           uint32_t j = i;
-          while (j < R && uni64(S.w_key[j] >> 32) == r) ++j;
-          for (uint32_t x = i + lane; x < j; x += 64) atomicSub(&S.resident[(uint32_t)S.w_key[x]], 1u);
+          while (j < R && uni64(S.w_key[S.stage[j]] >> 32) == r) ++j;
+          for (uint32_t x = i + lane; x < j; x += 64) atomicSub(&S.mq_pos[(uint32_t)S.w_key[S.stage[x]]], 1u << 16);
           wsync();
           S.retired += j - i;
           S.st_retires += j - i;
@@ -1109,27 +1158,29 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     const uint64_t c3 = __builtin_amdgcn_s_memtime();
     if (__ballot(S.bad != 0)) break;
 
-    // Memory phase: the arrivals below H (H <= H0).  Up to GQ head entries
-    // of each SM whose head may be below H0 are loaded; H is lowered so that
-    // every due arrival is among them, and so that at most kWinCap are due.
-    uint64_t H = H0;
+    // Memory phase: the arrivals whose key (cycle, id) is below K <= H0 << 32.
+    // Up to GQ head entries of each SM whose head may be below H0 are loaded;
+    // K is lowered so that every due arrival is among them, and so that at
+    // most kWinCap are due -- the rest, possibly of the same cycle, wait for
+    // the next window (they complete after it starts, and no arrival of a
+    // cycle below H0 can still appear).
     uint32_t M = 0;
     {
       uint32_t elo[NB][GQ], ehi[NB][GQ], eop[NB][GQ], cnt[NB], hd[NB];
       bool ld[NB];
-      uint64_t Hl = H0;
+      uint64_t Kl = H0 << 32;
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j) {
         const uint32_t s = lane + 64u * j;
         const bool valid = j < S.nslot && s < S.nsm;
         const uint32_t pos = valid ? S.mq_pos[s] : 0u;
         hd[j] = pos & 0xFFu;
-        cnt[j] = pos >> 8;
-        ld[j] = cnt[j] > 0 && S.mq_head[s] < H0;
+        cnt[j] = (pos >> 8) & 0xFFu;
+        ld[j] = valid && cnt[j] > 0 && S.mq_head[s] < H0;
 #pragma unroll
         for (uint32_t q = 0; q < GQ; ++q) {
-          elo[j][q] = eop[j][q] = 0;
-          ehi[j][q] = 0xFFFFFFFFu;
+          eop[j][q] = 0;
+          elo[j][q] = ehi[j][q] = 0xFFFFFFFFu;
           if (ld[j] && q < cnt[j]) {
             const uint32_t* e = S.mq_g + ((uint64_t)s * kRing + (hd[j] + q) % kRing) * 3u;
             elo[j][q] = e[0];
@@ -1138,27 +1189,26 @@ __device__ __forceinline__ void window_body(const Launch& L) {
           }
         }
         if (ld[j] && cnt[j] > GQ) {
-          const uint64_t x = (uint64_t)ehi[j][GQ - 1] + 1;
-          Hl = x < Hl ? x : Hl;
+          const uint64_t x = (((uint64_t)ehi[j][GQ - 1] << 32) | elo[j][GQ - 1]) + 1;
+          Kl = x < Kl ? x : Kl;
         }
       }
-      H = uni64(wave_min_u64(Hl));
-      M = wave_sum_u32(due_count(ehi, H));
-      if (M > kWinCap) {  // keep the prefix, in cycle order, that fits
-        uint64_t lo = T + 1, hi = H;
+      uint64_t K = wmin64(Kl);
+      M = wave_sum_u32(due_count(ehi, elo, K));
+      if (M > kWinCap) {  // keep the kWinCap smallest keys
+        uint64_t lo = T << 32, hi = K;  // count(< lo) = 0, count(< hi) > kWinCap
         while (hi - lo > 1) {
-          const uint64_t mid = (lo + hi) / 2;
-          if (wave_sum_u32(due_count(ehi, mid)) <= kWinCap)
+          const uint64_t mid = lo + (hi - lo) / 2;
+          if (wave_sum_u32(due_count(ehi, elo, mid)) <= kWinCap)
             lo = mid;
           else
             hi = mid;
         }
-        H = lo;
-        M = wave_sum_u32(due_count(ehi, H));
-        if (M > kWinCap) S.bad |= kBadWindow;
+        K = lo;
+        M = wave_sum_u32(due_count(ehi, elo, K));
       }
-      if (!__ballot(S.bad != 0)) {
-        uint32_t p = wave_excl_scan_u32(due_count(ehi, H), lane);
+      {
+        uint32_t p = wave_excl_scan_u32(due_count(ehi, elo, K));
 #pragma unroll
         for (uint32_t j = 0; j < NB; ++j) {
           const uint32_t s = lane + 64u * j;
@@ -1166,7 +1216,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
             uint32_t d = 0;
 #pragma unroll
             for (uint32_t q = 0; q < GQ; ++q) {
-              if (ehi[j][q] < H) {
+              if ((((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K) {
                 S.w_key[p + d] = ((uint64_t)ehi[j][q] << 32) | elo[j][q];
                 S.w_aux[p + d] = eop[j][q] | (s << 16);
                 ++d;
@@ -1176,7 +1226,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
             p += d;
             if (ld[j]) {
               const uint32_t left = cnt[j] - d;
-              S.mq_pos[s] = ((hd[j] + d) % kRing) | (left << 8);
+              S.mq_pos[s] = (S.mq_pos[s] & 0xFFFF0000u) | ((hd[j] + d) % kRing) | (left << 8);
               if (left) {
                 uint32_t nh = ehi[j][GQ - 1] + 1;  // lower bound when the next entry was not loaded
 #pragma unroll
