@@ -82,6 +82,7 @@ def main() -> int:
     ap.add_argument("--streams", type=int, default=2,
                     help="consecutive steps alternate over this many HIP streams, so one graph's launch "
                          "overlaps the tail of the previous one")
+    ap.add_argument("--launch-log", type=str, default="", help="write one JSON line per timed launch to this file")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
                     help="only run a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -149,6 +150,7 @@ def main() -> int:
     # one scratch area per stream; each graph's outputs are its own
     scratches = [torch.empty(max_scratch, dtype=torch.uint8, device=dev) for _ in streams]
     launches = []  # (start event, end event, algorithmic bytes, node-sims)
+    launch_info = []  # (graph, first record, records)
 
     def step(k, gi, record):
         stream, scratch = streams[k % len(streams)], scratches[k % len(streams)]
@@ -164,6 +166,7 @@ def main() -> int:
             if record:
                 e1.record(stream)
                 launches.append((e0, e1, abps * b, n * b))
+                launch_info.append((gi, first, b))
 
     for k, gi in enumerate(warm_graphs):
         step(k, gi, False)
@@ -181,6 +184,10 @@ def main() -> int:
     node_sims = sum(prepared[gi][4] * ok_per_graph[gi] for gi in step_graphs)
     sims = B_PER_GRAPH * len(step_graphs)
     durs = np.array([a.elapsed_time(b) * 1e-3 for a, b, _, _ in launches])
+    if args.launch_log:
+        with open(args.launch_log, "w") as f:
+            for (gi, first, b), d in zip(launch_info, durs):
+                f.write(json.dumps({"graph": gi, "first": first, "sims": b, "ms": float(d * 1e3)}) + "\n")
     abytes = np.array([x for _, _, x, _ in launches], dtype=np.float64)
     # dominant kernel: the simulation kernel (the only kernel in the step).
     # achieved: algorithmic bytes per launch / mean launch duration; with

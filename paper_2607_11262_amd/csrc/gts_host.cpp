@@ -314,14 +314,14 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
   if (windowed) {
-    // LDS per simulation: fixed tables plus qp later-ready entries per lane.
-    // A large batch wants eight simulations per CU (the register limit); a
-    // small one fewer, so it takes the largest qp that still gives each
-    // simulation a wave slot (fewer entries spill to scratch).
-    constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kCus = 256, kMaxQp = 160;
+    // LDS per simulation: fixed tables plus qp later-ready entries per lane;
+    // take the largest qp that keeps twelve simulations per CU (the register
+    // limit of the kernel).  Measured: fewer, larger simulations per CU are
+    // slower even for batches that fill only part of the chip.
+    constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qp).total; };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
-    uint32_t want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (B + kCus - 1) / kCus));
+    uint32_t want = kWavesPerCu;
     if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU
       want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (uint32_t)std::strtoul(w, nullptr, 10)));
     constexpr uint32_t kMinQp = 2;
