@@ -14,10 +14,13 @@
  * reading used is the one listed in DESIGN.md ("Readings").
  *
  *  R2  Resources (Sec. 5.2 compute: tensor cores, CUDA cores, SFUs; memory:
- *      TMA/LSU front end, L2, DRAM).  TENSOR/ALU/SFU nodes occupy the
- *      per-subpartition lanes of their SM named by their warps (lane of warp
- *      w = w mod n_subpart; Sec. 2.2 subpartitions, Sec. 5.3 warp-group
- *      issue across subpartitions).  SMEM nodes occupy the SM's shared-memory
+ *      TMA/LSU front end, L2, DRAM).  Each subpartition of an SM has one
+ *      pipeline per compute class (Sec. 5.2: one pipeline per execution-unit
+ *      type); a TENSOR/ALU/SFU node occupies the lanes of its own class's
+ *      pipelines named by its warps (lane of warp w = w mod n_subpart;
+ *      Sec. 2.2 subpartitions, Sec. 5.3 warp-group issue across
+ *      subpartitions), so nodes of different classes never delay each other
+ *      on a lane.  SMEM nodes occupy the SM's shared-memory
  *      pipe.  GLOAD/GSTORE nodes occupy the SM's global-memory engine, then
  *      the chip-wide L2 server (or DRAM server when the op's MISS flag is
  *      set).  SYNC nodes occupy nothing.
@@ -230,7 +233,7 @@ static void issue(sim_t *S, uint32_t v, uint64_t t) {
   uint32_t cls = S->op_cls[p];
   if (cls == K_TENSOR || cls == K_ALU || cls == K_SFU) {
     uint64_t s = t;
-    uint64_t *lanes = S->lane_av + sm * S->nsub;
+    uint64_t *lanes = S->lane_av + (sm * 3 + cls) * S->nsub;  /* class cls's lanes */
     if (!nocont)
       for (uint32_t l = 0; l < S->nsub; l++)
         if (S->lanes[p] >> l & 1) s = max64(s, lanes[l]);
@@ -350,7 +353,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
     S.cta_left[c] = cta_node_begin[c + 1] - cta_node_begin[c];
     for (uint32_t v = cta_node_begin[c]; v < cta_node_begin[c + 1]; v++) S.node_cta[v] = c;
   }
-  ALLOC(S.resident, S.nsm); ALLOC(S.lane_av, (uint64_t)S.nsm * S.nsub);
+  ALLOC(S.resident, S.nsm); ALLOC(S.lane_av, (uint64_t)S.nsm * 3 * S.nsub);
   ALLOC(S.smem_av, S.nsm); ALLOC(S.eng_av, S.nsm);
   ALLOC(S.kstart, S.K);
   for (uint32_t k = 0; k < S.K; k++) S.kstart[k] = -1;

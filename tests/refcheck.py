@@ -43,7 +43,7 @@ def cdiv(a: int, b: int) -> int:
 
 
 def durations(g, rec):
-    """Per op: dict(kind, lanes, occ, occ_m, lat, dram)."""
+    """Per op: dict(kind, cls, lanes, occ, occ_m, lat, dram)."""
     nsub = H.get(rec, "n_subpart")
     rates = [H.get(rec, f) for f in ("rate_tensor", "rate_alu", "rate_sfu", "rate_smem", "rate_gmem", "rate_l2",
                                        "rate_dram")]
@@ -55,7 +55,7 @@ def durations(g, rec):
         if cls in (TENSOR, ALU, SFU):
             lanes = sorted({w % nsub for w in range(32) if warps >> w & 1})
             occ = max(1, cdiv(work * 65536 * nsub, len(lanes) * rates[cls]))
-            out.append(dict(kind="compute", lanes=lanes, occ=occ, lat=lats[cls]))
+            out.append(dict(kind="compute", cls=cls, lanes=lanes, occ=occ, lat=lats[cls]))
         elif cls == SMEM:
             out.append(dict(kind="smem", occ=max(1, cdiv(work * 65536, rates[3])), lat=lats[3]))
         elif cls == SYNC:
@@ -114,9 +114,10 @@ def verify_schedule(g, rec, flags, cycles, cta):
         sm = int(cta_sm[node_cta[v]])
         r = int(ready[v])
         if d["kind"] == "compute":
-            s = r if nocont else max([r] + [lane_av.get((sm, l), 0) for l in d["lanes"]])
+            # one pipeline per (SM, compute class, subpartition lane)
+            s = r if nocont else max([r] + [lane_av.get((sm, d["cls"], l), 0) for l in d["lanes"]])
             for l in d["lanes"]:
-                lane_av[(sm, l)] = s + d["occ"]
+                lane_av[(sm, d["cls"], l)] = s + d["occ"]
             assert st[v] == s and fi[v] == s + d["occ"] + d["lat"], f"compute node {v}: {st[v], fi[v]} != {s}"
         elif d["kind"] == "smem":
             s = r if nocont else max(r, smem_av.get(sm, 0))

@@ -41,6 +41,8 @@ MUTANTS = [
      "uint64_t m = max64(t, *av);", False),
     ("residency_ignores_warps", "s = s < wl ? s : wl;", ";", False),
     ("residency_ignores_smem", "if (kernel_smem[k]) s =", "if (0) s =", False),
+    ("compute_classes_share_lanes", "uint64_t *lanes = S->lane_av + (sm * 3 + cls) * S->nsub;",
+     "uint64_t *lanes = S->lane_av + sm * 3 * S->nsub;", False),
     ("multi_lane_uses_first_lane", "if (S->lanes[p] >> l & 1) s = max64(s, lanes[l]);",
      "if (S->lanes[p] >> l & 1) { s = max64(s, lanes[l]); break; }", False),
     ("smem_latency_dropped", "if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)",

@@ -190,7 +190,8 @@ def test_invariants(seed):
         sm = int(a.cta[node_cta[v], 0])
         if d["kind"] == "compute":
             for lane in d["lanes"]:
-                tot[("lane", sm, lane)] = tot.get(("lane", sm, lane), 0) + d["occ"]
+                key = ("lane", sm, d["cls"], lane)
+                tot[key] = tot.get(key, 0) + d["occ"]
         elif d["kind"] == "smem":
             tot[("smem", sm)] = tot.get(("smem", sm), 0) + d["occ"]
         elif d["kind"] == "gmem":
