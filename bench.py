@@ -15,6 +15,16 @@ Prints one JSON line: simulated tile-nodes per second (value), simulations
 per second, the roofline of the simulation kernel (algorithmic bytes per
 launch / mean launch time from HIP events, against 8 TB/s HBM) and the CPU
 oracle timed on a bounded sample of the same workload on this host.
+
+    python bench.py --workload pipelining
+
+runs the software-pipelining case study instead (Sec. 7.1, Table 4): the
+fused GEMM + SiLU persistent kernel in four pipeline organisations x five
+tile shapes x four edge-class sets (80 graphs of 270-1020 nodes), each
+simulated under 4096 seeded single-SM Hopper machines (tensor rate 0.5-4x,
+DRAM 1.5-8 TB/s, TMA 50-200 B/cycle); its line adds the case-study table
+(normalised performance and Tensor Core utilisation per organisation at
+Table 3's H100 with FP8 rate), read off GPU timelines.
 """
 from __future__ import annotations
 
@@ -72,6 +82,7 @@ def recorded_traffic(n_launch: int):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining"), default="gemm_design_sweep")
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
@@ -95,6 +106,7 @@ def main() -> int:
     import torch
 
     from paper_2607_11262_amd import api
+    from paper_2607_11262_amd.gen import pipelining as PL
     from paper_2607_11262_amd.gen import workloads as W
 
     if not torch.cuda.is_available():
@@ -114,11 +126,28 @@ def main() -> int:
     dev = torch.device("cuda:0")
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(max(1, args.streams) - 1)]
 
-    params = W.sweep_params()
+    pipelining = args.workload == "pipelining"
+    if pipelining:
+        n_graphs = len(PL.case_study_graphs())
+
+        def make(gi):
+            return PL.case_study_graph(gi), PL.sample_hopper_1sm(gi, B_PER_GRAPH)
+
+        def describe(gi):
+            return PL.case_study_graphs()[gi]
+    else:
+        params = W.sweep_params()
+        n_graphs = len(params)
+
+        def make(gi):
+            return W.sweep_graph(params[gi]), W.config_hw(2, B=B_PER_GRAPH, index=gi)
+
+        def describe(gi):
+            return params[gi]
     if args.graphs:
         order = [int(x) for x in args.graphs.split(",")]
     else:
-        order = list(range(64))
+        order = list(range(n_graphs))
     step_graphs = [order[i % len(order)] for i in range(args.steps)]
     warm_graphs = [order[i % len(order)] for i in range(args.warmup)]
     needed = sorted(set(step_graphs) | set(warm_graphs))
@@ -130,8 +159,7 @@ def main() -> int:
     budget = int(args.mem_budget_gb * (1 << 30)) // max(1, args.streams)
     max_scratch = 0
     for gi in needed:
-        g = W.sweep_graph(params[gi])
-        hw = W.config_hw(2, B=B_PER_GRAPH, index=gi)
+        g, hw = make(gi)
         dg = api.upload(g)
         hs = api.upload_hw(hw)
         per_sim = api.scratch_bytes(dg, 1, flags) - api.scratch_bytes(dg, 0, flags)
@@ -144,7 +172,7 @@ def main() -> int:
         outs = api.alloc_outputs(dg, B_PER_GRAPH, flags, dev)
         prepared[gi] = (dg, hs, chunk, outs, g.n_nodes, alg_bytes_per_sim(g))
         host_graphs[gi] = (g, hw)
-        print(f"[bench] graph {gi} {params[gi]} N={g.n_nodes} E={g.n_edges} chunk={chunk}", file=sys.stderr,
+        print(f"[bench] graph {gi} {describe(gi)} N={g.n_nodes} E={g.n_edges} chunk={chunk}", file=sys.stderr,
               flush=True)
     t_gen = time.time() - t_gen
     # one scratch area per stream; each graph's outputs are its own
@@ -195,7 +223,7 @@ def main() -> int:
     # over the timed region) is higher and is reported beside it.
     achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
     aggregate_gbs = float(abytes.sum() / elapsed / 1e9)
-    traffic = recorded_traffic(len(launches))
+    traffic = None if pipelining else recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
     cpu = None
@@ -243,7 +271,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": "gemm_design_sweep", "graphs": step_graphs, "sims_per_graph": B_PER_GRAPH,
+        "config": {"workload": args.workload, "graphs": step_graphs, "sims_per_graph": B_PER_GRAPH,
                    "outputs": "makespan+status+digest", "parallelism": "one wavefront per simulation",
                    "streams": len(streams)},
         "simulations_per_s": sims / elapsed,
@@ -260,8 +288,32 @@ def main() -> int:
         "parity_sample": parity,
         "setup_s": t_gen,
     }
+    if pipelining:
+        out["case_study"] = case_study(api, torch, PL)
     print(json.dumps(out))
     return 0
+
+
+def case_study(api, torch, PL):
+    """Sec. 7.1 table from GPU timelines at Table 3's H100 (one SM, FP8
+    tensor rate): per tile, each organisation's performance relative to naive
+    2-stage and its Tensor Core utilisation (full tile graphs)."""
+    from paper_2607_11262_amd import timeline as TL
+    from paper_2607_11262_amd.gen import hw as H
+    rec = H.preset("H100", n_sm=1, tensor_permille=2000)[None, :]
+    table = {}
+    for tile in PL.TILES:
+        row = {}
+        for org in PL.ORGANIZATIONS:
+            g = PL.gemm_silu(org, *tile)
+            res = api.simulate(api.upload(g), rec, api.OUT_NODES | api.OUT_DIGEST)
+            torch.cuda.synchronize()
+            cyc, mk, st, _ = api.to_numpy(res)
+            row[org] = {"makespan": int(mk[0]), "tensor_util": round(TL.utilization(g, rec[0], cyc[0])["tensor"], 4)}
+        for org in PL.ORGANIZATIONS:
+            row[org]["perf_vs_naive"] = round(row["naive"]["makespan"] / row[org]["makespan"], 4)
+        table["x".join(map(str, tile))] = row
+    return table
 
 
 if __name__ == "__main__":

@@ -69,8 +69,9 @@ __device__ __forceinline__ uint32_t clamp_occ(uint64_t x) {
 }
 
 // Per-op duration entry: x = occupancy (engine occupancy for memory ops),
-// y = L2/DRAM occupancy, z = latency, w = class | dram << 3 | lane mask << 8.
-__device__ uint4 op_entry(const OpDev& o, const uint32_t* hw) {
+// y = L2/DRAM occupancy, z = latency, w = class | dram << 3 | lane mask << 8
+// | first server word of the class's lanes << 16 (compute ops).
+__device__ uint4 op_entry(const OpDev& o, const uint32_t* hw, uint32_t props) {
   const uint32_t nsub = hw[HW_NSUB];
   const uint64_t work = o.work;
   uint4 e = make_uint4(0, 0, 0, o.cls);
@@ -81,7 +82,7 @@ __device__ uint4 op_entry(const OpDev& o, const uint32_t* hw) {
     const uint64_t k = (uint64_t)__popc(lanes);
     e.x = clamp_occ(cdiv64(work * 65536ull * nsub, k * hw[HW_RATE + o.cls]));
     e.z = hw[HW_LAT + o.cls];
-    e.w |= lanes << 8;
+    e.w |= lanes << 8 | (compute_slot(props, o.cls) * nsub) << 16;
   } else if (o.cls == C_SMEM) {
     e.x = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + R_SMEM]));
     e.z = hw[HW_LAT + L_SMEM];

@@ -20,6 +20,18 @@ constexpr uint32_t kGraphSmallOutdeg = 4u;      // every out-degree is below 0xF
 constexpr uint32_t kGraphHasShared = 8u;        // some CTA receives cross-CTA edges
 constexpr uint32_t kGraphComputeFeedsData = 16u;  // every non-memory node has a DATA or
                                                   // SYNC out-edge inside its CTA
+constexpr uint32_t kGraphClassShift = 5u;         // bits 5-7: the op table has TENSOR /
+                                                  // ALU / SFU ops (one bit per class)
+
+// Compute pipelines: every subpartition of an SM has one lane per compute
+// class.  Server state holds lanes only for the classes a graph uses, class
+// slot-major: slot(c) = number of used classes below c.
+__host__ __device__ inline uint32_t compute_slots(uint32_t props) {
+  return (uint32_t)__builtin_popcount((props >> kGraphClassShift) & 7u);
+}
+__host__ __device__ inline uint32_t compute_slot(uint32_t props, uint32_t cls) {
+  return (uint32_t)__builtin_popcount((props >> kGraphClassShift) & ((1u << cls) - 1u));
+}
 
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
@@ -84,6 +96,12 @@ enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC 
 // state is updated with atomics by the windowed kernel.
 constexpr uint32_t kDevOrder = 1u, kDevShared = 2u;
 
+// Per-SM server words: compute lanes (slots x n_subpart), then the shared-
+// memory pipe and the global-memory engine.
+__host__ __device__ inline uint32_t server_stride(uint32_t props, uint32_t nsub) {
+  return compute_slots(props) * nsub + 2u;
+}
+
 // Per-simulation scratch regions (byte offsets within one simulation's slice).
 struct SimLayout {
   uint64_t off_state;   // u64 per node: acc (low 32) | released in-edges (high 32)
@@ -133,14 +151,15 @@ struct Launch {
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
-// even words).  NS / NSUB: largest n_sm / n_subpart of the batch; QP: later
-// ready entries per lane held in LDS.
+// even words).  NS: largest n_sm of the batch; SS: server words per SM
+// (server_stride at the largest n_subpart); QP: later ready entries per lane
+// held in LDS.
 struct WinLds {
   uint32_t optab, srv, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
   uint32_t w_key, w_aux, w_fin, stage;
   uint32_t total;
 };
-__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB, uint32_t QP) {
+__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP) {
   WinLds L;
   uint32_t o = 0;
   auto take = [&o](uint32_t words, bool wide) {
@@ -150,7 +169,7 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t NSUB
     return r;
   };
   L.optab = take(4u * P, true);
-  L.srv = take(NS * (NSUB + 2u), false);
+  L.srv = take(NS * SS, false);
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
   L.nr_cnt = take(64, false);

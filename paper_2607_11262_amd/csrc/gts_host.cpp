@@ -188,9 +188,12 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   d->node_cta.swap(node_cta);
   bool any_shared = false;
   for (uint32_t v = 0; v < N && !any_shared; ++v) any_shared = d->shared[v] != 0;
+  uint32_t classes = 0;
+  for (uint32_t p = 0; p < P; ++p)
+    if (is_compute(h->op_cls[p])) classes |= 1u << h->op_cls[p];
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
              (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
-             (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u);
+             (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift;
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   return GTS_OK;
@@ -286,7 +289,8 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
            uint32_t* out_cycles, uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, uint8_t* sims,
            uint32_t flags, hipStream_t st) {
   constexpr uint32_t kLdsBudget = 64 * 1024;
-  const uint32_t server_bytes = 4u * (max_nsm * (max_nsub + 2) + max_nsm);
+  const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
+  const uint32_t server_bytes = 4u * (max_nsm * sstride + max_nsm);
   const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
   const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
   const uint32_t lds_general = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
@@ -319,7 +323,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // limit of the kernel).  Measured: fewer, larger simulations per CU are
     // slower even for batches that fill only part of the chip.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
-    auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, max_nsub, qp).total; };
+    auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp).total; };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
     uint32_t want = kWavesPerCu;
     if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU

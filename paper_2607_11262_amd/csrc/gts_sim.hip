@@ -11,8 +11,9 @@
 //
 // Timing rules (GTSim Sec. 5.1-5.3, readings fixed where the paper is
 // silent; the CPU oracle states the same rules independently):
-//  * servers: per-subpartition lanes of each SM for tensor / CUDA-core / SFU
-//    work (lane of warp w = w mod n_subpart), one shared-memory pipe and one
+//  * servers: per subpartition of each SM one lane for each compute class
+//    (tensor / CUDA-core / SFU pipelines; lane of warp w = w mod n_subpart),
+//    one shared-memory pipe and one
 //    global-memory engine per SM, one chip-wide L2 and one DRAM server; all
 //    FIFO, non-preemptive, "available at cycle a";
 //  * durations: occ = max(1, ceil(work * 2^16 * n_subpart / (k * rate_q16)))
@@ -46,7 +47,8 @@ struct Sim {
   uint32_t b, lane, flags, nsm, nsub, sstride;
   // storage
   uint4* optab;
-  uint32_t* srv;        // [nsm][nsub + 2]: lanes, smem pipe, memory engine
+  uint32_t smem_w;      // server word of the shared-memory pipe (the engine follows)
+  uint32_t* srv;        // [nsm][sstride]: compute lanes, smem pipe, memory engine
   uint32_t* resident;   // [nsm]
   uint64_t* state;      // [N]
   CtaState* cst;        // [C]
@@ -207,6 +209,7 @@ struct Sim {
     uint32_t* S = srv + sm * sstride;
     if (cls <= C_SFU) {
       const uint32_t lanes = (od.w >> 8) & 0xFFu;
+      S += od.w >> 16;  // this class's lanes
       uint32_t a = 0;
       if (!nocont && lane < nsub && ((lanes >> lane) & 1u)) a = S[lane];
       uint64_t s = (uint64_t)t;
@@ -221,11 +224,11 @@ struct Sim {
       release(v, rec, 0, s + 1, rec.cta, sm);
       release(v, rec, 1, f, rec.cta, sm);
     } else if (cls == C_SMEM) {
-      const uint32_t a = S[nsub];
+      const uint32_t a = S[smem_w];
       const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
       const uint64_t f = s + od.x + od.z;
       if (!complete(v, rec, s, f, sm)) return;
-      if (lane == 0) S[nsub] = (uint32_t)(s + od.x);
+      if (lane == 0) S[smem_w] = (uint32_t)(s + od.x);
       release(v, rec, 0, s + 1, rec.cta, sm);
       release(v, rec, 1, f, rec.cta, sm);
     } else if (cls == C_SYNC) {
@@ -234,13 +237,13 @@ struct Sim {
       release(v, rec, 0, (uint64_t)t + 1, rec.cta, sm);
       release(v, rec, 1, f, rec.cta, sm);
     } else {
-      const uint32_t a = S[nsub + 1];
+      const uint32_t a = S[smem_w + 1];
       const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
       if (s + od.x > kMaxCycle) {
         overflow = 1;
         return;
       }
-      if (lane == 0) S[nsub + 1] = (uint32_t)(s + od.x);
+      if (lane == 0) S[smem_w + 1] = (uint32_t)(s + od.x);
       release(v, rec, 0, s + 1, rec.cta, sm);
       push_one(mkkey(s, kEvMem, v), sm);
     }
@@ -280,7 +283,8 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.flags = L.flags;
   S.nsm = S.hw[HW_NSM];
   S.nsub = S.hw[HW_NSUB];
-  S.sstride = S.nsub + 2;
+  S.sstride = server_stride(S.G.props, S.nsub);
+  S.smem_w = S.sstride - 2;
   uint8_t* sim = L.sims + (uint64_t)b * L.layout.stride;
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
@@ -306,7 +310,7 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   }
 
   // Setup: duration table, idle servers, zeroed node / CTA state.
-  for (uint32_t p = lane; p < S.G.n_ops; p += 64) S.optab[p] = op_entry(S.G.ops[p], S.hw);
+  for (uint32_t p = lane; p < S.G.n_ops; p += 64) S.optab[p] = op_entry(S.G.ops[p], S.hw, S.G.props);
   const uint32_t nsrv = S.nsm * S.sstride + S.nsm;
   for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
   for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);

@@ -212,7 +212,7 @@ template <uint32_t NB>
 struct WSim {
   Image G;
   const uint32_t* hw;
-  uint32_t b, lane, flags, nsm, nsub, sstride, nslot, QF;
+  uint32_t b, lane, flags, nsm, nsub, sstride, smem_w, nslot, QF;
   bool nocont, ofin;
   bool mem_only;  // CTA bookkeeping on memory nodes only (compute nodes always feed a later memory node)
   // LDS
@@ -644,25 +644,26 @@ struct WSim {
         uint64_t st = ev_t[j], f = 0;
         if (cls <= C_SFU) {
           const uint32_t lanes = (od.w >> 8) & 0xFFu;
+          uint32_t* La = S + (od.w >> 16);  // this class's lanes
           if (!nocont)
             for (uint32_t l = 0; l < nsub; ++l)
-              if ((lanes >> l) & 1u) st = S[l] > st ? S[l] : st;
+              if ((lanes >> l) & 1u) st = La[l] > st ? La[l] : st;
           f = st + od.x + od.z;
           if (f <= kMaxCycle)
             for (uint32_t l = 0; l < nsub; ++l)
-              if ((lanes >> l) & 1u) S[l] = (uint32_t)(st + od.x);
+              if ((lanes >> l) & 1u) La[l] = (uint32_t)(st + od.x);
         } else if (cls == C_SMEM) {
-          if (!nocont) st = S[nsub] > st ? S[nsub] : st;
+          if (!nocont) st = S[smem_w] > st ? S[smem_w] : st;
           f = st + od.x + od.z;
-          if (f <= kMaxCycle) S[nsub] = (uint32_t)(st + od.x);
+          if (f <= kMaxCycle) S[smem_w] = (uint32_t)(st + od.x);
         } else if (cls == C_SYNC) {
           f = st + od.z;
         } else {  // memory node: engine now, L2/DRAM in the memory phase
-          if (!nocont) st = S[nsub + 1] > st ? S[nsub + 1] : st;
+          if (!nocont) st = S[smem_w + 1] > st ? S[smem_w + 1] : st;
           is_mem[j] = true;
           f = st + od.x;  // end of engine occupancy
           if (f <= kMaxCycle) {
-            S[nsub + 1] = (uint32_t)f;
+            S[smem_w + 1] = (uint32_t)f;
             mq_push(ev_s[j], mkkey(st, kEvMem, ev_v[j]), rec[j].op());
           }
         }
@@ -939,7 +940,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.mem_only = (L.img.props & kGraphComputeFeedsData) != 0;
   S.nsm = S.hw[HW_NSM];
   S.nsub = S.hw[HW_NSUB];
-  S.sstride = S.nsub + 2;
+  S.sstride = server_stride(S.G.props, S.nsub);
+  S.smem_w = S.sstride - 2;
   S.nslot = (S.nsm + 63) / 64;
   S.QF = L.qp;
   const uint32_t lane = S.lane;
@@ -949,7 +951,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.fr_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_rp);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
   S.ret_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_ret);
-  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, L.max_nsub, L.qp);
+  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.srv = lds + W.srv;
   S.mq_head = lds + W.mq_head;
@@ -985,7 +987,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   // CTAs that receive cross-CTA edges (the others are zeroed at dispatch).
   uint64_t lm = ~0ull;
   for (uint32_t q = lane; q < S.G.n_ops; q += 64) {
-    const uint4 e = op_entry(S.G.ops[q], S.hw);
+    const uint4 e = op_entry(S.G.ops[q], S.hw, S.G.props);
     S.optab[q] = e;
     const uint32_t cls = e.w & 7u;
     if (cls == C_GLOAD || cls == C_GSTORE) {

@@ -151,9 +151,12 @@ def csr_from_edges(n_nodes: int, src: np.ndarray, dst: np.ndarray, kind: np.ndar
 class GraphBuilder:
     """Incremental builder for small hand-written graphs (tests, examples).
 
-    Nodes must be added CTA by CTA and CTAs kernel by kernel."""
+    Nodes must be added CTA by CTA and CTAs kernel by kernel.  Edges of the
+    kinds in `drop` are ignored as they are added (the Table 4 ablation:
+    a pair that also carries a kept kind keeps that edge)."""
 
-    def __init__(self):
+    def __init__(self, drop=()):
+        self.drop = frozenset(int(k) for k in drop)
         self.ops = OpTable()
         self.node_op: list = []
         self.cta_begin: list = [0]
@@ -189,6 +192,8 @@ class GraphBuilder:
         return len(self.node_op) - 1
 
     def edge(self, u: int, v: int, kind: int = DATA):
+        if int(kind) in self.drop:
+            return
         self.src.append(int(u))
         self.dst.append(int(v))
         self.kind.append(int(kind))
