@@ -165,6 +165,23 @@ int gts_graph_validate(const gts_graph_host *h);
  * the simulation kernels read).  Needs no GPU. */
 int gts_graph_device_bytes(const gts_graph_host *h, uint64_t *bytes);
 
+/* Template sharing (GTSim Sec. 6.4: CTAs that execute isomorphic tile graphs
+ * share one graph structure; each logical CTA keeps only light metadata).
+ * Validates h and reports how its device image shares structure: a kernel
+ * whose CTAs all have the same node count and the same local successor lists
+ * and edge kinds, with no edge leaving or entering a CTA, keeps one template
+ * of node records; its CTAs then differ only in op ids, grouped into classes
+ * (at most 255 per kernel) by a class x slot op table of at most 128 entries
+ * per graph.  Outputs (any may be NULL): *templated_kernels, *template_nodes
+ * (records of all templates), *expanded_nodes (nodes of the kernels without
+ * a template), *class_ops (table entries).  The device image always also
+ * holds every node's expanded record.  Setting the environment variable
+ * GTS_TEMPLATES=0 before an upload turns sharing off (this call then reports
+ * no templated kernel).  Needs no GPU.  Returns GTS_OK or a validation
+ * error. */
+int gts_graph_templates(const gts_graph_host *h, uint32_t *templated_kernels, uint32_t *template_nodes,
+                        uint32_t *expanded_nodes, uint32_t *class_ops);
+
 /* Validates h, builds its device image on the host and copies it into the
  * caller's device buffer dev_image (dev_bytes >= gts_graph_device_bytes) on
  * hip_stream, waiting for the copy to finish before returning.  On success

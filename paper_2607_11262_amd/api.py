@@ -27,7 +27,7 @@ ERRORS = {-1: "GTS_E_ARG", -2: "GTS_E_CYCLE", -3: "GTS_E_EDGE_ORDER", -4: "GTS_E
 SIM_OK, SIM_INFEASIBLE, SIM_OVERFLOW, SIM_DEADLOCK = 0, 1, 2, 3
 OUT_NODES, OUT_DIGEST, NO_CONTENTION, ORDER_AT_FINISH = 1, 2, 4, 8
 
-EXPORTS = ("gts_graph_validate", "gts_graph_device_bytes", "gts_graph_upload", "gts_graph_release", "gts_graph_sizes",
+EXPORTS = ("gts_graph_validate", "gts_graph_device_bytes", "gts_graph_templates", "gts_graph_upload", "gts_graph_release", "gts_graph_sizes",
            "gts_scratch_bytes", "gts_simulate_batch", "gts_hwset_device_bytes", "gts_hwset_upload",
            "gts_hwset_release", "gts_simulate_hwset", "gts_hw_validate", "gts_strerror", "gts_last_error")
 
@@ -61,6 +61,7 @@ def lib():
         vp, u32, u64p = ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint64)
         L.gts_graph_validate.argtypes = [vp]
         L.gts_graph_device_bytes.argtypes = [vp, u64p]
+        L.gts_graph_templates.argtypes = [vp] + [ctypes.POINTER(u32)] * 4
         L.gts_graph_upload.argtypes = [vp, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
         L.gts_graph_release.argtypes = [vp]
         L.gts_graph_sizes.argtypes = [vp] + [ctypes.POINTER(u32)] * 5
@@ -120,6 +121,15 @@ def device_bytes(g) -> int:
     n = ctypes.c_uint64(0)
     _check(lib().gts_graph_device_bytes(ctypes.byref(h), ctypes.byref(n)), "gts_graph_device_bytes")
     return int(n.value)
+
+
+def templates(g) -> dict:
+    """How the device image shares CTA structure (gts_graph_templates)."""
+    h, _keep = _host_struct(g)
+    out = [ctypes.c_uint32(0) for _ in range(4)]
+    _check(lib().gts_graph_templates(ctypes.byref(h), *[ctypes.byref(x) for x in out]), "gts_graph_templates")
+    keys = ("templated_kernels", "template_nodes", "expanded_nodes", "class_ops")
+    return {k: int(x.value) for k, x in zip(keys, out)}
 
 
 def hw_validate(rec) -> int:

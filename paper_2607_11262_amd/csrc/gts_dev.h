@@ -36,7 +36,8 @@ __host__ __device__ inline uint32_t compute_slot(uint32_t props, uint32_t cls) {
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
   uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots, off_indeg;
-  uint32_t max_cta_nodes, max_outdeg;
+  uint64_t off_tnodes, off_tsucc, off_tindeg, off_cclass, off_tops;
+  uint32_t max_cta_nodes, max_outdeg, n_tnodes, n_tsucc, n_tops, pad;
 };
 
 struct OpDev {                  // one distinct operation descriptor
@@ -65,9 +66,22 @@ struct CtaDev {                 // 32 B, one per CTA
 };
 constexpr uint32_t kCtaShared = 0x80000000u;
 
-struct KernelDev {              // 16 B, one per kernel
+// Template sharing (Sec. 6.4: CTAs that run isomorphic tile graphs share one
+// graph structure).  A kernel whose CTAs all have the same node count and the
+// same local successor lists (no cross-CTA edges) keeps one "template" of
+// node records: successor targets are local indices, and the op field is a
+// slot.  The CTAs differ only in op ids (e.g. an L2-miss variant of a load
+// for a first-touch tile): each CTA has a class, and the op of slot s in
+// class q is tops[t_ops + q * t_nslot + s].  The expanded records stay in the
+// image for the general kernel.
+struct KernelDev {              // 32 B, one per kernel
   uint32_t cta_begin, cta_end, warps, smem;
+  uint32_t node_begin;          // first node of the kernel
+  uint32_t t_n;                 // nodes per CTA if templated, else 0
+  uint32_t t_base;              // first template record (and in-degree) of the kernel
+  uint32_t t_ops;               // tops offset (low 16) | slots per class (high 16)
 };
+constexpr uint32_t kMaxTops = 128;   // class x slot op entries per graph (held in LDS)
 
 // Device-side view passed to kernels by value.
 struct Image {
@@ -78,7 +92,12 @@ struct Image {
   const KernelDev* kernels;
   const uint32_t* roots;
   const uint16_t* indeg;        // in-degree per node
-  uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props;
+  const NodeDev* tnodes;        // template records (succ: local index | bits)
+  const uint32_t* tsucc;        // template successors beyond the records' inline ones
+  const uint16_t* tindeg;       // in-degree per template record
+  const uint8_t* cclass;        // class of each CTA of a templated kernel
+  const uint16_t* tops;         // [n_tops] class x slot -> op id
+  uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props, n_tops;
 };
 
 // Hardware record word indices (gts_hw_params field order).
@@ -153,13 +172,13 @@ struct Launch {
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
 // even words).  NS: largest n_sm of the batch; SS: server words per SM
 // (server_stride at the largest n_subpart); QP: later ready entries per lane
-// held in LDS.
+// held in LDS; NT: template class x slot op entries (u16).
 struct WinLds {
-  uint32_t optab, srv, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
+  uint32_t optab, tops, srv, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
   uint32_t w_key, w_aux, w_fin, stage;
   uint32_t total;
 };
-__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP) {
+__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP, uint32_t NT) {
   WinLds L;
   uint32_t o = 0;
   auto take = [&o](uint32_t words, bool wide) {
@@ -169,6 +188,7 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, 
     return r;
   };
   L.optab = take(4u * P, true);
+  L.tops = take((NT + 1u) / 2u, false);
   L.srv = take(NS * SS, false);
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -50,12 +51,110 @@ uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 bool is_compute(uint8_t c) { return c <= gts::C_SFU; }
 bool is_memory(uint8_t c) { return c == gts::C_GLOAD || c == gts::C_GSTORE; }
 
+// A kernel whose CTAs share one template of node records.
+struct KTemplate {
+  uint32_t t_n = 0;     // nodes per CTA (0: not templated)
+  uint32_t t_base = 0;  // first template record
+  uint32_t t_ops = 0;   // first class x slot entry
+  uint32_t nslot = 0;
+  uint32_t tsucc = 0;   // first template successor
+};
+
 // Everything the image needs that is derived from a valid host graph.
 struct Derived {
   std::vector<uint32_t> indeg, node_cta, roots, root_begin, root_count;
   std::vector<uint8_t> shared;  // node has an in-edge from another CTA
   uint32_t props = 0, max_cta_nodes = 0, max_outdeg = 0;
+  std::vector<KTemplate> ktmpl;  // per kernel
+  std::vector<uint8_t> cclass;   // per CTA: class within its templated kernel
+  std::vector<uint16_t> tslot;   // per template record: slot
+  std::vector<uint16_t> tops;    // class x slot -> op
+  uint32_t n_tnodes = 0, n_tsucc = 0;
 };
+
+// Template sharing: find the kernels whose CTAs run isomorphic tile graphs
+// (same node count, same local successor lists and kinds, no cross-CTA
+// edges) and group their CTAs into classes by the op ids of their nodes.
+// Kernels that would take the class x slot table past kMaxTops entries, or
+// that have more than 255 classes, stay expanded.  GTS_TEMPLATES=0 turns the
+// detection off.
+void find_templates(const gts_graph_host* h, Derived* d) {
+  const uint32_t K = h->n_kernels, C = h->n_ctas;
+  d->ktmpl.assign(K, KTemplate());
+  d->cclass.assign(C, 0);
+  d->tslot.clear();
+  d->tops.clear();
+  d->n_tnodes = d->n_tsucc = 0;
+  if (const char* e = std::getenv("GTS_TEMPLATES"))
+    if (std::strcmp(e, "0") == 0) return;
+  const uint32_t* nb = h->cta_node_begin;
+  for (uint32_t k = 0; k < K; ++k) {
+    const uint32_t c0 = h->kernel_cta_begin[k], c1 = h->kernel_cta_begin[k + 1];
+    const uint32_t n = nb[c0 + 1] - nb[c0];
+    if (c1 - c0 < 2) continue;
+    bool ok = true;
+    for (uint32_t c = c0; c < c1 && ok; ++c) ok = nb[c + 1] - nb[c] == n;
+    // identical local structure, every edge inside its CTA, no shared node
+    for (uint32_t c = c0; c < c1 && ok; ++c) {
+      for (uint32_t i = 0; i < n && ok; ++i) {
+        const uint32_t u = nb[c] + i, u0 = nb[c0] + i;
+        if (d->shared[u]) ok = false;
+        const uint32_t e0 = h->succ_ptr[u0], deg = h->succ_ptr[u + 1] - h->succ_ptr[u];
+        if (deg != h->succ_ptr[u0 + 1] - e0) ok = false;
+        for (uint32_t j = 0; j < deg && ok; ++j) {
+          const uint32_t a = h->succ[h->succ_ptr[u] + j], a0 = h->succ[e0 + j];
+          const uint32_t v = a & GTS_EDGE_TARGET_MASK, v0 = a0 & GTS_EDGE_TARGET_MASK;
+          ok = (a >> GTS_EDGE_KIND_SHIFT) == (a0 >> GTS_EDGE_KIND_SHIFT) && v >= nb[c] && v < nb[c] + n &&
+               v - nb[c] == v0 - nb[c0];
+        }
+      }
+    }
+    if (!ok) continue;
+    // classes by op vector, slots by op column
+    std::map<std::vector<uint16_t>, uint32_t> classes;
+    std::vector<uint32_t> cls(c1 - c0);
+    std::vector<std::vector<uint16_t>> class_ops;
+    for (uint32_t c = c0; c < c1 && ok; ++c) {
+      std::vector<uint16_t> ops(h->node_op + nb[c], h->node_op + nb[c] + n);
+      auto it = classes.find(ops);
+      if (it == classes.end()) {
+        if (classes.size() >= 255) ok = false;
+        it = classes.emplace(ops, (uint32_t)class_ops.size()).first;
+        class_ops.push_back(ops);
+      }
+      cls[c - c0] = it->second;
+    }
+    if (!ok) continue;
+    const uint32_t nclass = (uint32_t)class_ops.size();
+    std::map<std::vector<uint16_t>, uint32_t> slots;
+    std::vector<uint16_t> slot_of(n);
+    std::vector<std::vector<uint16_t>> slot_cols;
+    for (uint32_t i = 0; i < n; ++i) {
+      std::vector<uint16_t> col(nclass);
+      for (uint32_t q = 0; q < nclass; ++q) col[q] = class_ops[q][i];
+      auto it = slots.find(col);
+      if (it == slots.end()) {
+        it = slots.emplace(col, (uint32_t)slot_cols.size()).first;
+        slot_cols.push_back(col);
+      }
+      slot_of[i] = (uint16_t)it->second;
+    }
+    const uint32_t nslot = (uint32_t)slot_cols.size();
+    if (d->tops.size() + (uint64_t)nclass * nslot > gts::kMaxTops) continue;
+    KTemplate& t = d->ktmpl[k];
+    t.t_n = n;
+    t.t_base = d->n_tnodes;
+    t.t_ops = (uint32_t)d->tops.size();
+    t.nslot = nslot;
+    t.tsucc = d->n_tsucc;
+    for (uint32_t q = 0; q < nclass; ++q)
+      for (uint32_t s = 0; s < nslot; ++s) d->tops.push_back(slot_cols[s][q]);
+    for (uint32_t c = c0; c < c1; ++c) d->cclass[c] = (uint8_t)cls[c - c0];
+    d->tslot.insert(d->tslot.end(), slot_of.begin(), slot_of.end());
+    d->n_tnodes += n;
+    d->n_tsucc += h->succ_ptr[nb[c0] + n] - h->succ_ptr[nb[c0]];
+  }
+}
 
 int check_graph(const gts_graph_host* h, Derived* d) {
   if (!h) return fail(GTS_E_ARG, "graph is NULL");
@@ -196,14 +295,16 @@ int check_graph(const gts_graph_host* h, Derived* d) {
              (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift;
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
+  find_templates(h, d);
   return GTS_OK;
 }
 
 struct ImageLayout {
-  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, total;
+  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, tnodes, tsucc, tindeg, cclass, tops, total;
 };
 
-ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
+ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
+  const uint64_t n_roots = d.roots.size();
   ImageLayout L;
   uint64_t off = align_up(sizeof(gts::ImageHeader), gts::kAlign);
   L.ops = off;
@@ -220,6 +321,16 @@ ImageLayout image_layout(const gts_graph_host* h, uint64_t n_roots) {
   off = align_up(off + n_roots * 4, gts::kAlign);
   L.indeg = off;
   off = align_up(off + (uint64_t)h->n_nodes * 2, gts::kAlign);
+  L.tnodes = off;
+  off = align_up(off + (uint64_t)d.n_tnodes * sizeof(gts::NodeDev), gts::kAlign);
+  L.tsucc = off;
+  off = align_up(off + (uint64_t)d.n_tsucc * 4, gts::kAlign);
+  L.tindeg = off;
+  off = align_up(off + (uint64_t)d.n_tnodes * 2, gts::kAlign);
+  L.cclass = off;
+  off = align_up(off + (uint64_t)h->n_ctas, gts::kAlign);
+  L.tops = off;
+  off = align_up(off + d.tops.size() * 2, gts::kAlign);
   L.total = off;
   return L;
 }
@@ -323,7 +434,9 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // limit of the kernel).  Measured: fewer, larger simulations per CU are
     // slower even for batches that fill only part of the chip.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
-    auto bytes = [&](uint32_t qp) { return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp).total; };
+    auto bytes = [&](uint32_t qp) {
+      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops).total;
+    };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
     uint32_t want = kWavesPerCu;
     if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU
@@ -387,7 +500,27 @@ int gts_graph_device_bytes(const gts_graph_host* h, uint64_t* bytes) {
   Derived d;
   int rc = check_graph(h, &d);
   if (rc) return rc;
-  *bytes = image_layout(h, d.roots.size()).total;
+  *bytes = image_layout(h, d).total;
+  return GTS_OK;
+}
+
+int gts_graph_templates(const gts_graph_host* h, uint32_t* templated_kernels, uint32_t* template_nodes,
+                        uint32_t* expanded_nodes, uint32_t* class_ops) {
+  g_last_error.clear();
+  Derived d;
+  int rc = check_graph(h, &d);
+  if (rc) return rc;
+  uint32_t nk = 0, expanded = 0;
+  for (uint32_t k = 0; k < h->n_kernels; ++k) {
+    if (d.ktmpl[k].t_n)
+      ++nk;
+    else
+      expanded += h->cta_node_begin[h->kernel_cta_begin[k + 1]] - h->cta_node_begin[h->kernel_cta_begin[k]];
+  }
+  if (templated_kernels) *templated_kernels = nk;
+  if (template_nodes) *template_nodes = d.n_tnodes;
+  if (expanded_nodes) *expanded_nodes = expanded;
+  if (class_ops) *class_ops = (uint32_t)d.tops.size();
   return GTS_OK;
 }
 
@@ -399,7 +532,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   Derived d;
   int rc = check_graph(h, &d);
   if (rc) return rc;
-  const ImageLayout L = image_layout(h, d.roots.size());
+  const ImageLayout L = image_layout(h, d);
   if (!dev_image) return fail(GTS_E_ARG, "device image buffer is NULL");
   if (dev_bytes < L.total)
     return fail(GTS_E_SCRATCH, "device image needs %llu bytes, got %llu", (unsigned long long)L.total,
@@ -426,8 +559,16 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   hdr->off_kernels = L.kernels;
   hdr->off_roots = L.roots;
   hdr->off_indeg = L.indeg;
+  hdr->off_tnodes = L.tnodes;
+  hdr->off_tsucc = L.tsucc;
+  hdr->off_tindeg = L.tindeg;
+  hdr->off_cclass = L.cclass;
+  hdr->off_tops = L.tops;
   hdr->max_cta_nodes = d.max_cta_nodes;
   hdr->max_outdeg = d.max_outdeg;
+  hdr->n_tnodes = d.n_tnodes;
+  hdr->n_tsucc = d.n_tsucc;
+  hdr->n_tops = (uint32_t)d.tops.size();
   auto* ops = reinterpret_cast<gts::OpDev*>(img.data() + L.ops);
   for (uint32_t p = 0; p < h->n_ops; ++p) {
     ops[p].cls = h->op_cls[p];
@@ -480,7 +621,42 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     ks[k].cta_end = h->kernel_cta_begin[k + 1];
     ks[k].warps = h->kernel_warps[k];
     ks[k].smem = h->kernel_smem[k];
+    ks[k].node_begin = h->cta_node_begin[h->kernel_cta_begin[k]];
+    const KTemplate& t = d.ktmpl[k];
+    ks[k].t_n = t.t_n;
+    ks[k].t_base = t.t_base;
+    ks[k].t_ops = t.t_ops | t.nslot << 16;
   }
+  // template records: the first CTA's nodes with local successor targets and
+  // slots for ops; their successors in the same form
+  auto* tn = reinterpret_cast<gts::NodeDev*>(img.data() + L.tnodes);
+  auto* ts = reinterpret_cast<uint32_t*>(img.data() + L.tsucc);
+  auto* ti = reinterpret_cast<uint16_t*>(img.data() + L.tindeg);
+  for (uint32_t k = 0; k < h->n_kernels; ++k) {
+    const KTemplate& t = d.ktmpl[k];
+    if (!t.t_n) continue;
+    const uint32_t base = h->cta_node_begin[h->kernel_cta_begin[k]];
+    const uint32_t e_base = h->succ_ptr[base];
+    for (uint32_t i = 0; i < t.t_n; ++i) {
+      const uint32_t u = base + i;
+      const uint32_t deg = h->succ_ptr[u + 1] - h->succ_ptr[u];
+      gts::NodeDev& r = tn[t.t_base + i];
+      r.op_nsucc = (uint32_t)d.tslot[t.t_base + i] | (std::min<uint32_t>(deg, 0xFFFFu) << 16);
+      r.cta = i;
+      r.succ_begin = t.tsucc + (h->succ_ptr[u] - e_base);
+      for (uint32_t j = 0; j < deg; ++j) {
+        const uint32_t a = succ_dev[h->succ_ptr[u] + j];
+        ts[r.succ_begin + j] = ((a & GTS_EDGE_TARGET_MASK) - base) | (a & ~GTS_EDGE_TARGET_MASK);
+      }
+      for (uint32_t j = 0; j < gts::kInlineSucc; ++j) {
+        r.succ[j] = j < deg ? ts[r.succ_begin + j] : 0u;
+        r.sindeg[j] = j < deg ? nodes[u].sindeg[j] : (uint16_t)0;
+      }
+      ti[t.t_base + i] = (uint16_t)d.indeg[u];
+    }
+  }
+  std::memcpy(img.data() + L.cclass, d.cclass.data(), d.cclass.size());
+  if (!d.tops.empty()) std::memcpy(img.data() + L.tops, d.tops.data(), d.tops.size() * 2);
   if (!d.roots.empty()) std::memcpy(img.data() + L.roots, d.roots.data(), d.roots.size() * 4);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
@@ -498,6 +674,12 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.kernels = reinterpret_cast<const gts::KernelDev*>(base + L.kernels);
   g->img.roots = reinterpret_cast<const uint32_t*>(base + L.roots);
   g->img.indeg = reinterpret_cast<const uint16_t*>(base + L.indeg);
+  g->img.tnodes = reinterpret_cast<const gts::NodeDev*>(base + L.tnodes);
+  g->img.tsucc = reinterpret_cast<const uint32_t*>(base + L.tsucc);
+  g->img.tindeg = reinterpret_cast<const uint16_t*>(base + L.tindeg);
+  g->img.cclass = reinterpret_cast<const uint8_t*>(base + L.cclass);
+  g->img.tops = reinterpret_cast<const uint16_t*>(base + L.tops);
+  g->img.n_tops = (uint32_t)d.tops.size();
   g->img.n_nodes = h->n_nodes;
   g->img.n_edges = h->n_edges;
   g->img.n_ctas = h->n_ctas;

@@ -217,6 +217,7 @@ struct WSim {
   bool mem_only;  // CTA bookkeeping on memory nodes only (compute nodes always feed a later memory node)
   // LDS
   uint4* optab;
+  uint16_t* tops;  // template class x slot -> op
   // mq_pos[s]: SM s's ring head (bits 0-7) and entry count (bits 8-15), and
   // its resident CTAs (bits 16-31)
   uint32_t *srv, *mq_head, *mq_pos, *dsc, *nr_cnt, *fr_cnt, *fr_min, *fr_hot;
@@ -234,6 +235,10 @@ struct WSim {
   uint32_t* out_cycles;
   // uniform control
   uint32_t next_cta, retired, cur_k, k_begin, k_end, kstart_k, kstart_t, kstart_valid;
+  // the kernel whose CTAs are live (kernels run one after another) and its
+  // template: nodes per CTA (0: expanded records), first node, first CTA, CTAs,
+  // first template record, class x slot table offset and slots per class
+  uint32_t run_k, t_n, t_node0, t_kc0, t_nc, t_base, t_ops, t_nslot;
   uint64_t slots, l2_av, dram_av, Lm, Hnear;
   // per lane
   uint64_t digest;
@@ -424,7 +429,7 @@ struct WSim {
                                                uint32_t s) {
     const uint32_t n = rec.nsucc();
     for (uint32_t k = 0; k < n; ++k) {
-      const uint32_t ent = k < kInlineSucc ? rec.succ(k) : G.succ[rec.sb() + k];
+      const uint32_t ent = k < kInlineSucc ? rec.succ(k) : succ_of(rec, k);
       const uint32_t bits = ent >> GTS_EDGE_KIND_SHIFT;
       if (k < kInlineSucc && !(bits & kDevShared)) continue;  // done by the batched path
       const bool at_issue = (bits & kDevOrder) && !ofin;
@@ -435,7 +440,7 @@ struct WSim {
       if (bits & kDevShared) {
         release_shared(w, r, rec.cta(), s);
       } else {
-        const uint32_t ind = G.indeg[w];
+        const uint32_t ind = indeg_of(rec, w);
         const uint64_t sv = ind != 1 ? state[w] : 0ull;
         const uint32_t cnt = (uint32_t)(sv >> 32) + 1u;
         uint32_t acc = (uint32_t)sv;
@@ -444,6 +449,47 @@ struct WSim {
         if (cnt == ind) rq_push(s, acc, w);
       }
     }
+  }
+
+  // ---- node records: expanded, or the running kernel's template with the
+  // CTA derived from the node id, the op looked up by the CTA's class and
+  // the successors moved from local to global ids
+  __device__ __forceinline__ Rec rec_of(uint32_t v) const {
+    if (t_n == 0) return load_rec(G.nodes, v);
+    const uint32_t rel = v >= t_node0 ? v - t_node0 : 0u;  // idle lanes pass node 0
+    uint32_t ci = rel / t_n;
+    ci = ci < t_nc ? ci : t_nc - 1u;
+    const uint32_t loc = rel - ci * t_n < t_n ? rel - ci * t_n : 0u;
+    const uint32_t c = t_kc0 + ci;
+    Rec r = load_rec(G.tnodes, t_base + loc);
+    const uint32_t q = G.cclass[c];
+    const uint32_t base = t_node0 + ci * t_n;
+    r.a.x = (r.a.x & 0xFFFF0000u) | tops[t_ops + q * t_nslot + (r.a.x & 0xFFFFu)];
+    r.a.y = c;
+    r.a.w += base;
+    r.b.x += base;
+    r.b.y += base;
+    return r;
+  }
+  // successor k of a record beyond the inline ones, and an unshared node's in-degree
+  __device__ __forceinline__ uint32_t succ_of(const Rec& r, uint32_t k) const {
+    if (t_n == 0) return G.succ[r.sb() + k];
+    return G.tsucc[r.sb() + k] + t_node0 + (r.cta() - t_kc0) * t_n;
+  }
+  __device__ __forceinline__ uint32_t indeg_of(const Rec& r, uint32_t w) const {
+    if (t_n == 0) return G.indeg[w];
+    return G.tindeg[t_base + (w - t_node0 - (r.cta() - t_kc0) * t_n)];
+  }
+  __device__ __forceinline__ void load_template() {
+    const KernelDev kd = G.kernels[cur_k];
+    run_k = cur_k;
+    t_n = uni(kd.t_n);
+    t_node0 = uni(kd.node_begin);
+    t_kc0 = uni(kd.cta_begin);
+    t_nc = uni(kd.cta_end) - t_kc0;
+    t_base = uni(kd.t_base);
+    t_ops = uni(kd.t_ops & 0xFFFFu);
+    t_nslot = uni(kd.t_ops >> 16);
   }
 
   __device__ __forceinline__ void load_kernel() {
@@ -481,6 +527,7 @@ struct WSim {
         ++k;
       }
       if (k == 0) return;
+      if (run_k != cur_k) load_template();  // the first CTAs of a kernel: it is now the running one
       if (!kstart_valid || kstart_k != cur_k) {
         kstart_valid = 1;
         kstart_k = cur_k;
@@ -628,7 +675,7 @@ struct WSim {
       ev_t[w] = (uint32_t)(key >> 32);
       ev_v[w] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
       ev_s[w] = ok[w] ? w_aux[i] : 0u;
-      rec[w] = load_rec(G.nodes, ev_v[w]);
+      rec[w] = rec_of(ev_v[w]);
     }
     // timing on the SM's servers
     uint64_t rel_i[W], rel_f[W];
@@ -874,7 +921,7 @@ struct WSim {
       tt[j] = (uint32_t)(key >> 32);
       ff[j] = ok[j] ? w_fin[slot] : 0u;
       ss[j] = ok[j] ? w_aux[slot] >> 16 : 0u;
-      rec[j] = load_rec(G.nodes, vv[j]);
+      rec[j] = rec_of(vv[j]);
     }
     uint64_t sv[W][kInlineSucc];
     bool sel[W][kInlineSucc];
@@ -951,8 +998,9 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.fr_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_rp);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
   S.ret_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_ret);
-  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp);
+  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
+  S.tops = reinterpret_cast<uint16_t*>(lds + W.tops);
   S.srv = lds + W.srv;
   S.mq_head = lds + W.mq_head;
   S.mq_pos = lds + W.mq_pos;
@@ -997,6 +1045,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   }
   lm = wmin64(lm);
   S.Lm = lm < kWindowMax ? lm : kWindowMax;
+  for (uint32_t i = lane; i < S.G.n_tops; i += 64) S.tops[i] = S.G.tops[i];
   for (uint32_t i = lane; i < S.nsm * S.sstride; i += 64) S.srv[i] = 0;
   for (uint32_t i = lane; i < S.nsm; i += 64) {
     S.mq_head[i] = 0xFFFFFFFFu;
@@ -1025,6 +1074,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.retired = 0;
   S.cur_k = 0;
   S.load_kernel();
+  S.run_k = 0xFFFFFFFFu;  // no CTA dispatched yet
+  S.t_n = 0;
   S.kstart_k = 0;
   S.kstart_t = 0;
   S.kstart_valid = 0;
