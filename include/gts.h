@@ -67,9 +67,14 @@ extern "C" {
 #define GTS_GLOAD  4  /* global->shared tile load (TMA / cp.async); bytes     */
 #define GTS_GSTORE 5  /* shared->global tile store; bytes                     */
 #define GTS_SYNC   6  /* barrier / signal-wait node; no resource, work unused */
-#define GTS_N_CLASSES 7
+#define GTS_REMOTE 7  /* DSMEM access to another CTA of the cluster over the
+                         SM-cluster NoC (Sec. 5.2); work = bytes            */
+#define GTS_N_CLASSES 8
 
 #define GTS_OPF_MISS 1u  /* GLOAD/GSTORE: served by DRAM instead of L2       */
+/* REMOTE: the target CTA's rank within the source CTA's cluster is
+ * (flags >> GTS_OPF_RANK_SHIFT); no other flag bit is set. */
+#define GTS_OPF_RANK_SHIFT 4
 
 /* ---- edge kinds (Sec. 4.1 edge semantics) ------------------------------ */
 /* succ[] entries are  target | (kind << GTS_EDGE_KIND_SHIFT).              */
@@ -95,6 +100,8 @@ extern "C" {
 #define GTS_MAX_WARPS   32u           /* warps per CTA (op warp masks are u32) */
 #define GTS_MAX_SM      1024u
 #define GTS_MAX_SUBPART 8u
+#define GTS_MAX_CLUSTER 16u           /* CTAs per thread-block cluster        */
+#define GTS_MAX_NOC     64u           /* SMs per NoC domain                   */
 
 /* ---- hardware parameters (Table 3; integer cycles, Q16.16 rates) -------- */
 /* Rates are work units per core cycle in Q16.16 (value * 65536), per SM for
@@ -125,7 +132,20 @@ typedef struct gts_hw_params {
   uint32_t lat[7];           /* GTS_LAT_*, each <= 2^30                      */
   uint32_t cta_launch_lat;   /* added to every CTA's launch, <= 2^30         */
   uint32_t kernel_launch_lat;/* added to a kernel's first-wave CTAs, <= 2^30 */
-  uint32_t reserved[11];     /* must be zero                                 */
+  /* SM-cluster NoC (Sec. 5.2 DSMEM; Sec. 7.2 crossbar vs mesh, mapping).  SM
+   * s belongs to NoC domain s / noc_nodes as its node s % noc_nodes; a
+   * cluster's CTAs are placed on distinct SMs of one domain.  noc_nodes = 0:
+   * no NoC (a kernel with clusters of more than one CTA is then INFEASIBLE). */
+  uint32_t noc_nodes;        /* SMs per domain, 0 .. GTS_MAX_NOC             */
+  uint32_t noc_width;        /* 0: crossbar; else a mesh noc_width wide with
+                                noc_nodes / noc_width rows (XY routing)      */
+  uint32_t noc_rate_q16;     /* bytes per cycle of one crossbar port / mesh
+                                link, Q16.16, >= 1 when noc_nodes > 0        */
+  uint32_t noc_lat;          /* crossbar traversal / mesh per-hop cycles,
+                                <= 2^24                                      */
+  uint32_t noc_map;          /* cluster placement: 0 strips of consecutive
+                                nodes, 1 compact blocks (mesh)               */
+  uint32_t reserved[6];      /* must be zero                                 */
 } gts_hw_params;
 
 /* ---- host-side graph (Sec. 4.1; dictionary-encoded descriptors) --------- */
@@ -135,12 +155,17 @@ typedef struct gts_hw_params {
  * is non-empty.  An op is one distinct (class, flags, work, warp mask) tuple;
  * node v executes op node_op[v].  The successors of v are
  * succ[succ_ptr[v] .. succ_ptr[v+1]).  Validity: acyclic; no duplicate (u,v);
- * cta(u) <= cta(v) for every edge; in-degree <= GTS_MAX_INDEG; compute ops
- * (TENSOR/ALU/SFU) have a non-empty warp mask inside [0, warps of the kernel
- * of every CTA that uses them).  An empty graph has all counts zero. */
+ * cta(u) <= cta(v) for every edge, except between two CTAs of one cluster
+ * (whose CTAs are dispatched together); in-degree <= GTS_MAX_INDEG; compute
+ * ops (TENSOR/ALU/SFU) have a non-empty warp mask inside [0, warps of the
+ * kernel of every CTA that uses them); the CTAs of kernel k form clusters of
+ * kernel_cluster[k] consecutive CTAs (1 .. GTS_MAX_CLUSTER, dividing the
+ * kernel's CTA count; kernel_cluster = NULL means 1 for every kernel), and a
+ * REMOTE op's target rank is below the cluster size of every kernel that
+ * uses it.  An empty graph has all counts zero. */
 typedef struct gts_graph_host {
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops;
-  const uint8_t  *op_cls;           /* [n_ops]  GTS_TENSOR .. GTS_SYNC       */
+  const uint8_t  *op_cls;           /* [n_ops]  GTS_TENSOR .. GTS_REMOTE     */
   const uint8_t  *op_flags;         /* [n_ops]  GTS_OPF_*                    */
   const uint32_t *op_work;          /* [n_ops]                               */
   const uint32_t *op_warps;         /* [n_ops]  warp mask within the CTA     */
@@ -151,6 +176,7 @@ typedef struct gts_graph_host {
   const uint32_t *kernel_cta_begin; /* [n_kernels + 1]                       */
   const uint16_t *kernel_warps;     /* [n_kernels], 1 .. GTS_MAX_WARPS       */
   const uint32_t *kernel_smem;      /* [n_kernels], shared memory per CTA    */
+  const uint8_t  *kernel_cluster;   /* [n_kernels] CTAs per cluster, or NULL */
 } gts_graph_host;
 
 typedef struct gts_graph gts_graph;  /* opaque handle to an uploaded graph */

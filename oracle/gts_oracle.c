@@ -66,20 +66,51 @@
  *  R11 digest = sum over v of mix64(((start<<32)|finish) ^ mix64(v+1)),
  *      mod 2^64, mix64 = the SplitMix64 finaliser (Steele, Lea, Flood 2014).
  *  R12 NO_CONTENTION: servers never delay (start = ready, m = s).
+ *  R13 Clusters (Sec. 5.2: thread-block clusters communicate through
+ *      distributed shared memory).  Kernel k's CTAs form clusters of
+ *      cl = kernel_cluster[k] consecutive CTAs; rank = (c - first CTA of k)
+ *      mod cl.  SM s is node s mod D of NoC domain s / D (D = noc_nodes).
+ *      A kernel with cl > 1 dispatches whole clusters in index order, all
+ *      launched in the same step: for domain d = 0, 1, ... and slot j = 0,
+ *      1, ... of the placement list, the first (d, j) whose SMs
+ *      d*D + node(j, r), r < cl, all exist and all have a free slot takes
+ *      the cluster (rank r on node(j, r)); if none, dispatch waits.
+ *      Placement lists (Sec. 7.2 mapping): strips, node(j, r) = j*cl + r for
+ *      j < D / cl; blocks (noc_map 1 on a W x H mesh), bh = the largest
+ *      divisor of cl with bh*bh <= cl such that bw = cl / bh divides W and
+ *      bh divides H: block j in row-major block order, rank r at
+ *      x = (j mod (W/bw))*bw + r mod bw, y = (j div (W/bw))*bh + r div bw;
+ *      without such a shape, or on a crossbar, strips.
+ *  R14 REMOTE nodes (Sec. 5.2 DSMEM over the SM-cluster NoC; the target is
+ *      carried by the node): target CTA = first CTA of the source's cluster
+ *      + rank (op flags >> 4); route from node a (source SM) to node b
+ *      (target CTA's SM) of their domain.  Crossbar (noc_width 0): the
+ *      injection port of a and the ejection port of b, latency noc_lat.
+ *      Mesh (noc_width W, H = D / W rows, node i at (i mod W, i div W)):
+ *      the directed links of the XY route (x first), hops = |dx| + |dy|,
+ *      latency hops * noc_lat.  occ = max(1, cdiv(work*65536, noc_rate));
+ *      start s = max(t, avail of every server on the route), each set to
+ *      s + occ; finish = s + occ + latency; ORDER edges at s + 1, DATA /
+ *      SYNC at finish.  Reading: the route is reserved as a whole, like a
+ *      multi-lane compute node (no per-hop store-and-forward).
+ *  R15 A kernel with cl > 1 or with REMOTE nodes is INFEASIBLE when
+ *      noc_nodes = 0, when cl > noc_nodes, or when no placement of R13 has
+ *      all its SMs in the machine.
  */
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 /* ---- interface formats (restated, not shared) ---------------------------- */
-enum { K_TENSOR = 0, K_ALU = 1, K_SFU = 2, K_SMEM = 3, K_GLOAD = 4, K_GSTORE = 5, K_SYNC = 6 };
+enum { K_TENSOR = 0, K_ALU = 1, K_SFU = 2, K_SMEM = 3, K_GLOAD = 4, K_GSTORE = 5, K_SYNC = 6, K_REMOTE = 7 };
 enum { E_DATA = 0, E_ORDER = 1, E_SYNC = 2 };
 /* hardware record: 32 u32 words */
 enum {
   HW_NSM = 0, HW_NSUB = 1, HW_MAXCTA = 2, HW_MAXWARPS = 3, HW_SMEM = 4,
   HW_RATE = 5,  /* +0 tensor +1 alu +2 sfu +3 smem +4 gmem +5 l2 +6 dram */
   HW_LAT = 12,  /* +0 tensor +1 alu +2 sfu +3 smem +4 l2 +5 dram +6 sync */
-  HW_CTALAT = 19, HW_KLAT = 20
+  HW_CTALAT = 19, HW_KLAT = 20,
+  HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25
 };
 enum { F_NODES = 1, F_DIGEST = 2, F_NOCONT = 4, F_ORDER_FIN = 8 };
 enum { ST_OK = 0, ST_INFEASIBLE = 1, ST_OVERFLOW = 2, ST_DEADLOCK = 3 };
@@ -143,9 +174,11 @@ typedef struct {
   const uint32_t *succ_ptr, *succ, *cta_node_begin, *kernel_cta_begin;
   const uint16_t *kernel_warps;
   const uint32_t *kernel_smem;
+  const uint8_t *kernel_cluster;
   /* hw */
   uint32_t nsm, nsub, flags;
   const uint32_t *hw;
+  uint32_t noc_d, noc_w;   /* SMs per NoC domain, mesh width (0: crossbar) */
   /* derived per op */
   uint64_t *occ, *occm, *lat; uint32_t *lanes; int *to_dram;
   uint64_t *slots;
@@ -156,6 +189,7 @@ typedef struct {
   /* per SM */
   uint64_t *resident, *lane_av, *smem_av, *eng_av;
   uint64_t l2_av, dram_av;
+  uint64_t *noc_av;        /* per domain node: 4 link/port servers */
   /* control */
   heap_t heap;
   uint32_t next_cta; uint64_t retired;
@@ -200,11 +234,71 @@ static int complete(sim_t *S, uint32_t v, uint64_t start, uint64_t finish) {
   return 1;
 }
 
+/* R13: node of rank r in placement slot j of a domain, or -1 if the list has
+ * no slot j */
+static int64_t slot_node(const sim_t *S, uint32_t cl, uint32_t j, uint32_t r) {
+  uint32_t D = S->noc_d, W = S->noc_w;
+  if (S->hw[HW_NOC_MAP] == 1 && W > 0) {
+    uint32_t H = D / W, bh = 0;
+    for (uint32_t h = 1; h * h <= cl; h++)
+      if (cl % h == 0 && W % (cl / h) == 0 && H % h == 0) bh = h;
+    if (bh) {
+      uint32_t bw = cl / bh, nbx = W / bw, nby = H / bh;
+      if (j >= nbx * nby) return -1;
+      uint32_t x = (j % nbx) * bw + r % bw, y = (j / nbx) * bh + r / bw;
+      return (int64_t)y * W + x;
+    }
+  }
+  if (j >= D / cl) return -1;
+  return (int64_t)j * cl + r;
+}
+
+/* R13: first placement (domain-major, then slot) whose SMs exist and, if
+ * `need_free`, all have a free slot for kernel k; writes the SM of each rank */
+static int place_cluster(const sim_t *S, uint32_t k, uint32_t cl, int need_free, uint64_t *sm_of_rank) {
+  uint32_t ndom = (S->nsm + S->noc_d - 1) / S->noc_d;
+  for (uint32_t d = 0; d < ndom; d++)
+    for (uint32_t j = 0; slot_node(S, cl, j, 0) >= 0; j++) {
+      int ok = 1;
+      for (uint32_t r = 0; r < cl && ok; r++) {
+        uint64_t s = (uint64_t)d * S->noc_d + (uint64_t)slot_node(S, cl, j, r);
+        if (s >= S->nsm) ok = 0;
+        else if (need_free && S->resident[s] >= S->slots[k]) ok = 0;
+        else sm_of_rank[r] = s;
+      }
+      if (ok) return 1;
+    }
+  return 0;
+}
+
+static void push_roots(sim_t *S, uint32_t c, uint64_t launch) {
+  for (uint32_t v = S->cta_node_begin[c]; v < S->cta_node_begin[c + 1]; v++)
+    if (S->cnt[v] == S->indeg[v])
+      heap_push(&S->heap, mkkey(max64(S->acc[v], launch), EV_READY, v));
+}
+
 static void dispatch(sim_t *S, uint64_t t) {
   while (S->next_cta < S->C) {
     uint32_t c = S->next_cta;
     uint32_t k = S->cta_kernel[c];
     if (S->retired < S->kernel_cta_begin[k]) break;   /* previous kernel still running */
+    uint32_t cl = S->kernel_cluster[k];
+    if (cl > 1) {                                        /* R13: a whole cluster */
+      uint64_t sm_of_rank[16];
+      if (!place_cluster(S, k, cl, 1, sm_of_rank)) break;
+      if (S->kstart[k] < 0) S->kstart[k] = (int64_t)t;
+      uint64_t launch = t + S->hw[HW_CTALAT];
+      if ((uint64_t)S->kstart[k] == t) launch += S->hw[HW_KLAT];
+      if (launch > MAXCYC) { S->overflow = 1; return; }
+      for (uint32_t r = 0; r < cl; r++) {
+        S->cta_sm[c + r] = (int64_t)sm_of_rank[r];
+        S->cta_launch[c + r] = (uint32_t)launch;
+        S->resident[sm_of_rank[r]]++;
+      }
+      for (uint32_t r = 0; r < cl; r++) push_roots(S, c + r, launch);
+      S->next_cta += cl;
+      continue;
+    }
     int64_t best = -1; uint64_t bestfree = 0;
     for (uint32_t m = 0; m < S->nsm; m++) {
       uint64_t fr = S->slots[k] - S->resident[m];
@@ -218,9 +312,7 @@ static void dispatch(sim_t *S, uint64_t t) {
     S->cta_sm[c] = best;
     S->cta_launch[c] = (uint32_t)launch;
     S->resident[best]++;
-    for (uint32_t v = S->cta_node_begin[c]; v < S->cta_node_begin[c + 1]; v++)
-      if (S->cnt[v] == S->indeg[v])
-        heap_push(&S->heap, mkkey(max64(S->acc[v], launch), EV_READY, v));
+    push_roots(S, c, launch);
     S->next_cta++;
   }
 }
@@ -252,6 +344,30 @@ static void issue(sim_t *S, uint32_t v, uint64_t t) {
     if (!complete(S, v, t, t + S->lat[p])) return;
     release_out(S, v, 0, t + 1);
     release_out(S, v, 1, S->fin[v]);
+  } else if (cls == K_REMOTE) { /* R14 */
+    uint32_t k = S->cta_kernel[c], cl = S->kernel_cluster[k], kb = S->kernel_cta_begin[k];
+    uint32_t tgt = kb + (c - kb) / cl * cl + (S->op_flags[p] >> 4);
+    uint64_t D = S->noc_d, dom = sm / D;
+    uint64_t a = sm % D, b = (uint64_t)S->cta_sm[tgt] % D;
+    uint64_t *route[2 * 64];
+    uint32_t nr = 0, lat_mult = 1;
+    uint64_t *dav = S->noc_av + dom * D * 4;
+    if (S->noc_w == 0) {           /* crossbar: injection port of a, ejection port of b */
+      route[nr++] = &dav[a * 4 + 0];
+      route[nr++] = &dav[b * 4 + 1];
+    } else {                        /* mesh, XY routing: link (node, dir), dir 0 +x 1 -x 2 +y 3 -y */
+      uint64_t W = S->noc_w, x = a % W, y = a / W, xb = b % W, yb = b / W;
+      while (x != xb) { uint32_t dir = xb > x ? 0 : 1; route[nr++] = &dav[(y * W + x) * 4 + dir]; x = dir == 0 ? x + 1 : x - 1; }
+      while (y != yb) { uint32_t dir = yb > y ? 2 : 3; route[nr++] = &dav[(y * W + x) * 4 + dir]; y = dir == 2 ? y + 1 : y - 1; }
+      lat_mult = nr;
+    }
+    uint64_t s = t;
+    if (!nocont)
+      for (uint32_t i = 0; i < nr; i++) s = max64(s, *route[i]);
+    for (uint32_t i = 0; i < nr; i++) *route[i] = s + S->occ[p];
+    if (!complete(S, v, s, s + S->occ[p] + S->lat[p] * lat_mult)) return;
+    release_out(S, v, 0, s + 1);
+    release_out(S, v, 1, S->fin[v]);
   } else { /* GLOAD / GSTORE: engine now, global server at MEM_ARRIVE */
     uint64_t s = nocont ? t : max64(t, S->eng_av[sm]);
     if (s + S->occ[p] > MAXCYC) { S->overflow = 1; return; }
@@ -280,7 +396,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
                   const uint32_t *op_work, const uint32_t *op_warps, const uint16_t *node_op,
                   const uint32_t *succ_ptr, const uint32_t *succ, const uint32_t *cta_node_begin,
                   const uint32_t *kernel_cta_begin, const uint16_t *kernel_warps,
-                  const uint32_t *kernel_smem, const uint32_t *hw, uint32_t flags,
+                  const uint32_t *kernel_smem, const uint8_t *kernel_cluster, const uint32_t *hw, uint32_t flags,
                   uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
                   uint64_t *out_digest, uint32_t *out_cta) {
   (void)n_edges;
@@ -291,8 +407,9 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   S.op_cls = op_cls; S.op_flags = op_flags; S.op_work = op_work; S.op_warps = op_warps;
   S.node_op = node_op; S.succ_ptr = succ_ptr; S.succ = succ;
   S.cta_node_begin = cta_node_begin; S.kernel_cta_begin = kernel_cta_begin;
-  S.kernel_warps = kernel_warps; S.kernel_smem = kernel_smem;
+  S.kernel_warps = kernel_warps; S.kernel_smem = kernel_smem; S.kernel_cluster = kernel_cluster;
   S.hw = hw; S.nsm = hw[HW_NSM]; S.nsub = hw[HW_NSUB]; S.flags = flags;
+  S.noc_d = hw[HW_NOC_NODES]; S.noc_w = hw[HW_NOC_W];
   int rc = 0;
 
   /* R9 residency per kernel */
@@ -305,6 +422,16 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
     s = s < wl ? s : wl;
     S.slots[k] = s;
     if (s == 0) infeasible = 1;
+  }
+  /* R15: clusters and REMOTE nodes need a NoC that can place them */
+  for (uint32_t k = 0; k < S.K && !infeasible; k++) {
+    uint32_t cl = kernel_cluster[k];
+    int remote = 0;
+    for (uint32_t v = cta_node_begin[kernel_cta_begin[k]]; v < cta_node_begin[kernel_cta_begin[k + 1]]; v++)
+      if (op_cls[node_op[v]] == K_REMOTE) remote = 1;
+    if (cl == 1 && !remote) continue;
+    uint64_t sm_of_rank[16];
+    if (S.noc_d == 0 || cl > S.noc_d || !place_cluster(&S, k, cl, 0, sm_of_rank)) infeasible = 1;
   }
   if (infeasible) {
     *out_status = ST_INFEASIBLE; *out_makespan = 0xFFFFFFFFu;
@@ -331,6 +458,9 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
       S.lat[p] = hw[HW_LAT + 3];
     } else if (cls == K_SYNC) {
       S.lat[p] = max64(1, hw[HW_LAT + 6]);
+    } else if (cls == K_REMOTE) {
+      S.occ[p] = hw[HW_NOC_RATE] ? max64(1, cdiv(w * 65536ull, hw[HW_NOC_RATE])) : 1;
+      S.lat[p] = hw[HW_NOC_LAT];
     } else {
       int dram = (op_flags[p] & 1) != 0;
       S.to_dram[p] = dram;
@@ -355,6 +485,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   }
   ALLOC(S.resident, S.nsm); ALLOC(S.lane_av, (uint64_t)S.nsm * 3 * S.nsub);
   ALLOC(S.smem_av, S.nsm); ALLOC(S.eng_av, S.nsm);
+  ALLOC(S.noc_av, S.noc_d ? ((uint64_t)S.nsm + S.noc_d) / S.noc_d * S.noc_d * 4 : 1);
   ALLOC(S.kstart, S.K);
   for (uint32_t k = 0; k < S.K; k++) S.kstart[k] = -1;
   ALLOC(S.heap.a, (uint64_t)S.N + S.C);
@@ -407,5 +538,6 @@ done:
   free(S.indeg); free(S.cnt); free(S.node_cta); free(S.acc); free(S.st); free(S.fin);
   free(S.cta_sm); free(S.cta_launch); free(S.cta_left); free(S.cta_maxfin); free(S.cta_kernel);
   free(S.resident); free(S.lane_av); free(S.smem_av); free(S.eng_av); free(S.kstart); free(S.heap.a);
+  free(S.noc_av);
   return rc;
 }

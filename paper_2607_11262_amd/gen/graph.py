@@ -5,7 +5,10 @@ carries an execution group (a warp mask within its CTA), an operation
 descriptor (resource class + work) and, reduced to what the timing model
 reads, a tile descriptor (bytes / FLOPs and whether the access misses L2).
 Edges are DATA (producer -> consumer), ORDER (program order of one warp) or
-SYNC (cross-warp signal/wait, barrier, buffer reuse).
+SYNC (cross-warp signal/wait, barrier, buffer reuse).  A kernel's CTAs may
+form thread-block clusters (consecutive CTAs, dispatched together onto one
+NoC domain); a REMOTE node moves bytes to another CTA of its cluster, whose
+rank sits in the op flags (Sec. 5.2 DSMEM / SM-cluster NoC).
 
 Descriptors are dictionary-encoded: ``ops`` lists the distinct
 (class, flags, work, warp_mask) tuples and every node stores an op index.
@@ -19,10 +22,16 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-TENSOR, ALU, SFU, SMEM, GLOAD, GSTORE, SYNC = range(7)
-CLASS_NAMES = ("TENSOR", "ALU", "SFU", "SMEM", "GLOAD", "GSTORE", "SYNC")
+TENSOR, ALU, SFU, SMEM, GLOAD, GSTORE, SYNC, REMOTE = range(8)
+CLASS_NAMES = ("TENSOR", "ALU", "SFU", "SMEM", "GLOAD", "GSTORE", "SYNC", "REMOTE")
 COMPUTE_CLASSES = (TENSOR, ALU, SFU)
 MISS = 1
+RANK_SHIFT = 4      # REMOTE ops: target rank = flags >> RANK_SHIFT
+MAX_CLUSTER = 16
+
+
+def remote_flags(rank: int) -> int:
+    return int(rank) << RANK_SHIFT
 
 DATA, ORDER, SYNC_EDGE = 0, 1, 2
 KIND_SHIFT = 30
@@ -48,6 +57,12 @@ class TileGraph:
     kernel_smem: np.ndarray       # u32 [K]
     name: str = "graph"
     meta: dict = field(default_factory=dict)
+    kernel_cluster: np.ndarray = None  # u8 [K] CTAs per cluster (None: all 1)
+
+    def __post_init__(self):
+        if self.kernel_cluster is None:
+            self.kernel_cluster = np.ones(int(self.kernel_warps.shape[0]), dtype=np.uint8)
+        self.kernel_cluster = np.asarray(self.kernel_cluster, dtype=np.uint8)
 
     @property
     def n_nodes(self) -> int:
@@ -93,13 +108,15 @@ class TileGraph:
         for a in (self.op_cls, self.op_flags, self.op_work, self.op_warps, self.node_op, self.succ_ptr,
                   self.succ, self.cta_node_begin, self.kernel_cta_begin, self.kernel_warps, self.kernel_smem):
             h.update(np.ascontiguousarray(a).tobytes())
+        if np.any(self.kernel_cluster != 1):
+            h.update(np.ascontiguousarray(self.kernel_cluster).tobytes())
         return h.hexdigest()
 
     def arrays(self) -> dict:
         return dict(op_cls=self.op_cls, op_flags=self.op_flags, op_work=self.op_work, op_warps=self.op_warps,
                     node_op=self.node_op, succ_ptr=self.succ_ptr, succ=self.succ,
                     cta_node_begin=self.cta_node_begin, kernel_cta_begin=self.kernel_cta_begin,
-                    kernel_warps=self.kernel_warps, kernel_smem=self.kernel_smem)
+                    kernel_warps=self.kernel_warps, kernel_smem=self.kernel_smem, kernel_cluster=self.kernel_cluster)
 
 
 class OpTable:
@@ -163,17 +180,19 @@ class GraphBuilder:
         self.kernel_begin: list = [0]
         self.kernel_warps: list = []
         self.kernel_smem: list = []
+        self.kernel_cluster: list = []
         self.src: list = []
         self.dst: list = []
         self.kind: list = []
         self._open_cta = False
 
-    def kernel(self, warps: int, smem: int = 0):
+    def kernel(self, warps: int, smem: int = 0, cluster: int = 1):
         self._close_cta()
         if self.kernel_warps:
             self.kernel_begin.append(len(self.cta_begin) - 1)
         self.kernel_warps.append(int(warps))
         self.kernel_smem.append(int(smem))
+        self.kernel_cluster.append(int(cluster))
         return len(self.kernel_warps) - 1
 
     def cta(self):
@@ -211,7 +230,8 @@ class GraphBuilder:
                          cta_node_begin=np.array(self.cta_begin, dtype=np.uint32),
                          kernel_cta_begin=np.array(kb, dtype=np.uint32),
                          kernel_warps=np.array(self.kernel_warps, dtype=np.uint16),
-                         kernel_smem=np.array(self.kernel_smem, dtype=np.uint32), name=name)
+                         kernel_smem=np.array(self.kernel_smem, dtype=np.uint32), name=name,
+                         kernel_cluster=np.array(self.kernel_cluster, dtype=np.uint8))
 
 
 def empty_graph() -> TileGraph:
@@ -244,13 +264,23 @@ def validate(g: TileGraph) -> None:
         raise ValidationError("kernel warps out of range")
     if np.any(g.node_op >= P):
         raise ValidationError("node op out of range")
-    if np.any(g.op_cls > SYNC):
+    if np.any(g.op_cls > REMOTE):
         raise ValidationError("op class out of range")
+    cl = g.kernel_cluster.astype(np.int64)
+    if cl.shape[0] != K or np.any(cl < 1) or np.any(cl > MAX_CLUSTER) or np.any(np.diff(kb) % cl != 0):
+        raise ValidationError("cluster sizes must be 1..16 and divide each kernel's CTA count")
+    remote = g.op_cls == REMOTE
+    if np.any(remote & ((g.op_flags & ((1 << RANK_SHIFT) - 1)) != 0)):
+        raise ValidationError("REMOTE op with flags other than the rank")
     compute = np.isin(g.op_cls, COMPUTE_CLASSES)
     if np.any(compute & (g.op_warps == 0)):
         raise ValidationError("compute op with empty warp mask")
     node_cta = g.node_cta()
     node_kernel = g.cta_kernel()[node_cta]
+    nrem = remote[g.node_op.astype(np.int64)]
+    rank = (g.op_flags.astype(np.int64) >> RANK_SHIFT)[g.node_op.astype(np.int64)]
+    if np.any(nrem & (rank >= cl[node_kernel])):
+        raise ValidationError("REMOTE target rank outside the cluster")
     warps_lim = g.kernel_warps.astype(np.int64)[node_kernel]
     mask = g.op_warps.astype(np.int64)[g.node_op.astype(np.int64)]
     ncomp = compute[g.node_op.astype(np.int64)]
@@ -261,8 +291,13 @@ def validate(g: TileGraph) -> None:
         raise ValidationError("edge target or kind out of range")
     if np.any(src == dst):
         raise ValidationError("self loop")
-    if np.any(node_cta[src] > node_cta[dst]):
-        raise ValidationError("edge from a later CTA to an earlier one")
+    # a cluster's CTAs are dispatched together: edges between them may go
+    # either way
+    ck = g.cta_kernel()
+    cluster_id = kb[ck] + (np.arange(C) - kb[ck]) // cl[ck] * cl[ck]  # first CTA of the cluster
+    back = node_cta[src] > node_cta[dst]
+    if np.any(back & (cluster_id[node_cta[src]] != cluster_id[node_cta[dst]])):
+        raise ValidationError("edge from a later CTA to an earlier one outside a cluster")
     if src.size:
         key = src * N + dst
         if np.unique(key).size != key.size:

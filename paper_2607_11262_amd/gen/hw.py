@@ -32,6 +32,7 @@ FIELDS = {
     "rate_dram": 11,
     "lat_tensor": 12, "lat_alu": 13, "lat_sfu": 14, "lat_smem": 15, "lat_l2": 16, "lat_dram": 17,
     "lat_sync": 18, "cta_launch_lat": 19, "kernel_launch_lat": 20,
+    "noc_nodes": 21, "noc_width": 22, "noc_rate": 23, "noc_lat": 24, "noc_map": 25,
 }
 NWORDS = 32
 

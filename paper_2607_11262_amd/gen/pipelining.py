@@ -167,7 +167,8 @@ def without_edges(g: TileGraph, kinds) -> TileGraph:
     return TileGraph(op_cls=g.op_cls, op_flags=g.op_flags, op_work=g.op_work, op_warps=g.op_warps,
                      node_op=g.node_op, succ_ptr=succ_ptr, succ=succ, cta_node_begin=g.cta_node_begin,
                      kernel_cta_begin=g.kernel_cta_begin, kernel_warps=g.kernel_warps, kernel_smem=g.kernel_smem,
-                     name=g.name + "_no_" + "_".join(names[k] for k in sorted(kinds)), meta=dict(g.meta))
+                     name=g.name + "_no_" + "_".join(names[k] for k in sorted(kinds)), meta=dict(g.meta),
+                     kernel_cluster=g.kernel_cluster)
 
 
 ABLATIONS = {"full": (), "no_order": (ORDER,), "no_sync": (SYNC_EDGE,), "data_only": (ORDER, SYNC_EDGE)}

@@ -29,11 +29,12 @@ import os
 import numpy as np
 
 from paper_2607_11262_amd.gen import hw as H
-from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, ORDER, SFU, SMEM, SYNC, SYNC_EDGE, TENSOR,
-                                             GraphBuilder)
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, ORDER, REMOTE, SFU, SMEM, SYNC, SYNC_EDGE,
+                                             TENSOR, GraphBuilder, remote_flags)
 
 MAXCYC = 0xFFFFFFFE
-CLASS = {"TENSOR": TENSOR, "ALU": ALU, "SFU": SFU, "SMEM": SMEM, "GLOAD": GLOAD, "GSTORE": GSTORE, "SYNC": SYNC}
+CLASS = {"TENSOR": TENSOR, "ALU": ALU, "SFU": SFU, "SMEM": SMEM, "GLOAD": GLOAD, "GSTORE": GSTORE, "SYNC": SYNC,
+         "REMOTE": REMOTE}
 KIND = {"D": DATA, "O": ORDER, "S": SYNC_EDGE}
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_schedules.json")
 
@@ -60,6 +61,10 @@ def durations(g, rec):
             out.append(dict(kind="smem", occ=max(1, cdiv(work * 65536, rates[3])), lat=lats[3]))
         elif cls == SYNC:
             out.append(dict(kind="sync", lat=max(1, lats[6])))
+        elif cls == REMOTE:
+            rate = H.get(rec, "noc_rate")
+            out.append(dict(kind="remote", occ=max(1, cdiv(work * 65536, rate)) if rate else 1,
+                            lat=H.get(rec, "noc_lat"), rank=int(g.op_flags[p]) >> 4))
         else:
             out.append(dict(kind="gmem", occ=max(1, cdiv(work * 65536, rates[4])),
                             occ_m=max(1, cdiv(work * 65536, rates[6] if miss else rates[5])),
@@ -107,8 +112,9 @@ def verify_schedule(g, rec, flags, cycles, cta):
     ops = g.node_op.astype(np.int64)
     nsub = H.get(rec, "n_subpart")
     order = np.lexsort((np.arange(N), ready))  # FIFO (ready, id)
-    lane_av, smem_av, eng_av = {}, {}, {}
+    lane_av, smem_av, eng_av, noc_av = {}, {}, {}, {}
     gstart = {}
+    D, W = H.get(rec, "noc_nodes"), H.get(rec, "noc_width")
     for v in order:
         d = dur[ops[v]]
         sm = int(cta_sm[node_cta[v]])
@@ -125,6 +131,14 @@ def verify_schedule(g, rec, flags, cycles, cta):
             assert st[v] == s and fi[v] == s + d["occ"] + d["lat"], f"smem node {v}"
         elif d["kind"] == "sync":
             assert st[v] == r and fi[v] == r + d["lat"], f"sync node {v}"
+        elif d["kind"] == "remote":
+            c = int(node_cta[v])
+            target = cluster_first(g, c) + d["rank"]
+            servers, hops = noc_route(sm, int(cta_sm[target]), D, W)
+            s = r if nocont else max([r] + [noc_av.get(x, 0) for x in servers])
+            for x in servers:
+                noc_av[x] = s + d["occ"]
+            assert st[v] == s and fi[v] == s + d["occ"] + d["lat"] * hops, f"remote node {v}: {st[v], fi[v]} != {s}"
         else:
             s = r if nocont else max(r, eng_av.get(sm, 0))
             eng_av[sm] = s + d["occ"]
@@ -142,6 +156,64 @@ def verify_schedule(g, rec, flags, cycles, cta):
     exp_sm, exp_launch = dispatch_from_retires(g, rec, fi)
     assert np.array_equal(exp_sm, cta_sm), "CTA -> SM mapping"
     assert np.array_equal(exp_launch, launch), "CTA launch cycles"
+
+
+def cluster_first(g, c: int) -> int:
+    k = int(g.cta_kernel()[c])
+    kb, cl = int(g.kernel_cta_begin[k]), int(g.kernel_cluster[k])
+    return kb + (c - kb) // cl * cl
+
+
+def noc_route(src_sm: int, dst_sm: int, D: int, W: int):
+    """Servers a transfer between two SMs of one NoC domain holds, and the
+    latency multiplier: a crossbar's injection and ejection ports (one
+    traversal), or the mesh links of the dimension-order route, x first
+    (one latency per hop)."""
+    dom, a, b = src_sm // D, src_sm % D, dst_sm % D
+    assert dst_sm // D == dom
+    if W == 0:
+        return [("in", dom, a), ("out", dom, b)], 1
+    (x, y), (xb, yb) = (a % W, a // W), (b % W, b // W)
+    links = []
+    while x != xb:
+        step = 1 if xb > x else -1
+        links.append(("x", dom, x, y, step))
+        x += step
+    while y != yb:
+        step = 1 if yb > y else -1
+        links.append(("y", dom, x, y, step))
+        y += step
+    return links, len(links)
+
+
+def cluster_placements(rec, cl: int):
+    """Every placement of a cluster of cl CTAs, in the order dispatch tries
+    them: lists of SMs by rank, domain by domain; strips of consecutive
+    nodes, or (compact mapping on a mesh) the most square bw x bh blocks
+    that tile the mesh, row-major."""
+    D, W = H.get(rec, "noc_nodes"), H.get(rec, "noc_width")
+    nsm = H.get(rec, "n_sm")
+    shape = None
+    if H.get(rec, "noc_map") == 1 and W:
+        Hh = D // W
+        fits = [bh for bh in range(1, cl + 1) if cl % bh == 0 and bh * bh <= cl and W % (cl // bh) == 0
+                and Hh % bh == 0]
+        shape = (cl // max(fits), max(fits)) if fits else None
+    per_domain = []
+    if shape:
+        bw, bh = shape
+        for by in range(D // W // bh):
+            for bx in range(W // bw):
+                per_domain.append([(by * bh + r // bw) * W + bx * bw + r % bw for r in range(cl)])
+    else:
+        per_domain = [[j * cl + r for r in range(cl)] for j in range(D // cl)]
+    out = []
+    for d in range(-(-nsm // D)):
+        for nodes in per_domain:
+            sms = [d * D + n for n in nodes]
+            if all(s < nsm for s in sms):
+                out.append(sms)
+    return out
 
 
 def dispatch_from_retires(g, rec, finish):
@@ -169,6 +241,19 @@ def dispatch_from_retires(g, rec, finish):
             k = int(cta_kernel[nxt])
             if retired < kb[k]:
                 return
+            cl = int(g.kernel_cluster[k])
+            if cl > 1:  # a whole cluster on the first placement with room on each SM
+                fit = [p for p in cluster_placements(rec, cl) if all(resident[s] < slots[k] for s in p)]
+                if not fit:
+                    return
+                kstart.setdefault(k, t)
+                la = t + H.get(rec, "cta_launch_lat") + (H.get(rec, "kernel_launch_lat") if kstart[k] == t else 0)
+                for r, s in enumerate(fit[0]):
+                    sm_of[nxt + r], launch[nxt + r] = s, la
+                    resident[s] += 1
+                    pending.append((int(retire[nxt + r]), nxt + r))
+                nxt += cl
+                continue
             free = [slots[k] - resident[m] for m in range(nsm)]
             best = max(range(nsm), key=lambda m: (free[m], -m))
             if free[best] <= 0:
@@ -229,11 +314,13 @@ def load_golden():
         src = cases[c["same_graph_as"]] if "same_graph_as" in c else c
         b = GraphBuilder()
         for k in src["kernels"]:
-            b.kernel(k["warps"], k["smem"])
+            b.kernel(k["warps"], k["smem"], k.get("cluster", 1))
             for cta in k["ctas"]:
                 b.cta()
-                for cls, work, warps, miss in cta:
-                    b.node(CLASS[cls], work, warps, 1 if miss else 0)
+                for cls, work, warps, extra in cta:
+                    # fourth field: the L2-miss flag, or a REMOTE node's target rank
+                    flags = remote_flags(extra) if cls == "REMOTE" else (1 if extra else 0)
+                    b.node(CLASS[cls], work, warps, flags)
         for u, v, kd in src["edges"]:
             b.edge(u, v, KIND[kd])
         g = b.build(c["name"])

@@ -24,7 +24,7 @@ MUTANTS = [
     ("lane_is_warp_div_nsub", "lanes |= 1u << (wp % S.nsub)", "lanes |= 1u << (wp / S.nsub % S.nsub)", False),
     ("dispatch_tie_highest_sm", "if (fr > bestfree) { bestfree = fr; best = m; }",
      "if (fr >= bestfree && fr > 0) { bestfree = fr; best = m; }", False),
-    ("no_kernel_launch_latency", "launch += S->hw[HW_KLAT];", ";", False),
+    ("no_kernel_launch_latency", "launch += S->hw[HW_KLAT];", ";", True),
     ("misses_served_by_l2", "S.to_dram[p] = dram;", "S.to_dram[p] = 0;", False),
     ("gmem_finish_ignores_engine", "max64(s + S->occ[p], m + S->occm[p])", "(m + S->occm[p])", False),
     ("ready_ignores_launch", "mkkey(max64(S->acc[w], S->cta_launch[c]), EV_READY, w)", "mkkey(S->acc[w], EV_READY, w)",
@@ -43,12 +43,20 @@ MUTANTS = [
     ("residency_ignores_smem", "if (kernel_smem[k]) s =", "if (0) s =", False),
     ("compute_classes_share_lanes", "uint64_t *lanes = S->lane_av + (sm * 3 + cls) * S->nsub;",
      "uint64_t *lanes = S->lane_av + sm * 3 * S->nsub;", False),
+    ("mesh_routes_y_first", "while (x != xb) { uint32_t dir = xb > x ? 0 : 1; route[nr++] = &dav[(y * W + x) * 4 + dir]; x = dir == 0 ? x + 1 : x - 1; }\n      while (y != yb) { uint32_t dir = yb > y ? 2 : 3; route[nr++] = &dav[(y * W + x) * 4 + dir]; y = dir == 2 ? y + 1 : y - 1; }",
+     "while (y != yb) { uint32_t dir = yb > y ? 2 : 3; route[nr++] = &dav[(y * W + x) * 4 + dir]; y = dir == 2 ? y + 1 : y - 1; }\n      while (x != xb) { uint32_t dir = xb > x ? 0 : 1; route[nr++] = &dav[(y * W + x) * 4 + dir]; x = dir == 0 ? x + 1 : x - 1; }", False),
+    ("crossbar_without_ejection_port", "route[nr++] = &dav[b * 4 + 1];", ";", False),
+    ("mesh_latency_once", "      lat_mult = nr;\n", "", False),
+    ("placement_ignores_mapping", "if (S->hw[HW_NOC_MAP] == 1 && W > 0) {", "if (0) {", False),
+    ("cluster_dispatched_like_single_ctas", "    if (cl > 1) {                                        /* R13: a whole cluster */",
+     "    if (0) {", False),
+    ("remote_target_rank_ignored", "uint32_t tgt = kb + (c - kb) / cl * cl + (S->op_flags[p] >> 4);", "uint32_t tgt = c;", False),
     ("multi_lane_uses_first_lane", "if (S->lanes[p] >> l & 1) s = max64(s, lanes[l]);",
      "if (S->lanes[p] >> l & 1) { s = max64(s, lanes[l]); break; }", False),
     ("smem_latency_dropped", "if (!complete(S, v, s, s + S->occ[p] + S->lat[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)",
      "if (!complete(S, v, s, s + S->occ[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)", False),
     ("sync_node_zero_latency_allowed", "S.lat[p] = max64(1, hw[HW_LAT + 6]);", "S.lat[p] = hw[HW_LAT + 6];", False),
-    ("cta_launch_latency_dropped", "uint64_t launch = t + S->hw[HW_CTALAT];", "uint64_t launch = t;", False),
+    ("cta_launch_latency_dropped", "uint64_t launch = t + S->hw[HW_CTALAT];", "uint64_t launch = t;", True),
 ]
 
 

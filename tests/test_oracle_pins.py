@@ -18,9 +18,10 @@ import pytest
 
 import oracle
 import refcheck
+from clustered import clustered_graph, noc_machine
 from paper_2607_11262_amd.gen import hw as H
 from paper_2607_11262_amd.gen import workloads as W
-from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, SFU, SMEM, SYNC, TENSOR, GraphBuilder,
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, REMOTE, SFU, SMEM, SYNC, TENSOR, GraphBuilder,
                                              empty_graph, validate)
 from paper_2607_11262_amd.gen.rng import SplitMix64
 
@@ -141,6 +142,37 @@ def test_verifier_random(seed):
     assert r.status == 0
     refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
     assert r.makespan == int(r.cycles[:, 1].max()) if g.n_nodes else 0
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_verifier_clusters(seed):
+    """Clusters and REMOTE nodes (R13-R15): placement re-derived from the
+    retire cycles, every transfer's start from its route's FIFO servers."""
+    rng = SplitMix64(seed, 15)
+    g = clustered_graph(rng)
+    validate(g)
+    rec = noc_machine(rng)
+    flags = rng.choice([0, 0, 0, 4, 8])
+    r = oracle.simulate(g, rec, flags, want_cta=True)
+    D = H.get(rec, "noc_nodes")
+    placeable = True
+    for k in range(g.n_kernels):
+        cl = int(g.kernel_cluster[k])
+        nodes = g.node_op[g.cta_node_begin[g.kernel_cta_begin[k]]:g.cta_node_begin[g.kernel_cta_begin[k + 1]]]
+        if cl > 1 or np.any(g.op_cls[nodes] == REMOTE):
+            placeable &= D > 0 and cl <= D and bool(refcheck.cluster_placements(rec, cl))
+    if min(refcheck.slots_per_kernel(g, rec)) == 0 or not placeable:
+        assert r.status == 1
+        return
+    assert r.status == 0
+    refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+    # a cluster's CTAs share a launch cycle and sit on distinct SMs of one domain
+    for k in range(g.n_kernels):
+        cl = int(g.kernel_cluster[k])
+        for c0 in range(int(g.kernel_cta_begin[k]), int(g.kernel_cta_begin[k + 1]), cl):
+            sms = r.cta[c0:c0 + cl, 0].astype(np.int64)
+            assert len(set(sms.tolist())) == cl and len(set((sms // D).tolist())) == 1
+            assert len(set(r.cta[c0:c0 + cl, 1].tolist())) == 1
 
 
 def _small_workloads():
