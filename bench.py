@@ -25,6 +25,17 @@ simulated under 4096 seeded single-SM Hopper machines (tensor rate 0.5-4x,
 DRAM 1.5-8 TB/s, TMA 50-200 B/cycle); its line adds the case-study table
 (normalised performance and Tensor Core utilisation per organisation at
 Table 3's H100 with FP8 rate), read off GPU timelines.
+
+    python bench.py --workload noc
+
+runs the NoC-enabled fusion case study (Sec. 7.2): the cluster-fused
+attention block (32 heads, one cluster per head, clusters of 2-16 CTAs,
+communication over the SM-cluster NoC or through DRAM; 8 graphs of
+12K-61K nodes), each under 4096 seeded H100 machines with a 16-SM-domain
+crossbar or 4 x 4 mesh NoC (any of three placements, port bandwidth 8-64
+B/cycle, latency 60-400 cycles, DRAM 1.5-8 TB/s, tensor 0.5-4x); its line
+adds the case-study table (NoC vs DRAM cycles and mean NoC residence per
+topology and placement) read off GPU timelines.
 """
 from __future__ import annotations
 
@@ -82,7 +93,7 @@ def recorded_traffic(n_launch: int):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining"), default="gemm_design_sweep")
+    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining", "noc"), default="gemm_design_sweep")
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
@@ -106,6 +117,7 @@ def main() -> int:
     import torch
 
     from paper_2607_11262_amd import api
+    from paper_2607_11262_amd.gen import clusterfusion as CF
     from paper_2607_11262_amd.gen import pipelining as PL
     from paper_2607_11262_amd.gen import workloads as W
 
@@ -127,7 +139,17 @@ def main() -> int:
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(max(1, args.streams) - 1)]
 
     pipelining = args.workload == "pipelining"
-    if pipelining:
+    noc = args.workload == "noc"
+    noc_graphs = [(S, comm) for S in CF.CLUSTER_SIZES for comm in CF.COMMS]
+    if noc:
+        n_graphs = len(noc_graphs)
+
+        def make(gi):
+            return CF.cluster_attention(noc_graphs[gi][0], comm=noc_graphs[gi][1]), CF.sample_noc_machines(gi, B_PER_GRAPH)
+
+        def describe(gi):
+            return noc_graphs[gi]
+    elif pipelining:
         n_graphs = len(PL.case_study_graphs())
 
         def make(gi):
@@ -223,7 +245,7 @@ def main() -> int:
     # over the timed region) is higher and is reported beside it.
     achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
     aggregate_gbs = float(abytes.sum() / elapsed / 1e9)
-    traffic = None if pipelining else recorded_traffic(len(launches))
+    traffic = None if (pipelining or noc) else recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
     cpu = None
@@ -280,7 +302,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_over_algorithmic": (traffic / float(abytes.mean())) if traffic else None,
-                     "kernel": "gts_sim_window", "launches": len(launches),
+                     "kernel": "gts_sim_wave" if noc else "gts_sim_window", "launches": len(launches),
                      "mean_launch_ms": float(durs.mean() * 1e3),
                      "streams": len(streams), "aggregate_gbs": aggregate_gbs,
                      "aggregate_frac": aggregate_gbs / HBM_PEAK_GBS},
@@ -290,8 +312,37 @@ def main() -> int:
     }
     if pipelining:
         out["case_study"] = case_study(api, torch, PL)
+    if noc:
+        out["case_study"] = noc_case_study(api, torch, CF)
     print(json.dumps(out))
     return 0
+
+
+def noc_case_study(api, torch, CF):
+    """Sec. 7.2 table from GPU timelines on Table 3's H100 with a 16-node
+    crossbar or a 4 x 4 mesh of the same total bandwidth and mean latency:
+    per cluster size, kernel cycles with NoC and with DRAM communication,
+    and the mean NoC residence of a request per topology and placement."""
+    from paper_2607_11262_amd import timeline as TL
+    topos = (("crossbar", "strips"), ("mesh", "strips"), ("mesh", "blocks"), ("mesh", "strided"))
+    recs = np.stack([CF.noc_h100(t, m) for t, m in topos])
+    table = {}
+    for S in CF.CLUSTER_SIZES:
+        row = {}
+        for comm in CF.COMMS:
+            g = CF.cluster_attention(S, comm=comm)
+            res = api.simulate(api.upload(g), recs, api.OUT_NODES | api.OUT_DIGEST)
+            torch.cuda.synchronize()
+            cyc, mk, st, _ = api.to_numpy(res)
+            for i, (t, m) in enumerate(topos):
+                key = f"{t}-{m}"
+                row.setdefault(key, {})[f"cycles_{comm}"] = int(mk[i])
+                if comm == "noc":
+                    row[key]["noc_residence"] = round(TL.noc_residence(g, cyc[i]), 1)
+        for key in row:
+            row[key]["noc_speedup_vs_dram"] = round(row[key]["cycles_dram"] / row[key]["cycles_noc"], 4)
+        table[f"cluster{S}"] = row
+    return table
 
 
 def case_study(api, torch, PL):

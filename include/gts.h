@@ -144,7 +144,8 @@ typedef struct gts_hw_params {
   uint32_t noc_lat;          /* crossbar traversal / mesh per-hop cycles,
                                 <= 2^24                                      */
   uint32_t noc_map;          /* cluster placement: 0 strips of consecutive
-                                nodes, 1 compact blocks (mesh)               */
+                                nodes, 1 compact blocks (mesh), 2 strided
+                                (ranks noc_nodes / cluster nodes apart)      */
   uint32_t reserved[6];      /* must be zero                                 */
 } gts_hw_params;
 

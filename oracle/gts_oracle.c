@@ -80,7 +80,9 @@
  *      divisor of cl with bh*bh <= cl such that bw = cl / bh divides W and
  *      bh divides H: block j in row-major block order, rank r at
  *      x = (j mod (W/bw))*bw + r mod bw, y = (j div (W/bw))*bh + r div bw;
- *      without such a shape, or on a crossbar, strips.
+ *      without such a shape, or on a crossbar, strips; strided (noc_map 2),
+ *      node(j, r) = j + r * (D / cl) for j < D / cl (ranks spread over the
+ *      domain, as a placement that ignores the topology would).
  *  R14 REMOTE nodes (Sec. 5.2 DSMEM over the SM-cluster NoC; the target is
  *      carried by the node): target CTA = first CTA of the source's cluster
  *      + rank (op flags >> 4); route from node a (source SM) to node b
@@ -250,6 +252,7 @@ static int64_t slot_node(const sim_t *S, uint32_t cl, uint32_t j, uint32_t r) {
     }
   }
   if (j >= D / cl) return -1;
+  if (S->hw[HW_NOC_MAP] == 2) return (int64_t)j + (int64_t)r * (D / cl);
   return (int64_t)j * cl + r;
 }
 

@@ -89,6 +89,11 @@ __device__ uint4 op_entry(const OpDev& o, const uint32_t* hw, uint32_t props) {
   } else if (o.cls == C_SYNC) {
     const uint32_t l = hw[HW_LAT + L_SYNC];
     e.z = l < 1 ? 1 : l;
+  } else if (o.cls == C_REMOTE) {  // x = NoC occupancy, z = latency per traversal / hop, w: rank << 16
+    const uint32_t rate = hw[HW_NOC_RATE];
+    e.x = rate ? clamp_occ(cdiv64(work * 65536ull, rate)) : 1u;
+    e.z = hw[HW_NOC_LAT];
+    e.w |= (uint32_t)(o.flags >> GTS_OPF_RANK_SHIFT) << 16;
   } else {
     const uint32_t dram = o.flags & GTS_OPF_MISS;
     e.x = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + R_GMEM]));

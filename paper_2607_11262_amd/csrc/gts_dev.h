@@ -22,6 +22,8 @@ constexpr uint32_t kGraphComputeFeedsData = 16u;  // every non-memory node has a
                                                   // SYNC out-edge inside its CTA
 constexpr uint32_t kGraphClassShift = 5u;         // bits 5-7: the op table has TENSOR /
                                                   // ALU / SFU ops (one bit per class)
+constexpr uint32_t kGraphClusters = 256u;         // some kernel has clusters of more than
+                                                  // one CTA or REMOTE nodes
 
 // Compute pipelines: every subpartition of an SM has one lane per compute
 // class.  Server state holds lanes only for the classes a graph uses, class
@@ -74,13 +76,16 @@ constexpr uint32_t kCtaShared = 0x80000000u;
 // for a first-touch tile): each CTA has a class, and the op of slot s in
 // class q is tops[t_ops + q * t_nslot + s].  The expanded records stay in the
 // image for the general kernel.
-struct KernelDev {              // 32 B, one per kernel
+struct KernelDev {              // 48 B, one per kernel
   uint32_t cta_begin, cta_end, warps, smem;
   uint32_t node_begin;          // first node of the kernel
   uint32_t t_n;                 // nodes per CTA if templated, else 0
   uint32_t t_base;              // first template record (and in-degree) of the kernel
   uint32_t t_ops;               // tops offset (low 16) | slots per class (high 16)
+  uint32_t cluster;             // CTAs per cluster | kKernelRemote
+  uint32_t pad[3];
 };
+constexpr uint32_t kKernelRemote = 0x10000u;  // the kernel has REMOTE nodes
 constexpr uint32_t kMaxTops = 128;   // class x slot op entries per graph (held in LDS)
 
 // Device-side view passed to kernels by value.
@@ -107,7 +112,8 @@ enum : uint32_t {
 };
 enum : uint32_t { R_TENSOR = 0, R_ALU, R_SFU, R_SMEM, R_GMEM, R_L2, R_DRAM };
 enum : uint32_t { L_TENSOR = 0, L_ALU, L_SFU, L_SMEM, L_L2, L_DRAM, L_SYNC };
-enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC };
+enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC, C_REMOTE };
+enum : uint32_t { HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25 };
 // Device-image edge encoding: target | bits << 30.  DATA and SYNC edges time
 // identically (released at the source's finish) and share bit pattern 0;
 // bit 30 marks an ORDER edge (released at the source's start + 1), bit 31 an
@@ -167,6 +173,7 @@ struct Launch {
   uint32_t max_nsm;            // largest n_sm of the batch
   uint32_t max_nsub;           // largest n_subpart of the batch
   uint32_t qp;                 // windowed kernel: later ready entries per lane held in LDS
+  uint32_t noc_words;          // general kernel: NoC server words after the per-SM servers
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on

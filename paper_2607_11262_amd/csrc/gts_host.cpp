@@ -29,7 +29,7 @@ struct gts_graph {
 
 struct gts_hwset {
   const uint32_t* dev;  // [B][32] in the caller's device buffer
-  uint32_t B, max_nsm, max_nsub;
+  uint32_t B, max_nsm, max_nsub, max_noc;
 };
 
 namespace {
@@ -49,6 +49,7 @@ int fail(int code, const char* fmt, ...) {
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
 bool is_compute(uint8_t c) { return c <= gts::C_SFU; }
+uint32_t cluster_of(const gts_graph_host* h, uint32_t k) { return h->kernel_cluster ? h->kernel_cluster[k] : 1u; }
 bool is_memory(uint8_t c) { return c == gts::C_GLOAD || c == gts::C_GSTORE; }
 
 // A kernel whose CTAs share one template of node records.
@@ -91,7 +92,7 @@ void find_templates(const gts_graph_host* h, Derived* d) {
   for (uint32_t k = 0; k < K; ++k) {
     const uint32_t c0 = h->kernel_cta_begin[k], c1 = h->kernel_cta_begin[k + 1];
     const uint32_t n = nb[c0 + 1] - nb[c0];
-    if (c1 - c0 < 2) continue;
+    if (c1 - c0 < 2 || cluster_of(h, k) > 1) continue;
     bool ok = true;
     for (uint32_t c = c0; c < c1 && ok; ++c) ok = nb[c + 1] - nb[c] == n;
     // identical local structure, every edge inside its CTA, no shared node
@@ -184,6 +185,10 @@ int check_graph(const gts_graph_host* h, Derived* d) {
     if (h->kernel_cta_begin[k + 1] <= h->kernel_cta_begin[k]) return fail(GTS_E_RANGE, "kernel %u has no CTA", k);
     if (h->kernel_warps[k] < 1 || h->kernel_warps[k] > GTS_MAX_WARPS)
       return fail(GTS_E_RANGE, "kernel %u has %u warps per CTA (1..%u)", k, h->kernel_warps[k], GTS_MAX_WARPS);
+    const uint32_t cl = cluster_of(h, k);
+    if (cl < 1 || cl > GTS_MAX_CLUSTER || (h->kernel_cta_begin[k + 1] - h->kernel_cta_begin[k]) % cl)
+      return fail(GTS_E_RANGE, "kernel %u has clusters of %u CTAs (1..%u, dividing its CTA count)", k, cl,
+                  GTS_MAX_CLUSTER);
   }
   if (h->cta_node_begin[0] != 0 || h->cta_node_begin[C] != N)
     return fail(GTS_E_RANGE, "cta_node_begin must run from 0 to n_nodes");
@@ -195,7 +200,8 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   // ops
   for (uint32_t p = 0; p < P; ++p) {
     if (h->op_cls[p] >= GTS_N_CLASSES) return fail(GTS_E_RANGE, "op %u has class %u", p, h->op_cls[p]);
-    if (h->op_flags[p] & ~GTS_OPF_MISS) return fail(GTS_E_RANGE, "op %u has unknown flags 0x%x", p, h->op_flags[p]);
+    const uint32_t allowed = h->op_cls[p] == GTS_REMOTE ? 0xF0u : GTS_OPF_MISS;
+    if (h->op_flags[p] & ~allowed) return fail(GTS_E_RANGE, "op %u has unknown flags 0x%x", p, h->op_flags[p]);
     if (is_compute(h->op_cls[p]) && h->op_warps[p] == 0)
       return fail(GTS_E_RANGE, "compute op %u has an empty warp mask", p);
   }
@@ -216,6 +222,16 @@ int check_graph(const gts_graph_host* h, Derived* d) {
       if (w < 32 && (h->op_warps[p] >> w) != 0)
         return fail(GTS_E_RANGE, "node %u runs on warps 0x%x outside its %u-warp CTA", v, h->op_warps[p], w);
     }
+    if (h->op_cls[p] == GTS_REMOTE && (uint32_t)(h->op_flags[p] >> GTS_OPF_RANK_SHIFT) >=
+                                          cluster_of(h, cta_kernel[node_cta[v]]))
+      return fail(GTS_E_RANGE, "node %u targets rank %u outside its cluster", v, h->op_flags[p] >> GTS_OPF_RANK_SHIFT);
+  }
+  // first CTA of each CTA's cluster (clusters are dispatched together, so
+  // edges between their CTAs may go either way)
+  std::vector<uint32_t> cluster_first(C);
+  for (uint32_t c = 0; c < C; ++c) {
+    const uint32_t k = cta_kernel[c], kb = h->kernel_cta_begin[k], cl = cluster_of(h, k);
+    cluster_first[c] = kb + (c - kb) / cl * cl;
   }
   // edges: range, self loops, CTA order, duplicates, in-degree
   std::vector<uint32_t> indeg(N, 0), stamp(N, 0xFFFFFFFFu), intra_in(N, 0);
@@ -229,7 +245,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
       if (kind > GTS_EDGE_SYNC) return fail(GTS_E_RANGE, "edge %u has kind %u", e, kind);
       if (v >= N) return fail(GTS_E_RANGE, "edge %u targets node %u of %u", e, v, N);
       if (v == u) return fail(GTS_E_CYCLE, "self loop on node %u", u);
-      if (node_cta[u] > node_cta[v])
+      if (node_cta[u] > node_cta[v] && cluster_first[node_cta[u]] != cluster_first[node_cta[v]])
         return fail(GTS_E_EDGE_ORDER, "edge %u -> %u goes from CTA %u back to CTA %u", u, v, node_cta[u], node_cta[v]);
       if (stamp[v] == u) return fail(GTS_E_DUP, "duplicate edge %u -> %u", u, v);
       stamp[v] = u;
@@ -288,11 +304,16 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   bool any_shared = false;
   for (uint32_t v = 0; v < N && !any_shared; ++v) any_shared = d->shared[v] != 0;
   uint32_t classes = 0;
-  for (uint32_t p = 0; p < P; ++p)
+  bool clusters = false;
+  for (uint32_t p = 0; p < P; ++p) {
     if (is_compute(h->op_cls[p])) classes |= 1u << h->op_cls[p];
+    if (h->op_cls[p] == GTS_REMOTE) clusters = true;
+  }
+  for (uint32_t k = 0; k < K; ++k) clusters |= cluster_of(h, k) > 1;
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
              (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
-             (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift;
+             (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift |
+             (clusters ? gts::kGraphClusters : 0u);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   find_templates(h, d);
@@ -371,7 +392,18 @@ int check_hw(const gts_hw_params* hw, uint32_t index) {
   }
   if (hw->cta_launch_lat > (1u << 30) || hw->kernel_launch_lat > (1u << 30))
     return fail(GTS_E_HW, "hw[%u] launch latency exceeds 2^30", index);
-  for (int i = 0; i < 11; ++i)
+  if (hw->noc_nodes > GTS_MAX_NOC) return fail(GTS_E_HW, "hw[%u].noc_nodes = %u (0..%u)", index, hw->noc_nodes, GTS_MAX_NOC);
+  if (hw->noc_nodes) {
+    if (hw->noc_width > hw->noc_nodes || (hw->noc_width && hw->noc_nodes % hw->noc_width))
+      return fail(GTS_E_HW, "hw[%u].noc_width = %u does not divide noc_nodes = %u", index, hw->noc_width,
+                  hw->noc_nodes);
+    if (hw->noc_rate_q16 == 0) return fail(GTS_E_HW, "hw[%u].noc_rate_q16 is zero", index);
+  } else if (hw->noc_width || hw->noc_rate_q16 || hw->noc_map) {
+    return fail(GTS_E_HW, "hw[%u] sets NoC fields without noc_nodes", index);
+  }
+  if (hw->noc_lat > (1u << 24)) return fail(GTS_E_HW, "hw[%u].noc_lat = %u exceeds 2^24", index, hw->noc_lat);
+  if (hw->noc_map > 2) return fail(GTS_E_HW, "hw[%u].noc_map = %u (0 strips, 1 blocks, 2 strided)", index, hw->noc_map);
+  for (int i = 0; i < 6; ++i)
     if (hw->reserved[i]) return fail(GTS_E_HW, "hw[%u].reserved[%d] is not zero", index, i);
   return GTS_OK;
 }
@@ -396,12 +428,15 @@ int check_sim_args(const gts_graph* g, uint32_t B, const uint32_t* out_cycles, c
 // whose CTAs end in memory nodes and whose cross-CTA edges leave memory
 // nodes go to the windowed kernel first; simulations it cannot finish within
 // its queue capacities (and every other graph) run on the general kernel.
-int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_nsm, uint32_t max_nsub,
+int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc,
            uint32_t* out_cycles, uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, uint8_t* sims,
            uint32_t flags, hipStream_t st) {
   constexpr uint32_t kLdsBudget = 64 * 1024;
   const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
-  const uint32_t server_bytes = 4u * (max_nsm * sstride + max_nsm);
+  // NoC servers (four per domain node) follow the per-SM servers: at most
+  // ceil(n_sm / D) * D <= n_sm + D nodes
+  const uint32_t noc_words = (g->img.props & gts::kGraphClusters) && max_noc ? 4u * (max_nsm + max_noc) : 0u;
+  const uint32_t server_bytes = 4u * (max_nsm * sstride + max_nsm + noc_words);
   const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
   const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
   const uint32_t lds_general = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
@@ -421,11 +456,13 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.retry_only = 0;
   L.max_nsm = max_nsm;
   L.max_nsub = max_nsub;
+  L.noc_words = noc_words;
   L.qp = 0;
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
-  bool windowed = (g->img.props & need_props) == need_props && g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
+  bool windowed = (g->img.props & need_props) == need_props && !(g->img.props & gts::kGraphClusters) &&
+                  g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
   if (windowed) {
@@ -626,6 +663,10 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     ks[k].t_n = t.t_n;
     ks[k].t_base = t.t_base;
     ks[k].t_ops = t.t_ops | t.nslot << 16;
+    bool remote = false;
+    for (uint32_t v = h->cta_node_begin[ks[k].cta_begin]; v < h->cta_node_begin[ks[k].cta_end] && !remote; ++v)
+      remote = h->op_cls[h->node_op[v]] == GTS_REMOTE;
+    ks[k].cluster = cluster_of(h, k) | (remote ? gts::kKernelRemote : 0u);
   }
   // template records: the first CTA's nodes with local successor targets and
   // slots for ops; their successors in the same form
@@ -725,12 +766,13 @@ int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_
   int rc = check_sim_args(g, B, out_cycles, out_makespan, out_status, out_digest, flags);
   if (rc || B == 0) return rc;
   if (!hw_host) return fail(GTS_E_ARG, "hw_host is NULL");
-  uint32_t max_nsm = 0, max_nsub = 0;
+  uint32_t max_nsm = 0, max_nsub = 0, max_noc = 0;
   for (uint32_t b = 0; b < B; ++b) {
     rc = check_hw(&hw_host[b], b);
     if (rc) return rc;
     max_nsm = std::max(max_nsm, hw_host[b].n_sm);
     max_nsub = std::max(max_nsub, hw_host[b].n_subpart);
+    max_noc = std::max(max_noc, hw_host[b].noc_nodes);
   }
   const uint64_t need = hw_area_bytes(B) + sim_scratch_bytes(g, B);
   if (!scratch) return fail(GTS_E_ARG, "scratch is NULL");
@@ -741,7 +783,7 @@ int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_
   uint8_t* base = static_cast<uint8_t*>(scratch);
   hipError_t e = hipMemcpyAsync(base, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return fail(GTS_E_HIP, "hw upload: %s", hipGetErrorString(e));
-  return launch(g, reinterpret_cast<const uint32_t*>(base), B, max_nsm, max_nsub, out_cycles, out_makespan,
+  return launch(g, reinterpret_cast<const uint32_t*>(base), B, max_nsm, max_nsub, max_noc, out_cycles, out_makespan,
                 out_status, out_digest, base + hw_area_bytes(B), flags, st);
 }
 
@@ -758,12 +800,13 @@ int gts_hwset_upload(const gts_hw_params* hw_host, uint32_t B, void* dev_buf, ui
   if (!out) return fail(GTS_E_ARG, "out is NULL");
   *out = nullptr;
   if (B && !hw_host) return fail(GTS_E_ARG, "hw_host is NULL");
-  uint32_t max_nsm = 0, max_nsub = 0;
+  uint32_t max_nsm = 0, max_nsub = 0, max_noc = 0;
   for (uint32_t b = 0; b < B; ++b) {
     int rc = check_hw(&hw_host[b], b);
     if (rc) return rc;
     max_nsm = std::max(max_nsm, hw_host[b].n_sm);
     max_nsub = std::max(max_nsub, hw_host[b].n_subpart);
+    max_noc = std::max(max_noc, hw_host[b].noc_nodes);
   }
   if (B && !dev_buf) return fail(GTS_E_ARG, "dev_buf is NULL");
   if (dev_bytes < (uint64_t)B * sizeof(gts_hw_params))
@@ -781,6 +824,7 @@ int gts_hwset_upload(const gts_hw_params* hw_host, uint32_t B, void* dev_buf, ui
   h->B = B;
   h->max_nsm = max_nsm;
   h->max_nsub = max_nsub;
+  h->max_noc = max_noc;
   *out = h;
   return GTS_OK;
 }
@@ -804,7 +848,7 @@ int gts_simulate_hwset(const gts_graph* g, const gts_hwset* hw, uint32_t first, 
   if (scratch_bytes < need)
     return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
                 (unsigned long long)scratch_bytes);
-  return launch(g, hw->dev + (uint64_t)first * gts::HW_WORDS, B, hw->max_nsm, hw->max_nsub, out_cycles,
+  return launch(g, hw->dev + (uint64_t)first * gts::HW_WORDS, B, hw->max_nsm, hw->max_nsub, hw->max_noc, out_cycles,
                 out_makespan, out_status, out_digest, static_cast<uint8_t*>(scratch), flags,
                 reinterpret_cast<hipStream_t>(hip_stream));
 }

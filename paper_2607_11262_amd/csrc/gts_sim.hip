@@ -29,7 +29,14 @@
 //    m + occ_m) + latency;
 //  * release: ORDER edges at start + 1 (issue time), DATA / SYNC edges at
 //    finish (completion); a node becomes ready at the latest release of its
-//    in-edges, not before its CTA's launch.
+//    in-edges, not before its CTA's launch;
+//  * clusters (Sec. 5.2 DSMEM): a kernel's clusters of consecutive CTAs are
+//    dispatched whole onto the first NoC domain and placement slot (strips
+//    of nodes, or compact blocks on a mesh) whose SMs all have a free slot;
+//    a REMOTE node reserves every server of its route (crossbar injection
+//    and ejection ports, or the mesh links of the XY route) at once:
+//    start = max(t, their availability), finish = start + occ + latency
+//    (once per hop on a mesh).
 #include <hip/hip_runtime.h>
 
 #include "../../include/gts.h"
@@ -50,6 +57,8 @@ struct Sim {
   uint32_t smem_w;      // server word of the shared-memory pipe (the engine follows)
   uint32_t* srv;        // [nsm][sstride]: compute lanes, smem pipe, memory engine
   uint32_t* resident;   // [nsm]
+  uint32_t* noc;        // [domains][noc_d][4]: crossbar ports / mesh links
+  uint32_t noc_d, noc_w, noc_map;
   uint64_t* state;      // [N]
   CtaState* cst;        // [C]
   uint64_t* pkey;       // [cap]
@@ -57,6 +66,7 @@ struct Sim {
   uint32_t* out_cycles;
   // uniform control state
   uint32_t npend, next_cta, retired, cur_k, kstart_k, kstart_t, kstart_valid;
+  uint32_t run_kb, run_cl;  // first CTA and cluster size of the kernel whose CTAs are live
   uint64_t l2_av, dram_av, digest;
   uint32_t makespan, nfin, overflow;
 
@@ -145,12 +155,105 @@ struct Sim {
     return true;
   }
 
+  // Node of rank r in placement slot j of a NoC domain, or -1 when the
+  // placement list has no slot j: strips of consecutive nodes, on a mesh
+  // with the compact mapping the most square blocks that tile it, or with
+  // the strided mapping ranks noc_d / cl nodes apart.
+  __device__ int32_t slot_node(uint32_t cl, uint32_t j, uint32_t r) const {
+    if (noc_map == 1 && noc_w > 0) {
+      const uint32_t rows = noc_d / noc_w;
+      uint32_t bh = 0;
+      for (uint32_t h = 1; h * h <= cl; ++h)
+        if (cl % h == 0 && noc_w % (cl / h) == 0 && rows % h == 0) bh = h;
+      if (bh) {
+        const uint32_t bw = cl / bh, nbx = noc_w / bw;
+        if (j >= nbx * (rows / bh)) return -1;
+        return (int32_t)(((j / nbx) * bh + r / bw) * noc_w + (j % nbx) * bw + r % bw);
+      }
+    }
+    if (j >= noc_d / cl) return -1;
+    return noc_map == 2 ? (int32_t)(j + r * (noc_d / cl)) : (int32_t)(j * cl + r);
+  }
+
+  // First placement, domain by domain and slot by slot, whose SMs all exist
+  // (and, with `slots`, all have a free slot); lane r < cl gets rank r's SM.
+  __device__ bool place(uint32_t cl, uint64_t slots, bool need_free, uint32_t& mysm) const {
+    const uint32_t ndom = (nsm + noc_d - 1) / noc_d;
+    const uint64_t want = cl >= 64 ? ~0ull : ((1ull << cl) - 1ull);
+    for (uint32_t d = 0; d < ndom; ++d)
+      for (uint32_t j = 0; slot_node(cl, j, 0) >= 0; ++j) {
+        bool ok = false;
+        uint32_t s = 0;
+        if (lane < cl) {
+          s = d * noc_d + (uint32_t)slot_node(cl, j, lane);
+          ok = s < nsm && (!need_free || resident[s] < slots);
+        }
+        if ((__ballot(ok) & want) == want) {
+          mysm = s;
+          return true;
+        }
+      }
+    return false;
+  }
+
+  __device__ void push_roots(uint32_t c, const CtaDev& cd, uint64_t launch, uint32_t sm) {
+    const uint32_t nroots = cd.root_count & ~kCtaShared;
+    for (uint32_t r0 = 0; r0 < nroots; r0 += 64) {
+      const uint32_t ri = r0 + lane;
+      bool ready = false;
+      uint64_t key = 0;
+      if (ri < nroots) {
+        const uint32_t v = G.roots[cd.root_begin + ri];
+        const uint64_t s = pld(&state[v]);
+        const uint32_t indeg = G.indeg[v];
+        if ((uint32_t)(s >> 32) == indeg) {
+          const uint32_t acc = (uint32_t)s;
+          ready = true;
+          key = mkkey(acc > launch ? acc : launch, kEvReady, v);
+        }
+      }
+      push_lanes(ready, key, sm);
+    }
+  }
+
   __device__ void dispatch(uint32_t t) {
     while (next_cta < G.n_ctas && !overflow) {
       while (next_cta >= G.kernels[cur_k].cta_end) ++cur_k;
       const KernelDev kd = G.kernels[cur_k];
       if (retired < kd.cta_begin) return;  // the previous kernel is still running
       const uint64_t slots = kernel_slots(kd, hw);
+      const uint32_t cl = kd.cluster & 0xFFFFu;
+      run_kb = kd.cta_begin;
+      run_cl = cl;
+      if (cl > 1) {  // a whole cluster onto the first placement with room
+        uint32_t mysm = 0;
+        if (!place(cl, slots, true, mysm)) return;
+        if (!kstart_valid || kstart_k != cur_k) {
+          kstart_valid = 1;
+          kstart_k = cur_k;
+          kstart_t = t;
+        }
+        const uint64_t launch = (uint64_t)t + hw[HW_CTALAT] + (kstart_t == t ? hw[HW_KLAT] : 0u);
+        if (launch > kMaxCycle) {
+          overflow = 1;
+          return;
+        }
+        const uint32_t c0 = next_cta;
+        if (lane < cl) {
+          pst(&cst[c0 + lane].sm, mysm);
+          pst(&cst[c0 + lane].launch, (uint32_t)launch);
+          pst(&cst[c0 + lane].left, G.ctas[c0 + lane].node_count);
+          pst(&cst[c0 + lane].maxfin, 0u);
+          resident[mysm] += 1;  // distinct SMs
+        }
+        next_cta += cl;
+        for (uint32_t r = 0; r < cl; ++r) {
+          const CtaDev cd = G.ctas[c0 + r];
+          push_roots(c0 + r, cd, launch, (uint32_t)__shfl((int)mysm, (int)r, 64));
+        }
+        __builtin_amdgcn_wave_barrier();
+        continue;
+      }
       uint64_t best = 0;
       for (uint32_t m = lane; m < nsm; m += 64) {
         const uint64_t fr = slots - resident[m];
@@ -180,23 +283,7 @@ struct Sim {
         resident[sm] += 1;
       }
       ++next_cta;
-      const uint32_t nroots = cd.root_count & ~kCtaShared;
-      for (uint32_t r0 = 0; r0 < nroots; r0 += 64) {
-        const uint32_t ri = r0 + lane;
-        bool ready = false;
-        uint64_t key = 0;
-        if (ri < nroots) {
-          const uint32_t v = G.roots[cd.root_begin + ri];
-          const uint64_t s = pld(&state[v]);
-          const uint32_t indeg = G.indeg[v];
-          if ((uint32_t)(s >> 32) == indeg) {
-            const uint32_t acc = (uint32_t)s;
-            ready = true;
-            key = mkkey(acc > launch ? acc : launch, kEvReady, v);
-          }
-        }
-        push_lanes(ready, key, sm);
-      }
+      push_roots(c, cd, launch, sm);
       __builtin_amdgcn_wave_barrier();
     }
   }
@@ -235,6 +322,45 @@ struct Sim {
       const uint64_t f = (uint64_t)t + od.z;
       if (!complete(v, rec, t, f, sm)) return;
       release(v, rec, 0, (uint64_t)t + 1, rec.cta, sm);
+      release(v, rec, 1, f, rec.cta, sm);
+    } else if (cls == C_REMOTE) {
+      // the target CTA (same cluster) and the route between the two SMs'
+      // nodes of their NoC domain; lane i holds route server i
+      const uint32_t c = rec.cta;
+      const uint32_t tgt = run_kb + (c - run_kb) / run_cl * run_cl + ((od.w >> 16) & 0xFu);
+      const uint32_t tsm = uni(pld(&cst[tgt].sm));
+      const uint32_t dom = sm / noc_d, a = sm % noc_d, bn = tsm % noc_d;
+      uint32_t* dav = noc + dom * noc_d * 4u;
+      uint32_t nr, idx = 0;
+      uint64_t lat = od.z;
+      if (noc_w == 0) {  // crossbar: injection port of a, ejection port of b
+        nr = 2;
+        idx = lane == 0 ? a * 4u : bn * 4u + 1u;
+      } else {           // mesh: x links first, then y links
+        const int32_t xa = (int32_t)(a % noc_w), ya = (int32_t)(a / noc_w);
+        const int32_t xb = (int32_t)(bn % noc_w), yb = (int32_t)(bn / noc_w);
+        const uint32_t dx = (uint32_t)(xb > xa ? xb - xa : xa - xb), dy = (uint32_t)(yb > ya ? yb - ya : ya - yb);
+        nr = dx + dy;
+        lat *= nr;
+        if (lane < dx) {
+          const int32_t x = xb > xa ? xa + (int32_t)lane : xa - (int32_t)lane;
+          idx = ((uint32_t)ya * noc_w + (uint32_t)x) * 4u + (xb > xa ? 0u : 1u);
+        } else if (lane < nr) {
+          const uint32_t i = lane - dx;
+          const int32_t y = yb > ya ? ya + (int32_t)i : ya - (int32_t)i;
+          idx = ((uint32_t)y * noc_w + (uint32_t)xb) * 4u + (yb > ya ? 2u : 3u);
+        }
+      }
+      uint64_t s = (uint64_t)t;
+      if (!nocont) {
+        const uint32_t av = lane < nr ? dav[idx] : 0u;
+        uint64_t m = uni64(wave_max_u64(av));
+        s = m > s ? m : s;
+      }
+      const uint64_t f = s + od.x + lat;
+      if (!complete(v, rec, s, f, sm)) return;
+      if (lane < nr) dav[idx] = (uint32_t)(s + od.x);
+      release(v, rec, 0, s + 1, rec.cta, sm);
       release(v, rec, 1, f, rec.cta, sm);
     } else {
       const uint32_t a = S[smem_w + 1];
@@ -293,6 +419,10 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.optab = L.lds_optab ? reinterpret_cast<uint4*>(lds) : reinterpret_cast<uint4*>(sim + L.layout.off_optab);
   S.srv = lds + (L.lds_optab ? 4u * S.G.n_ops : 0u);
   S.resident = S.srv + S.nsm * S.sstride;
+  S.noc = S.resident + S.nsm;
+  S.noc_d = S.hw[HW_NOC_NODES];
+  S.noc_w = S.hw[HW_NOC_W];
+  S.noc_map = S.hw[HW_NOC_MAP];
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
   const uint32_t lane = S.lane;
 
@@ -300,6 +430,13 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   bool infeasible = false;
   for (uint32_t k = lane; k < S.G.n_kernels; k += 64)
     infeasible |= kernel_slots(S.G.kernels[k], S.hw) == 0;
+  // clusters and REMOTE nodes need a NoC domain that can hold a cluster
+  for (uint32_t k = 0; k < S.G.n_kernels && (S.G.props & kGraphClusters); ++k) {
+    const uint32_t cw = S.G.kernels[k].cluster, cl = cw & 0xFFFFu;
+    if (cl == 1 && !(cw & kKernelRemote)) continue;
+    uint32_t unused = 0;
+    if (S.noc_d == 0 || cl > S.noc_d || !S.place(cl, 0, false, unused)) infeasible = true;
+  }
   if (__ballot(infeasible)) {
     if (lane == 0) {
       L.out_makespan[b] = 0xFFFFFFFFu;
@@ -311,7 +448,7 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
 
   // Setup: duration table, idle servers, zeroed node / CTA state.
   for (uint32_t p = lane; p < S.G.n_ops; p += 64) S.optab[p] = op_entry(S.G.ops[p], S.hw, S.G.props);
-  const uint32_t nsrv = S.nsm * S.sstride + S.nsm;
+  const uint32_t nsrv = S.nsm * S.sstride + S.nsm + L.noc_words;
   for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
   for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);
   for (uint32_t c = lane; c < S.G.n_ctas; c += 64) {
@@ -326,6 +463,8 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.next_cta = 0;
   S.retired = 0;
   S.cur_k = 0;
+  S.run_kb = 0;
+  S.run_cl = 1;
   S.kstart_k = 0;
   S.kstart_t = 0;
   S.kstart_valid = 0;

@@ -112,3 +112,29 @@ def profile(g, rec, cycles, bins: int = 64, makespan=None) -> dict:
         with np.errstate(invalid="ignore", divide="ignore"):
             out[name] = np.where(width > 0, np.diff(tot) / (capacity(rec, name) * width), 0.0)
     return out
+
+
+def ready_cycles(g, cycles) -> np.ndarray:
+    """Each node's ready cycle re-derived from its in-edges' releases (ORDER
+    at the source's start + 1, DATA / SYNC at its finish); nodes without
+    in-edges get their start (their CTA's launch is not part of a result)."""
+    cycles = np.asarray(cycles).astype(np.int64)
+    src = np.repeat(np.arange(g.n_nodes, dtype=np.int64), np.diff(g.succ_ptr.astype(np.int64)))
+    dst = (g.succ & np.uint32((1 << 30) - 1)).astype(np.int64)
+    kind = (g.succ >> np.uint32(30)).astype(np.int64)
+    rel = np.where(kind == 1, cycles[src, 0] + 1, cycles[src, 1])
+    ready = np.full(g.n_nodes, -1, dtype=np.int64)
+    np.maximum.at(ready, dst, rel)
+    return np.where(ready < 0, cycles[:, 0], ready)
+
+
+def noc_residence(g, cycles) -> float:
+    """Mean NoC residence of the REMOTE requests (Sec. 7.2): from the cycle a
+    transfer is ready to its finish (queueing for the route, occupancy and
+    traversal latency)."""
+    from .gen.graph import REMOTE
+    cycles = np.asarray(cycles)
+    m = np.asarray(g.op_cls)[np.asarray(g.node_op)] == REMOTE
+    if not m.any():
+        return 0.0
+    return float((cycles[m, 1].astype(np.int64) - ready_cycles(g, cycles)[m]).mean())

@@ -57,7 +57,7 @@ def noc_machine(rng):
     rec[H.FIELDS["noc_width"]] = width
     rec[H.FIELDS["noc_rate"]] = rng.randint(H.Q16 // 2, 64 * H.Q16)
     rec[H.FIELDS["noc_lat"]] = rng.randint(0, 300)
-    rec[H.FIELDS["noc_map"]] = rng.randint(0, 1)
+    rec[H.FIELDS["noc_map"]] = rng.randint(0, 2)
     rec[H.FIELDS["max_warps_per_sm"]] = 64
     rec[H.FIELDS["smem_per_sm"]] = 64 * 1024
     return rec

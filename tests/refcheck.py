@@ -189,8 +189,8 @@ def noc_route(src_sm: int, dst_sm: int, D: int, W: int):
 def cluster_placements(rec, cl: int):
     """Every placement of a cluster of cl CTAs, in the order dispatch tries
     them: lists of SMs by rank, domain by domain; strips of consecutive
-    nodes, or (compact mapping on a mesh) the most square bw x bh blocks
-    that tile the mesh, row-major."""
+    nodes, (compact mapping on a mesh) the most square bw x bh blocks that
+    tile the mesh, row-major, or (strided mapping) ranks D / cl nodes apart."""
     D, W = H.get(rec, "noc_nodes"), H.get(rec, "noc_width")
     nsm = H.get(rec, "n_sm")
     shape = None
@@ -205,6 +205,8 @@ def cluster_placements(rec, cl: int):
         for by in range(D // W // bh):
             for bx in range(W // bw):
                 per_domain.append([(by * bh + r // bw) * W + bx * bw + r % bw for r in range(cl)])
+    elif H.get(rec, "noc_map") == 2:  # strided: ranks spread D / cl apart
+        per_domain = [[j + r * (D // cl) for r in range(cl)] for j in range(D // cl)]
     else:
         per_domain = [[j * cl + r for r in range(cl)] for j in range(D // cl)]
     out = []

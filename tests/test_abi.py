@@ -9,8 +9,8 @@ import pytest
 from paper_2607_11262_amd import api
 from paper_2607_11262_amd.gen import hw as H
 from paper_2607_11262_amd.gen import workloads as W
-from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, ORDER, TENSOR, GraphBuilder, TileGraph,
-                                             empty_graph)
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, ORDER, REMOTE, TENSOR, GraphBuilder, TileGraph,
+                                             ValidationError, empty_graph, remote_flags, validate)
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -123,5 +123,49 @@ def test_hw_validation():
         r[H.FIELDS[field]] = val
         assert api.hw_validate(r) == -5, field
     r = H.preset("H100")
-    r[25] = 1  # reserved word
+    r[26] = 1  # reserved word
     assert api.hw_validate(r) == -5
+
+
+def test_noc_hw_validation():
+    noc = dict(noc_nodes=16, noc_width=4, noc_rate=8 * H.Q16, noc_lat=20, noc_map=1)
+    assert api.hw_validate(H.preset("H100", **noc)) == 0
+    assert api.hw_validate(H.preset("H100", **dict(noc, noc_width=0, noc_map=0))) == 0
+    for field, val in (("noc_nodes", 65), ("noc_width", 3), ("noc_width", 32), ("noc_rate", 0),
+                       ("noc_lat", (1 << 24) + 1), ("noc_map", 3)):
+        assert api.hw_validate(H.preset("H100", **dict(noc, **{field: val}))) == -5, field
+    # NoC fields without a NoC
+    assert api.hw_validate(H.preset("H100", noc_width=4)) == -5
+
+
+def _cluster_kernel(cl=2, n_ctas=4, back=None, rank=1, flags=0):
+    b = GraphBuilder()
+    b.kernel(4, 0, cl)
+    ids = []
+    for c in range(n_ctas):
+        b.cta()
+        ids.append((b.node(REMOTE, 256, 1, remote_flags(rank) | flags), b.node(ALU, 64, 1)))
+    if back is not None:
+        u, v = back
+        b.edge(ids[u][0], ids[v][1])
+    return b.build()
+
+
+def test_cluster_validation_codes():
+    cases = [
+        (_cluster_kernel(), 0),
+        (_cluster_kernel(back=(1, 0)), 0),             # back edge inside a cluster
+        (_cluster_kernel(back=(3, 2)), 0),
+        (_cluster_kernel(back=(2, 1)), -3),            # back edge between clusters
+        (_cluster_kernel(cl=3, n_ctas=4), -4),         # clusters must divide the CTA count
+        (_cluster_kernel(cl=17, n_ctas=17), -4),       # at most 16 CTAs per cluster
+        (_cluster_kernel(rank=2), -4),                 # rank outside the cluster
+        (_cluster_kernel(flags=1), -4),                # REMOTE ops carry only the rank
+    ]
+    for g, code in cases:
+        assert api.validate_code(g) == code
+        if code == 0:
+            validate(g)
+        else:
+            with pytest.raises(ValidationError):
+                validate(g)

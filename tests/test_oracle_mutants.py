@@ -48,6 +48,7 @@ MUTANTS = [
     ("crossbar_without_ejection_port", "route[nr++] = &dav[b * 4 + 1];", ";", False),
     ("mesh_latency_once", "      lat_mult = nr;\n", "", False),
     ("placement_ignores_mapping", "if (S->hw[HW_NOC_MAP] == 1 && W > 0) {", "if (0) {", False),
+    ("strided_mapping_ignored", "if (S->hw[HW_NOC_MAP] == 2) return", "if (0) return", False),
     ("cluster_dispatched_like_single_ctas", "    if (cl > 1) {                                        /* R13: a whole cluster */",
      "    if (0) {", False),
     ("remote_target_rank_ignored", "uint32_t tgt = kb + (c - kb) / cl * cl + (S->op_flags[p] >> 4);", "uint32_t tgt = c;", False),
