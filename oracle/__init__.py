@@ -41,7 +41,7 @@ def _open(path):
     lib = ctypes.CDLL(path)
     p = ctypes.c_void_p
     u32 = ctypes.c_uint32
-    lib.gtso_simulate.argtypes = [u32, u32, u32, u32, u32] + [p] * 12 + [p, u32] + [p] * 5
+    lib.gtso_simulate.argtypes = [u32, u32, u32, u32, u32] + [p] * 13 + [p, u32] + [p] * 5
     lib.gtso_simulate.restype = ctypes.c_int
     return lib
 
@@ -90,7 +90,8 @@ def simulate(g, hw, flags: int = 0, want_nodes: bool = True, want_cta: bool = Fa
     arrs = [_c(g.op_cls, np.uint8), _c(g.op_flags, np.uint8), _c(g.op_work, np.uint32), _c(g.op_warps, np.uint32),
             _c(g.node_op, np.uint16), _c(g.succ_ptr, np.uint32), _c(g.succ, np.uint32),
             _c(g.cta_node_begin, np.uint32), _c(g.kernel_cta_begin, np.uint32), _c(g.kernel_warps, np.uint16),
-            _c(g.kernel_smem, np.uint32), _c(g.kernel_cluster, np.uint8)]
+            _c(g.kernel_smem, np.uint32), _c(g.kernel_cluster, np.uint8),
+            _c(g.node_tile, np.uint32) if g.node_tile is not None else None]
     N = int(arrs[4].shape[0])
     C = int(arrs[7].shape[0]) - 1
     hw = _c(hw, np.uint32)

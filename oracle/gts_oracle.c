@@ -98,6 +98,17 @@
  *  R15 A kernel with cl > 1 or with REMOTE nodes is INFEASIBLE when
  *      noc_nodes = 0, when cl > noc_nodes, or when no placement of R13 has
  *      all its SMs in the machine.
+ *  R16 L2 as a fully associative LRU cache of C = l2_lines 128-B lines
+ *      (Sec. 5.2: hits and misses from tile-derived accesses mapped to cache
+ *      lines).  A GLOAD / GSTORE node with a tile id accesses the
+ *      n = cdiv(work, 128) lines of that tile, in order, at its L2 arrival
+ *      (MEM_ARRIVE, in (cycle, id) order).  With D = the number of distinct
+ *      lines of other tiles accessed since the tile's last access, each of
+ *      its lines sits at stack distance D + n - 1, so the access hits (all
+ *      lines) iff the tile was accessed before and D + n <= C, and misses
+ *      (all lines) otherwise; either way the tile becomes most recent.  A
+ *      hit is served by the L2 server, a miss by the DRAM server (R7).
+ *      Nodes without a tile id, or C = 0, keep the op's MISS flag.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -112,8 +123,9 @@ enum {
   HW_RATE = 5,  /* +0 tensor +1 alu +2 sfu +3 smem +4 gmem +5 l2 +6 dram */
   HW_LAT = 12,  /* +0 tensor +1 alu +2 sfu +3 smem +4 l2 +5 dram +6 sync */
   HW_CTALAT = 19, HW_KLAT = 20,
-  HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25
+  HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25, HW_L2_LINES = 26
 };
+#define NO_TILE 0xFFFFFFFFu
 enum { F_NODES = 1, F_DIGEST = 2, F_NOCONT = 4, F_ORDER_FIN = 8 };
 enum { ST_OK = 0, ST_INFEASIBLE = 1, ST_OVERFLOW = 2, ST_DEADLOCK = 3 };
 
@@ -177,12 +189,14 @@ typedef struct {
   const uint16_t *kernel_warps;
   const uint32_t *kernel_smem;
   const uint8_t *kernel_cluster;
+  const uint32_t *node_tile;   /* or NULL */
   /* hw */
   uint32_t nsm, nsub, flags;
   const uint32_t *hw;
   uint32_t noc_d, noc_w;   /* SMs per NoC domain, mesh width (0: crossbar) */
   /* derived per op */
   uint64_t *occ, *occm, *lat; uint32_t *lanes; int *to_dram;
+  uint64_t *occ_l2, *occ_d, *lat_l2, *lat_d;  /* memory ops served by L2 / by DRAM */
   uint64_t *slots;
   /* per node */
   uint32_t *indeg, *cnt, *node_cta, *acc, *st, *fin;
@@ -192,6 +206,8 @@ typedef struct {
   uint64_t *resident, *lane_av, *smem_av, *eng_av;
   uint64_t l2_av, dram_av;
   uint64_t *noc_av;        /* per domain node: 4 link/port servers */
+  /* R16: tiles in recency order (most recent first) and their lines */
+  uint32_t *lru_tile, *lru_lines; uint32_t lru_n;
   /* control */
   heap_t heap;
   uint32_t next_cta; uint64_t retired;
@@ -381,13 +397,32 @@ static void issue(sim_t *S, uint32_t v, uint64_t t) {
   }
 }
 
+/* R16: one tile access; returns 1 on a hit */
+static int lru_access(sim_t *S, uint32_t tile, uint32_t n) {
+  uint64_t D = 0;
+  uint32_t i = 0;
+  while (i < S->lru_n && S->lru_tile[i] != tile) D += S->lru_lines[i++];
+  int found = i < S->lru_n;
+  int hit = found && D + n <= S->hw[HW_L2_LINES];
+  if (!found) S->lru_n++;
+  memmove(S->lru_tile + 1, S->lru_tile, (size_t)i * sizeof *S->lru_tile);
+  memmove(S->lru_lines + 1, S->lru_lines, (size_t)i * sizeof *S->lru_lines);
+  S->lru_tile[0] = tile;
+  S->lru_lines[0] = n;
+  return hit;
+}
+
 static void mem_arrive(sim_t *S, uint32_t v, uint64_t t) {
   uint32_t p = S->node_op[v];
-  uint64_t *av = S->to_dram[p] ? &S->dram_av : &S->l2_av;
+  int dram = S->to_dram[p];
+  if (S->node_tile && S->node_tile[v] != NO_TILE && S->hw[HW_L2_LINES])
+    dram = !lru_access(S, S->node_tile[v], (uint32_t)cdiv(S->op_work[p], 128));
+  uint64_t *av = dram ? &S->dram_av : &S->l2_av;
+  uint64_t occm = dram ? S->occ_d[p] : S->occ_l2[p];
   uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);
-  *av = m + S->occm[p];
+  *av = m + occm;
   uint64_t s = S->st[v];
-  uint64_t f = max64(s + S->occ[p], m + S->occm[p]) + S->lat[p];
+  uint64_t f = max64(s + S->occ[p], m + occm) + (dram ? S->lat_d[p] : S->lat_l2[p]);
   if (!complete(S, v, s, f)) return;
   release_out(S, v, 1, f);
 }
@@ -399,7 +434,8 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
                   const uint32_t *op_work, const uint32_t *op_warps, const uint16_t *node_op,
                   const uint32_t *succ_ptr, const uint32_t *succ, const uint32_t *cta_node_begin,
                   const uint32_t *kernel_cta_begin, const uint16_t *kernel_warps,
-                  const uint32_t *kernel_smem, const uint8_t *kernel_cluster, const uint32_t *hw, uint32_t flags,
+                  const uint32_t *kernel_smem, const uint8_t *kernel_cluster, const uint32_t *node_tile,
+                  const uint32_t *hw, uint32_t flags,
                   uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
                   uint64_t *out_digest, uint32_t *out_cta) {
   (void)n_edges;
@@ -411,6 +447,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   S.node_op = node_op; S.succ_ptr = succ_ptr; S.succ = succ;
   S.cta_node_begin = cta_node_begin; S.kernel_cta_begin = kernel_cta_begin;
   S.kernel_warps = kernel_warps; S.kernel_smem = kernel_smem; S.kernel_cluster = kernel_cluster;
+  S.node_tile = node_tile;
   S.hw = hw; S.nsm = hw[HW_NSM]; S.nsub = hw[HW_NSUB]; S.flags = flags;
   S.noc_d = hw[HW_NOC_NODES]; S.noc_w = hw[HW_NOC_W];
   int rc = 0;
@@ -445,6 +482,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
 
   /* R3 durations per op */
   ALLOC(S.occ, S.P); ALLOC(S.occm, S.P); ALLOC(S.lat, S.P); ALLOC(S.lanes, S.P); ALLOC(S.to_dram, S.P);
+  ALLOC(S.occ_l2, S.P); ALLOC(S.occ_d, S.P); ALLOC(S.lat_l2, S.P); ALLOC(S.lat_d, S.P);
   for (uint32_t p = 0; p < S.P; p++) {
     uint64_t w = op_work[p];
     uint32_t cls = op_cls[p];
@@ -470,6 +508,10 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
       S.occ[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + 4]));
       S.occm[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + (dram ? 6 : 5)]));
       S.lat[p] = hw[HW_LAT + (dram ? 5 : 4)];
+      S.occ_l2[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + 5]));
+      S.occ_d[p] = max64(1, cdiv(w * 65536ull, hw[HW_RATE + 6]));
+      S.lat_l2[p] = hw[HW_LAT + 4];
+      S.lat_d[p] = hw[HW_LAT + 5];
     }
   }
 
@@ -489,6 +531,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   ALLOC(S.resident, S.nsm); ALLOC(S.lane_av, (uint64_t)S.nsm * 3 * S.nsub);
   ALLOC(S.smem_av, S.nsm); ALLOC(S.eng_av, S.nsm);
   ALLOC(S.noc_av, S.noc_d ? ((uint64_t)S.nsm + S.noc_d) / S.noc_d * S.noc_d * 4 : 1);
+  ALLOC(S.lru_tile, S.N); ALLOC(S.lru_lines, S.N);
   ALLOC(S.kstart, S.K);
   for (uint32_t k = 0; k < S.K; k++) S.kstart[k] = -1;
   ALLOC(S.heap.a, (uint64_t)S.N + S.C);
@@ -541,6 +584,7 @@ done:
   free(S.indeg); free(S.cnt); free(S.node_cta); free(S.acc); free(S.st); free(S.fin);
   free(S.cta_sm); free(S.cta_launch); free(S.cta_left); free(S.cta_maxfin); free(S.cta_kernel);
   free(S.resident); free(S.lane_av); free(S.smem_av); free(S.eng_av); free(S.kstart); free(S.heap.a);
-  free(S.noc_av);
+  free(S.noc_av); free(S.lru_tile); free(S.lru_lines);
+  free(S.occ_l2); free(S.occ_d); free(S.lat_l2); free(S.lat_d);
   return rc;
 }

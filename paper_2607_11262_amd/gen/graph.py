@@ -8,7 +8,9 @@ Edges are DATA (producer -> consumer), ORDER (program order of one warp) or
 SYNC (cross-warp signal/wait, barrier, buffer reuse).  A kernel's CTAs may
 form thread-block clusters (consecutive CTAs, dispatched together onto one
 NoC domain); a REMOTE node moves bytes to another CTA of its cluster, whose
-rank sits in the op flags (Sec. 5.2 DSMEM / SM-cluster NoC).
+rank sits in the op flags (Sec. 5.2 DSMEM / SM-cluster NoC).  Global loads
+and stores may name the tile they touch (``node_tile``), for the LRU L2 of
+Sec. 5.2; the tile's 128-B lines are the access's cache lines.
 
 Descriptors are dictionary-encoded: ``ops`` lists the distinct
 (class, flags, work, warp_mask) tuples and every node stores an op index.
@@ -28,6 +30,8 @@ COMPUTE_CLASSES = (TENSOR, ALU, SFU)
 MISS = 1
 RANK_SHIFT = 4      # REMOTE ops: target rank = flags >> RANK_SHIFT
 MAX_CLUSTER = 16
+NO_TILE = 0xFFFFFFFF
+LINE_BYTES = 128
 
 
 def remote_flags(rank: int) -> int:
@@ -58,11 +62,14 @@ class TileGraph:
     name: str = "graph"
     meta: dict = field(default_factory=dict)
     kernel_cluster: np.ndarray = None  # u8 [K] CTAs per cluster (None: all 1)
+    node_tile: np.ndarray = None       # u32 [N] tile of a load / store, NO_TILE otherwise (None: no tiles)
 
     def __post_init__(self):
         if self.kernel_cluster is None:
             self.kernel_cluster = np.ones(int(self.kernel_warps.shape[0]), dtype=np.uint8)
         self.kernel_cluster = np.asarray(self.kernel_cluster, dtype=np.uint8)
+        if self.node_tile is not None:
+            self.node_tile = np.asarray(self.node_tile, dtype=np.uint32)
 
     @property
     def n_nodes(self) -> int:
@@ -110,13 +117,16 @@ class TileGraph:
             h.update(np.ascontiguousarray(a).tobytes())
         if np.any(self.kernel_cluster != 1):
             h.update(np.ascontiguousarray(self.kernel_cluster).tobytes())
+        if self.node_tile is not None:
+            h.update(np.ascontiguousarray(self.node_tile).tobytes())
         return h.hexdigest()
 
     def arrays(self) -> dict:
         return dict(op_cls=self.op_cls, op_flags=self.op_flags, op_work=self.op_work, op_warps=self.op_warps,
                     node_op=self.node_op, succ_ptr=self.succ_ptr, succ=self.succ,
                     cta_node_begin=self.cta_node_begin, kernel_cta_begin=self.kernel_cta_begin,
-                    kernel_warps=self.kernel_warps, kernel_smem=self.kernel_smem, kernel_cluster=self.kernel_cluster)
+                    kernel_warps=self.kernel_warps, kernel_smem=self.kernel_smem, kernel_cluster=self.kernel_cluster,
+                    node_tile=self.node_tile)
 
 
 class OpTable:
@@ -277,6 +287,19 @@ def validate(g: TileGraph) -> None:
         raise ValidationError("compute op with empty warp mask")
     node_cta = g.node_cta()
     node_kernel = g.cta_kernel()[node_cta]
+    if g.node_tile is not None:
+        tiles = g.node_tile.astype(np.int64)
+        mem_node = np.isin(g.op_cls, (GLOAD, GSTORE))[g.node_op.astype(np.int64)]
+        if tiles.shape[0] != N or np.any(~mem_node & (tiles != NO_TILE)):
+            raise ValidationError("only loads and stores carry tile ids")
+        has = tiles != NO_TILE
+        lines = -(-g.op_work.astype(np.int64)[g.node_op.astype(np.int64)] // LINE_BYTES)
+        if has.any():
+            t, l = tiles[has], lines[has]
+            first = {}
+            for a, b in zip(t.tolist(), l.tolist()):
+                if first.setdefault(a, b) != b:
+                    raise ValidationError("a tile is accessed with different sizes")
     nrem = remote[g.node_op.astype(np.int64)]
     rank = (g.op_flags.astype(np.int64) >> RANK_SHIFT)[g.node_op.astype(np.int64)]
     if np.any(nrem & (rank >= cl[node_kernel])):

@@ -32,8 +32,14 @@ FIELDS = {
     "rate_dram": 11,
     "lat_tensor": 12, "lat_alu": 13, "lat_sfu": 14, "lat_smem": 15, "lat_l2": 16, "lat_dram": 17,
     "lat_sync": 18, "cta_launch_lat": 19, "kernel_launch_lat": 20,
-    "noc_nodes": 21, "noc_width": 22, "noc_rate": 23, "noc_lat": 24, "noc_map": 25,
+    "noc_nodes": 21, "noc_width": 22, "noc_rate": 23, "noc_lat": 24, "noc_map": 25, "l2_lines": 26,
 }
+L2_MIB = {"A100": 40, "H100": 50, "B200": 126}  # L2 capacity (LRU model: l2_lines = MiB * 8192)
+
+
+def l2_lines(mib: float) -> int:
+    """128-B lines of an L2 of `mib` MiB."""
+    return int(mib * (1 << 20)) // 128
 NWORDS = 32
 
 

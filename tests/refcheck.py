@@ -29,8 +29,10 @@ import os
 import numpy as np
 
 from paper_2607_11262_amd.gen import hw as H
-from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, ORDER, REMOTE, SFU, SMEM, SYNC, SYNC_EDGE,
-                                             TENSOR, GraphBuilder, remote_flags)
+from collections import OrderedDict
+
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, LINE_BYTES, NO_TILE, ORDER, REMOTE, SFU,
+                                             SMEM, SYNC, SYNC_EDGE, TENSOR, GraphBuilder, remote_flags)
 
 MAXCYC = 0xFFFFFFFE
 CLASS = {"TENSOR": TENSOR, "ALU": ALU, "SFU": SFU, "SMEM": SMEM, "GLOAD": GLOAD, "GSTORE": GSTORE, "SYNC": SYNC,
@@ -68,7 +70,9 @@ def durations(g, rec):
         else:
             out.append(dict(kind="gmem", occ=max(1, cdiv(work * 65536, rates[4])),
                             occ_m=max(1, cdiv(work * 65536, rates[6] if miss else rates[5])),
-                            lat=lats[5] if miss else lats[4], dram=bool(miss)))
+                            lat=lats[5] if miss else lats[4], dram=bool(miss),
+                            occ_l2=max(1, cdiv(work * 65536, rates[5])), occ_dram=max(1, cdiv(work * 65536, rates[6])),
+                            lat_l2=lats[4], lat_dram=lats[5], lines=cdiv(work, LINE_BYTES)))
     return out
 
 
@@ -144,14 +148,31 @@ def verify_schedule(g, rec, flags, cycles, cta):
             eng_av[sm] = s + d["occ"]
             assert st[v] == s, f"gmem node {v} start {st[v]} != {s}"
             gstart[v] = s
-    # global L2 / DRAM servers in FIFO order of (arrival = engine start, id)
+    # global L2 / DRAM servers in FIFO order of (arrival = engine start, id);
+    # with an L2 capacity, tracked tiles replay an explicit LRU of 128-B lines
     av = {False: 0, True: 0}
+    cap = H.get(rec, "l2_lines")
+    lines = OrderedDict()  # (tile, line) -> None, least recent first
     for v in sorted(gstart, key=lambda x: (gstart[x], x)):
         d = dur[ops[v]]
         s = gstart[v]
-        m = s if nocont else max(s, av[d["dram"]])
-        av[d["dram"]] = m + d["occ_m"]
-        assert fi[v] == max(s + d["occ"], m + d["occ_m"]) + d["lat"], f"gmem node {v} finish"
+        dram, occ_m, lat = d["dram"], d["occ_m"], d["lat"]
+        tile = int(g.node_tile[v]) if g.node_tile is not None else NO_TILE
+        if cap and tile != NO_TILE:
+            hits = []
+            for i in range(d["lines"]):
+                key = (tile, i)
+                hits.append(key in lines)
+                lines[key] = None
+                lines.move_to_end(key)
+                while len(lines) > cap:
+                    lines.popitem(last=False)
+            assert all(hits) or not any(hits), f"node {v}: a whole-tile access hits all its lines or none"
+            dram = not all(hits)
+            occ_m, lat = (d["occ_dram"], d["lat_dram"]) if dram else (d["occ_l2"], d["lat_l2"])
+        m = s if nocont else max(s, av[dram])
+        av[dram] = m + occ_m
+        assert fi[v] == max(s + d["occ"], m + occ_m) + lat, f"gmem node {v} finish"
     # CTA dispatch re-simulated from retire cycles
     exp_sm, exp_launch = dispatch_from_retires(g, rec, fi)
     assert np.array_equal(exp_sm, cta_sm), "CTA -> SM mapping"
@@ -315,17 +336,22 @@ def load_golden():
     for c in doc["cases"]:
         src = cases[c["same_graph_as"]] if "same_graph_as" in c else c
         b = GraphBuilder()
+        tiles = []
         for k in src["kernels"]:
             b.kernel(k["warps"], k["smem"], k.get("cluster", 1))
             for cta in k["ctas"]:
                 b.cta()
-                for cls, work, warps, extra in cta:
-                    # fourth field: the L2-miss flag, or a REMOTE node's target rank
+                for cls, work, warps, extra, *tile in cta:
+                    # fourth field: the L2-miss flag, or a REMOTE node's target rank;
+                    # optional fifth: the tile a load / store touches
                     flags = remote_flags(extra) if cls == "REMOTE" else (1 if extra else 0)
                     b.node(CLASS[cls], work, warps, flags)
+                    tiles.append(tile[0] if tile else NO_TILE)
         for u, v, kd in src["edges"]:
             b.edge(u, v, KIND[kd])
         g = b.build(c["name"])
+        if any(t != NO_TILE for t in tiles):
+            g.node_tile = np.array(tiles, dtype=np.uint32)
         rec = H.toy(**c["hw"])
         out.append((c, g, rec))
     return out

@@ -26,7 +26,15 @@ MUTANTS = [
      "if (fr >= bestfree && fr > 0) { bestfree = fr; best = m; }", False),
     ("no_kernel_launch_latency", "launch += S->hw[HW_KLAT];", ";", True),
     ("misses_served_by_l2", "S.to_dram[p] = dram;", "S.to_dram[p] = 0;", False),
-    ("gmem_finish_ignores_engine", "max64(s + S->occ[p], m + S->occm[p])", "(m + S->occm[p])", False),
+    ("gmem_finish_ignores_engine", "max64(s + S->occ[p], m + occm)", "(m + occm)", False),
+    ("lru_hit_needs_strict_room", "int hit = found && D + n <= S->hw[HW_L2_LINES];",
+     "int hit = found && D + n < S->hw[HW_L2_LINES];", False),
+    ("lru_ignores_own_lines", "int hit = found && D + n <= S->hw[HW_L2_LINES];",
+     "int hit = found && D < S->hw[HW_L2_LINES];", False),
+    ("lru_first_access_can_hit", "int hit = found && D + n <= S->hw[HW_L2_LINES];",
+     "int hit = D + n <= S->hw[HW_L2_LINES];", False),
+    ("lru_is_fifo", "  memmove(S->lru_tile + 1, S->lru_tile, (size_t)i * sizeof *S->lru_tile);\n  memmove(S->lru_lines + 1, S->lru_lines, (size_t)i * sizeof *S->lru_lines);\n  S->lru_tile[0] = tile;\n  S->lru_lines[0] = n;",
+     "  if (!found) { memmove(S->lru_tile + 1, S->lru_tile, (size_t)i * sizeof *S->lru_tile); memmove(S->lru_lines + 1, S->lru_lines, (size_t)i * sizeof *S->lru_lines); S->lru_tile[0] = tile; S->lru_lines[0] = n; }", False),
     ("ready_ignores_launch", "mkkey(max64(S->acc[w], S->cta_launch[c]), EV_READY, w)", "mkkey(S->acc[w], EV_READY, w)",
      False),
     ("retire_at_last_finish", "if (finish > S->cta_maxfin[c]) S->cta_maxfin[c] = (uint32_t)finish;",

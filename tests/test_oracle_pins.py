@@ -19,6 +19,7 @@ import pytest
 import oracle
 import refcheck
 from clustered import clustered_graph, noc_machine
+from tiled import with_tiles
 from paper_2607_11262_amd.gen import hw as H
 from paper_2607_11262_amd.gen import workloads as W
 from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, REMOTE, SFU, SMEM, SYNC, TENSOR, GraphBuilder,
@@ -173,6 +174,57 @@ def test_verifier_clusters(seed):
             sms = r.cta[c0:c0 + cl, 0].astype(np.int64)
             assert len(set(sms.tolist())) == cl and len(set((sms // D).tolist())) == 1
             assert len(set(r.cta[c0:c0 + cl, 1].tolist())) == 1
+
+
+@pytest.mark.parametrize("seed", range(100))
+def test_verifier_lru_l2(seed):
+    """R16: each tracked access replayed on an explicit LRU of 128-B lines
+    (the paper's definition) decides L2 or DRAM; the oracle's whole-tile
+    rule must agree on every node."""
+    rng = SplitMix64(seed, 16)
+    g = with_tiles(W.random_graph(rng, n_nodes_max=rng.choice([10, 40, 120]), n_kernels_max=2, ctas_max=4), rng)
+    validate(g)
+    rec = H.sample_random(rng)
+    rec[H.FIELDS["l2_lines"]] = rng.choice([1, 2, 8, 40, 200, 4096])
+    flags = rng.choice([0, 0, 4, 8])
+    r = oracle.simulate(g, rec, flags, want_cta=True)
+    if r.status == 1:
+        return
+    assert r.status == 0
+    refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+
+
+def test_lru_l2_capacity_monotone():
+    """LRU is a stack algorithm: for a fixed access order a larger L2 never
+    turns a hit into a miss.  A DATA chain of loads fixes the order, so every
+    finish only shrinks as the capacity grows, and an L2 that holds every
+    tile misses exactly on first touches."""
+    rng = SplitMix64(3, 17)
+    b = GraphBuilder()
+    b.kernel(1, 0)
+    b.cta()
+    seq = [rng.randint(0, 11) for _ in range(120)]
+    prev_v = None
+    for t in seq:
+        v = b.node(GLOAD, 256 * (1 + t % 3), 1)
+        if prev_v is not None:
+            b.edge(prev_v, v, DATA)
+        prev_v = v
+    g = b.build()
+    g.node_tile = np.array(seq, dtype=np.uint32)
+    validate(g)
+    rec = H.toy(rate_dram=H.Q16)  # misses much slower than hits
+    prev = None
+    for cap in (2, 6, 12, 20, 30, 1 << 20):
+        rec[H.FIELDS["l2_lines"]] = cap
+        r = oracle.simulate(g, rec, 0)
+        fin = r.cycles[:, 1].astype(np.int64)
+        if prev is not None:
+            assert np.all(fin <= prev), cap
+        prev = fin
+    dur = np.diff(np.concatenate([[0], r.cycles[:, 1].astype(np.int64)]))
+    first = np.array([t not in seq[:i] for i, t in enumerate(seq)])
+    assert len(set(dur[first].tolist()) & set(dur[~first].tolist())) == 0
 
 
 def _small_workloads():
