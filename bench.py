@@ -36,6 +36,13 @@ crossbar or 4 x 4 mesh NoC (any of three placements, port bandwidth 8-64
 B/cycle, latency 60-400 cycles, DRAM 1.5-8 TB/s, tensor 0.5-4x); its line
 adds the case-study table (NoC vs DRAM cycles and mean NoC residence per
 topology and placement) read off GPU timelines.
+
+    python bench.py --workload l2lru
+
+runs eight GEMMs of the design sweep (the smallest of 40K-300K nodes) with
+tile ids (the LRU L2 of Sec. 5.2), each under 4096 seeded H100 sweep
+machines with an L2 of 4-64 MiB; its line adds the kernel cycles of one GEMM across L2 sizes
+(static first-touch flags vs LRU) read off the GPU.
 """
 from __future__ import annotations
 
@@ -93,7 +100,8 @@ def recorded_traffic(n_launch: int):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining", "noc"), default="gemm_design_sweep")
+    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining", "noc", "l2lru"),
+                    default="gemm_design_sweep")
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
@@ -140,8 +148,23 @@ def main() -> int:
 
     pipelining = args.workload == "pipelining"
     noc = args.workload == "noc"
+    lru = args.workload == "l2lru"
     noc_graphs = [(S, comm) for S in CF.CLUSTER_SIZES for comm in CF.COMMS]
-    if noc:
+    if lru:
+        all_params = W.sweep_params()
+        lru_params = [q for q in sorted(all_params, key=W.sweep_nodes) if 40_000 <= W.sweep_nodes(q) <= 300_000][:8]
+        n_graphs = len(lru_params)
+
+        def make(gi):
+            g = W.gemm(*lru_params[gi], tiles=True)
+            hw = W.config_hw(2, B=B_PER_GRAPH, index=gi)
+            rng = np.random.default_rng(5000 + gi)
+            hw[:, 26] = (rng.integers(4, 65, size=B_PER_GRAPH) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
+            return g, hw
+
+        def describe(gi):
+            return lru_params[gi]
+    elif noc:
         n_graphs = len(noc_graphs)
 
         def make(gi):
@@ -245,7 +268,7 @@ def main() -> int:
     # over the timed region) is higher and is reported beside it.
     achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
     aggregate_gbs = float(abytes.sum() / elapsed / 1e9)
-    traffic = None if (pipelining or noc) else recorded_traffic(len(launches))
+    traffic = None if (pipelining or noc or lru) else recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
     cpu = None
@@ -302,7 +325,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_over_algorithmic": (traffic / float(abytes.mean())) if traffic else None,
-                     "kernel": "gts_sim_wave" if noc else "gts_sim_window", "launches": len(launches),
+                     "kernel": "gts_sim_wave" if (noc or lru) else "gts_sim_window", "launches": len(launches),
                      "mean_launch_ms": float(durs.mean() * 1e3),
                      "streams": len(streams), "aggregate_gbs": aggregate_gbs,
                      "aggregate_frac": aggregate_gbs / HBM_PEAK_GBS},
@@ -314,8 +337,25 @@ def main() -> int:
         out["case_study"] = case_study(api, torch, PL)
     if noc:
         out["case_study"] = noc_case_study(api, torch, CF)
+    if lru:
+        out["case_study"] = lru_case_study(api, torch, W)
     print(json.dumps(out))
     return 0
+
+
+def lru_case_study(api, torch, W):
+    """One GEMM (4096 x 4096 x 2048, 128 x 128 x 64 tiles, 3 stages) on
+    Table 3's H100 across L2 sizes: kernel cycles under the static
+    first-touch flags (0 MiB) and under the LRU L2."""
+    from paper_2607_11262_amd.gen import hw as H
+    g = W.gemm(4096, 4096, 2048, 128, 128, 64, 3, tiles=True)
+    sizes = (0, 0.5, 2, 8, 32, 50)
+    recs = np.stack([H.preset("H100", l2_lines=H.l2_lines(m)) for m in sizes])
+    res = api.simulate(api.upload(g), recs, api.OUT_DIGEST)
+    torch.cuda.synchronize()
+    _, mk, st, _ = api.to_numpy(res)
+    return {"graph": "gemm 4096x4096x2048 128x128x64 s3", "nodes": g.n_nodes,
+            "cycles_by_l2_mib": {("static" if m == 0 else str(m)): int(c) for m, c in zip(sizes, mk)}}
 
 
 def noc_case_study(api, torch, CF):

@@ -75,6 +75,8 @@ extern "C" {
 /* REMOTE: the target CTA's rank within the source CTA's cluster is
  * (flags >> GTS_OPF_RANK_SHIFT); no other flag bit is set. */
 #define GTS_OPF_RANK_SHIFT 4
+#define GTS_NO_TILE 0xFFFFFFFFu  /* node_tile entry of an untracked node    */
+#define GTS_LINE_BYTES 128u      /* L2 line of the LRU model                */
 
 /* ---- edge kinds (Sec. 4.1 edge semantics) ------------------------------ */
 /* succ[] entries are  target | (kind << GTS_EDGE_KIND_SHIFT).              */
@@ -146,7 +148,14 @@ typedef struct gts_hw_params {
   uint32_t noc_map;          /* cluster placement: 0 strips of consecutive
                                 nodes, 1 compact blocks (mesh), 2 strided
                                 (ranks noc_nodes / cluster nodes apart)      */
-  uint32_t reserved[6];      /* must be zero                                 */
+  /* L2 as a fully associative LRU cache of l2_lines 128-B lines (Sec. 5.2):
+   * a load / store that names its tile (node_tile) touches the tile's
+   * cdiv(bytes, 128) lines at its L2 arrival and hits (L2 server) iff the
+   * tile was touched before and its lines plus the distinct lines of other
+   * tiles touched since fit in l2_lines, else misses (DRAM server).  0: the
+   * op's GTS_OPF_MISS flag decides, as for nodes without a tile. */
+  uint32_t l2_lines;
+  uint32_t reserved[5];      /* must be zero                                 */
 } gts_hw_params;
 
 /* ---- host-side graph (Sec. 4.1; dictionary-encoded descriptors) --------- */
@@ -163,7 +172,9 @@ typedef struct gts_hw_params {
  * kernel_cluster[k] consecutive CTAs (1 .. GTS_MAX_CLUSTER, dividing the
  * kernel's CTA count; kernel_cluster = NULL means 1 for every kernel), and a
  * REMOTE op's target rank is below the cluster size of every kernel that
- * uses it.  An empty graph has all counts zero. */
+ * uses it; only GLOAD / GSTORE nodes carry a tile, and every node of one
+ * tile has the same cdiv(work, 128) lines.  An empty graph has all counts
+ * zero. */
 typedef struct gts_graph_host {
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops;
   const uint8_t  *op_cls;           /* [n_ops]  GTS_TENSOR .. GTS_REMOTE     */
@@ -178,6 +189,8 @@ typedef struct gts_graph_host {
   const uint16_t *kernel_warps;     /* [n_kernels], 1 .. GTS_MAX_WARPS       */
   const uint32_t *kernel_smem;      /* [n_kernels], shared memory per CTA    */
   const uint8_t  *kernel_cluster;   /* [n_kernels] CTAs per cluster, or NULL */
+  const uint32_t *node_tile;        /* [n_nodes] tile of a GLOAD / GSTORE, or
+                                       GTS_NO_TILE; NULL: no node has one    */
 } gts_graph_host;
 
 typedef struct gts_graph gts_graph;  /* opaque handle to an uploaded graph */

@@ -45,7 +45,8 @@ class _GraphHost(ctypes.Structure):
                 ("op_warps", ctypes.c_void_p), ("node_op", ctypes.c_void_p), ("succ_ptr", ctypes.c_void_p),
                 ("succ", ctypes.c_void_p), ("cta_node_begin", ctypes.c_void_p),
                 ("kernel_cta_begin", ctypes.c_void_p), ("kernel_warps", ctypes.c_void_p),
-                ("kernel_smem", ctypes.c_void_p), ("kernel_cluster", ctypes.c_void_p)]
+                ("kernel_smem", ctypes.c_void_p), ("kernel_cluster", ctypes.c_void_p),
+                ("node_tile", ctypes.c_void_p)]
 
 
 _lib = None
@@ -98,7 +99,9 @@ def _host_struct(g):
                 kernel_cta_begin=np.ascontiguousarray(g.kernel_cta_begin, np.uint32),
                 kernel_warps=np.ascontiguousarray(g.kernel_warps, np.uint16),
                 kernel_smem=np.ascontiguousarray(g.kernel_smem, np.uint32),
-                kernel_cluster=np.ascontiguousarray(g.kernel_cluster, np.uint8))
+                kernel_cluster=np.ascontiguousarray(g.kernel_cluster, np.uint8),
+                node_tile=(np.ascontiguousarray(g.node_tile, np.uint32) if g.node_tile is not None
+                           else np.zeros(0, np.uint32)))
     h = _GraphHost(n_nodes=arrs["node_op"].shape[0], n_edges=arrs["succ"].shape[0],
                    n_ctas=arrs["cta_node_begin"].shape[0] - 1, n_kernels=arrs["kernel_warps"].shape[0],
                    n_ops=arrs["op_cls"].shape[0],

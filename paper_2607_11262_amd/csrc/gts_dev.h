@@ -24,6 +24,7 @@ constexpr uint32_t kGraphClassShift = 5u;         // bits 5-7: the op table has 
                                                   // ALU / SFU ops (one bit per class)
 constexpr uint32_t kGraphClusters = 256u;         // some kernel has clusters of more than
                                                   // one CTA or REMOTE nodes
+constexpr uint32_t kGraphTiles = 512u;            // some load / store names its tile
 
 // Compute pipelines: every subpartition of an SM has one lane per compute
 // class.  Server state holds lanes only for the classes a graph uses, class
@@ -38,7 +39,7 @@ __host__ __device__ inline uint32_t compute_slot(uint32_t props, uint32_t cls) {
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
   uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots, off_indeg;
-  uint64_t off_tnodes, off_tsucc, off_tindeg, off_cclass, off_tops;
+  uint64_t off_tnodes, off_tsucc, off_tindeg, off_cclass, off_tops, off_tile;
   uint32_t max_cta_nodes, max_outdeg, n_tnodes, n_tsucc, n_tops, pad;
 };
 
@@ -102,7 +103,9 @@ struct Image {
   const uint16_t* tindeg;       // in-degree per template record
   const uint8_t* cclass;        // class of each CTA of a templated kernel
   const uint16_t* tops;         // [n_tops] class x slot -> op id
+  const uint32_t* tile;         // [N] tile of each load / store (kGraphTiles), else null
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props, n_tops;
+  uint32_t n_tiles;             // distinct tiles
 };
 
 // Hardware record word indices (gts_hw_params field order).
@@ -113,7 +116,8 @@ enum : uint32_t {
 enum : uint32_t { R_TENSOR = 0, R_ALU, R_SFU, R_SMEM, R_GMEM, R_L2, R_DRAM };
 enum : uint32_t { L_TENSOR = 0, L_ALU, L_SFU, L_SMEM, L_L2, L_DRAM, L_SYNC };
 enum : uint32_t { C_TENSOR = 0, C_ALU, C_SFU, C_SMEM, C_GLOAD, C_GSTORE, C_SYNC, C_REMOTE };
-enum : uint32_t { HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25 };
+enum : uint32_t { HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25,
+                  HW_L2_LINES = 26 };
 // Device-image edge encoding: target | bits << 30.  DATA and SYNC edges time
 // identically (released at the source's finish) and share bit pattern 0;
 // bit 30 marks an ORDER edge (released at the source's start + 1), bit 31 an
@@ -136,6 +140,7 @@ struct SimLayout {
   uint64_t off_rp;      // windowed kernel: later ready entries beyond LDS, [kPoolSpill][64] u64
   uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
   uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
+  uint64_t off_lru;     // general kernel: LRU L2 tiles, most recent first ([n_tiles] x {tile, lines})
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };

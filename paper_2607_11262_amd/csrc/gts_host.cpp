@@ -9,6 +9,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <unordered_map>
 #include <new>
 #include <string>
 #include <vector>
@@ -71,6 +72,7 @@ struct Derived {
   std::vector<uint16_t> tslot;   // per template record: slot
   std::vector<uint16_t> tops;    // class x slot -> op
   uint32_t n_tnodes = 0, n_tsucc = 0;
+  uint32_t n_tiles = 0;          // distinct tiles named by loads / stores
 };
 
 // Template sharing: find the kernels whose CTAs run isomorphic tile graphs
@@ -226,6 +228,22 @@ int check_graph(const gts_graph_host* h, Derived* d) {
                                           cluster_of(h, cta_kernel[node_cta[v]]))
       return fail(GTS_E_RANGE, "node %u targets rank %u outside its cluster", v, h->op_flags[p] >> GTS_OPF_RANK_SHIFT);
   }
+  // tiles: only loads / stores, one line count per tile
+  uint32_t n_tiles = 0;
+  if (h->node_tile) {
+    std::unordered_map<uint32_t, uint32_t> lines;
+    for (uint32_t v = 0; v < N; ++v) {
+      const uint32_t t = h->node_tile[v];
+      if (t == GTS_NO_TILE) continue;
+      const uint32_t p = h->node_op[v];
+      if (!is_memory(h->op_cls[p])) return fail(GTS_E_RANGE, "node %u is not a load or store but names tile %u", v, t);
+      const uint32_t n = (h->op_work[p] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES;
+      auto it = lines.emplace(t, n).first;
+      if (it->second != n)
+        return fail(GTS_E_RANGE, "tile %u is touched with %u and with %u lines (node %u)", t, it->second, n, v);
+    }
+    n_tiles = (uint32_t)lines.size();
+  }
   // first CTA of each CTA's cluster (clusters are dispatched together, so
   // edges between their CTAs may go either way)
   std::vector<uint32_t> cluster_first(C);
@@ -310,10 +328,11 @@ int check_graph(const gts_graph_host* h, Derived* d) {
     if (h->op_cls[p] == GTS_REMOTE) clusters = true;
   }
   for (uint32_t k = 0; k < K; ++k) clusters |= cluster_of(h, k) > 1;
+  d->n_tiles = n_tiles;
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
              (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
              (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift |
-             (clusters ? gts::kGraphClusters : 0u);
+             (clusters ? gts::kGraphClusters : 0u) | (n_tiles ? gts::kGraphTiles : 0u);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   find_templates(h, d);
@@ -321,7 +340,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
 }
 
 struct ImageLayout {
-  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, tnodes, tsucc, tindeg, cclass, tops, total;
+  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, tnodes, tsucc, tindeg, cclass, tops, tile, total;
 };
 
 ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
@@ -352,11 +371,13 @@ ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
   off = align_up(off + (uint64_t)h->n_ctas, gts::kAlign);
   L.tops = off;
   off = align_up(off + d.tops.size() * 2, gts::kAlign);
+  L.tile = off;
+  off = align_up(off + (d.n_tiles ? (uint64_t)h->n_nodes * 4 : 0u), gts::kAlign);
   L.total = off;
   return L;
 }
 
-gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
+gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t n_tiles) {
   gts::SimLayout s;
   uint64_t off = 0;
   s.off_state = off;
@@ -368,6 +389,8 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P) {
   off = align_up(off + s.pend_cap * 12, gts::kAlign);
   s.off_optab = off;
   off = align_up(off + (uint64_t)P * 16, gts::kAlign);
+  s.off_lru = off;
+  off = align_up(off + (uint64_t)n_tiles * 8, gts::kAlign);
   // The windowed kernel's per-SM queues overlay the general kernel's pending
   // list (a simulation the windowed kernel hands back is restarted from
   // scratch by the general kernel).
@@ -403,13 +426,13 @@ int check_hw(const gts_hw_params* hw, uint32_t index) {
   }
   if (hw->noc_lat > (1u << 24)) return fail(GTS_E_HW, "hw[%u].noc_lat = %u exceeds 2^24", index, hw->noc_lat);
   if (hw->noc_map > 2) return fail(GTS_E_HW, "hw[%u].noc_map = %u (0 strips, 1 blocks, 2 strided)", index, hw->noc_map);
-  for (int i = 0; i < 6; ++i)
+  for (int i = 0; i < 5; ++i)
     if (hw->reserved[i]) return fail(GTS_E_HW, "hw[%u].reserved[%d] is not zero", index, i);
   return GTS_OK;
 }
 
 uint64_t sim_scratch_bytes(const gts_graph* g, uint32_t B) {
-  return (uint64_t)B * sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops).stride;
+  return (uint64_t)B * sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops, g->img.n_tiles).stride;
 }
 
 int check_sim_args(const gts_graph* g, uint32_t B, const uint32_t* out_cycles, const uint32_t* out_makespan,
@@ -444,7 +467,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.img = g->img;
   L.hw = hw_dev;
   L.sims = sims;
-  L.layout = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops);
+  L.layout = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops, g->img.n_tiles);
   L.out_cycles = (flags & GTS_OUT_NODES) ? out_cycles : nullptr;
   L.out_makespan = out_makespan;
   L.out_status = out_status;
@@ -461,7 +484,8 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
-  bool windowed = (g->img.props & need_props) == need_props && !(g->img.props & gts::kGraphClusters) &&
+  bool windowed = (g->img.props & need_props) == need_props &&
+                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTiles)) &&
                   g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
@@ -601,6 +625,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   hdr->off_tindeg = L.tindeg;
   hdr->off_cclass = L.cclass;
   hdr->off_tops = L.tops;
+  hdr->off_tile = L.tile;
   hdr->max_cta_nodes = d.max_cta_nodes;
   hdr->max_outdeg = d.max_outdeg;
   hdr->n_tnodes = d.n_tnodes;
@@ -697,6 +722,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     }
   }
   std::memcpy(img.data() + L.cclass, d.cclass.data(), d.cclass.size());
+  if (d.n_tiles) std::memcpy(img.data() + L.tile, h->node_tile, (size_t)h->n_nodes * 4);
   if (!d.tops.empty()) std::memcpy(img.data() + L.tops, d.tops.data(), d.tops.size() * 2);
   if (!d.roots.empty()) std::memcpy(img.data() + L.roots, d.roots.data(), d.roots.size() * 4);
 
@@ -721,6 +747,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.cclass = reinterpret_cast<const uint8_t*>(base + L.cclass);
   g->img.tops = reinterpret_cast<const uint16_t*>(base + L.tops);
   g->img.n_tops = (uint32_t)d.tops.size();
+  g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
+  g->img.n_tiles = d.n_tiles;
   g->img.n_nodes = h->n_nodes;
   g->img.n_edges = h->n_edges;
   g->img.n_ctas = h->n_ctas;

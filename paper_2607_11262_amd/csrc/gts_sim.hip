@@ -36,7 +36,11 @@
 //    a REMOTE node reserves every server of its route (crossbar injection
 //    and ejection ports, or the mesh links of the XY route) at once:
 //    start = max(t, their availability), finish = start + occ + latency
-//    (once per hop on a mesh).
+//    (once per hop on a mesh);
+//  * LRU L2 (tiles): a load / store that names its tile, on a machine with
+//    an L2 capacity, hits iff the tile was touched before and its lines plus
+//    the distinct lines of other tiles touched since fit, else goes to DRAM;
+//    the tile then becomes the most recent.
 #include <hip/hip_runtime.h>
 
 #include "../../include/gts.h"
@@ -59,6 +63,8 @@ struct Sim {
   uint32_t* resident;   // [nsm]
   uint32_t* noc;        // [domains][noc_d][4]: crossbar ports / mesh links
   uint32_t noc_d, noc_w, noc_map;
+  uint2* lru;           // [n_tiles] {tile, lines}, most recent first (scratch)
+  uint32_t lru_n, l2_lines;
   uint64_t* state;      // [N]
   CtaState* cst;        // [C]
   uint64_t* pkey;       // [cap]
@@ -375,20 +381,93 @@ struct Sim {
     }
   }
 
+  // Inclusive prefix sum across the wave.
+  __device__ uint32_t wave_incl_sum(uint32_t x) const {
+    for (uint32_t o = 1; o < 64; o <<= 1) {
+      const uint32_t y = (uint32_t)__shfl_up((int)x, o, 64);
+      if (lane >= o) x += y;
+    }
+    return x;
+  }
+
+  // One access of tile x (n lines) to the LRU L2 of `cap` lines; true on a
+  // hit.  The list holds each tile at most once, most recent first, and only
+  // tiles that can still hit: every entry's lines plus those above it fit in
+  // cap (a deeper tile would miss on its next access anyway, as if absent).
+  __device__ bool lru_access(uint32_t x, uint32_t n, uint32_t cap) {
+    bool found = false;
+    uint32_t pos = lru_n;
+    uint64_t above = 0, run = 0;
+    for (uint32_t i0 = 0; i0 < lru_n; i0 += 64) {
+      const uint32_t i = i0 + lane;
+      const uint2 e = i < lru_n ? pld(&lru[i]) : make_uint2(GTS_NO_TILE, 0u);
+      const uint32_t incl = wave_incl_sum(e.y);
+      const uint64_t m = __ballot(i < lru_n && e.x == x);
+      if (m) {
+        const uint32_t j = (uint32_t)__ffsll((unsigned long long)m) - 1u;
+        pos = i0 + j;
+        above = run + uni((uint32_t)__shfl((int)(incl - e.y), (int)j, 64));
+        found = true;
+        break;
+      }
+      run += uni((uint32_t)__shfl((int)incl, 63, 64));
+    }
+    const bool hit = found && above + n <= cap;
+    // entries [0, pos) move down one place, back to front; x goes on top
+    for (uint32_t i1 = pos; i1 > 0; i1 = i1 > 64 ? i1 - 64 : 0) {
+      const uint32_t lo = i1 > 64 ? i1 - 64 : 0;
+      const uint32_t i = lo + lane;
+      uint2 e = make_uint2(0, 0);
+      if (i < i1) e = pld(&lru[i]);
+      __builtin_amdgcn_s_waitcnt(0);
+      if (i < i1) pst(&lru[i + 1], e);
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+    if (!found) ++lru_n;
+    if (lane == 0) pst(&lru[0], make_uint2(x, n));
+    __builtin_amdgcn_s_waitcnt(0);
+    // drop the entries that can no longer hit
+    run = 0;
+    uint32_t keep = lru_n;
+    for (uint32_t i0 = 0; i0 < lru_n; i0 += 64) {
+      const uint32_t i = i0 + lane;
+      const uint32_t ln = i < lru_n ? pld(&lru[i]).y : 0u;
+      const uint32_t incl = wave_incl_sum(ln);
+      const uint64_t m = __ballot(i < lru_n && run + incl > cap);
+      if (m) {
+        keep = i0 + (uint32_t)__ffsll((unsigned long long)m) - 1u;
+        break;
+      }
+      run += uni((uint32_t)__shfl((int)incl, 63, 64));
+    }
+    lru_n = keep;
+    return hit;
+  }
+
   __device__ void mem_arrive(uint32_t v, uint32_t t, uint32_t sm) {
     const NodeDev rec = G.nodes[v];
     const uint4 od = optab[rec.op_nsucc & 0xFFFFu];
-    const bool dram = (od.w >> 3) & 1u;
+    bool dram = (od.w >> 3) & 1u;
+    uint64_t occm = od.y, lat = od.z;
+    if (G.tile && l2_lines) {
+      const uint32_t x = G.tile[v];
+      if (x != GTS_NO_TILE) {
+        const uint64_t work = G.ops[rec.op_nsucc & 0xFFFFu].work;
+        dram = !lru_access(x, (uint32_t)((work + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES), l2_lines);
+        occm = clamp_occ(cdiv64(work * 65536ull, hw[HW_RATE + (dram ? R_DRAM : R_L2)]));
+        lat = hw[HW_LAT + (dram ? L_DRAM : L_L2)];
+      }
+    }
     const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
     const uint64_t av = dram ? dram_av : l2_av;
     const uint64_t m = nocont ? (uint64_t)t : (av > t ? av : (uint64_t)t);
-    const uint64_t mend = m + od.y;
+    const uint64_t mend = m + occm;
     if (dram)
       dram_av = mend;
     else
       l2_av = mend;
     const uint64_t e = (uint64_t)t + od.x;
-    const uint64_t f = (e > mend ? e : mend) + od.z;
+    const uint64_t f = (e > mend ? e : mend) + lat;
     if (!complete(v, rec, t, f, sm)) return;
     release(v, rec, 1, f, rec.cta, sm);
   }
@@ -423,6 +502,9 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.noc_d = S.hw[HW_NOC_NODES];
   S.noc_w = S.hw[HW_NOC_W];
   S.noc_map = S.hw[HW_NOC_MAP];
+  S.lru = reinterpret_cast<uint2*>(sim + L.layout.off_lru);
+  S.lru_n = 0;
+  S.l2_lines = S.hw[HW_L2_LINES];
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
   const uint32_t lane = S.lane;
 

@@ -18,7 +18,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import hw as hwmod
-from .graph import (ALU, DATA, GLOAD, GSTORE, MISS, ORDER, SFU, SYNC, SYNC_EDGE, TENSOR, GraphBuilder,
+from .graph import (NO_TILE, ALU, DATA, GLOAD, GSTORE, MISS, ORDER, SFU, SYNC, SYNC_EDGE, TENSOR, GraphBuilder,
                     OpTable, TileGraph, csr_from_edges, empty_graph)
 from .rng import SplitMix64
 
@@ -217,12 +217,40 @@ def _gemm_kernel(ops: OpTable, M, N, K, BM, BN, BK, S, per_warp, a_miss_first_to
     return k
 
 
-def gemm(M=1024, N=1024, K=1024, BM=128, BN=128, BK=32, S=2, per_warp=False) -> TileGraph:
-    """Tiled GEMM C = A B in fp16 (config 1: 1024^3, 128x128x32, 2 stages)."""
+def gemm(M=1024, N=1024, K=1024, BM=128, BN=128, BK=32, S=2, per_warp=False, tiles=False) -> TileGraph:
+    """Tiled GEMM C = A B in fp16 (config 1: 1024^3, 128x128x32, 2 stages).
+    tiles: also name the tile every load / store touches (A block (m, k),
+    B block (n, k), C block (m, n)), for the LRU L2 model."""
     ops = OpTable()
     k = _gemm_kernel(ops, M, N, K, BM, BN, BK, S, per_warp, True, True)
-    return _assemble([k], ops, f"gemm_{M}x{N}x{K}_{BM}x{BN}x{BK}_s{S}",
-                     dict(M=M, N=N, K=K, BM=BM, BN=BN, BK=BK, S=S, per_warp=per_warp))
+    g = _assemble([k], ops, f"gemm_{M}x{N}x{K}_{BM}x{BN}x{BK}_s{S}",
+                  dict(M=M, N=N, K=K, BM=BM, BN=BN, BK=BK, S=S, per_warp=per_warp))
+    if tiles:
+        g.node_tile = gemm_tile_ids(M, N, K, BM, BN, BK, S, per_warp)
+    return g
+
+
+def gemm_tile_ids(M, N, K, BM, BN, BK, S, per_warp=False) -> np.ndarray:
+    """Tile id of every node of gemm(...): A blocks first (row-panel major),
+    then B blocks, then C blocks; NO_TILE for MMA nodes."""
+    T = K // BK
+    gm, gn = M // BM, N // BN
+    roles = gemm_template(T, S, per_warp)[0]
+    local = np.full(len(roles), -1, dtype=np.int64)
+    kind = np.zeros(len(roles), dtype=np.int64)  # 1 A, 2 B, 3 C
+    for i, r in enumerate(roles):
+        if r[0] == "lA":
+            kind[i], local[i] = 1, r[1]
+        elif r[0] == "lB":
+            kind[i], local[i] = 2, r[1]
+        elif r[0] == "st":
+            kind[i] = 3
+    c = np.arange(gm * gn, dtype=np.int64)[:, None]
+    mi, ni = c // gn, c % gn
+    ids = np.where(kind == 1, mi * T + local,
+          np.where(kind == 2, gm * T + ni * T + local,
+          np.where(kind == 3, gm * T + gn * T + mi * gn + ni, NO_TILE)))
+    return ids.astype(np.uint32).ravel()
 
 
 def _attention_kernel(ops: OpTable, batch, heads, kv_heads, seqlen, d, q_tile, kv_tile, causal,

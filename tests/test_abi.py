@@ -123,7 +123,7 @@ def test_hw_validation():
         r[H.FIELDS[field]] = val
         assert api.hw_validate(r) == -5, field
     r = H.preset("H100")
-    r[26] = 1  # reserved word
+    r[27] = 1  # reserved word
     assert api.hw_validate(r) == -5
 
 
@@ -169,3 +169,27 @@ def test_cluster_validation_codes():
         else:
             with pytest.raises(ValidationError):
                 validate(g)
+
+
+def test_tile_validation_codes():
+    g = W.gemm(512, 512, 256, 128, 128, 64, 2, tiles=True)
+    assert api.validate_code(g) == 0
+    validate(g)
+    bad = g.node_tile.copy()
+    mma = int(np.flatnonzero(g.op_cls[g.node_op] == TENSOR)[0])
+    bad[mma] = 7  # a compute node naming a tile
+    g2 = _mutate(g, node_tile=bad)
+    assert api.validate_code(g2) == -4
+    with pytest.raises(ValidationError):
+        validate(g2)
+    # one tile touched with two sizes: a C-block id on an A load
+    loads = np.flatnonzero(g.op_cls[g.node_op] == GLOAD)
+    bad = g.node_tile.copy()
+    bad[loads[0]] = int(g.node_tile[-1])
+    g3 = _mutate(g, node_tile=bad)
+    assert api.validate_code(g3) == -4
+    with pytest.raises(ValidationError):
+        validate(g3)
+    # tiles go to the device image; sharing is unaffected
+    assert api.device_bytes(g) > api.device_bytes(_mutate(g, node_tile=None))
+    assert api.templates(g)["templated_kernels"] == 1
