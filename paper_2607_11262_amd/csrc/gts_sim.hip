@@ -96,14 +96,19 @@ struct Sim {
 
   // Release the out-edges of a node selected by `which`: 0 = ORDER edges
   // released at issue, 1 = every other edge, released at completion.
+  static_assert(kInlineSucc == 3, "release reads the record's three inline successor copies");
   __device__ void release(uint32_t v, const NodeDev& rec, uint32_t which, uint64_t r, uint32_t src_cta,
                           uint32_t src_sm) {
     const bool ofin = (flags & GTS_ORDER_AT_FINISH) != 0;
-    const uint32_t succ_end = G.nodes[v + 1].succ_begin;
-    for (uint32_t e0 = rec.succ_begin; e0 < succ_end; e0 += 64) {
+    const uint32_t deg = rec.op_nsucc >> 16;
+    const uint32_t n = deg < 0xFFFFu ? deg : G.nodes[v + 1].succ_begin - rec.succ_begin;
+    for (uint32_t e0 = 0; e0 < n; e0 += 64) {
       const uint32_t e = e0 + lane;
-      const bool active = e < succ_end;
-      const uint32_t ent = active ? G.succ[e] : 0u;
+      const bool active = e < n;
+      // the first successors and their in-degrees are copied into the record
+      uint32_t ent = 0;
+      if (active)
+        ent = e == 0 ? rec.succ[0] : e == 1 ? rec.succ[1] : e == 2 ? rec.succ[2] : G.succ[rec.succ_begin + e];
       const uint32_t kind = ent >> GTS_EDGE_KIND_SHIFT;
       const uint32_t w = ent & GTS_EDGE_TARGET_MASK;
       const bool at_issue = (kind & kDevOrder) && !ofin;
@@ -113,8 +118,12 @@ struct Sim {
       uint32_t aux = 0;
       if (sel) {
         const uint64_t s = pld(&state[w]);
-        const uint32_t nr_cta = G.nodes[w].cta;
-        const uint32_t nr_indeg = G.indeg[w];
+        const uint32_t nr_indeg = e == 0   ? (uint32_t)rec.sindeg[0]
+                                  : e == 1 ? (uint32_t)rec.sindeg[1]
+                                  : e == 2 ? (uint32_t)rec.sindeg[2]
+                                           : (uint32_t)G.indeg[w];
+        // an edge into a node without cross-CTA in-edges stays in the source's CTA
+        const uint32_t nr_cta = (kind & kDevShared) ? G.nodes[w].cta : src_cta;
         uint32_t acc = (uint32_t)s;
         const uint32_t cnt = (uint32_t)(s >> 32) + 1;
         acc = r > acc ? (uint32_t)r : acc;
@@ -567,15 +576,30 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
       dispatch_due = false;
       continue;
     }
-    // minimum pending key (unique: cycle, phase, id)
+    // minimum pending key (unique: cycle, phase, id) with its aux word; four
+    // independent loads per lane per pass, and the last entry (which fills
+    // the taken one's place) loaded alongside
+    const uint32_t last = S.npend - 1;
+    const uint64_t lk = pld(&S.pkey[last]);
+    const uint32_t la = pld(&S.paux[last]);
     uint64_t best = ~0ull;
-    uint32_t bi = 0;
-    for (uint32_t i = lane; i < S.npend; i += 64) {
-      const uint64_t k = pld(&S.pkey[i]);
-      if (k < best) {
-        best = k;
-        bi = i;
+    uint32_t bi = 0, ba = 0;
+    for (uint32_t i0 = 0; i0 < S.npend; i0 += 256) {
+      uint64_t k[4];
+      uint32_t a[4];
+#pragma unroll
+      for (uint32_t j = 0; j < 4; ++j) {
+        const uint32_t i = i0 + j * 64u + lane;
+        k[j] = i < S.npend ? pld(&S.pkey[i]) : ~0ull;
+        a[j] = i < S.npend ? pld(&S.paux[i]) : 0u;
       }
+#pragma unroll
+      for (uint32_t j = 0; j < 4; ++j)
+        if (k[j] < best) {
+          best = k[j];
+          bi = i0 + j * 64u + lane;
+          ba = a[j];
+        }
     }
     const uint64_t mn = uni64(wave_min_u64(best));
     const uint64_t who = __ballot(best == mn);
@@ -589,15 +613,10 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
       dispatch_due = false;
       continue;
     }
-    const uint32_t aux = uni(pld(&S.paux[idx]));
-    const uint32_t last = S.npend - 1;
-    if (idx != last) {
-      const uint64_t lk = pld(&S.pkey[last]);
-      const uint32_t la = pld(&S.paux[last]);
-      if (lane == 0) {
-        pst(&S.pkey[idx], lk);
-        pst(&S.paux[idx], la);
-      }
+    const uint32_t aux = uni((uint32_t)__shfl(ba, src, 64));
+    if (idx != last && lane == 0) {
+      pst(&S.pkey[idx], lk);
+      pst(&S.paux[idx], la);
     }
     S.npend = last;
     if (kind == kEvRetire) {
