@@ -157,7 +157,7 @@ def main() -> int:
 
         def make(gi):
             g = W.gemm(*lru_params[gi], tiles=True)
-            hw = W.config_hw(2, B=B_PER_GRAPH, index=gi)
+            hw = W.workload_hw("gemm_design_sweep", B=B_PER_GRAPH, index=gi)
             rng = np.random.default_rng(5000 + gi)
             hw[:, 26] = (rng.integers(4, 65, size=B_PER_GRAPH) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
             return g, hw
@@ -185,7 +185,7 @@ def main() -> int:
         n_graphs = len(params)
 
         def make(gi):
-            return W.sweep_graph(params[gi]), W.config_hw(2, B=B_PER_GRAPH, index=gi)
+            return W.sweep_graph(params[gi]), W.workload_hw("gemm_design_sweep", B=B_PER_GRAPH, index=gi)
 
         def describe(gi):
             return params[gi]

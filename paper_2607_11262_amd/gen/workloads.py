@@ -218,7 +218,7 @@ def _gemm_kernel(ops: OpTable, M, N, K, BM, BN, BK, S, per_warp, a_miss_first_to
 
 
 def gemm(M=1024, N=1024, K=1024, BM=128, BN=128, BK=32, S=2, per_warp=False, tiles=False) -> TileGraph:
-    """Tiled GEMM C = A B in fp16 (config 1: 1024^3, 128x128x32, 2 stages).
+    """Tiled GEMM C = A B in fp16 (the 1024^3 workload: 128x128x32 tiles, 2 stages).
     tiles: also name the tile every load / store touches (A block (m, k),
     B block (n, k), C block (m, n)), for the LRU L2 model."""
     ops = OpTable()
@@ -312,7 +312,7 @@ def _coalesce(k: _Kernel) -> _Kernel:
 
 
 def flash_attention(batch=8, heads=32, seqlen=4096, d=128, q_tile=128, kv_tile=64, causal=False) -> TileGraph:
-    """Config 3: FlashAttention-style forward, warp-specialised, non-causal."""
+    """FlashAttention-style forward, warp-specialised, non-causal (B8 H32 S4096 d128 by default)."""
     ops = OpTable()
     if not causal:
         # all CTAs share one template: build the op matrix vectorised
@@ -346,7 +346,7 @@ def flash_attention(batch=8, heads=32, seqlen=4096, d=128, q_tile=128, kv_tile=6
 
 def splitkv_decode(batch=64, q_heads=32, kv_heads=8, d=128, kv_min=512, kv_max=32768, split=256,
                    kv_tile=64, seed=1004) -> TileGraph:
-    """Config 4: split-KV decode attention (one query token per sequence).
+    """Split-KV decode attention (one query token per sequence; 64 sequences by default).
     One CTA per (sequence, KV head, split of `split` tokens) runs the
     warp-specialised attention pipeline over <= split/kv_tile KV tiles and
     stores a partial (fp32 O + log-sum-exp); one reduction CTA per
@@ -437,7 +437,7 @@ def _elementwise_kernel(ops: OpTable, rows, row_tile, stages, in_hit):
 
 def decoder_layer(tokens=2048, hidden=4096, heads=32, kv_heads=8, ffn=14336, d=128, tile=64, bk=32,
                   stages=3, row_tile=16) -> TileGraph:
-    """Config 5: one Llama-like decoder layer in prefill, nine kernels with
+    """One Llama-like decoder layer in prefill (2048 tokens by default), nine kernels with
     implicit kernel boundaries: RMSNorm, QKV GEMM, RoPE, causal attention,
     O-projection, RMSNorm, fused gate+up GEMM, SwiGLU, down GEMM.  GEMMs use
     64x64x32 CTA tiles with one MMA node per warp quadrant (6 nodes per
@@ -469,7 +469,7 @@ def decoder_layer(tokens=2048, hidden=4096, heads=32, kv_heads=8, ffn=14336, d=1
 
 
 # --------------------------------------------------------------------------
-# Config 2 sweep
+# GEMM design sweep
 # --------------------------------------------------------------------------
 
 SWEEP_MNK = (1024, 2048, 4096, 8192)
@@ -502,35 +502,40 @@ def sweep_nodes(params) -> int:
 # The five workload configurations
 # --------------------------------------------------------------------------
 
-CONFIGS = {
-    1: dict(name="gemm_1024_a100", B=16),
-    2: dict(name="gemm_design_sweep", B=4096, graphs=64),
-    3: dict(name="flash_attention_fwd", B=256),
-    4: dict(name="splitkv_decode", B=1024),
-    5: dict(name="decoder_layer_prefill", B=64),
+# The benchmark workloads by name: batch size, and the number n behind their
+# seeds (graph seed 1000 + n, hardware seed 2000 + n).
+WORKLOADS = {
+    "gemm_1024_a100": dict(n=1, B=16),
+    "gemm_design_sweep": dict(n=2, B=4096, graphs=64),
+    "flash_attention_b8_h32_s4096": dict(n=3, B=256),
+    "splitkv_decode_b64": dict(n=4, B=1024),
+    "decoder_layer_prefill_2048": dict(n=5, B=64),
 }
 
 
-def config_graph(k: int, index: int = 0) -> TileGraph:
-    if k == 1:
+def workload_graph(name: str, index: int = 0) -> TileGraph:
+    """Graph of a named workload (`index`: which GEMM of the design sweep)."""
+    if name == "gemm_1024_a100":
         return gemm(1024, 1024, 1024, 128, 128, 32, 2)
-    if k == 2:
+    if name == "gemm_design_sweep":
         return sweep_graph(sweep_params()[index])
-    if k == 3:
+    if name == "flash_attention_b8_h32_s4096":
         return flash_attention()
-    if k == 4:
-        return splitkv_decode(seed=1004)
-    if k == 5:
+    if name == "splitkv_decode_b64":
+        return splitkv_decode(seed=1000 + WORKLOADS[name]["n"])
+    if name == "decoder_layer_prefill_2048":
         return decoder_layer()
-    raise KeyError(k)
+    raise KeyError(name)
 
 
-def config_hw(k: int, B: int | None = None, index: int = 0) -> np.ndarray:
-    B = CONFIGS[k]["B"] if B is None else B
-    seed = 2000 + k
-    if k == 1:
+def workload_hw(name: str, B: int | None = None, index: int = 0) -> np.ndarray:
+    """Hardware records of a named workload: A100-based for the 1024^3 GEMM,
+    H100-based sweeps otherwise (each design-sweep GEMM its own stream)."""
+    B = WORKLOADS[name]["B"] if B is None else B
+    seed = 2000 + WORKLOADS[name]["n"]
+    if name == "gemm_1024_a100":
         return hwmod.sample_a100_sweep(seed, B)
-    if k == 2:
+    if name == "gemm_design_sweep":
         return hwmod.sample_h100_sweep(seed, B, stream=index + 1)
     return hwmod.sample_h100_sweep(seed, B)
 
@@ -602,5 +607,5 @@ def random_graph(rng: SplitMix64, n_nodes_max=12, n_kernels_max=2, ctas_max=3, e
 
 
 __all__ = ["gemm", "flash_attention", "splitkv_decode", "decoder_layer", "sweep_params", "sweep_graph",
-           "sweep_nodes", "config_graph", "config_hw", "random_graph", "CONFIGS", "gemm_template",
+           "sweep_nodes", "workload_graph", "workload_hw", "random_graph", "WORKLOADS", "gemm_template",
            "attention_template", "empty_graph"]

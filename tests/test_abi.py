@@ -53,7 +53,7 @@ def _mutate(g, **kw):
 
 
 def test_valid_graphs():
-    for g in (W.config_graph(1), W.splitkv_decode(batch=3, seed=1), empty_graph(),
+    for g in (W.workload_graph("gemm_1024_a100"), W.splitkv_decode(batch=3, seed=1), empty_graph(),
               W.decoder_layer(tokens=128, hidden=256, heads=4, kv_heads=2, ffn=512, d=64)):
         assert api.validate_code(g) == 0
         assert api.device_bytes(g) > 0

@@ -8,8 +8,8 @@ from paper_2607_11262_amd.gen.graph import (GLOAD, GSTORE, MISS, TENSOR, Validat
                                              empty_graph, validate)
 
 
-def test_config1_gemm_counts():
-    g = W.config_graph(1)
+def test_gemm_1024_counts():
+    g = W.workload_graph("gemm_1024_a100")
     validate(g)
     assert g.n_nodes == 64 * (32 * 3 + 1) == 6208
     assert g.n_ctas == 64 and g.n_kernels == 1
@@ -23,8 +23,8 @@ def test_config1_gemm_counts():
     assert int((cls == TENSOR).sum()) == 64 * 32
 
 
-def test_config3_attention_counts():
-    g = W.config_graph(3)
+def test_flash_attention_counts():
+    g = W.workload_graph("flash_attention_b8_h32_s4096")
     assert g.n_ctas == 8 * 32 * 32
     assert g.n_nodes == 8192 * 322 == 2_637_824
     c = W.flash_attention(1, 2, 1024, 128, 128, 64)
@@ -33,7 +33,7 @@ def test_config3_attention_counts():
 
 
 def test_decoder_counts_formula():
-    """Config 5 node count from the template formula (the full graph is
+    """Decoder-layer node count from the template formula (the full graph is
     generated in the GPU tests): GEMMs with 64x64x32 tiles and 6 nodes per
     k-step, causal attention with 2(i+1) KV tiles for query block i."""
     def gemm_nodes(M, N, K):
@@ -81,9 +81,9 @@ def test_reproducible_digests():
     b = W.splitkv_decode(batch=5, seed=11)
     c = W.splitkv_decode(batch=5, seed=12)
     assert a.digest() == b.digest() != c.digest()
-    assert W.config_graph(1).digest() == W.config_graph(1).digest()
-    assert np.array_equal(W.config_hw(3, B=8), W.config_hw(3, B=8))
-    assert not np.array_equal(W.config_hw(2, B=8, index=0), W.config_hw(2, B=8, index=1))
+    assert W.workload_graph("gemm_1024_a100").digest() == W.workload_graph("gemm_1024_a100").digest()
+    assert np.array_equal(W.workload_hw("flash_attention_b8_h32_s4096", B=8), W.workload_hw("flash_attention_b8_h32_s4096", B=8))
+    assert not np.array_equal(W.workload_hw("gemm_design_sweep", B=8, index=0), W.workload_hw("gemm_design_sweep", B=8, index=1))
 
 
 def test_hw_presets_table3():

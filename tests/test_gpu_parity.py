@@ -100,29 +100,29 @@ def test_small_workloads(torch_cuda, name):
         compare(g, hws, flags, run_gpu(torch_cuda, g, hws, flags))
 
 
-def test_config1_full(torch_cuda):
-    g = W.config_graph(1)
-    hws = W.config_hw(1)
-    note(f"config 1 N={g.n_nodes} B={hws.shape[0]}")
+def test_gemm_1024_full(torch_cuda):
+    g = W.workload_graph("gemm_1024_a100")
+    hws = W.workload_hw("gemm_1024_a100")
+    note(f"gemm 1024 N={g.n_nodes} B={hws.shape[0]}")
     compare(g, hws, ALL, run_gpu(torch_cuda, g, hws, ALL))
 
 
-def test_config4_full(torch_cuda):
-    g = W.config_graph(4)
-    hws = W.config_hw(4)
-    note(f"config 4 N={g.n_nodes} B={hws.shape[0]}")
+def test_splitkv_decode_full(torch_cuda):
+    g = W.workload_graph("splitkv_decode_b64")
+    hws = W.workload_hw("splitkv_decode_b64")
+    note(f"split-KV decode N={g.n_nodes} B={hws.shape[0]}")
     gpu = run_gpu(torch_cuda, g, hws, ALL)
     compare(g, hws, ALL, gpu, sims=range(0, 1024, 64), nodes=True)      # per node, 16 sampled sims
     compare(g, hws, ALL, gpu, sims=range(1, 1024, 8), nodes=False)      # makespan/digest/status
 
 
-def test_config2_sweep_sample(torch_cuda):
+def test_gemm_design_sweep_sample(torch_cuda):
     ps = W.sweep_params()
     idx = sorted(range(64), key=lambda i: W.sweep_nodes(ps[i]))[:4]
     for i in idx:
         g = W.sweep_graph(ps[i])
-        hws = W.config_hw(2, B=256, index=i)
-        note(f"config 2 graph {i} {ps[i]} N={g.n_nodes} B=256")
+        hws = W.workload_hw("gemm_design_sweep", B=256, index=i)
+        note(f"design sweep graph {i} {ps[i]} N={g.n_nodes} B=256")
         gpu = run_gpu(torch_cuda, g, hws, ALL)
         assert (gpu[2] == api.SIM_INFEASIBLE).any() or True
         compare(g, hws, ALL, gpu, sims=range(0, 256, 4), nodes=True)
@@ -133,7 +133,7 @@ def test_empty_graph_and_zero_batch(torch_cuda):
     hws = H.sample_h100_sweep(3, 4)
     cyc, mk, st, dg = run_gpu(torch_cuda, g, hws, ALL)
     assert st.tolist() == [0] * 4 and mk.tolist() == [0] * 4 and dg.tolist() == [0] * 4
-    dgr = api.upload(W.config_graph(1))
+    dgr = api.upload(W.workload_graph("gemm_1024_a100"))
     res = api.simulate(dgr, np.zeros((0, 32), np.uint32), ALL)
     torch_cuda.cuda.synchronize()
     assert res.makespan.numel() == 0
@@ -202,15 +202,15 @@ def test_digest_only_mode_matches(torch_cuda):
     assert np.array_equal(a[1], b[1]) and np.array_equal(a[3], b[3]) and np.array_equal(a[2], b[2])
 
 
-def test_config2_bench_launch(torch_cuda):
+def test_gemm_design_sweep_bench_launch(torch_cuda):
     """The bench's launch shape: one sweep graph against its 4096 resident
     hardware records in one launch (digest outputs), sampled against the
     oracle; per-node cycles on two of the records."""
     ps = W.sweep_params()
     for gi in (0, 7):
         g = W.sweep_graph(ps[gi])
-        hws = W.config_hw(2, B=4096, index=gi)
-        note(f"config 2 bench launch graph {gi} N={g.n_nodes} B=4096")
+        hws = W.workload_hw("gemm_design_sweep", B=4096, index=gi)
+        note(f"design sweep bench launch graph {gi} N={g.n_nodes} B=4096")
         dg = api.upload(g)
         hs = api.upload_hw(hws)
         flags = api.OUT_DIGEST
@@ -224,32 +224,32 @@ def test_config2_bench_launch(torch_cuda):
         compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
 
 
-def test_config3_full(torch_cuda):
+def test_flash_attention_full(torch_cuda):
     """FlashAttention forward, 2.6M nodes, all 256 records in one launch."""
-    g = W.config_graph(3)
-    hws = W.config_hw(3)
-    note(f"config 3 N={g.n_nodes} B={hws.shape[0]}")
+    g = W.workload_graph("flash_attention_b8_h32_s4096")
+    hws = W.workload_hw("flash_attention_b8_h32_s4096")
+    note(f"flash attention N={g.n_nodes} B={hws.shape[0]}")
     gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
     compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 16))
     sub = hws[[3, 128, 255]]
     compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
 
 
-def test_config4_digest_all(torch_cuda):
+def test_splitkv_decode_digest_all(torch_cuda):
     """Split-KV decode: every one of the 1024 records, digest and makespan."""
-    g = W.config_graph(4)
-    hws = W.config_hw(4)
-    note(f"config 4 N={g.n_nodes} B={hws.shape[0]} (all)")
+    g = W.workload_graph("splitkv_decode_b64")
+    hws = W.workload_hw("splitkv_decode_b64")
+    note(f"split-KV decode N={g.n_nodes} B={hws.shape[0]} (all)")
     gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
     compare(g, hws, api.OUT_DIGEST, gpu, threads=16)
 
 
-def test_config5_full(torch_cuda):
+def test_decoder_layer_full(torch_cuda):
     """Decoder layer, 20.5M nodes over nine kernels, all 64 records in one
     launch; per-node cycles on two records."""
-    g = W.config_graph(5)
-    hws = W.config_hw(5)
-    note(f"config 5 N={g.n_nodes} B={hws.shape[0]}")
+    g = W.workload_graph("decoder_layer_prefill_2048")
+    hws = W.workload_hw("decoder_layer_prefill_2048")
+    note(f"decoder layer N={g.n_nodes} B={hws.shape[0]}")
     gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
     compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 8))
     sub = hws[[5, 63]]

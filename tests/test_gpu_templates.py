@@ -54,12 +54,12 @@ def test_templated_random_graphs(torch_cuda, chunk, monkeypatch):
         _same(on, off)
 
 
-def test_templated_config_graphs_on_off(torch_cuda, monkeypatch):
+def test_templated_workload_graphs_on_off(torch_cuda, monkeypatch):
     # GEMM (one template, 4 classes), flash attention, and the decoder layer
     # (8 of 9 kernels shared, attention expanded), on sweep machines
-    hws = W.config_hw(2, B=6, index=3)
+    hws = W.workload_hw("gemm_design_sweep", B=6, index=3)
     for name, g in (("gemm 2048x2048x1024", W.gemm(2048, 2048, 1024, 128, 128, 64, 3)),
-                    ("attention", W.config_graph(3)), ("decoder layer", W.config_graph(5))):
+                    ("attention", W.workload_graph("flash_attention_b8_h32_s4096")), ("decoder layer", W.workload_graph("decoder_layer_prefill_2048"))):
         note(f"{name} N={g.n_nodes} {api.templates(g)}")
         on = _run(torch_cuda, g, hws, api.OUT_DIGEST)
         monkeypatch.setenv("GTS_TEMPLATES", "0")

@@ -31,8 +31,8 @@ def test_logical_to_physical_ratio():
     assert rs == 64 and rb == 4096
 
 
-def test_config5_kernels():
-    g = W.config_graph(5)
+def test_decoder_layer_kernels():
+    g = W.workload_graph("decoder_layer_prefill_2048")
     t = api.templates(g)
     # the attention kernel (causal: CTAs of different lengths) stays expanded
     assert t["templated_kernels"] == g.n_kernels - 1
@@ -98,7 +98,7 @@ def test_random_templated_graphs_match_the_rule():
 
 
 def test_variable_cta_sizes_and_cross_cta_edges_are_not_shared():
-    assert api.templates(W.config_graph(4))["templated_kernels"] == 0  # split-KV decode
+    assert api.templates(W.workload_graph("splitkv_decode_b64"))["templated_kernels"] == 0  # split-KV decode
     for seed in range(10):
         rng = SplitMix64(seed, 77)
         g = templated_graph(rng, n_kernels=2, n_local=(4, 8), cross_kernel=1)
