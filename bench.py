@@ -119,7 +119,7 @@ def main() -> int:
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); simulations are independent, "
-              "so a multi-GPU run would shard the batch (see DESIGN.md).", file=sys.stderr)
+              "so a multi-GPU run would shard the batch across GPUs.", file=sys.stderr)
         return 2
 
     import torch

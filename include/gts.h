@@ -14,10 +14,15 @@
  *     at issue, data edges at completion, TB
  *     retire / re-dispatch ......................... Sec. 5.1, Sec. 5.3
  *   - resources as (latency, width, throughput) ... Sec. 5.2
+ *   - DSMEM / SM-cluster NoC, thread-block
+ *     clusters ..................................... Sec. 5.2, Sec. 7.2
+ *   - L2 as a fully associative LRU of lines ...... Sec. 5.2
+ *   - template sharing of isomorphic CTA graphs ... Sec. 6.4
  *   - hardware parameters ......................... Sec. 6.1, Table 3
  * Every point the paper leaves open (integer cycles, tie-breaking, phase order
- * within a cycle, servers, residency) is fixed by the rules in the design doc and
- * restated next to the code that implements it.
+ * within a cycle, servers, residency, NoC arithmetic) is fixed by one set of
+ * timing rules, restated at the top of each kernel source (gts_sim.hip,
+ * gts_window.hip) and next to the code that implements each rule.
  *
  * Conventions
  *   - Every entry point returns an int status: GTS_OK (0) or a negative
@@ -44,7 +49,8 @@ extern "C" {
 #define GTS_OK            0
 #define GTS_E_ARG        -1  /* null pointer, zero/oversized count, bad flag   */
 #define GTS_E_CYCLE      -2  /* graph has a directed cycle (incl. self-loop)   */
-#define GTS_E_EDGE_ORDER -3  /* cross-CTA edge from a higher to a lower CTA    */
+#define GTS_E_EDGE_ORDER -3  /* edge from a higher to a lower CTA, not within
+                                one cluster                                  */
 #define GTS_E_RANGE      -4  /* index / class / warp mask / degree out of range*/
 #define GTS_E_HW         -5  /* invalid hardware parameter record             */
 #define GTS_E_SCRATCH    -6  /* scratch or device image buffer too small       */
@@ -268,7 +274,8 @@ int gts_hwset_device_bytes(uint32_t B, uint64_t *bytes);
 /* Validates hw_host[0..B) (GTS_E_HW names the first bad record), copies the
  * records into the caller's device buffer dev_buf (>= gts_hwset_device_bytes)
  * on hip_stream and waits for the copy.  *out receives a handle that refers
- * to (does not own) dev_buf and remembers the largest n_sm / n_subpart. */
+ * to (does not own) dev_buf and remembers the largest n_sm / n_subpart /
+ * noc_nodes of the set. */
 int gts_hwset_upload(const gts_hw_params *hw_host, uint32_t B, void *dev_buf, uint64_t dev_bytes,
                      void *hip_stream, gts_hwset **out);
 

@@ -11,7 +11,7 @@
  * Method.  A serial event-driven list scheduler over one binary heap keyed
  * (cycle, phase, id), exactly the rules below, one simulation per call.
  * Where the paper fixes a behaviour the rule cites it; where it is silent the
- * reading used is the one listed in DESIGN.md ("Readings").
+ * reading used is stated with the rule.
  *
  *  R2  Resources (Sec. 5.2 compute: tensor cores, CUDA cores, SFUs; memory:
  *      TMA/LSU front end, L2, DRAM).  Each subpartition of an SM has one

@@ -9,7 +9,8 @@ are core cycles.
 Table 3 (Sec. 6.1) gives, per GPU: SMs, core MHz, CUDA cores and SFUs per SM,
 tensor-core FMAs per clock per SM, SRAM bandwidth/latency, L2 bandwidth
 (B/cycle) / latency, DRAM bandwidth (GB/s) / latency, TMA issue rate
-(B/cycle, Sec. 5.2 "about 100 B/cycle").  Conversions (readings, DESIGN.md):
+(B/cycle; Sec. 5.2 measures roughly 100 B per cycle).  Conversions (readings
+where the paper is silent):
   - tensor FLOP/cycle = 2 x FMAs/clk (work is counted in FLOPs);
   - DRAM B/cycle = MB/s / core MHz, floored once into Q16.16;
   - the TMA rate is per SM; A100 has no TMA and its engine (cp.async through
