@@ -113,6 +113,8 @@ def main() -> int:
                     help="consecutive steps alternate over this many HIP streams, so one graph's launch "
                          "overlaps the tail of the previous one")
     ap.add_argument("--launch-log", type=str, default="", help="write one JSON line per timed launch to this file")
+    ap.add_argument("--phase-stats", action="store_true",
+                    help="after the timed region, report the windowed kernel's per-phase counters per graph")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
                     help="only run a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -271,6 +273,13 @@ def main() -> int:
     traffic = None if (pipelining or noc or lru) else recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
+    phases = None
+    if args.phase_stats:
+        if noc or lru:  # clustered and tiled graphs run on the general kernel, which keeps no such counters
+            print("--phase-stats covers the windowed kernel only", file=sys.stderr)
+        else:
+            phases = phase_stats(api, torch, prepared, scratches[0], streams[0], sorted(set(step_graphs)), flags)
+
     cpu = None
     parity = None
     if not args.no_cpu_baseline:
@@ -339,8 +348,45 @@ def main() -> int:
         out["case_study"] = noc_case_study(api, torch, CF)
     if lru:
         out["case_study"] = lru_case_study(api, torch, W)
+    if phases is not None:
+        out["phase_stats"] = phases
     print(json.dumps(out))
     return 0
+
+
+PHASE_COLUMNS = ("windows", "local_steps", "local_nodes", "memory_arrivals", "retirements", "max_arrivals",
+                 "clk_scan", "clk_retire", "clk_local", "clk_gather", "clk_memory")
+
+
+def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
+    """Where a windowed-kernel simulation spends its time: one untimed launch
+    of each graph's first chunk, then the per-simulation counter block the
+    kernel writes at the end of each simulation's scratch slice (windows,
+    local steps, nodes issued by them, memory arrivals, retirements, the
+    largest memory batch, and shader-clock ticks in the window scan,
+    retirement, local, ring-gather and memory phases), averaged over the
+    feasible simulations."""
+    rows = {}
+    for gi in graphs:
+        dg, hs, chunk, (cyc, mk, st, dgst), n, _ = prepared[gi]
+        stride = api.scratch_bytes(dg, 2, flags) - api.scratch_bytes(dg, 1, flags)
+        api.simulate_hwset_into(dg, hs, 0, chunk, flags, None, mk[:chunk], st[:chunk], dgst[:chunk], scratch, stream)
+        torch.cuda.synchronize()
+        blk = scratch[:chunk * stride].view(chunk, stride)[:, stride - 128:].contiguous().view(torch.int64)
+        ok = (st[:chunk] == 0).cpu().numpy()
+        if not ok.any():
+            continue
+        m = blk.cpu().numpy()[ok][:, :len(PHASE_COLUMNS)].astype(np.float64).mean(axis=0)
+        row = {k: round(float(v), 1) for k, v in zip(PHASE_COLUMNS, m)}
+        clk = m[6:11]
+        row["nodes_per_local_step"] = round(float(m[2] / max(m[1], 1)), 2)
+        row["arrivals_per_window"] = round(float(m[3] / max(m[0], 1)), 2)
+        row["clk_share"] = {k[4:]: round(float(c / clk.sum()), 3) for k, c in zip(PHASE_COLUMNS[6:], clk)}
+        row["clk_per_local_step"] = round(float(m[8] / max(m[1], 1)))
+        row["clk_per_window_memory"] = round(float((m[9] + m[10]) / max(m[0], 1)))
+        rows[str(gi)] = row
+        print(f"[bench] phase stats graph {gi}: {json.dumps(row)}", file=sys.stderr, flush=True)
+    return rows
 
 
 def lru_case_study(api, torch, W):
