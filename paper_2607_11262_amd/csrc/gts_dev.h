@@ -103,7 +103,7 @@ struct Image {
   const uint16_t* tindeg;       // in-degree per template record
   const uint8_t* cclass;        // class of each CTA of a templated kernel
   const uint16_t* tops;         // [n_tops] class x slot -> op id
-  const uint32_t* tile;         // [N] tile of each load / store (kGraphTiles), else null
+  const uint32_t* tile;         // [N] tile of each load / store, numbered 0..n_tiles-1 (kGraphTiles), else null
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props, n_tops;
   uint32_t n_tiles;             // distinct tiles
 };
@@ -140,7 +140,8 @@ struct SimLayout {
   uint64_t off_rp;      // windowed kernel: later ready entries beyond LDS, [kPoolSpill][64] u64
   uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
   uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
-  uint64_t off_lru;     // general kernel: LRU L2 tiles, most recent first ([n_tiles] x {tile, lines})
+  uint64_t off_lru;     // general kernel: LRU L2, latest access stamp per tile ([n_tiles] u32)
+  uint64_t off_lru_bit; // general kernel: LRU L2, Fenwick tree of lines over stamps ([N + 1] u64)
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };

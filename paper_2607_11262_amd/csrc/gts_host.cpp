@@ -390,7 +390,9 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t n_tiles) 
   s.off_optab = off;
   off = align_up(off + (uint64_t)P * 16, gts::kAlign);
   s.off_lru = off;
-  off = align_up(off + (uint64_t)n_tiles * 8, gts::kAlign);
+  off = align_up(off + (uint64_t)n_tiles * 4, gts::kAlign);
+  s.off_lru_bit = off;
+  off = align_up(off + (n_tiles ? ((uint64_t)N + 1) * 8 : 0u), gts::kAlign);
   // The windowed kernel's per-SM queues overlay the general kernel's pending
   // list (a simulation the windowed kernel hands back is restarted from
   // scratch by the general kernel).
@@ -722,7 +724,16 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     }
   }
   std::memcpy(img.data() + L.cclass, d.cclass.data(), d.cclass.size());
-  if (d.n_tiles) std::memcpy(img.data() + L.tile, h->node_tile, (size_t)h->n_nodes * 4);
+  if (d.n_tiles) {
+    // tiles numbered densely in order of first appearance (the kernel indexes
+    // its per-tile stamps by them)
+    std::unordered_map<uint32_t, uint32_t> dense;
+    uint32_t* out = reinterpret_cast<uint32_t*>(img.data() + L.tile);
+    for (uint32_t v = 0; v < h->n_nodes; ++v) {
+      const uint32_t x = h->node_tile[v];
+      out[v] = x == GTS_NO_TILE ? GTS_NO_TILE : dense.emplace(x, (uint32_t)dense.size()).first->second;
+    }
+  }
   if (!d.tops.empty()) std::memcpy(img.data() + L.tops, d.tops.data(), d.tops.size() * 2);
   if (!d.roots.empty()) std::memcpy(img.data() + L.roots, d.roots.data(), d.roots.size() * 4);
 

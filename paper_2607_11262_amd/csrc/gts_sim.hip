@@ -63,8 +63,13 @@ struct Sim {
   uint32_t* resident;   // [nsm]
   uint32_t* noc;        // [domains][noc_d][4]: crossbar ports / mesh links
   uint32_t noc_d, noc_w, noc_map;
-  uint2* lru;           // [n_tiles] {tile, lines}, most recent first (scratch)
-  uint32_t lru_n, l2_lines;
+  // LRU L2 state (scratch): each tile's latest access stamp (1-based count
+  // of tile accesses, 0 = never) and a Fenwick tree over stamps holding, at
+  // each tile's latest stamp, that tile's line count
+  uint32_t* lru_last;   // [n_tiles], tiles numbered densely at upload
+  uint64_t* lru_bit;    // [N + 1], entry 0 unused
+  uint32_t lru_now, l2_lines;
+  uint64_t lru_total;   // lines of all distinct tiles touched so far
   uint64_t* state;      // [N]
   CtaState* cst;        // [C]
   uint64_t* pkey;       // [cap]
@@ -391,65 +396,44 @@ struct Sim {
   }
 
   // Inclusive prefix sum across the wave.
-  __device__ uint32_t wave_incl_sum(uint32_t x) const {
-    for (uint32_t o = 1; o < 64; o <<= 1) {
-      const uint32_t y = (uint32_t)__shfl_up((int)x, o, 64);
-      if (lane >= o) x += y;
-    }
-    return x;
-  }
-
   // One access of tile x (n lines) to the LRU L2 of `cap` lines; true on a
-  // hit.  The list holds each tile at most once, most recent first, and only
-  // tiles that can still hit: every entry's lines plus those above it fit in
-  // cap (a deeper tile would miss on its next access anyway, as if absent).
+  // hit: x was touched before and its lines plus those of the distinct tiles
+  // touched since fit in cap.  Those tiles are the ones whose latest stamp
+  // follows x's, so their lines are the tree's total minus its prefix sum up
+  // to x's stamp.  Lanes 0-31 read the prefix's nodes (x's stamp with its k
+  // lowest set bits cleared) and move x's lines off the nodes covering its
+  // old stamp; lanes 32-63 add them on the nodes covering the new one; a node
+  // covering both keeps its value.  Three dependent round trips per access.
   __device__ bool lru_access(uint32_t x, uint32_t n, uint32_t cap) {
-    bool found = false;
-    uint32_t pos = lru_n;
-    uint64_t above = 0, run = 0;
-    for (uint32_t i0 = 0; i0 < lru_n; i0 += 64) {
-      const uint32_t i = i0 + lane;
-      const uint2 e = i < lru_n ? pld(&lru[i]) : make_uint2(GTS_NO_TILE, 0u);
-      const uint32_t incl = wave_incl_sum(e.y);
-      const uint64_t m = __ballot(i < lru_n && e.x == x);
-      if (m) {
-        const uint32_t j = (uint32_t)__ffsll((unsigned long long)m) - 1u;
-        pos = i0 + j;
-        above = run + uni((uint32_t)__shfl((int)(incl - e.y), (int)j, 64));
-        found = true;
-        break;
-      }
-      run += uni((uint32_t)__shfl((int)incl, 63, 64));
-    }
-    const bool hit = found && above + n <= cap;
-    // entries [0, pos) move down one place, back to front; x goes on top
-    for (uint32_t i1 = pos; i1 > 0; i1 = i1 > 64 ? i1 - 64 : 0) {
-      const uint32_t lo = i1 > 64 ? i1 - 64 : 0;
-      const uint32_t i = lo + lane;
-      uint2 e = make_uint2(0, 0);
-      if (i < i1) e = pld(&lru[i]);
-      __builtin_amdgcn_s_waitcnt(0);
-      if (i < i1) pst(&lru[i + 1], e);
-      __builtin_amdgcn_s_waitcnt(0);
-    }
-    if (!found) ++lru_n;
-    if (lane == 0) pst(&lru[0], make_uint2(x, n));
+    const uint32_t N = G.n_nodes;  // at most N tile accesses, so stamps stay <= N < 2^30
+    const uint32_t t = uni(pld(&lru_last[x]));
+    const uint32_t now = ++lru_now;
+    const uint32_t k = lane & 31u;
+    const bool low = lane < 32u;
+    uint32_t d = t;
+    const uint32_t pc = (uint32_t)__popc(t);
+    for (uint32_t s = 0; s < pc; ++s)
+      if (s < k) d &= d - 1u;
+    const bool pre = low && d != 0u;
+    // k-th node covering the lane's stamp: stamp, then + lowest set bit
+    uint32_t u = low ? t : now;
+    const uint32_t steps = 32u - (uint32_t)__clz(N);
+    for (uint32_t s = 0; s < steps; ++s)
+      if (s < k && u != 0u && u <= N) u += u & (0u - u);
+    const uint32_t other = low ? now : t;
+    const bool both = other != 0u && u - (u & (0u - u)) < other && other <= u;
+    const bool upd = u != 0u && u <= N && !both;
+    const uint64_t pv = pre ? pld(&lru_bit[d]) : 0ull;
+    const uint64_t uv = upd ? pld(&lru_bit[u]) : 0ull;
+    uint64_t prefix = pv;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) prefix += __shfl_xor(prefix, o, 64);
+    prefix = uni64(prefix);
+    const bool hit = t != 0u && lru_total - prefix + n <= (uint64_t)cap;
+    if (upd) pst(&lru_bit[u], low ? uv - n : uv + n);
+    if (lane == 0) pst(&lru_last[x], now);
+    if (t == 0u) lru_total += n;
     __builtin_amdgcn_s_waitcnt(0);
-    // drop the entries that can no longer hit
-    run = 0;
-    uint32_t keep = lru_n;
-    for (uint32_t i0 = 0; i0 < lru_n; i0 += 64) {
-      const uint32_t i = i0 + lane;
-      const uint32_t ln = i < lru_n ? pld(&lru[i]).y : 0u;
-      const uint32_t incl = wave_incl_sum(ln);
-      const uint64_t m = __ballot(i < lru_n && run + incl > cap);
-      if (m) {
-        keep = i0 + (uint32_t)__ffsll((unsigned long long)m) - 1u;
-        break;
-      }
-      run += uni((uint32_t)__shfl((int)incl, 63, 64));
-    }
-    lru_n = keep;
     return hit;
   }
 
@@ -511,8 +495,10 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.noc_d = S.hw[HW_NOC_NODES];
   S.noc_w = S.hw[HW_NOC_W];
   S.noc_map = S.hw[HW_NOC_MAP];
-  S.lru = reinterpret_cast<uint2*>(sim + L.layout.off_lru);
-  S.lru_n = 0;
+  S.lru_last = reinterpret_cast<uint32_t*>(sim + L.layout.off_lru);
+  S.lru_bit = reinterpret_cast<uint64_t*>(sim + L.layout.off_lru_bit);
+  S.lru_now = 0;
+  S.lru_total = 0;
   S.l2_lines = S.hw[HW_L2_LINES];
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
   const uint32_t lane = S.lane;
@@ -542,6 +528,10 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   const uint32_t nsrv = S.nsm * S.sstride + S.nsm + L.noc_words;
   for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
   for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);
+  if (S.G.tile && S.l2_lines) {
+    for (uint32_t x = lane; x < S.G.n_tiles; x += 64) pst(&S.lru_last[x], 0u);
+    for (uint32_t i = lane; i <= S.G.n_nodes; i += 64) pst(&S.lru_bit[i], (uint64_t)0);
+  }
   for (uint32_t c = lane; c < S.G.n_ctas; c += 64) {
     pst(&S.cst[c].sm, 0u);
     pst(&S.cst[c].launch, 0u);
