@@ -256,7 +256,10 @@ int gts_scratch_bytes(const gts_graph *g, uint32_t B, uint32_t flags, uint64_t *
  *   out_digest   [B]  order-independent 64-bit digest of all (start, finish)
  *                pairs; required iff flags & GTS_OUT_DIGEST
  * Errors in arguments or in any hw record (GTS_E_HW, with the record index in
- * gts_last_error()) are reported before anything is enqueued.  Per-simulation
+ * gts_last_error()) are reported before anything is enqueued; so is
+ * GTS_E_HW for a batch whose largest n_sm and n_subpart need more LDS for
+ * the per-SM servers than one workgroup may hold on the current device
+ * (about 108 KiB at 1024 SMs x 8 subpartitions).  Per-simulation
  * outcomes go to out_status.  Results are valid once hip_stream completes;
  * calls on different streams with disjoint scratch and outputs are
  * independent.  B = 0 is a no-op. */

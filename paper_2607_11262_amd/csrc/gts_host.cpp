@@ -453,18 +453,49 @@ int check_sim_args(const gts_graph* g, uint32_t B, const uint32_t* out_cycles, c
 // whose CTAs end in memory nodes and whose cross-CTA edges leave memory
 // nodes go to the windowed kernel first; simulations it cannot finish within
 // its queue capacities (and every other graph) run on the general kernel.
+constexpr uint32_t kLdsBudget = 64 * 1024;
+
+// LDS of the general kernel: every SM's servers, then NoC servers (four per
+// domain node; at most ceil(n_sm / D) * D <= n_sm + D nodes), then the op
+// table when it still fits the budget (else it stays in scratch).
+struct GeneralLds {
+  uint32_t server_bytes, noc_words, total;
+  bool optab;
+};
+GeneralLds general_lds(const gts_graph* g, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc) {
+  GeneralLds r;
+  const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
+  r.noc_words = (g->img.props & gts::kGraphClusters) && max_noc ? 4u * (max_nsm + max_noc) : 0u;
+  r.server_bytes = 4u * (max_nsm * sstride + max_nsm + r.noc_words);
+  const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
+  r.optab = r.server_bytes + optab_bytes <= kLdsBudget;
+  r.total = r.server_bytes + (r.optab ? (uint32_t)optab_bytes : 0u);
+  return r;
+}
+
+// The largest records (many SMs x many subpartitions x three compute
+// classes) can need more LDS for the general kernel's servers than one
+// workgroup may hold on the current device: refused before anything is
+// enqueued.
+int check_lds(const gts_graph* g, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc) {
+  const uint32_t need = general_lds(g, max_nsm, max_nsub, max_noc).total;
+  int dev = 0, max_lds = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    return fail(GTS_E_HIP, "cannot query the device's LDS limit");
+  if ((uint64_t)need > (uint64_t)max_lds)
+    return fail(GTS_E_HW, "servers of %u SMs x %u subpartitions need %u B of LDS per simulation; the device allows %d",
+                max_nsm, max_nsub, need, max_lds);
+  return GTS_OK;
+}
+
 int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc,
            uint32_t* out_cycles, uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, uint8_t* sims,
            uint32_t flags, hipStream_t st) {
-  constexpr uint32_t kLdsBudget = 64 * 1024;
   const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
-  // NoC servers (four per domain node) follow the per-SM servers: at most
-  // ceil(n_sm / D) * D <= n_sm + D nodes
-  const uint32_t noc_words = (g->img.props & gts::kGraphClusters) && max_noc ? 4u * (max_nsm + max_noc) : 0u;
-  const uint32_t server_bytes = 4u * (max_nsm * sstride + max_nsm + noc_words);
-  const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
-  const bool lds_optab = server_bytes + optab_bytes <= kLdsBudget;
-  const uint32_t lds_general = server_bytes + (lds_optab ? (uint32_t)optab_bytes : 0u);
+  const GeneralLds gl = general_lds(g, max_nsm, max_nsub, max_noc);
+  const uint32_t noc_words = gl.noc_words, server_bytes = gl.server_bytes, lds_general = gl.total;
+  const bool lds_optab = gl.optab;
   gts::Launch L;
   L.img = g->img;
   L.hw = hw_dev;
@@ -818,6 +849,8 @@ int gts_simulate_batch(const gts_graph* g, const gts_hw_params* hw_host, uint32_
   if (scratch_bytes < need)
     return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
                 (unsigned long long)scratch_bytes);
+  rc = check_lds(g, max_nsm, max_nsub, max_noc);
+  if (rc) return rc;
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
   uint8_t* base = static_cast<uint8_t*>(scratch);
   hipError_t e = hipMemcpyAsync(base, hw_host, (size_t)B * sizeof(gts_hw_params), hipMemcpyHostToDevice, st);
@@ -887,6 +920,8 @@ int gts_simulate_hwset(const gts_graph* g, const gts_hwset* hw, uint32_t first, 
   if (scratch_bytes < need)
     return fail(GTS_E_SCRATCH, "scratch needs %llu bytes, got %llu", (unsigned long long)need,
                 (unsigned long long)scratch_bytes);
+  rc = check_lds(g, hw->max_nsm, hw->max_nsub, hw->max_noc);
+  if (rc) return rc;
   return launch(g, hw->dev + (uint64_t)first * gts::HW_WORDS, B, hw->max_nsm, hw->max_nsub, hw->max_noc, out_cycles,
                 out_makespan, out_status, out_digest, static_cast<uint8_t*>(scratch), flags,
                 reinterpret_cast<hipStream_t>(hip_stream));

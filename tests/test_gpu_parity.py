@@ -254,3 +254,37 @@ def test_decoder_layer_full(torch_cuda):
     compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 8))
     sub = hws[[5, 63]]
     compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
+
+
+@pytest.mark.parametrize("nsub", [1, 4])
+def test_sm_count_boundaries(torch_cuda, nsub):
+    """Machines at the SM counts where the windowed kernel changes how many
+    SMs a lane carries (64, 128, 192, 256 SMs), past its 256-SM limit (the
+    general kernel takes those), up to the record's 1024-SM maximum, in one
+    batch and each alone: bit-exact against the oracle."""
+    counts = [1, 63, 64, 65, 128, 129, 192, 255, 256, 257, 511, 1024]
+    hws = np.stack([H.preset("H100", n_sm=n, n_subpart=nsub) for n in counts])
+    graphs = (("gemm", W.gemm(2048, 2048, 512, 128, 128, 32, 3)),
+              ("decoder_tiny", W.decoder_layer(tokens=256, hidden=512, heads=8, kv_heads=2, ffn=1024, d=64)))
+    for name, g in graphs:
+        note(f"{name} N={g.n_nodes} n_sub={nsub} n_sm={counts}")
+        compare(g, hws, ALL, run_gpu(torch_cuda, g, hws))
+        for i in (2, 8, 9, 11):  # alone: the launch picks its kernel from this record's SM count
+            compare(g, hws[i:i + 1], ALL, run_gpu(torch_cuda, g, hws[i:i + 1]))
+
+
+def test_largest_records(torch_cuda):
+    """1024 SMs x 8 subpartitions (the record's maxima) on a graph that uses
+    all three compute classes: the general kernel's per-SM servers then take
+    108 KiB of LDS.  Either bit-exact against the oracle, or -- on a device
+    whose workgroups hold less -- a GTS_E_HW error before any kernel runs."""
+    g = W.decoder_layer(tokens=256, hidden=512, heads=8, kv_heads=2, ffn=1024, d=64)
+    hws = np.stack([H.preset("H100", n_sm=1024, n_subpart=8), H.preset("H100", n_sm=1000, n_subpart=7)])
+    note(f"decoder_tiny N={g.n_nodes} n_sm=1024/1000 n_sub=8/7")
+    try:
+        gpu = run_gpu(torch_cuda, g, hws)
+    except api.GtsError as e:
+        assert e.code == -5 and "LDS" in str(e), str(e)
+        note(f"refused: {e}")
+        return
+    compare(g, hws, ALL, gpu)
