@@ -113,6 +113,10 @@ def main() -> int:
                     help="consecutive steps alternate over this many HIP streams, so one graph's launch "
                          "overlaps the tail of the previous one")
     ap.add_argument("--launch-log", type=str, default="", help="write one JSON line per timed launch to this file")
+    ap.add_argument("--host-io", action="store_true",
+                    help="after the timed region, time the same steps through host buffers: hardware records "
+                         "passed from host memory per call (gts_simulate_batch) and results copied back, then "
+                         "also with each step's graph uploaded from host arrays")
     ap.add_argument("--phase-stats", action="store_true",
                     help="after the timed region, report the windowed kernel's per-phase counters per graph")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -273,6 +277,9 @@ def main() -> int:
     traffic = None if (pipelining or noc or lru) else recorded_traffic(len(launches))
     statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
 
+    host_io_rates = host_io(api, torch, prepared, host_graphs, scratches, streams, step_graphs, flags) \
+        if args.host_io else None
+
     phases = None
     if args.phase_stats:
         if noc or lru:  # clustered and tiled graphs run on the general kernel, which keeps no such counters
@@ -350,8 +357,50 @@ def main() -> int:
         out["case_study"] = lru_case_study(api, torch, W)
     if phases is not None:
         out["phase_stats"] = phases
+    if host_io_rates is not None:
+        out["host_io"] = host_io_rates
     print(json.dumps(out))
     return 0
+
+
+def host_io(api, torch, prepared, host_graphs, scratches, streams, step_graphs, flags):
+    """The timed steps again, end to end from host memory (never the
+    headline value): (a) each launch passes its hardware records from host
+    memory (the C ABI copies them over PCIe into scratch) and each step's
+    makespan / status / digest come back to pinned host memory; (b) as (a),
+    with each step's graph also uploaded from its host arrays (validation and
+    image construction on the CPU, then the copy)."""
+    pinned = {gi: [torch.empty(prepared[gi][3][i].shape, dtype=prepared[gi][3][i].dtype, pin_memory=True)
+                   for i in (1, 2, 3)] for gi in set(step_graphs)}
+    rates = {}
+    for mode in ("records", "records+graph"):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        nodes = 0
+        keep = []  # uploaded images stay alive until every launch that reads them is done
+        for k, gi in enumerate(step_graphs):
+            stream, scratch = streams[k % len(streams)], scratches[k % len(streams)]
+            dg, hs, chunk, (cyc, mk, st, dgst), n, _ = prepared[gi]
+            g, hw = host_graphs[gi]
+            if mode == "records+graph":
+                dg = api.upload(g, stream)
+                keep.append(dg)
+            for first in range(0, B_PER_GRAPH, chunk):
+                b = min(chunk, B_PER_GRAPH - first)
+                api.simulate_into(dg, hw[first:first + b], flags, None, mk[first:first + b], st[first:first + b],
+                                  dgst[first:first + b], scratch, stream)
+            with torch.cuda.stream(stream):
+                for dst, src in zip(pinned[gi], (mk, st, dgst)):
+                    dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        keep.clear()
+        for gi in set(step_graphs):
+            nodes_ok = prepared[gi][4] * int((pinned[gi][1] == 0).sum().item())
+            nodes += nodes_ok * step_graphs.count(gi)
+        rates[mode] = {"value": nodes / dt, "unit": "simulated tile-nodes/s", "seconds": dt}
+        print(f"[bench] host io {mode}: {nodes / dt:.4e} tile-nodes/s over {dt:.2f} s", file=sys.stderr, flush=True)
+    return rates
 
 
 PHASE_COLUMNS = ("windows", "local_steps", "local_nodes", "memory_arrivals", "retirements", "max_arrivals",
