@@ -293,14 +293,16 @@ struct WSim {
   }
 
   // Smallest entry of each SM slot with its index (far indices carry bit 31).
+  // Selects rather than branches: a branch per slot costs more exec-mask
+  // bookkeeping than the compare it guards.
   __device__ __forceinline__ static void consider(uint64_t k, uint32_t i, uint64_t (&best)[NB], uint32_t (&bi)[NB]) {
     const uint32_t j = (uint32_t)(k >> 30) & 3u;
 #pragma unroll
-    for (uint32_t jj = 0; jj < NB; ++jj)
-      if (j == jj && k < best[jj]) {
-        best[jj] = k;
-        bi[jj] = i;
-      }
+    for (uint32_t jj = 0; jj < NB; ++jj) {
+      const bool t = (j == jj) & (k < best[jj]);
+      best[jj] = t ? k : best[jj];
+      bi[jj] = t ? i : bi[jj];
+    }
   }
   __device__ __forceinline__ void scan_far(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
     for (uint32_t i0 = 0; i0 < n; i0 += 8) {
@@ -630,11 +632,11 @@ struct WSim {
     for (uint32_t rep = 0; rep < NB; ++rep) {
       uint32_t sel = NB, mx = 0;
 #pragma unroll
-      for (uint32_t j = 0; j < NB; ++j)
-        if (((taken >> j) & 1u) && (sel == NB || bi[j] > mx)) {
-          sel = j;
-          mx = bi[j];
-        }
+      for (uint32_t j = 0; j < NB; ++j) {
+        const bool t = ((taken >> j) & 1u) & ((sel == NB) | (bi[j] > mx));
+        sel = t ? j : sel;
+        mx = t ? bi[j] : mx;
+      }
       if (sel != NB) {
         taken &= ~(1u << sel);
         if (mx & 0x80000000u) {
