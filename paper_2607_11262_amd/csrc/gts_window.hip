@@ -58,6 +58,7 @@ namespace {
 constexpr uint64_t kNoKey = ~0ull;
 constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u;
 constexpr uint32_t GQ = 3;               // ring entries loaded per SM and window
+constexpr uint32_t kMaxSubpart = GTS_MAX_SUBPART;
 
 // Node state: latest release cycle (low word) | released in-edges (high word).
 __device__ __forceinline__ uint32_t* st_acc(uint64_t* st) { return reinterpret_cast<uint32_t*>(st); }
@@ -679,7 +680,11 @@ struct WSim {
       ev_s[w] = ok[w] ? w_aux[i] : 0u;
       rec[w] = rec_of(ev_v[w]);
     }
-    // timing on the SM's servers
+    // timing on the SM's servers: the node holds its class's subpartition
+    // lanes (compute), the shared-memory pipe, or the global-memory engine
+    // (memory nodes; L2 / DRAM follow in the memory phase), SYNC nothing;
+    // every held server becomes free at start + occupancy.  One code path
+    // for all classes, the server reads issued together.
     uint64_t rel_i[W], rel_f[W];
     bool is_mem[W];
 #pragma unroll
@@ -689,37 +694,31 @@ struct WSim {
       if (ok[j]) {
         const uint4 od = optab[rec[j].op()];
         const uint32_t cls = od.w & 7u;
-        uint32_t* S = srv + ev_s[j] * sstride;
-        uint64_t st = ev_t[j], f = 0;
-        if (cls <= C_SFU) {
-          const uint32_t lanes = (od.w >> 8) & 0xFFu;
-          uint32_t* La = S + (od.w >> 16);  // this class's lanes
-          if (!nocont)
-            for (uint32_t l = 0; l < nsub; ++l)
-              if ((lanes >> l) & 1u) st = La[l] > st ? La[l] : st;
-          f = st + od.x + od.z;
-          if (f <= kMaxCycle)
-            for (uint32_t l = 0; l < nsub; ++l)
-              if ((lanes >> l) & 1u) La[l] = (uint32_t)(st + od.x);
-        } else if (cls == C_SMEM) {
-          if (!nocont) st = S[smem_w] > st ? S[smem_w] : st;
-          f = st + od.x + od.z;
-          if (f <= kMaxCycle) S[smem_w] = (uint32_t)(st + od.x);
-        } else if (cls == C_SYNC) {
-          f = st + od.z;
-        } else {  // memory node: engine now, L2/DRAM in the memory phase
-          if (!nocont) st = S[smem_w + 1] > st ? S[smem_w + 1] : st;
-          is_mem[j] = true;
-          f = st + od.x;  // end of engine occupancy
-          if (f <= kMaxCycle) {
-            S[smem_w + 1] = (uint32_t)f;
-            mq_push(ev_s[j], mkkey(st, kEvMem, ev_v[j]), rec[j].op());
-          }
+        const bool comp = cls <= C_SFU;
+        is_mem[j] = cls == C_GLOAD || cls == C_GSTORE;
+        const uint32_t held = comp ? (od.w >> 8) & 0xFFu : (cls == C_SYNC ? 0u : 1u);
+        uint32_t* Sv = srv + ev_s[j] * sstride + (comp ? (od.w >> 16) : smem_w + (is_mem[j] ? 1u : 0u));
+        uint64_t st = ev_t[j];
+        if (!nocont) {
+          uint32_t busy = 0;
+#pragma unroll
+          for (uint32_t l = 0; l < kMaxSubpart; ++l)
+            if (l < nsub) {
+              const uint32_t a = Sv[comp ? l : 0u];
+              busy = ((held >> l) & 1u) && a > busy ? a : busy;
+            }
+          st = busy > st ? busy : st;
         }
+        const uint64_t f = st + od.x + (is_mem[j] ? 0u : od.z);
         if (f > kMaxCycle) {
           bad |= kBadOverflow;
           ok[j] = false;
         } else {
+          const uint32_t free_at = (uint32_t)(st + od.x);
+#pragma unroll
+          for (uint32_t l = 0; l < kMaxSubpart; ++l)
+            if (l < nsub && ((held >> l) & 1u)) Sv[comp ? l : 0u] = free_at;
+          if (is_mem[j]) mq_push(ev_s[j], mkkey(st, kEvMem, ev_v[j]), rec[j].op());
           rel_i[j] = st + 1;
           rel_f[j] = f;
           if (!is_mem[j]) record(ev_v[j], st, f);
