@@ -293,6 +293,32 @@ struct WSim {
     far_push(l, key);
   }
 
+  // Up to kInlineSucc entries of one lane onto SM s's lists (want[k]): the
+  // near slots are reserved with all atomics in flight, then filled; as for
+  // one push at a time, the first free slots go to near entries and the rest
+  // to far (hot).  The order within a list does not matter.
+  __device__ __forceinline__ void rq_push_n(uint32_t s, const bool (&want)[kInlineSucc],
+                                            const uint32_t (&cyc)[kInlineSucc], const uint32_t (&v)[kInlineSucc]) {
+    const uint32_t l = s & 63u;
+    uint32_t slot[kInlineSucc];
+#pragma unroll
+    for (uint32_t k = 0; k < kInlineSucc; ++k) slot[k] = want[k] && cyc[k] < Hnear ? atomicAdd(&nr_cnt[l], 1u) : kNear;
+#pragma unroll
+    for (uint32_t k = 0; k < kInlineSucc; ++k) {
+      if (!want[k]) continue;
+      const uint64_t key = ((uint64_t)cyc[k] << 32) | ((uint64_t)(s >> 6) << 30) | v[k];
+      if (slot[k] < kNear) {
+        nr[slot[k] * 64u + l] = key;
+      } else {
+        if (cyc[k] < Hnear) {
+          atomicSub(&nr_cnt[l], 1u);
+          fr_hot[l] = 1u;
+        }
+        far_push(l, key);
+      }
+    }
+  }
+
   // Smallest entry of each SM slot with its index (far indices carry bit 31).
   // Selects rather than branches: a branch per slot costs more exec-mask
   // bookkeeping than the compare it guards.
@@ -749,19 +775,22 @@ struct WSim {
     }
 #pragma unroll
     for (uint32_t j = 0; j < W; ++j) {
+      bool rdy[kInlineSucc];
+      uint32_t racc[kInlineSucc], rw[kInlineSucc];
 #pragma unroll
       for (uint32_t k = 0; k < kInlineSucc; ++k) {
-        if (sel[j][k]) {
-          const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
-          const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
-          const uint64_t r = ((bits & kDevOrder) && !ofin) ? rel_i[j] : rel_f[j];
-          const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
-          uint32_t acc = (uint32_t)sv[j][k];
-          acc = r > acc ? (uint32_t)r : acc;
-          if (rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
-          if (cnt == rec[j].sindeg(k)) rq_push(ev_s[j], acc, w);
-        }
+        const uint32_t bits = rec[j].succ(k) >> GTS_EDGE_KIND_SHIFT;
+        const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
+        const uint64_t r = ((bits & kDevOrder) && !ofin) ? rel_i[j] : rel_f[j];
+        const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
+        uint32_t acc = (uint32_t)sv[j][k];
+        acc = r > acc ? (uint32_t)r : acc;
+        if (sel[j][k] && rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
+        rdy[k] = sel[j][k] && cnt == rec[j].sindeg(k);
+        racc[k] = acc;
+        rw[k] = w;
       }
+      rq_push_n(ev_s[j], rdy, racc, rw);
       if (ok[j]) {
         if (!is_mem[j] && !mem_only) {  // a compute node never completes its CTA
           const uint32_t mf = (uint32_t)rel_f[j] > cs[j].w ? (uint32_t)rel_f[j] : cs[j].w;
@@ -947,17 +976,20 @@ struct WSim {
 #pragma unroll
     for (uint32_t j = 0; j < W; ++j) {
       const uint32_t f = ff[j];
+      bool rdy[kInlineSucc];
+      uint32_t racc[kInlineSucc], rw[kInlineSucc];
 #pragma unroll
       for (uint32_t k = 0; k < kInlineSucc; ++k) {
-        if (sel[j][k]) {
-          const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
-          const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
-          uint32_t acc = (uint32_t)sv[j][k];
-          acc = f > acc ? f : acc;
-          if (rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
-          if (cnt == rec[j].sindeg(k)) rq_push(ss[j], acc, w);
-        }
+        const uint32_t w = rec[j].succ(k) & GTS_EDGE_TARGET_MASK;
+        const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
+        uint32_t acc = (uint32_t)sv[j][k];
+        acc = f > acc ? f : acc;
+        if (sel[j][k] && rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
+        rdy[k] = sel[j][k] && cnt == rec[j].sindeg(k);
+        racc[k] = acc;
+        rw[k] = w;
       }
+      rq_push_n(ss[j], rdy, racc, rw);
       if (ok[j]) {
         record(vv[j], tt[j], f);
         const uint32_t left = cs[j].z - 1u;
