@@ -1281,16 +1281,36 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       }
       uint64_t K = wmin64(Kl);
       M = wave_sum_u32(due_count(ehi, elo, K));
-      if (M > kWinCap) {  // keep the kWinCap smallest keys
-        uint64_t lo = T << 32, hi = K;  // count(< lo) = 0, count(< hi) > kWinCap
-        while (hi - lo > 1) {
-          const uint64_t mid = lo + (hi - lo) / 2;
-          if (wave_sum_u32(due_count(ehi, elo, mid)) <= kWinCap)
-            lo = mid;
-          else
-            hi = mid;
+      if (M > kWinCap) {
+        // keep at most kWinCap: the largest cycle boundary that does (a
+        // window spans at most 1024 cycles: a few halvings), or, when cycle T
+        // alone holds more, a boundary between the keys of cycle T
+        const uint64_t Kmax = K;  // count(< Kmax) > kWinCap
+        uint64_t lo = T, hi = Kmax >> 32;  // cycles; count(< T << 32) = 0
+        if (wave_sum_u32(due_count(ehi, elo, hi << 32)) <= kWinCap) {
+          lo = hi;
+        } else {
+          while (hi - lo > 1) {
+            const uint64_t mid = lo + (hi - lo) / 2;
+            if (wave_sum_u32(due_count(ehi, elo, mid << 32)) <= kWinCap)
+              lo = mid;
+            else
+              hi = mid;
+          }
         }
-        K = lo;
+        K = lo << 32;
+        if (lo == T) {
+          uint64_t klo = T << 32, khi = (T + 1) << 32;  // count(< khi) > kWinCap
+          khi = Kmax < khi ? Kmax : khi;
+          while (khi - klo > 1) {
+            const uint64_t mid = klo + (khi - klo) / 2;
+            if (wave_sum_u32(due_count(ehi, elo, mid)) <= kWinCap)
+              klo = mid;
+            else
+              khi = mid;
+          }
+          K = klo;
+        }
         M = wave_sum_u32(due_count(ehi, elo, K));
       }
       {

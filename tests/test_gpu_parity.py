@@ -288,3 +288,26 @@ def test_largest_records(torch_cuda):
         note(f"refused: {e}")
         return
     compare(g, hws, ALL, gpu)
+
+
+def test_simultaneous_arrivals_split(torch_cuda):
+    """Every SM's CTA starts with loads issued at one cycle: with 256 SMs
+    that is up to 512 memory arrivals of a single cycle, more than one
+    window of the windowed kernel takes, so the window boundary falls
+    between the keys of one cycle.  Bit-exact against the oracle."""
+    from paper_2607_11262_amd.gen.graph import ALU, GLOAD, GSTORE, MISS, GraphBuilder
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    for c in range(512):
+        b.cta()
+        la = b.node(GLOAD, 1024 * (c % 3 + 1), 0xF, MISS if c % 2 else 0)
+        lb = b.node(GLOAD, 2048, 0xF, MISS)
+        a = b.node(ALU, 4096, 0xF)
+        st = b.node(GSTORE, 512, 0xF, MISS)
+        b.edge(la, a)
+        b.edge(lb, a)
+        b.edge(a, st)
+    g = b.build("simultaneous_loads")
+    hws = np.stack([H.preset("H100", n_sm=n) for n in (256, 255, 200, 129, 64)])
+    note(f"simultaneous arrivals N={g.n_nodes}")
+    compare(g, hws, ALL, run_gpu(torch_cuda, g, hws, ALL))
