@@ -802,36 +802,63 @@ struct WSim {
     }
   }
 
-  // ---- rank sort of w_key[0, M) (M <= 64 E): stage[rank] = slot, where a
-  // key's rank counts the smaller keys (and, with ties, the equal keys in
-  // lower slots).  Every lane reads each key by an LDS broadcast.
+  // ---- sort of w_key[0, M) (M <= 64 E) by (key, slot): stage[i] = the
+  // slot of the i-th smallest (equal keys in slot order).  A bitonic network
+  // over 64 E positions, position lane * E + r in register r of the lane
+  // (slots past M sort last); partners in other lanes come by cross-lane
+  // shuffles, the rest are the lane's own registers.
   template <uint32_t E>
-  __device__ __forceinline__ void rank_sort(uint32_t M, bool ties) {
+  __device__ __forceinline__ void rank_sort(uint32_t M) {
+    static_assert(E == 1 || E == 2 || E == 4, "64, 128 or 256 positions");
+    constexpr uint32_t n = 64u * E;
     uint64_t k[E];
-    uint32_t rk[E];
+    uint32_t sl[E];
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
-      const uint32_t i = r * 64u + lane;
-      k[r] = i < M ? w_key[i] : kNoKey;
-      rk[r] = 0;
+      const uint32_t s = r * 64u + lane;
+      k[r] = s < M ? w_key[s] : kNoKey;
+      sl[r] = s;  // distinct, so every comparison is strict
     }
-    for (uint32_t i0 = 0; i0 < M; i0 += 16) {
-      uint64_t kk[16];
 #pragma unroll
-      for (uint32_t q = 0; q < 16; ++q) kk[q] = w_key[i0 + q < M ? i0 + q : M - 1];
+    for (uint32_t kk = 2; kk <= n; kk <<= 1) {
 #pragma unroll
-      for (uint32_t q = 0; q < 16; ++q)
+      for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+        if (j >= E) {
 #pragma unroll
-        for (uint32_t r = 0; r < E; ++r) {
-          const uint32_t i = r * 64u + lane;
-          const bool before = kk[q] < k[r] || (ties && kk[q] == k[r] && i0 + q < i);
-          rk[r] += (i0 + q < M && before) ? 1u : 0u;
+          for (uint32_t r = 0; r < E; ++r) {
+            const int lj = (int)(j / E);
+            const uint64_t pk = ((uint64_t)(uint32_t)__shfl_xor((int)(uint32_t)(k[r] >> 32), lj, 64) << 32) |
+                                (uint32_t)__shfl_xor((int)(uint32_t)k[r], lj, 64);
+            const uint32_t ps = (uint32_t)__shfl_xor((int)sl[r], lj, 64);
+            const uint32_t i = lane * E + r;
+            const bool keep_min = ((i & j) == 0) == ((i & kk) == 0);
+            const bool pless = pk < k[r] || (pk == k[r] && ps < sl[r]);
+            const bool take = keep_min == pless;
+            k[r] = take ? pk : k[r];
+            sl[r] = take ? ps : sl[r];
+          }
+        } else {
+#pragma unroll
+          for (uint32_t r = 0; r < E; ++r) {
+            if ((r & j) != 0) continue;  // r is the lower position of its pair
+            const uint32_t q = r | j, i = lane * E + r;
+            const bool up = (i & kk) == 0;
+            const bool qless = k[q] < k[r] || (k[q] == k[r] && sl[q] < sl[r]);
+            const bool sw = up == qless;
+            const uint64_t tk = k[r];
+            const uint32_t ts = sl[r];
+            k[r] = sw ? k[q] : k[r];
+            sl[r] = sw ? sl[q] : sl[r];
+            k[q] = sw ? tk : k[q];
+            sl[q] = sw ? ts : sl[q];
+          }
         }
+      }
     }
     wsync();
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r)
-      if (r * 64u + lane < M) stage[rk[r]] = r * 64u + lane;
+      if (lane * E + r < M) stage[lane * E + r] = sl[r];
     wsync();
   }
 
@@ -839,7 +866,7 @@ struct WSim {
   // serve them in that order, then complete them on their SMs' lanes.
   template <uint32_t E>
   __device__ __forceinline__ void memory_phase(uint32_t M) {
-    rank_sort<E>(M, false);  // arrival keys are distinct
+    rank_sort<E>(M);
     uint64_t k[E];
     uint32_t p[E];
 #pragma unroll
@@ -1207,11 +1234,11 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       }
       if (R) {
         if (R <= 64)
-          S.template rank_sort<1>(R, true);
+          S.template rank_sort<1>(R);
         else if (R <= 128)
-          S.template rank_sort<2>(R, true);
+          S.template rank_sort<2>(R);
         else
-          S.template rank_sort<4>(R, true);
+          S.template rank_sort<4>(R);
         bool stop = false;
         for (uint32_t i = 0; i < R && !stop;) {  // retirement i in cycle order is w_key[stage[i]]
           const uint64_t r = uni64(S.w_key[S.stage[i]] >> 32);
