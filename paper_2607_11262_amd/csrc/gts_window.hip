@@ -802,17 +802,16 @@ struct WSim {
     }
   }
 
-  // ---- sort of w_key[0, M) (M <= 64 E) by (key, slot): stage[i] = the
-  // slot of the i-th smallest (equal keys in slot order).  A bitonic network
+  // ---- sort of w_key[0, M) (M <= 64 E) by (key, slot): position lane * E
+  // + r gets the key and slot of the (lane * E + r)-th smallest (equal keys
+  // in slot order; rank_sort also writes stage[i] = that slot).  A bitonic network
   // over 64 E positions, position lane * E + r in register r of the lane
   // (slots past M sort last); partners in other lanes come by cross-lane
   // shuffles, the rest are the lane's own registers.
   template <uint32_t E>
-  __device__ __forceinline__ void rank_sort(uint32_t M) {
+  __device__ __forceinline__ void sort_batch(uint32_t M, uint64_t (&k)[E], uint32_t (&sl)[E]) {
     static_assert(E == 1 || E == 2 || E == 4, "64, 128 or 256 positions");
     constexpr uint32_t n = 64u * E;
-    uint64_t k[E];
-    uint32_t sl[E];
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
       const uint32_t s = r * 64u + lane;
@@ -855,6 +854,12 @@ struct WSim {
         }
       }
     }
+  }
+  template <uint32_t E>
+  __device__ __forceinline__ void rank_sort(uint32_t M) {
+    uint64_t k[E];
+    uint32_t sl[E];
+    sort_batch<E>(M, k, sl);
     wsync();
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r)
@@ -866,15 +871,11 @@ struct WSim {
   // serve them in that order, then complete them on their SMs' lanes.
   template <uint32_t E>
   __device__ __forceinline__ void memory_phase(uint32_t M) {
-    rank_sort<E>(M);
+    // arrival lane * E + r in (cycle, id) order: key k[r], slot p[r]
+    // (positions past M hold kNoKey)
     uint64_t k[E];
     uint32_t p[E];
-#pragma unroll
-    for (uint32_t r = 0; r < E; ++r) {
-      const uint32_t pos = lane * E + r;
-      p[r] = pos < M ? stage[pos] : 0u;
-      k[r] = pos < M ? w_key[p[r]] : kNoKey;
-    }
+    sort_batch<E>(M, k, p);
     Compose fl2{kNegCycle, 0}, fdr{kNegCycle, 0};
     uint4 od[E];
 #pragma unroll
@@ -928,28 +929,27 @@ struct WSim {
   // nodes; shared nodes use atomics), packs their slots into stage[] and
   // completes them W per lane.
   __device__ __forceinline__ void complete_arrivals() {
+    // each SM's split (first slot | count << 16), read once: completions
+    // push only to far lists, so the near lists it shares stay untouched
+    uint32_t sp[NB];
     uint32_t rounds = 0;
 #pragma unroll
     for (uint32_t j = 0; j < NB; ++j) {
       const uint32_t s = lane + 64u * j;
-      if (j < nslot && s < nsm) rounds = (dsc[s] >> 16) > rounds ? (dsc[s] >> 16) : rounds;
+      sp[j] = j < nslot && s < nsm ? dsc[s] : 0u;
+      rounds = (sp[j] >> 16) > rounds ? (sp[j] >> 16) : rounds;
     }
     rounds = (uint32_t)wmax64(rounds);
     for (uint32_t r = 0; r < rounds; ++r) {
       uint32_t cnt = 0;
 #pragma unroll
-      for (uint32_t j = 0; j < NB; ++j) {
-        const uint32_t s = lane + 64u * j;
-        if (j < nslot && s < nsm) cnt += r < (dsc[s] >> 16);
-      }
+      for (uint32_t j = 0; j < NB; ++j) cnt += r < (sp[j] >> 16);
       const uint32_t incl = wave_incl_sum_u32(cnt);
       const uint32_t E = lane_u32(incl, 63);
       uint32_t p = incl - cnt;
 #pragma unroll
-      for (uint32_t j = 0; j < NB; ++j) {
-        const uint32_t s = lane + 64u * j;
-        if (j < nslot && s < nsm && r < (dsc[s] >> 16)) stage[p++] = (dsc[s] & 0xFFFFu) + r;
-      }
+      for (uint32_t j = 0; j < NB; ++j)
+        if (r < (sp[j] >> 16)) stage[p++] = (sp[j] & 0xFFFFu) + r;
       wsync();
       if (E <= 64) {
         complete_events<1>(0, E);
