@@ -414,8 +414,11 @@ def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
     local steps, nodes issued by them, memory arrivals, retirements, the
     largest memory batch, and shader-clock ticks in the window scan,
     retirement, local, ring-gather and memory phases), averaged over the
-    feasible simulations."""
+    feasible simulations.  The clocks are read only in these launches
+    (GTS_WINDOW_CLOCKS): each read waits for every outstanding scalar and LDS
+    access, which the timed launches avoid."""
     rows = {}
+    os.environ["GTS_WINDOW_CLOCKS"] = "1"  # the kernel reads its clock only when asked
     for gi in graphs:
         dg, hs, chunk, (cyc, mk, st, dgst), n, _ = prepared[gi]
         stride = api.scratch_bytes(dg, 2, flags) - api.scratch_bytes(dg, 1, flags)
@@ -435,6 +438,7 @@ def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
         row["clk_per_window_memory"] = round(float((m[9] + m[10]) / max(m[0], 1)))
         rows[str(gi)] = row
         print(f"[bench] phase stats graph {gi}: {json.dumps(row)}", file=sys.stderr, flush=True)
+    os.environ.pop("GTS_WINDOW_CLOCKS", None)
     return rows
 
 

@@ -180,6 +180,7 @@ struct Launch {
   uint32_t max_nsub;           // largest n_subpart of the batch
   uint32_t qp;                 // windowed kernel: later ready entries per lane held in LDS
   uint32_t noc_words;          // general kernel: NoC server words after the per-SM servers
+  uint32_t clocks;             // windowed kernel: time its phases with the shader clock
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on

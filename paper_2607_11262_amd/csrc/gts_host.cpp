@@ -514,6 +514,8 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.max_nsub = max_nsub;
   L.noc_words = noc_words;
   L.qp = 0;
+  const char* clocks = std::getenv("GTS_WINDOW_CLOCKS");  // diagnostics: per-phase shader clocks
+  L.clocks = clocks && std::strcmp(clocks, "0") != 0 ? 1u : 0u;
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel

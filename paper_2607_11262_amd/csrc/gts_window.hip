@@ -1149,10 +1149,13 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.st_maxrq = S.st_maxmq = S.st_maxret = 0;
   S.tm0 = S.tm1 = S.tm2 = S.tm3 = S.tm4 = 0;
 
+  // phase clocks only on request: reading the clock waits for every
+  // outstanding scalar and LDS access
+  const bool clk = L.clocks != 0;
   S.dispatch(0);
   wsync();
   while (!__ballot(S.bad != 0)) {
-    const uint64_t c0 = __builtin_amdgcn_s_memtime();
+    const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
     // T: lower bound of the earliest pending event
     uint64_t tmin = kNoKey;
     {
@@ -1173,7 +1176,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (T == kNoKey) break;
     uint64_t H0 = T + S.Lm;
     H0 = H0 < 0xFFFFFFFFull ? H0 : 0xFFFFFFFFull;  // cycles never exceed kMaxCycle
-    const uint64_t c1 = __builtin_amdgcn_s_memtime();
+    const uint64_t c1 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
 
     // Retirement phase: retirements below H0, in cycle order, each distinct
     // cycle followed by dispatch.  More than kWinCap of them lower H0.
@@ -1256,7 +1259,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         if (__ballot(S.bad != 0)) break;
       }
     }
-    const uint64_t c2 = __builtin_amdgcn_s_memtime();
+    const uint64_t c2 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
 
     // Local phase.
     S.pool_rebuild(H0);
@@ -1268,7 +1271,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     }
     S.Hnear = 0;
     wsync();
-    const uint64_t c3 = __builtin_amdgcn_s_memtime();
+    const uint64_t c3 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
     if (__ballot(S.bad != 0)) break;
 
     // Memory phase: the arrivals whose key (cycle, id) is below K <= H0 << 32.
@@ -1374,7 +1377,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     }
     wsync();
     if (__ballot(S.bad != 0)) break;
-    const uint64_t c4 = __builtin_amdgcn_s_memtime();
+    const uint64_t c4 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
     if (M) {
       if (M <= 64)
         S.template memory_phase<1>(M);
@@ -1384,7 +1387,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         S.template memory_phase<4>(M);
     }
     wsync();
-    const uint64_t c5 = __builtin_amdgcn_s_memtime();
+    const uint64_t c5 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
     ++S.st_windows;
     S.st_mem += M;
     S.st_maxm = M > S.st_maxm ? M : S.st_maxm;
