@@ -159,7 +159,6 @@ constexpr uint32_t kRetireLds = 128;   // pending CTA retirements held in LDS ..
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
 constexpr uint32_t kWinCap = 128;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
-static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
 
@@ -184,44 +183,43 @@ struct Launch {
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on
-// even words).  NS: largest n_sm of the batch; SS: server words per SM
-// (server_stride at the largest n_subpart); QP: later ready entries per lane
-// held in LDS; NT: template class x slot op entries (u16).
+// even words).  The parts of fixed size come first, at constant offsets the
+// kernel addresses without registers; then the parts sized by the batch.
+// NS: largest n_sm of the batch; SS: server words per SM (server_stride at
+// the largest n_subpart); QP: later ready entries per lane held in LDS; NT:
+// template class x slot op entries (u16).
+constexpr uint32_t kWinNrCnt = 0, kWinFrCnt = 64, kWinFrMin = 128, kWinFrHot = 192;
+constexpr uint32_t kWinRetCnt = 256, kWinRetMin = 257;
+constexpr uint32_t kWinNr = 258;
+// the memory phase's split (per SM) and packed slots share the near lists,
+// which are empty from the end of a local phase to the next window start
+constexpr uint32_t kWinDsc = kWinNr, kWinStage = kWinNr + kWinMaxSm;
+constexpr uint32_t kWinRetL = kWinNr + 2u * 64u * kNear;
+constexpr uint32_t kWinWKey = kWinRetL + 2u * kRetireLds;
+constexpr uint32_t kWinWAux = kWinWKey + 2u * kWinCap;
+constexpr uint32_t kWinWFin = kWinWAux + kWinCap;
+constexpr uint32_t kWinFixed = (kWinWFin + kWinCap + 3u) & ~3u;  // the op table needs 16-B alignment
+static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0, "64-bit arrays on even words");
+static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 struct WinLds {
-  uint32_t optab, tops, srv, mq_head, mq_pos, dsc, nr_cnt, fr_cnt, fr_min, fr_hot, nr, fr, ret_cnt, ret_min, ret_l;
-  uint32_t w_key, w_aux, w_fin, stage;
+  uint32_t optab, tops, srv, mq_head, mq_pos, fr;
   uint32_t total;
 };
 __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP, uint32_t NT) {
   WinLds L;
-  uint32_t o = 0;
+  uint32_t o = kWinFixed;
   auto take = [&o](uint32_t words, bool wide) {
     if (wide) o = (o + 1u) & ~1u;
     const uint32_t r = o;
     o += words;
     return r;
   };
-  L.optab = take(4u * P, true);
+  L.optab = take(4u * P, false);
   L.tops = take((NT + 1u) / 2u, false);
   L.srv = take(NS * SS, false);
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
-  L.nr_cnt = take(64, false);
-  L.fr_cnt = take(64, false);
-  L.fr_min = take(64, false);
-  L.fr_hot = take(64, false);
-  L.nr = take(2u * 64u * kNear, true);
-  // the memory phase's split (per SM) and packed slots share the near lists,
-  // which are empty from the end of a local phase to the next window start
-  L.dsc = L.nr;
-  L.stage = L.nr + kWinMaxSm;
   L.fr = take(2u * 64u * QP, true);
-  L.ret_cnt = take(1, false);
-  L.ret_min = take(1, false);
-  L.ret_l = take(2u * kRetireLds, true);
-  L.w_key = take(2u * kWinCap, true);
-  L.w_aux = take(kWinCap, false);
-  L.w_fin = take(kWinCap, false);
   L.total = o;
   return L;
 }

@@ -244,7 +244,7 @@ struct WSim {
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
-  uint64_t st_windows, st_iters, st_local, st_mem, st_retires, st_maxm;
+  uint32_t st_windows, st_iters, st_local, st_mem, st_retires, st_maxm;
   uint32_t st_maxrq, st_maxmq, st_maxret;
   uint64_t tm0, tm1, tm2, tm3, tm4;
 
@@ -1064,20 +1064,20 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.srv = lds + W.srv;
   S.mq_head = lds + W.mq_head;
   S.mq_pos = lds + W.mq_pos;
-  S.dsc = lds + W.dsc;
-  S.nr_cnt = lds + W.nr_cnt;
-  S.fr_cnt = lds + W.fr_cnt;
-  S.fr_min = lds + W.fr_min;
-  S.fr_hot = lds + W.fr_hot;
-  S.nr = reinterpret_cast<uint64_t*>(lds + W.nr);
   S.fr = reinterpret_cast<uint64_t*>(lds + W.fr);
-  S.ret_cnt = lds + W.ret_cnt;
-  S.ret_min = lds + W.ret_min;
-  S.ret_l = reinterpret_cast<uint64_t*>(lds + W.ret_l);
-  S.w_key = reinterpret_cast<uint64_t*>(lds + W.w_key);
-  S.w_aux = lds + W.w_aux;
-  S.w_fin = lds + W.w_fin;
-  S.stage = lds + W.stage;
+  S.dsc = lds + kWinDsc;
+  S.nr_cnt = lds + kWinNrCnt;
+  S.fr_cnt = lds + kWinFrCnt;
+  S.fr_min = lds + kWinFrMin;
+  S.fr_hot = lds + kWinFrHot;
+  S.nr = reinterpret_cast<uint64_t*>(lds + kWinNr);
+  S.ret_cnt = lds + kWinRetCnt;
+  S.ret_min = lds + kWinRetMin;
+  S.ret_l = reinterpret_cast<uint64_t*>(lds + kWinRetL);
+  S.w_key = reinterpret_cast<uint64_t*>(lds + kWinWKey);
+  S.w_aux = lds + kWinWAux;
+  S.w_fin = lds + kWinWFin;
+  S.stage = lds + kWinStage;
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
 
   bool infeasible = false;
