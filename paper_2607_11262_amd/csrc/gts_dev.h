@@ -198,8 +198,12 @@ constexpr uint32_t kWinRetL = kWinNr + 2u * 64u * kNear;
 constexpr uint32_t kWinWKey = kWinRetL + 2u * kRetireLds;
 constexpr uint32_t kWinWAux = kWinWKey + 2u * kWinCap;
 constexpr uint32_t kWinWFin = kWinWAux + kWinCap;
-constexpr uint32_t kWinFixed = (kWinWFin + kWinCap + 3u) & ~3u;  // the op table needs 16-B alignment
-static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0, "64-bit arrays on even words");
+// per-simulation counters: phase clocks (u64, words 0-9), windows, local
+// steps, memory arrivals, retirements, largest memory batch (u32, 10-14)
+constexpr uint32_t kWinStats = kWinWFin + kWinCap;
+constexpr uint32_t kWinFixed = (kWinStats + 16u + 3u) & ~3u;  // the op table needs 16-B alignment
+static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinStats % 2 == 0,
+              "64-bit arrays on even words");
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 struct WinLds {
   uint32_t optab, tops, srv, mq_head, mq_pos, fr;

@@ -209,6 +209,10 @@ __device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], con
 
 // One simulation on one wavefront; NB = SMs per lane (ceil(n_sm / 64) of the
 // largest hardware record of the batch).
+// The simulation's LDS (dynamic, so it starts at LDS address 0).
+extern __shared__ uint32_t win_lds_words[];
+__device__ __forceinline__ uint32_t* lds_base() { return win_lds_words; }
+
 template <uint32_t NB>
 struct WSim {
   Image G;
@@ -244,9 +248,19 @@ struct WSim {
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
-  uint32_t st_windows, st_iters, st_local, st_mem, st_retires, st_maxm;
-  uint32_t st_maxrq, st_maxmq, st_maxret;
-  uint64_t tm0, tm1, tm2, tm3, tm4;
+  uint32_t st_local, st_maxrq, st_maxmq, st_maxret;
+  // uniform counters live in LDS (kWinStats), not in scalar registers: lane
+  // 0 adds to them with fire-and-forget LDS atomics
+  __device__ __forceinline__ void count(uint32_t word, uint32_t n) {
+    if (lane == 0) atomicAdd(reinterpret_cast<uint32_t*>(lds_base()) + kWinStats + word, n);
+  }
+  __device__ __forceinline__ void count_max(uint32_t word, uint32_t n) {
+    if (lane == 0) atomicMax(reinterpret_cast<uint32_t*>(lds_base()) + kWinStats + word, n);
+  }
+  __device__ __forceinline__ void count_clk(uint32_t phase, uint64_t ticks) {
+    if (lane == 0) atomicAdd(reinterpret_cast<unsigned long long*>(reinterpret_cast<uint32_t*>(lds_base()) + kWinStats) + phase,
+                             (unsigned long long)ticks);
+  }
 
   // ---- ready nodes of lane l's SMs, entries (cycle << 32 | SM slot << 30 |
   // node) with SM slot = SM / 64, in two lists: "near" holds only entries
@@ -1035,7 +1049,7 @@ template <uint32_t NB>
 __device__ __forceinline__ void window_body(const Launch& L) {
   const uint32_t b = blockIdx.x;
   if (b >= L.B) return;
-  extern __shared__ uint32_t lds[];
+  uint32_t* const lds = lds_base();
   WSim<NB> S;
   S.G = L.img;
   S.hw = L.hw + (uint64_t)b * HW_WORDS;
@@ -1145,9 +1159,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.makespan = 0;
   S.nfin = 0;
   S.bad = 0;
-  S.st_windows = S.st_iters = S.st_local = S.st_mem = S.st_retires = S.st_maxm = 0;
-  S.st_maxrq = S.st_maxmq = S.st_maxret = 0;
-  S.tm0 = S.tm1 = S.tm2 = S.tm3 = S.tm4 = 0;
+  S.st_local = S.st_maxrq = S.st_maxmq = S.st_maxret = 0;
+  if (lane < 16) lds[kWinStats + lane] = 0;
 
   // phase clocks only on request: reading the clock waits for every
   // outstanding scalar and LDS access
@@ -1230,7 +1243,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       if (single) {
         wsync();
         S.retired += dp;
-        S.st_retires += dp;
+        S.count(13, dp);
         S.dispatch((uint32_t)T);
         wsync();
         if (__ballot(S.bad != 0)) break;
@@ -1250,7 +1263,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
           for (uint32_t x = i + lane; x < j; x += 64) atomicSub(&S.mq_pos[(uint32_t)S.w_key[S.stage[x]]], 1u << 16);
           wsync();
           S.retired += j - i;
-          S.st_retires += j - i;
+          S.count(13, j - i);
           S.dispatch((uint32_t)r);
           i = j;
           stop = __ballot(S.bad != 0) != 0;
@@ -1266,7 +1279,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     wsync();
     S.Hnear = H0;
     for (;;) {
-      ++S.st_iters;
+      S.count(11, 1);
       if (!S.local_step(H0)) break;
     }
     S.Hnear = 0;
@@ -1388,14 +1401,16 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     }
     wsync();
     const uint64_t c5 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
-    ++S.st_windows;
-    S.st_mem += M;
-    S.st_maxm = M > S.st_maxm ? M : S.st_maxm;
-    S.tm0 += c1 - c0;
-    S.tm1 += c2 - c1;
-    S.tm2 += c3 - c2;
-    S.tm3 += c4 - c3;
-    S.tm4 += c5 - c4;
+    S.count(10, 1);
+    S.count(12, M);
+    S.count_max(14, M);
+    if (clk) {
+      S.count_clk(0, c1 - c0);
+      S.count_clk(1, c2 - c1);
+      S.count_clk(2, c3 - c2);
+      S.count_clk(3, c4 - c3);
+      S.count_clk(4, c5 - c4);
+    }
   }
 
   const uint64_t bad_any = __ballot(S.bad != 0);
@@ -1416,17 +1431,19 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   }
   if (lane == 0) {
     uint64_t* stats = reinterpret_cast<uint64_t*>(sim + L.layout.stride - kStatsBytes);
-    stats[0] = S.st_windows;
-    stats[1] = S.st_iters;
+    const uint32_t* cw = lds + kWinStats;
+    const uint64_t* ck = reinterpret_cast<const uint64_t*>(cw);
+    stats[0] = cw[10];
+    stats[1] = cw[11];
     stats[2] = nl;
-    stats[3] = S.st_mem;
-    stats[4] = S.st_retires;
-    stats[5] = S.st_maxm;
-    stats[6] = S.tm0;
-    stats[7] = S.tm1;
-    stats[8] = S.tm2;
-    stats[9] = S.tm3;
-    stats[10] = S.tm4;
+    stats[3] = cw[12];
+    stats[4] = cw[13];
+    stats[5] = cw[14];
+    stats[6] = ck[0];
+    stats[7] = ck[1];
+    stats[8] = ck[2];
+    stats[9] = ck[3];
+    stats[10] = ck[4];
     stats[11] = 0;
     stats[12] = why;
     stats[13] = mrq;
