@@ -201,8 +201,12 @@ constexpr uint32_t kWinWFin = kWinWAux + kWinCap;
 // per-simulation counters: phase clocks (u64, words 0-9), windows, local
 // steps, memory arrivals, retirements, largest memory batch (u32, 10-14)
 constexpr uint32_t kWinStats = kWinWFin + kWinCap;
-constexpr uint32_t kWinFixed = (kWinStats + 16u + 3u) & ~3u;  // the op table needs 16-B alignment
-static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinStats % 2 == 0,
+// dispatch state: next CTA, retired CTAs, current kernel, its first and end
+// CTA, the kernel whose start cycle is known, that cycle, whether known
+// (u32, words 0-7), CTA slots per SM of the current kernel (u64, words 8-9)
+constexpr uint32_t kWinCtl = kWinStats + 16u;
+constexpr uint32_t kWinFixed = (kWinCtl + 10u + 3u) & ~3u;  // the op table needs 16-B alignment
+static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinStats % 2 == 0 && kWinCtl % 2 == 0,
               "64-bit arrays on even words");
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 struct WinLds {

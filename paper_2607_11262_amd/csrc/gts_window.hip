@@ -239,12 +239,13 @@ struct WSim {
   uint64_t* ret_g;
   uint32_t* out_cycles;
   // uniform control
-  uint32_t next_cta, retired, cur_k, k_begin, k_end, kstart_k, kstart_t, kstart_valid;
+  // dispatch state lives in LDS (kWinCtl): it is needed once per dispatch,
+  // not in scalar registers across the event loop
   // the kernel whose CTAs are live (kernels run one after another) and its
   // template: nodes per CTA (0: expanded records), first node, first CTA, CTAs,
   // first template record, class x slot table offset and slots per class
   uint32_t run_k, t_n, t_node0, t_kc0, t_nc, t_base, t_ops, t_nslot;
-  uint64_t slots, l2_av, dram_av, Lm, Hnear;
+  uint64_t l2_av, dram_av, Lm, Hnear;
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
@@ -256,6 +257,9 @@ struct WSim {
   }
   __device__ __forceinline__ void count_max(uint32_t word, uint32_t n) {
     if (lane == 0) atomicMax(reinterpret_cast<uint32_t*>(lds_base()) + kWinStats + word, n);
+  }
+  __device__ __forceinline__ void count_retired(uint32_t n) {
+    if (lane == 0) atomicAdd(lds_base() + kWinCtl + 1, n);
   }
   __device__ __forceinline__ void count_clk(uint32_t phase, uint64_t ticks) {
     if (lane == 0) atomicAdd(reinterpret_cast<unsigned long long*>(reinterpret_cast<uint32_t*>(lds_base()) + kWinStats) + phase,
@@ -459,7 +463,7 @@ struct WSim {
     const uint32_t cw = G.nodes[w].cta;
     if (cw == src_cta) {
       rq_push(src_sm, acc, w);
-    } else if (cw < next_cta) {  // dispatched: ready at max(release, launch)
+    } else if (cw < uni(lds_base()[kWinCtl])) {  // dispatched: ready at max(release, launch)
       const uint32_t launch = gld(&cst[cw].launch);
       rq_push(gld(&cst[cw].sm), acc > launch ? acc : launch, w);
     }
@@ -523,9 +527,9 @@ struct WSim {
     if (t_n == 0) return G.indeg[w];
     return G.tindeg[t_base + (w - t_node0 - (r.cta() - t_kc0) * t_n)];
   }
-  __device__ __forceinline__ void load_template() {
-    const KernelDev kd = G.kernels[cur_k];
-    run_k = cur_k;
+  __device__ __forceinline__ void load_template(uint32_t k) {
+    const KernelDev kd = G.kernels[k];
+    run_k = k;
     t_n = uni(kd.t_n);
     t_node0 = uni(kd.node_begin);
     t_kc0 = uni(kd.cta_begin);
@@ -535,8 +539,9 @@ struct WSim {
     t_nslot = uni(kd.t_ops >> 16);
   }
 
-  __device__ __forceinline__ void load_kernel() {
-    const KernelDev kd = G.kernels[cur_k];
+  // first and end CTA and CTA slots per SM of kernel k
+  __device__ __forceinline__ void load_kernel(uint32_t k, uint32_t& k_begin, uint32_t& k_end, uint64_t& slots) const {
+    const KernelDev kd = G.kernels[k];
     k_begin = uni(kd.cta_begin);
     k_end = uni(kd.cta_end);
     slots = uni64(kernel_slots(kd, hw));
@@ -546,10 +551,32 @@ struct WSim {
   // up to 64 CTAs at a time are placed on SMs (most free slots, lowest id),
   // then set up by one lane each.
   __device__ __forceinline__ void dispatch(uint32_t t) {
+    uint32_t* const ctl = lds_base() + kWinCtl;
+    uint32_t next_cta = uni(ctl[0]), cur_k = uni(ctl[2]), k_begin = uni(ctl[3]), k_end = uni(ctl[4]);
+    uint32_t kstart_k = uni(ctl[5]), kstart_t = uni(ctl[6]), kstart_valid = uni(ctl[7]);
+    uint64_t slots = uni64(*reinterpret_cast<const uint64_t*>(ctl + 8));
+    const uint32_t retired = uni(ctl[1]);
+    dispatch_loop(t, next_cta, retired, cur_k, k_begin, k_end, kstart_k, kstart_t, kstart_valid, slots);
+    wsync();
+    if (lane == 0) {
+      ctl[0] = next_cta;
+      ctl[2] = cur_k;
+      ctl[3] = k_begin;
+      ctl[4] = k_end;
+      ctl[5] = kstart_k;
+      ctl[6] = kstart_t;
+      ctl[7] = kstart_valid;
+      *reinterpret_cast<uint64_t*>(ctl + 8) = slots;
+    }
+    wsync();
+  }
+  __device__ __forceinline__ void dispatch_loop(uint32_t t, uint32_t& next_cta, uint32_t retired, uint32_t& cur_k,
+                                                uint32_t& k_begin, uint32_t& k_end, uint32_t& kstart_k,
+                                                uint32_t& kstart_t, uint32_t& kstart_valid, uint64_t& slots) {
     while (next_cta < G.n_ctas) {
       while (next_cta >= k_end) {
         ++cur_k;
-        load_kernel();
+        load_kernel(cur_k, k_begin, k_end, slots);
       }
       if (retired < k_begin) return;  // the previous kernel is still running
       const uint32_t lim = k_end - next_cta < 64u ? k_end - next_cta : 64u;
@@ -570,7 +597,7 @@ struct WSim {
         ++k;
       }
       if (k == 0) return;
-      if (run_k != cur_k) load_template();  // the first CTAs of a kernel: it is now the running one
+      if (run_k != cur_k) load_template(cur_k);  // the first CTAs of a kernel: it is now the running one
       if (!kstart_valid || kstart_k != cur_k) {
         kstart_valid = 1;
         kstart_k = cur_k;
@@ -1144,15 +1171,23 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   mem_wait();
   __syncthreads();
 
-  S.next_cta = 0;
-  S.retired = 0;
-  S.cur_k = 0;
-  S.load_kernel();
+  {
+    uint32_t kb, ke;
+    uint64_t sl;
+    S.load_kernel(0, kb, ke, sl);
+    if (lane == 0) {
+      uint32_t* const ctl = lds + kWinCtl;
+      ctl[0] = 0;  // next CTA
+      ctl[1] = 0;  // retired
+      ctl[2] = 0;  // current kernel
+      ctl[3] = kb;
+      ctl[4] = ke;
+      ctl[5] = ctl[6] = ctl[7] = 0;
+      *reinterpret_cast<uint64_t*>(ctl + 8) = sl;
+    }
+  }
   S.run_k = 0xFFFFFFFFu;  // no CTA dispatched yet
   S.t_n = 0;
-  S.kstart_k = 0;
-  S.kstart_t = 0;
-  S.kstart_valid = 0;
   S.l2_av = 0;
   S.dram_av = 0;
   S.digest = 0;
@@ -1242,7 +1277,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       const uint32_t R = single ? 0u : dp;
       if (single) {
         wsync();
-        S.retired += dp;
+        S.count_retired(dp);
         S.count(13, dp);
         S.dispatch((uint32_t)T);
         wsync();
@@ -1262,7 +1297,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
           while (j < R && uni64(S.w_key[S.stage[j]] >> 32) == r) ++j;
           for (uint32_t x = i + lane; x < j; x += 64) atomicSub(&S.mq_pos[(uint32_t)S.w_key[S.stage[x]]], 1u << 16);
           wsync();
-          S.retired += j - i;
+          S.count_retired(j - i);
           S.count(13, j - i);
           S.dispatch((uint32_t)r);
           i = j;
