@@ -205,8 +205,12 @@ constexpr uint32_t kWinStats = kWinWFin + kWinCap;
 // CTA, the kernel whose start cycle is known, that cycle, whether known
 // (u32, words 0-7), CTA slots per SM of the current kernel (u64, words 8-9)
 constexpr uint32_t kWinCtl = kWinStats + 16u;
-constexpr uint32_t kWinFixed = (kWinCtl + 10u + 3u) & ~3u;  // the op table needs 16-B alignment
-static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinStats % 2 == 0 && kWinCtl % 2 == 0,
+// pointers the event loop needs rarely (u64 each): kept here rather than in
+// scalar registers
+constexpr uint32_t kWinPtrs = kWinCtl + 10u, kWinNumPtrs = 10u;
+constexpr uint32_t kWinFixed = (kWinPtrs + 2u * kWinNumPtrs + 3u) & ~3u;  // the op table needs 16-B alignment
+static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinStats % 2 == 0 && kWinCtl % 2 == 0 &&
+                  kWinPtrs % 2 == 0,
               "64-bit arrays on even words");
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 struct WinLds {

@@ -234,9 +234,7 @@ struct WSim {
   // scratch
   uint64_t* state;
   CtaState* cst;
-  uint64_t* fr_g;
   uint32_t* mq_g;
-  uint64_t* ret_g;
   uint32_t* out_cycles;
   // uniform control
   // dispatch state lives in LDS (kWinCtl): it is needed once per dispatch,
@@ -273,14 +271,21 @@ struct WSim {
   // cycles in fr_min.  At each window start the far entries below the window
   // end move to near; fr_hot marks a far list that still holds such entries
   // (near was full), which the local phase then scans as well.
+  // rarely used pointers, from LDS (kWinPtrs)
+  enum : uint32_t { kPSucc, kPIndeg, kPRoots, kPCtas, kPKernels, kPTsucc, kPTindeg, kPFrG, kPRetG, kPHw };
+  template <typename T>
+  __device__ __forceinline__ T* cold(uint32_t i) const {
+    return reinterpret_cast<T*>(uni64(reinterpret_cast<const uint64_t*>(lds_base() + kWinPtrs)[i]));
+  }
+
   __device__ __forceinline__ uint64_t fr_get(uint32_t l, uint32_t i) const {
-    return i < QF ? fr[i * 64u + l] : fr_g[(i - QF) * 64u + l];
+    return i < QF ? fr[i * 64u + l] : cold<uint64_t>(kPFrG)[(i - QF) * 64u + l];
   }
   __device__ __forceinline__ void fr_set(uint32_t l, uint32_t i, uint64_t k) {
     if (i < QF)
       fr[i * 64u + l] = k;
     else
-      fr_g[(i - QF) * 64u + l] = k;
+      cold<uint64_t>(kPFrG)[(i - QF) * 64u + l] = k;
   }
   __device__ __forceinline__ uint32_t fr_n(uint32_t l) const {
     const uint32_t n = fr_cnt[l];
@@ -417,13 +422,13 @@ struct WSim {
   // [0, kRetireLds) in LDS, the rest in scratch; ret_min holds a lower bound
   // of their cycles (exact after each retirement phase).
   __device__ __forceinline__ uint64_t ret_get(uint32_t i) const {
-    return i < kRetireLds ? ret_l[i] : ret_g[i - kRetireLds];
+    return i < kRetireLds ? ret_l[i] : cold<uint64_t>(kPRetG)[i - kRetireLds];
   }
   __device__ __forceinline__ void ret_set(uint32_t i, uint64_t k) {
     if (i < kRetireLds)
       ret_l[i] = k;
     else
-      ret_g[i - kRetireLds] = k;
+      cold<uint64_t>(kPRetG)[i - kRetireLds] = k;
   }
   __device__ __forceinline__ void ret_push(uint32_t cyc, uint32_t sm) {
     const uint32_t slot = atomicAdd(ret_cnt, 1u);
@@ -458,7 +463,7 @@ struct WSim {
     atomicMax(st_acc(&state[w]), (uint32_t)r);
     mem_wait();
     const uint32_t old = atomicAdd(st_cnt(&state[w]), 1u);
-    if (old + 1u != (uint32_t)G.indeg[w]) return;
+    if (old + 1u != (uint32_t)cold<const uint16_t>(kPIndeg)[w]) return;
     const uint32_t acc = gld(st_acc(&state[w]));
     const uint32_t cw = G.nodes[w].cta;
     if (cw == src_cta) {
@@ -520,15 +525,15 @@ struct WSim {
   }
   // successor k of a record beyond the inline ones, and an unshared node's in-degree
   __device__ __forceinline__ uint32_t succ_of(const Rec& r, uint32_t k) const {
-    if (t_n == 0) return G.succ[r.sb() + k];
-    return G.tsucc[r.sb() + k] + t_node0 + (r.cta() - t_kc0) * t_n;
+    if (t_n == 0) return cold<const uint32_t>(kPSucc)[r.sb() + k];
+    return cold<const uint32_t>(kPTsucc)[r.sb() + k] + t_node0 + (r.cta() - t_kc0) * t_n;
   }
   __device__ __forceinline__ uint32_t indeg_of(const Rec& r, uint32_t w) const {
-    if (t_n == 0) return G.indeg[w];
-    return G.tindeg[t_base + (w - t_node0 - (r.cta() - t_kc0) * t_n)];
+    if (t_n == 0) return cold<const uint16_t>(kPIndeg)[w];
+    return cold<const uint16_t>(kPTindeg)[t_base + (w - t_node0 - (r.cta() - t_kc0) * t_n)];
   }
   __device__ __forceinline__ void load_template(uint32_t k) {
-    const KernelDev kd = G.kernels[k];
+    const KernelDev kd = cold<const KernelDev>(kPKernels)[k];
     run_k = k;
     t_n = uni(kd.t_n);
     t_node0 = uni(kd.node_begin);
@@ -541,10 +546,10 @@ struct WSim {
 
   // first and end CTA and CTA slots per SM of kernel k
   __device__ __forceinline__ void load_kernel(uint32_t k, uint32_t& k_begin, uint32_t& k_end, uint64_t& slots) const {
-    const KernelDev kd = G.kernels[k];
+    const KernelDev kd = cold<const KernelDev>(kPKernels)[k];
     k_begin = uni(kd.cta_begin);
     k_end = uni(kd.cta_end);
-    slots = uni64(kernel_slots(kd, hw));
+    slots = uni64(kernel_slots(kd, cold<const uint32_t>(kPHw)));
   }
 
   // ---- wave-cooperative dispatch at cycle t (after the retirements at t):
@@ -603,7 +608,8 @@ struct WSim {
         kstart_k = cur_k;
         kstart_t = t;
       }
-      const uint64_t launch = (uint64_t)t + hw[HW_CTALAT] + (kstart_t == t ? hw[HW_KLAT] : 0u);
+      const uint32_t* const hwc = cold<const uint32_t>(kPHw);
+      const uint64_t launch = (uint64_t)t + hwc[HW_CTALAT] + (kstart_t == t ? hwc[HW_KLAT] : 0u);
       if (launch > kMaxCycle) {
         bad |= kBadOverflow;
         return;
@@ -611,7 +617,7 @@ struct WSim {
       const uint32_t c = next_cta + lane;
       uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
       if (lane < k) {
-        const uint4* p = reinterpret_cast<const uint4*>(G.ctas + c);
+        const uint4* p = reinterpret_cast<const uint4*>(cold<const CtaDev>(kPCtas) + c);
         c0 = p[0];  // node_begin, node_count, root_begin, root_count
         c1 = p[1];  // memory nodes, first three roots
         *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
@@ -626,12 +632,12 @@ struct WSim {
         const bool shared = (c0.w & kCtaShared) != 0;
         const uint32_t nroots = c0.w & ~kCtaShared;
         for (uint32_t r = 0; r < nroots; ++r) {
-          const uint32_t v = r == 0 ? c1.y : r == 1 ? c1.z : r == 2 ? c1.w : G.roots[c0.z + r];
+          const uint32_t v = r == 0 ? c1.y : r == 1 ? c1.z : r == 2 ? c1.w : cold<const uint32_t>(kPRoots)[c0.z + r];
           if (!shared) {  // no in-edges at all
             rq_push(mysm, (uint32_t)launch, v);
           } else {
             const uint64_t sv = gld(&state[v]);
-            if ((uint32_t)(sv >> 32) == (uint32_t)G.indeg[v]) {
+            if ((uint32_t)(sv >> 32) == (uint32_t)cold<const uint16_t>(kPIndeg)[v]) {
               const uint32_t acc = (uint32_t)sv;
               rq_push(mysm, acc > launch ? acc : (uint32_t)launch, v);
             }
@@ -1096,9 +1102,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   uint8_t* sim = L.sims + (uint64_t)b * L.layout.stride;
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
-  S.fr_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_rp);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
-  S.ret_g = reinterpret_cast<uint64_t*>(sim + L.layout.off_ret);
   const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.tops = reinterpret_cast<uint16_t*>(lds + W.tops);
@@ -1119,6 +1123,19 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.w_aux = lds + kWinWAux;
   S.w_fin = lds + kWinWFin;
   S.stage = lds + kWinStage;
+  if (lane == 0) {
+    uint64_t* const ptrs = reinterpret_cast<uint64_t*>(lds + kWinPtrs);
+    ptrs[S.kPSucc] = reinterpret_cast<uint64_t>(S.G.succ);
+    ptrs[S.kPIndeg] = reinterpret_cast<uint64_t>(S.G.indeg);
+    ptrs[S.kPRoots] = reinterpret_cast<uint64_t>(S.G.roots);
+    ptrs[S.kPCtas] = reinterpret_cast<uint64_t>(S.G.ctas);
+    ptrs[S.kPKernels] = reinterpret_cast<uint64_t>(S.G.kernels);
+    ptrs[S.kPTsucc] = reinterpret_cast<uint64_t>(S.G.tsucc);
+    ptrs[S.kPTindeg] = reinterpret_cast<uint64_t>(S.G.tindeg);
+    ptrs[S.kPFrG] = reinterpret_cast<uint64_t>(sim + L.layout.off_rp);
+    ptrs[S.kPRetG] = reinterpret_cast<uint64_t>(sim + L.layout.off_ret);
+    ptrs[S.kPHw] = reinterpret_cast<uint64_t>(S.hw);
+  }
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
 
   bool infeasible = false;
