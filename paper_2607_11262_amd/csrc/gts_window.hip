@@ -59,6 +59,7 @@ constexpr uint64_t kNoKey = ~0ull;
 constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u;
 constexpr uint32_t GQ = 3;               // ring entries loaded per SM and window
 constexpr uint32_t kMaxSubpart = GTS_MAX_SUBPART;
+constexpr uint32_t kSmallBatch = 16;  // batches this small are ordered by counting ranks
 
 // Node state: latest release cycle (low word) | released in-edges (high word).
 __device__ __forceinline__ uint32_t* st_acc(uint64_t* st) { return reinterpret_cast<uint32_t*>(st); }
@@ -859,6 +860,32 @@ struct WSim {
   __device__ __forceinline__ void sort_batch(uint32_t M, uint64_t (&k)[E], uint32_t (&sl)[E]) {
     static_assert(E == 1 || E == 2 || E == 4, "64, 128 or 256 positions");
     constexpr uint32_t n = 64u * E;
+    if (M <= kSmallBatch) {
+      // few keys (one SM's arrivals, say): count each key's rank across the
+      // lanes and pick, for each position, the key of that rank
+      const uint64_t mine = lane < M ? w_key[lane] : kNoKey;
+      uint32_t rank = 0;
+      for (uint32_t j = 0; j < M; ++j) {
+        const uint64_t kj = ((uint64_t)lane_u32((uint32_t)(mine >> 32), (int)j) << 32) | lane_u32((uint32_t)mine, (int)j);
+        rank += (kj < mine || (kj == mine && j < lane)) ? 1u : 0u;
+      }
+#pragma unroll
+      for (uint32_t r = 0; r < E; ++r) {
+        k[r] = kNoKey;
+        sl[r] = r * 64u + lane;
+      }
+      for (uint32_t j = 0; j < M; ++j) {
+        const uint32_t rj = lane_u32(rank, (int)j);
+        const uint64_t kj = ((uint64_t)lane_u32((uint32_t)(mine >> 32), (int)j) << 32) | lane_u32((uint32_t)mine, (int)j);
+#pragma unroll
+        for (uint32_t r = 0; r < E; ++r) {
+          const bool t = rj == lane * E + r;
+          k[r] = t ? kj : k[r];
+          sl[r] = t ? j : sl[r];
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
       const uint32_t s = r * 64u + lane;
@@ -1330,10 +1357,9 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     S.pool_rebuild(H0);
     wsync();
     S.Hnear = H0;
-    for (;;) {
-      S.count(11, 1);
-      if (!S.local_step(H0)) break;
-    }
+    uint32_t steps = 1;
+    while (S.local_step(H0)) ++steps;
+    S.count(11, steps);
     S.Hnear = 0;
     wsync();
     const uint64_t c3 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
