@@ -57,7 +57,10 @@ namespace {
 
 constexpr uint64_t kNoKey = ~0ull;
 constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u;
-constexpr uint32_t GQ = 3;               // ring entries loaded per SM and window
+// ring entries loaded per SM and window: as many as the registers allow
+// at three waves per SIMD (fewer cut windows short)
+template <uint32_t NB>
+constexpr uint32_t kGq = NB >= 4 ? 4u : 5u;
 constexpr uint32_t kMaxSubpart = GTS_MAX_SUBPART;
 constexpr uint32_t kSmallBatch = 16;  // batches this small are ordered by counting ranks
 
@@ -198,13 +201,13 @@ __device__ __forceinline__ bool needs_slow(const Rec r) {
 
 // Loaded ring entries whose key (cycle << 32 | kind << 30 | node) is below K.
 template <uint32_t NB>
-__device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][GQ], const uint32_t (&elo)[NB][GQ],
+__device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][kGq<NB>], const uint32_t (&elo)[NB][kGq<NB>],
                                               uint64_t K) {
   uint32_t c = 0;
 #pragma unroll
   for (uint32_t j = 0; j < NB; ++j)
 #pragma unroll
-    for (uint32_t q = 0; q < GQ; ++q) c += (((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K;
+    for (uint32_t q = 0; q < kGq<NB>; ++q) c += (((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K;
   return c;
 }
 
@@ -1366,6 +1369,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (__ballot(S.bad != 0)) break;
 
     // Memory phase: the arrivals whose key (cycle, id) is below K <= H0 << 32.
+    constexpr uint32_t GQ = kGq<NB>;
     // Up to GQ head entries of each SM whose head may be below H0 are loaded;
     // K is lowered so that every due arrival is among them, and so that at
     // most kWinCap are due -- the rest, possibly of the same cycle, wait for
