@@ -16,8 +16,8 @@
 //       out-edges (all inside the same CTA); memory nodes reserve the SM's
 //       engine and queue an arrival at their engine start;
 //   memory phase: the arrivals with cycle < H from all SMs are sorted by
-//       (cycle, node id) (each counts the smaller keys, read by LDS broadcast),
-//       served by the chip-wide L2 and DRAM FIFO servers through a max-plus
+//       (cycle, node id) (a bitonic network across the wave; a few keys by
+//       counting ranks), served by the chip-wide L2 and DRAM FIFO servers through a max-plus
 //       prefix scan, and completed by the lane that owns their SM (CTA
 //       bookkeeping, release of out-edges).
 //
@@ -39,7 +39,9 @@
 // Memory: ready nodes wait in a per-lane pool in LDS (spilling to scratch);
 // memory arrivals in per-SM rings in scratch, with each ring's position and a
 // lower bound of its head's cycle in LDS; pending retirements in LDS (spilling
-// to scratch).  Per-node state (released in-edges, latest release) lives in
+// to scratch).  Uniform state used rarely (dispatch state, counters, the
+// pointers of cold paths) lives in LDS too, not in scalar registers, which
+// the hot paths need.  Per-node state (released in-edges, latest release) lives in
 // scratch and counts up from zero: a CTA's nodes are zeroed when it is
 // dispatched (nodes that receive cross-CTA edges once at start), and node
 // records carry the first three successors with their in-degrees, so issuing
