@@ -155,9 +155,9 @@ constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs pe
 constexpr uint32_t kNear = 4;          // ready entries per lane due in the current window (LDS)
 constexpr uint32_t kPoolSpill = 240;   // later ready entries per lane beyond the LDS part
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
-constexpr uint32_t kRetireLds = 64;    // pending CTA retirements held in LDS ...
+constexpr uint32_t kRetireLds = 0;     // pending CTA retirements held in LDS ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
-constexpr uint32_t kWinCap = 192;      // memory arrivals (or retirements) per window
+constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice

@@ -537,7 +537,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     uint32_t want = kWavesPerCu;
     if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU
       want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (uint32_t)std::strtoul(w, nullptr, 10)));
-    constexpr uint32_t kMinQp = 1;
+    constexpr uint32_t kMinQp = 0;
     uint32_t qp = kMinQp;
     for (uint32_t q = kMinQp + 1; q <= kMaxQp; ++q)
       if (bytes(q) <= kLdsBudget && per_cu(q) >= std::min(want, per_cu(kMinQp))) qp = q;
