@@ -155,7 +155,7 @@ constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs pe
 constexpr uint32_t kNear = 4;          // ready entries per lane due in the current window (LDS)
 constexpr uint32_t kPoolSpill = 240;   // later ready entries per lane beyond the LDS part
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
-constexpr uint32_t kRetireLds = 0;     // pending CTA retirements held in LDS ...
+constexpr uint32_t kRetireLds = 0;     // pending CTA retirements held in LDS (none: the room went to kWinCap) ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
 constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
