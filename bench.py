@@ -110,7 +110,7 @@ def main() -> int:
                     help="device scratch budget, split evenly over the streams")
     ap.add_argument("--graphs", type=str, default="", help="comma-separated sweep graph indices (default: step order)")
     ap.add_argument("--streams", type=int, default=2,
-                    help="consecutive steps alternate over this many HIP streams, so one graph's launch "
+                    help="consecutive launches alternate over this many HIP streams, so one launch "
                          "overlaps the tail of the previous one")
     ap.add_argument("--launch-log", type=str, default="", help="write one JSON line per timed launch to this file")
     ap.add_argument("--host-io", action="store_true",
@@ -231,10 +231,15 @@ def main() -> int:
     launches = []  # (start event, end event, algorithmic bytes, node-sims)
     launch_info = []  # (graph, first record, records)
 
+    n_launched = [0]
+
     def step(k, gi, record):
-        stream, scratch = streams[k % len(streams)], scratches[k % len(streams)]
         dg, hs, chunk, (cyc, mk, st, dgst), n, abps = prepared[gi]
         for first in range(0, B_PER_GRAPH, chunk):
+            # launches (not steps) alternate over the streams: the chunks of a
+            # graph too large for one launch then run side by side
+            stream, scratch = streams[n_launched[0] % len(streams)], scratches[n_launched[0] % len(streams)]
+            n_launched[0] += 1
             b = min(chunk, B_PER_GRAPH - first)
             if record:
                 e0 = torch.cuda.Event(enable_timing=True)
