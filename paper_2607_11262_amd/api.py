@@ -208,15 +208,25 @@ def simulate_into(g: Graph, hw, flags, cyc, mk, st, dg, scratch, stream=None) ->
 
 def simulate(g: Graph, hw, flags: int = OUT_NODES | OUT_DIGEST, stream=None, scratch=None) -> Result:
     """Simulate g under every record of hw [B, 32] (uint32); returns device
-    tensors (valid after the stream synchronises)."""
+    tensors (valid after `stream` synchronises).
+
+    Scratch and outputs are allocated on the stream the kernels run on, so
+    torch's caching allocator hands their blocks to a later allocation only
+    after that stream's queued work (the simulation) has run, even when
+    `stream` is not the current stream.  A caller-provided scratch tensor
+    used on a side stream is marked with record_stream for the same reason."""
     import torch
     hw = np.ascontiguousarray(hw, dtype=np.uint32).reshape(-1, 32)
     B = hw.shape[0]
     need = scratch_bytes(g, B, flags)
-    if scratch is None or scratch.numel() < need:
-        scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=g.image.device)
-    cyc, mk, st, dg = alloc_outputs(g, B, flags, g.image.device)
-    simulate_into(g, hw, flags, cyc, mk, st, dg, scratch, stream)
+    s = stream if stream is not None else torch.cuda.current_stream()
+    with torch.cuda.stream(s):
+        if scratch is None or scratch.numel() < need:
+            scratch = torch.empty(max(need, 1), dtype=torch.uint8, device=g.image.device)
+        elif stream is not None:
+            scratch.record_stream(s)
+        cyc, mk, st, dg = alloc_outputs(g, B, flags, g.image.device)
+    simulate_into(g, hw, flags, cyc, mk, st, dg, scratch, s)
     return Result(cyc, mk, st, dg)
 
 

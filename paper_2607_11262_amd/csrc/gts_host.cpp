@@ -231,16 +231,18 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   // tiles: only loads / stores, one line count per tile
   uint32_t n_tiles = 0;
   if (h->node_tile) {
-    std::unordered_map<uint32_t, uint32_t> lines;
+    std::unordered_map<uint32_t, uint64_t> lines;
     for (uint32_t v = 0; v < N; ++v) {
       const uint32_t t = h->node_tile[v];
       if (t == GTS_NO_TILE) continue;
       const uint32_t p = h->node_op[v];
       if (!is_memory(h->op_cls[p])) return fail(GTS_E_RANGE, "node %u is not a load or store but names tile %u", v, t);
-      const uint32_t n = (h->op_work[p] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES;
+      // 64-bit, as in the kernels and the oracle: work near 2^32 must not wrap
+      const uint64_t n = ((uint64_t)h->op_work[p] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES;
       auto it = lines.emplace(t, n).first;
       if (it->second != n)
-        return fail(GTS_E_RANGE, "tile %u is touched with %u and with %u lines (node %u)", t, it->second, n, v);
+        return fail(GTS_E_RANGE, "tile %u is touched with %llu and with %llu lines (node %u)", t,
+                    (unsigned long long)it->second, (unsigned long long)n, v);
     }
     n_tiles = (uint32_t)lines.size();
   }

@@ -190,6 +190,20 @@ def test_tile_validation_codes():
     assert api.validate_code(g3) == -4
     with pytest.raises(ValidationError):
         validate(g3)
+    # line counts are 64-bit: work 0 and work 0xFFFFFFFF (0 and 2^25 lines)
+    # on one tile is an inconsistency, not a wrapped match
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    b.cta()
+    u = b.node(GLOAD, 0, 1)
+    w = b.node(GLOAD, 0xFFFFFFFF, 1)
+    b.edge(u, w, DATA)
+    g4 = b.build()
+    g4 = _mutate(g4, node_tile=np.array([5, 5], np.uint32))
+    assert api.validate_code(g4) == -4
+    with pytest.raises(ValidationError):
+        validate(g4)
+    assert api.validate_code(_mutate(g4, node_tile=np.array([5, 6], np.uint32))) == 0
     # tiles go to the device image; sharing is unaffected
     assert api.device_bytes(g) > api.device_bytes(_mutate(g, node_tile=None))
     assert api.templates(g)["templated_kernels"] == 1

@@ -124,7 +124,6 @@ def test_gemm_design_sweep_sample(torch_cuda):
         hws = W.workload_hw("gemm_design_sweep", B=256, index=i)
         note(f"design sweep graph {i} {ps[i]} N={g.n_nodes} B=256")
         gpu = run_gpu(torch_cuda, g, hws, ALL)
-        assert (gpu[2] == api.SIM_INFEASIBLE).any() or True
         compare(g, hws, ALL, gpu, sims=range(0, 256, 4), nodes=True)
 
 

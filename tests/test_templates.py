@@ -22,13 +22,23 @@ def test_gemm_is_one_template():
 
 
 def test_logical_to_physical_ratio():
-    """Sec. 6.4 stores 11.52K-88.58K physical nodes for 0.09M-45.35M logical
-    ones (ratios of about 8x to 512x); here the ratio is the CTA count and
-    grows with the GEMM size the same way."""
-    small = W.gemm(1024, 1024, 1024, 128, 128, 32, 2)
-    big = W.gemm(8192, 8192, 1024, 128, 128, 32, 2)
-    rs, rb = (g.n_nodes / api.templates(g)["template_nodes"] for g in (small, big))
-    assert rs == 64 and rb == 4096
+    """Sec. 6.4 (graph construction): 88.58K physical nodes stand for 45.35M
+    logical ones and 11.52K for 0.09M (92.16K).  Both ratios, 512 and 8, are
+    the CTA counts of the square GEMMs 4096^3 and 512^3 with 128 x 256 CTA
+    tiles (32 x 16 and 4 x 2 CTAs), the shapes of the paper's evaluated
+    range: with one template per kernel, logical / physical nodes is the
+    number of CTAs that share it."""
+    assert round(45.35e6 / 88.58e3) == 512 and round(92.16e3 / 11.52e3) == 8
+    big = W.gemm(4096, 4096, 4096, 128, 256, 64, 3)
+    small = W.gemm(512, 512, 512, 128, 256, 64, 3)
+    rb, rs = (g.n_nodes / api.templates(g)["template_nodes"] for g in (big, small))
+    assert rb == 512 and rs == 8
+    for g in (big, small):
+        t = api.templates(g)
+        assert t["templated_kernels"] == 1 and t["expanded_nodes"] == 0
+    # and it grows with the GEMM the same way at other shapes
+    assert W.gemm(8192, 8192, 1024, 128, 128, 32, 2).n_nodes / api.templates(
+        W.gemm(8192, 8192, 1024, 128, 128, 32, 2))["template_nodes"] == 4096
 
 
 def test_decoder_layer_kernels():
