@@ -32,13 +32,22 @@ def _run(cmd):
 
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
+    jobs = []
     objs = []
     for src in KERNELS:
         o = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        _run([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", o])
+        jobs.append([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", o])
         objs.append(o)
     host_o = os.path.join(BUILD, "gts_host.o")
-    _run([HIPCC, *HOST_FLAGS, "-x", "c++", "-c", os.path.join(CSRC, "gts_host.cpp"), "-o", host_o])
+    jobs.append([HIPCC, *HOST_FLAGS, "-x", "c++", "-c", os.path.join(CSRC, "gts_host.cpp"), "-o", host_o])
+    # the sources compile independently: all at once
+    procs = []
+    for cmd in jobs:
+        print("+", " ".join(cmd), flush=True)
+        procs.append((cmd, subprocess.Popen(cmd)))
+    failed = [cmd for cmd, p in procs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = OUT + f".tmp{os.getpid()}"
     _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", "-o", tmp, *objs, host_o])
     os.replace(tmp, OUT)
