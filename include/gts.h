@@ -293,6 +293,28 @@ int gts_simulate_hwset(const gts_graph *g, const gts_hwset *hw, uint32_t first, 
                        uint64_t *out_digest, void *scratch, uint64_t scratch_bytes,
                        uint32_t flags, void *hip_stream);
 
+/* ---- no-allocation entry point ------------------------------------------- */
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, results and errors as gts_simulate_hwset without the scratch
+ * pair: the simulations' scratch is a static device array of
+ * GTS_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held from the
+ * library's first use on that GPU until the process ends.  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine);
+ * on its first call on a device it looks up the array's device address once.
+ * B must satisfy gts_scratch_bytes(g, B, flags) - 128 * B (rounded up to 256)
+ * <= GTS_NOALLOC_SCRATCH_BYTES, i.e. the scratch gts_simulate_hwset would
+ * need; a larger B returns GTS_E_SCRATCH (the message names the largest B
+ * that fits) before anything is enqueued.  The array needs no
+ * initialisation and keeps the last call's contents.  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (other streams,
+ * other threads) race and give undefined results -- serialise them, e.g. on
+ * one stream. */
+#define GTS_NOALLOC_SCRATCH_BYTES (128ull << 20)
+int gts_simulate_hwset_noalloc(const gts_graph *g, const gts_hwset *hw, uint32_t first, uint32_t B,
+                               uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
+                               uint64_t *out_digest, uint32_t flags, void *hip_stream);
+
 /* Checks one hardware record on the host (GTS_OK or GTS_E_HW). */
 int gts_hw_validate(const gts_hw_params *hw);
 

@@ -29,7 +29,7 @@ OUT_NODES, OUT_DIGEST, NO_CONTENTION, ORDER_AT_FINISH = 1, 2, 4, 8
 
 EXPORTS = ("gts_graph_validate", "gts_graph_device_bytes", "gts_graph_templates", "gts_graph_upload", "gts_graph_release", "gts_graph_sizes",
            "gts_scratch_bytes", "gts_simulate_batch", "gts_hwset_device_bytes", "gts_hwset_upload",
-           "gts_hwset_release", "gts_simulate_hwset", "gts_hw_validate", "gts_strerror", "gts_last_error")
+           "gts_hwset_release", "gts_simulate_hwset", "gts_simulate_hwset_noalloc", "gts_hw_validate", "gts_strerror", "gts_last_error")
 
 
 class GtsError(RuntimeError):
@@ -73,6 +73,7 @@ def lib():
         L.gts_hwset_upload.argtypes = [vp, u32, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
         L.gts_hwset_release.argtypes = [vp]
         L.gts_simulate_hwset.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
+        L.gts_simulate_hwset_noalloc.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, u32, vp]
         L.gts_strerror.argtypes = [ctypes.c_int]
         L.gts_strerror.restype = ctypes.c_char_p
         L.gts_last_error.restype = ctypes.c_char_p
@@ -264,6 +265,21 @@ def simulate_hwset_into(g: Graph, hs: HwSet, first: int, B: int, flags, cyc, mk,
                                     ctypes.c_void_p(dg.data_ptr() if dg is not None else 0),
                                     ctypes.c_void_p(scratch.data_ptr()), scratch.numel(), flags, _stream(stream)),
            "gts_simulate_hwset")
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20  # GTS_NOALLOC_SCRATCH_BYTES
+
+
+def simulate_hwset_noalloc(g: Graph, hs: HwSet, first: int, B: int, flags, cyc, mk, st, dg, stream=None):
+    """As simulate_hwset_into, through gts_simulate_hwset_noalloc: the
+    library's own per-GPU scratch array instead of a caller buffer (nothing is
+    allocated; calls that overlap on one GPU race)."""
+    _check(lib().gts_simulate_hwset_noalloc(g.handle, hs.handle, first, B,
+                                            ctypes.c_void_p(cyc.data_ptr() if cyc is not None else 0),
+                                            ctypes.c_void_p(mk.data_ptr()), ctypes.c_void_p(st.data_ptr()),
+                                            ctypes.c_void_p(dg.data_ptr() if dg is not None else 0), flags,
+                                            _stream(stream)),
+           "gts_simulate_hwset_noalloc")
 
 
 def to_numpy(res: Result):

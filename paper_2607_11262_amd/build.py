@@ -21,7 +21,7 @@ ARCH = os.environ.get("GTS_OFFLOAD_ARCH", "gfx950")
 # Packed FP32 instructions are kept out of generated code (-packed-fp32-ops).
 DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
                 "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
-KERNELS = ("gts_sim.hip", "gts_window.hip")
+KERNELS = ("gts_sim.hip", "gts_window.hip", "gts_noalloc.hip")
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 
 

@@ -562,6 +562,24 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
 
 }  // namespace
 
+namespace gts {
+// For gts_simulate_hwset_noalloc (gts_noalloc.hip): B simulations of g must
+// fit a fixed scratch array of `limit` bytes.
+int check_fixed_scratch(const gts_graph* g, uint32_t B, uint64_t limit) {
+  g_last_error.clear();
+  if (!g) return fail(GTS_E_ARG, "graph handle is NULL");
+  const uint64_t need = sim_scratch_bytes(g, B);
+  if (need > limit)
+    return fail(GTS_E_SCRATCH,
+                "%u simulations of this graph need %llu bytes of scratch; the no-allocation entry point holds %llu "
+                "(at most %llu simulations per call)",
+                B, (unsigned long long)need, (unsigned long long)limit,
+                (unsigned long long)(limit / std::max<uint64_t>(1, sim_scratch_bytes(g, 1))));
+  return GTS_OK;
+}
+int report_hip(hipError_t e, const char* what) { return fail(GTS_E_HIP, "%s: %s", what, hipGetErrorString(e)); }
+}  // namespace gts
+
 extern "C" {
 
 const char* gts_strerror(int code) {
