@@ -204,11 +204,15 @@ typedef struct gts_graph gts_graph;  /* opaque handle to an uploaded graph */
 /* ---- entry points --------------------------------------------------------- */
 
 /* Checks every validity rule above on the host.  Needs no GPU.  Returns
- * GTS_OK or the first violated rule's code (message: gts_last_error()). */
+ * GTS_OK or the first violated rule's code (message: gts_last_error()).
+ * Follows Sec. 4.1 (nodes, data / order edges, the CTA and warp each node is
+ * bound to); the CTA-order and acyclicity rules are what keep the Sec. 5.1
+ * dispatch order deadlock-free. */
 int gts_graph_validate(const gts_graph_host *h);
 
 /* Validates h and returns in *bytes the size of its device image (the layout
- * the simulation kernels read).  Needs no GPU. */
+ * the simulation kernels read).  Needs no GPU.  Sizing only (no passage of
+ * the paper: the image layout is this library's). */
 int gts_graph_device_bytes(const gts_graph_host *h, uint64_t *bytes);
 
 /* Template sharing (GTSim Sec. 6.4: CTAs that execute isomorphic tile graphs
@@ -231,7 +235,11 @@ int gts_graph_templates(const gts_graph_host *h, uint32_t *templated_kernels, ui
 /* Validates h, builds its device image on the host and copies it into the
  * caller's device buffer dev_image (dev_bytes >= gts_graph_device_bytes) on
  * hip_stream, waiting for the copy to finish before returning.  On success
- * *out receives a new handle; h's arrays are not referenced afterwards. */
+ * *out receives a new handle; h's arrays are not referenced afterwards.
+ * Follows Sec. 4.3 (a graph built directly by the user is handed to the
+ * simulation backend) over the Sec. 4.1 graph model; isomorphic CTAs share
+ * one template (Sec. 6.4).  Errors: the validation codes above, GTS_E_SCRATCH
+ * when dev_bytes is too small, GTS_E_HIP when the copy fails. */
 int gts_graph_upload(const gts_graph_host *h, void *dev_image, uint64_t dev_bytes,
                      void *hip_stream, gts_graph **out);
 
@@ -244,10 +252,16 @@ int gts_graph_sizes(const gts_graph *g, uint32_t *n_nodes, uint32_t *n_edges,
 
 /* Bytes of device scratch gts_simulate_batch needs for B simulations of g
  * with these flags.  The scratch holds the batch's hardware records and every
- * simulation's private state; its contents need not be initialised. */
+ * simulation's private state; its contents need not be initialised.  Sizing
+ * only (no passage of the paper). */
 int gts_scratch_bytes(const gts_graph *g, uint32_t B, uint32_t flags, uint64_t *bytes);
 
-/* Simulates g under hw_host[0..B) (host array, read before return).  Outputs
+/* Simulates g under hw_host[0..B) (host array, read before return): the
+ * backend of Sec. 5 -- execution flow and release of order edges at issue,
+ * data edges at completion, thread-block retire and re-dispatch (Sec. 5.1,
+ * Sec. 5.3), resources as latency / width / throughput servers, the memory
+ * path and the NoC (Sec. 5.2) -- under the hardware parameters of Table 3
+ * (Sec. 6.1).  Outputs
  * (device pointers, written asynchronously on hip_stream):
  *   out_cycles   [B][n_nodes][2] u32 {start, finish}; required iff
  *                flags & GTS_OUT_NODES, else ignored (may be NULL)
@@ -274,7 +288,8 @@ typedef struct gts_hwset gts_hwset;  /* opaque handle to uploaded hw records */
 /* Bytes of device memory gts_hwset_upload needs for B records. */
 int gts_hwset_device_bytes(uint32_t B, uint64_t *bytes);
 
-/* Validates hw_host[0..B) (GTS_E_HW names the first bad record), copies the
+/* Hardware records of Table 3 (Sec. 6.1) resident in device memory.
+ * Validates hw_host[0..B) (GTS_E_HW names the first bad record), copies the
  * records into the caller's device buffer dev_buf (>= gts_hwset_device_bytes)
  * on hip_stream and waits for the copy.  *out receives a handle that refers
  * to (does not own) dev_buf and remembers the largest n_sm / n_subpart /
@@ -285,9 +300,11 @@ int gts_hwset_upload(const gts_hw_params *hw_host, uint32_t B, void *dev_buf, ui
 /* Frees the handle (not the caller's buffer).  NULL is accepted. */
 int gts_hwset_release(gts_hwset *hw);
 
-/* As gts_simulate_batch, for the B records hw[first .. first + B) of an
- * uploaded set (already in device memory: no host copy is made).  Output
- * row b belongs to record first + b.  Scratch: gts_scratch_bytes(g, B, ...). */
+/* As gts_simulate_batch (Sec. 5.1-5.3 under Table 3 parameters), for the B
+ * records hw[first .. first + B) of an uploaded set (already in device
+ * memory: no host copy is made).  Output row b belongs to record first + b.
+ * Scratch: gts_scratch_bytes(g, B, ...).  Errors as gts_simulate_batch, plus
+ * GTS_E_ARG when first + B exceeds the set. */
 int gts_simulate_hwset(const gts_graph *g, const gts_hwset *hw, uint32_t first, uint32_t B,
                        uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
                        uint64_t *out_digest, void *scratch, uint64_t scratch_bytes,
@@ -315,7 +332,8 @@ int gts_simulate_hwset_noalloc(const gts_graph *g, const gts_hwset *hw, uint32_t
                                uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
                                uint64_t *out_digest, uint32_t flags, void *hip_stream);
 
-/* Checks one hardware record on the host (GTS_OK or GTS_E_HW). */
+/* Checks one hardware record (Table 3 parameters) on the host (GTS_OK or
+ * GTS_E_HW). */
 int gts_hw_validate(const gts_hw_params *hw);
 
 const char *gts_strerror(int code);

@@ -5,7 +5,8 @@ cpu_baseline leg of bench.py may import this module; the product path
 (paper_2607_11262_amd.api / libgts.so) never does.
 
 The C oracle (gts_oracle.c) simulates one (graph, hardware record) pair per
-call.  Graph arguments are read from any object with the TileGraph array
+call of gtso_simulate; gts_oracle_simulate runs a batch of records, one after
+another.  Graph arguments are read from any object with the TileGraph array
 attributes (op_cls, op_flags, op_work, op_warps, node_op, succ_ptr, succ,
 cta_node_begin, kernel_cta_begin, kernel_warps, kernel_smem); this module
 does not import the product package.
@@ -43,6 +44,8 @@ def _open(path):
     u32 = ctypes.c_uint32
     lib.gtso_simulate.argtypes = [u32, u32, u32, u32, u32] + [p] * 13 + [p, u32] + [p] * 5
     lib.gtso_simulate.restype = ctypes.c_int
+    lib.gts_oracle_simulate.argtypes = [p, p, u32, p, p, p, p, u32]
+    lib.gts_oracle_simulate.restype = ctypes.c_int
     return lib
 
 
@@ -109,23 +112,54 @@ def simulate(g, hw, flags: int = 0, want_nodes: bool = True, want_cta: bool = Fa
     return OracleResult(cyc, int(mk[0]), int(st[0]), int(dg[0]), cta)
 
 
-def simulate_batch(g, hws, flags: int = 0, want_nodes: bool = False, threads: int = 1):
-    """Simulations of g under each record of hws [B, 32], distributed over
-    `threads` host threads (the C call releases the GIL).  Returns
-    (makespan u32[B], status i32[B], digest u64[B], cycles [B][N][2] or None)."""
+class _GraphHost(ctypes.Structure):
+    """The batched call's graph struct (field order of the library's host
+    graph, restated)."""
+    _fields_ = [(n, ctypes.c_uint32) for n in ("n_nodes", "n_edges", "n_ctas", "n_kernels", "n_ops")] + \
+               [(n, ctypes.c_void_p) for n in ("op_cls", "op_flags", "op_work", "op_warps", "node_op", "succ_ptr",
+                                               "succ", "cta_node_begin", "kernel_cta_begin", "kernel_warps",
+                                               "kernel_smem", "kernel_cluster", "node_tile")]
+
+
+def simulate_records(g, hws, flags: int = 0, want_nodes: bool = False):
+    """All records of hws [B, 32] in one call of gts_oracle_simulate (one
+    thread, record order).  Returns (makespan u32[B], status i32[B], digest
+    u64[B], cycles [B][N][2] or None)."""
+    lib = _load()
+    arrs = [_c(g.op_cls, np.uint8), _c(g.op_flags, np.uint8), _c(g.op_work, np.uint32), _c(g.op_warps, np.uint32),
+            _c(g.node_op, np.uint16), _c(g.succ_ptr, np.uint32), _c(g.succ, np.uint32),
+            _c(g.cta_node_begin, np.uint32), _c(g.kernel_cta_begin, np.uint32), _c(g.kernel_warps, np.uint16),
+            _c(g.kernel_smem, np.uint32), _c(g.kernel_cluster, np.uint8),
+            _c(g.node_tile, np.uint32) if g.node_tile is not None else None]
+    h = _GraphHost(int(arrs[4].shape[0]), int(arrs[6].shape[0]), int(arrs[7].shape[0]) - 1, int(arrs[9].shape[0]),
+                   int(arrs[0].shape[0]), *[(a.ctypes.data if a is not None and a.size else None) for a in arrs])
     hws = np.ascontiguousarray(hws, dtype=np.uint32).reshape(-1, 32)
     B = hws.shape[0]
+    mk = np.zeros(B, dtype=np.uint32)
+    st = np.zeros(B, dtype=np.int32)
+    dg = np.zeros(B, dtype=np.uint64)
+    cyc = np.zeros((B, h.n_nodes, 2), dtype=np.uint32) if want_nodes else None
+    rc = lib.gts_oracle_simulate(ctypes.byref(h), _ptr(hws), B, _ptr(cyc), _ptr(mk), _ptr(st), _ptr(dg), int(flags))
+    if rc != 0:
+        raise RuntimeError(f"oracle failed rc={rc}")
+    return mk, st, dg, cyc
 
-    def one(b):
-        return simulate(g, hws[b], flags, want_nodes=want_nodes)
 
-    if threads > 1 and B > 1:
-        with ThreadPoolExecutor(max_workers=threads) as ex:
-            res = list(ex.map(one, range(B)))
-    else:
-        res = [one(b) for b in range(B)]
-    mk = np.array([r.makespan for r in res], dtype=np.uint32)
-    st = np.array([r.status for r in res], dtype=np.int32)
-    dg = np.array([r.digest for r in res], dtype=np.uint64)
-    cyc = np.stack([r.cycles for r in res]) if want_nodes and B else None
+def simulate_batch(g, hws, flags: int = 0, want_nodes: bool = False, threads: int = 1):
+    """Simulations of g under each record of hws [B, 32]: runs of consecutive
+    records through gts_oracle_simulate, distributed over `threads` host
+    threads (the C call releases the GIL).  Returns (makespan u32[B], status
+    i32[B], digest u64[B], cycles [B][N][2] or None)."""
+    hws = np.ascontiguousarray(hws, dtype=np.uint32).reshape(-1, 32)
+    B = hws.shape[0]
+    if threads <= 1 or B <= 1:
+        return simulate_records(g, hws, flags, want_nodes)
+    step = max(1, B // (4 * threads))
+    runs = [(i, min(B, i + step)) for i in range(0, B, step)]
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        res = list(ex.map(lambda r: simulate_records(g, hws[r[0]:r[1]], flags, want_nodes), runs))
+    mk = np.concatenate([r[0] for r in res])
+    st = np.concatenate([r[1] for r in res])
+    dg = np.concatenate([r[2] for r in res])
+    cyc = np.concatenate([r[3] for r in res]) if want_nodes else None
     return mk, st, dg, cyc

@@ -588,3 +588,45 @@ done:
   free(S.occ_l2); free(S.occ_d); free(S.lat_l2); free(S.lat_d);
   return rc;
 }
+
+/* The batched call of the library's interface, restated: a graph given as
+ * one struct with the field order of the library's host graph (counts, then
+ * the array pointers), B hardware records of 32 words each, outputs per
+ * record b at out_cycles + b * 2 * n_nodes (optional), out_makespan[b],
+ * out_status[b], out_digest[b] (optional).  Each record is one independent
+ * simulation run by gtso_simulate, in record order.  Returns 0, -1 for a
+ * missing argument, -2 when host memory runs out. */
+typedef struct gtso_graph_host {
+  uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops;
+  const uint8_t *op_cls, *op_flags;
+  const uint32_t *op_work, *op_warps;
+  const uint16_t *node_op;
+  const uint32_t *succ_ptr, *succ, *cta_node_begin, *kernel_cta_begin;
+  const uint16_t *kernel_warps;
+  const uint32_t *kernel_smem;
+  const uint8_t *kernel_cluster; /* NULL: one CTA per cluster everywhere */
+  const uint32_t *node_tile;     /* NULL: no node names a tile */
+} gtso_graph_host;
+
+int gts_oracle_simulate(const gtso_graph_host *h, const uint32_t *hw, uint32_t B, uint32_t *out_cycles,
+                        uint32_t *out_makespan, int32_t *out_status, uint64_t *out_digest, uint32_t flags) {
+  if (!h || (B && (!hw || !out_makespan || !out_status))) return -1;
+  uint8_t *ones = NULL;
+  const uint8_t *cluster = h->kernel_cluster;
+  if (!cluster) {
+    ones = malloc(h->n_kernels ? h->n_kernels : 1);
+    if (!ones) return -2;
+    memset(ones, 1, h->n_kernels ? h->n_kernels : 1);
+    cluster = ones;
+  }
+  int rc = 0;
+  for (uint32_t b = 0; b < B && rc == 0; b++)
+    rc = gtso_simulate(h->n_nodes, h->n_edges, h->n_ctas, h->n_kernels, h->n_ops, h->op_cls, h->op_flags,
+                       h->op_work, h->op_warps, h->node_op, h->succ_ptr, h->succ, h->cta_node_begin,
+                       h->kernel_cta_begin, h->kernel_warps, h->kernel_smem, cluster, h->node_tile,
+                       hw + 32 * (uint64_t)b, flags,
+                       out_cycles ? out_cycles + 2 * (uint64_t)h->n_nodes * b : NULL, out_makespan + b,
+                       out_status + b, out_digest ? out_digest + b : NULL, NULL);
+  free(ones);
+  return rc;
+}

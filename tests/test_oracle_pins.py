@@ -306,3 +306,23 @@ def test_digest_matches_definition():
     for v, (s, f) in enumerate(r.cycles.tolist()):
         d = (d + mix64(((s << 32) | f) ^ mix64(v + 1))) % 2**64
     assert d == r.digest
+
+
+def test_batched_call_equals_one_record_calls():
+    """gts_oracle_simulate (records one after another in one call) gives each
+    record the result of its own gtso_simulate call, node by node; graphs
+    with and without cluster sizes and tiles."""
+    from clustered import clustered_graph, noc_machine
+    from paper_2607_11262_amd.gen.rng import SplitMix64
+    rng = SplitMix64(97)
+    cases = [(W.gemm(256, 256, 512, 64, 128, 32, 3), H.sample_h100_sweep(98, 6)),
+             (clustered_graph(rng), np.stack([noc_machine(rng) for _ in range(5)])),
+             (W.gemm(512, 512, 256, 64, 64, 32, 2, tiles=True),
+              np.stack([H.preset("H100", l2_lines=n) for n in (0, 64, 4096)]))]
+    for g, hws in cases:
+        hws = np.asarray(hws, dtype=np.uint32).reshape(-1, 32)
+        mk, st, dg, cyc = oracle.simulate_records(g, hws, oracle.F_NODES | oracle.F_DIGEST, want_nodes=True)
+        for b in range(hws.shape[0]):
+            r = oracle.simulate(g, hws[b], oracle.F_NODES | oracle.F_DIGEST)
+            assert (mk[b], st[b], dg[b]) == (r.makespan, r.status, r.digest)
+            assert np.array_equal(cyc[b], r.cycles)
