@@ -57,6 +57,20 @@ def _load():
     return _lib
 
 
+def build_sanitized(path: str) -> str:
+    """The oracle under AddressSanitizer and UBSan (gcc), for a process
+    started with the sanitizer runtimes preloaded."""
+    subprocess.check_call(["gcc", "-O1", "-g", "-std=c11", "-fPIC", "-shared", "-fsanitize=address,undefined",
+                           "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-o", path, _SRC])
+    return path
+
+
+def use_library(path: str) -> None:
+    """Route every later call to the oracle built at `path` (sanitizer runs)."""
+    global _lib
+    _lib = _open(path)
+
+
 def build_variant(source_text: str, path: str) -> None:
     """Compile an edited copy of the oracle source to `path` (used by the
     test that plants mistakes in the oracle to show the pins catch them)."""

@@ -58,30 +58,42 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_11262_amd.build`")
-        L = ctypes.CDLL(LIB_PATH)
-        vp, u32, u64p = ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint64)
-        L.gts_graph_validate.argtypes = [vp]
-        L.gts_graph_device_bytes.argtypes = [vp, u64p]
-        L.gts_graph_templates.argtypes = [vp] + [ctypes.POINTER(u32)] * 4
-        L.gts_graph_upload.argtypes = [vp, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
-        L.gts_graph_release.argtypes = [vp]
-        L.gts_graph_sizes.argtypes = [vp] + [ctypes.POINTER(u32)] * 5
-        L.gts_scratch_bytes.argtypes = [vp, u32, u32, u64p]
-        L.gts_simulate_batch.argtypes = [vp, vp, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
-        L.gts_hw_validate.argtypes = [vp]
-        L.gts_hwset_device_bytes.argtypes = [u32, u64p]
-        L.gts_hwset_upload.argtypes = [vp, u32, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
-        L.gts_hwset_release.argtypes = [vp]
-        L.gts_simulate_hwset.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
-        L.gts_simulate_hwset_noalloc.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, u32, vp]
-        L.gts_strerror.argtypes = [ctypes.c_int]
-        L.gts_strerror.restype = ctypes.c_char_p
-        L.gts_last_error.restype = ctypes.c_char_p
-        for name in EXPORTS:
-            if name not in ("gts_strerror", "gts_last_error"):
-                getattr(L, name).restype = ctypes.c_int
-        _lib = L
+        _lib = _bind(ctypes.CDLL(LIB_PATH))
     return _lib
+
+
+def use_library(path: str):
+    """Bind the calls to another build of the library at `path` (a CPU-only
+    sanitizer build of the host side, for tests); returns it."""
+    global _lib
+    _lib = _bind(ctypes.CDLL(path))
+    return _lib
+
+
+def _bind(L):
+    """Argument and return types of every exported call."""
+    vp, u32, u64p = ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(ctypes.c_uint64)
+    L.gts_graph_validate.argtypes = [vp]
+    L.gts_graph_device_bytes.argtypes = [vp, u64p]
+    L.gts_graph_templates.argtypes = [vp] + [ctypes.POINTER(u32)] * 4
+    L.gts_graph_upload.argtypes = [vp, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
+    L.gts_graph_release.argtypes = [vp]
+    L.gts_graph_sizes.argtypes = [vp] + [ctypes.POINTER(u32)] * 5
+    L.gts_scratch_bytes.argtypes = [vp, u32, u32, u64p]
+    L.gts_simulate_batch.argtypes = [vp, vp, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
+    L.gts_hw_validate.argtypes = [vp]
+    L.gts_hwset_device_bytes.argtypes = [u32, u64p]
+    L.gts_hwset_upload.argtypes = [vp, u32, vp, ctypes.c_uint64, vp, ctypes.POINTER(vp)]
+    L.gts_hwset_release.argtypes = [vp]
+    L.gts_simulate_hwset.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, vp, ctypes.c_uint64, u32, vp]
+    L.gts_simulate_hwset_noalloc.argtypes = [vp, vp, u32, u32, vp, vp, vp, vp, u32, vp]
+    L.gts_strerror.argtypes = [ctypes.c_int]
+    L.gts_strerror.restype = ctypes.c_char_p
+    L.gts_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name not in ("gts_strerror", "gts_last_error"):
+            getattr(L, name).restype = ctypes.c_int
+    return L
 
 
 def _check(rc: int, where: str):

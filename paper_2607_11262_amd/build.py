@@ -54,6 +54,19 @@ def build(verbose: bool = True) -> str:
     return OUT
 
 
+def build_host_sanitized(out: str) -> str:
+    """A CPU-only build of the host library (validation, device image
+    construction, argument checks) with g++ under AddressSanitizer and
+    UBSan, kernel launches replaced by stand-ins that report no device.
+    Load it into a process started with the sanitizer runtimes preloaded."""
+    cmd = ["g++", "-O1", "-g", "-std=c++17", "-fPIC", "-shared", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-D__HIP_PLATFORM_AMD__",
+           "-I/opt/rocm/include", os.path.join(CSRC, "gts_host.cpp"), os.path.join(CSRC, "gts_host_only.cpp"),
+           "-L/opt/rocm/lib", "-lamdhip64", "-o", out]
+    _run(cmd)
+    return out
+
+
 if __name__ == "__main__":
     build()
     sys.exit(0)
