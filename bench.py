@@ -1,56 +1,50 @@
 #!/usr/bin/env python3
 """Throughput of the batched tile-graph simulation on one MI355X.
 
-Workload: the GEMM design sweep -- 64 seeded GEMM tile graphs (M, N, K in
-{1,2,4,8}K; CTA tiles {64,128,256}^2 x {32,64}; 2-4 pipeline stages; 4 warps)
-each simulated under 4096 seeded H100-based hardware configurations (SMs
-64-192, DRAM 1.5-8 TB/s, shared memory 96-256 KiB, tensor rate 0.5-4x).
-One step = one graph of the sweep against its 4096 configurations
-(digest + makespan + status per simulation), step i using sweep graph i mod
-64.  Graph images and hardware records are resident in HBM before timing.
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W]
+Default workload, `gemm_design_sweep`: 64 seeded GEMM tile graphs (M, N, K in
+{1,2,4,8}K; CTA tiles {64,128,256}^2 x {32,64}; 2-4 pipeline stages; 4
+warps), each simulated under its own 4096 seeded H100-based hardware
+configurations (SMs 64-192, DRAM 1.5-8 TB/s, shared memory 96-256 KiB, tensor
+rate 0.5-4x): 262,144 simulations.  One step = the whole sweep, digest +
+makespan + status per simulation (per-node cycles for the whole sweep would
+be about 0.6 TB).
 
-Prints one JSON line: simulated tile-nodes per second (value), simulations
-per second, the roofline of the simulation kernel (algorithmic bytes per
-launch / mean launch time from HIP events, against 8 TB/s HBM) and the CPU
-oracle timed on a bounded sample of the same workload on this host.
+The other named workloads, one step = every hardware record of the graph in
+one launch, per-node (start, finish) cycles written for every simulation,
+and the same steps timed again with digest outputs only:
 
-    python bench.py --workload pipelining
+    gemm_1024_a100                 GEMM 1024^3, 128x128x32, 2 stages, 6,208 nodes x 16 A100-based records
+    flash_attention_b8_h32_s4096   flash attention fwd B8 H32 S4096 d128, 2,637,824 nodes x 256 records
+    splitkv_decode_b64             split-KV decode, 64 sequences, 456,528 nodes x 1024 records
+    decoder_layer_prefill_2048     Llama-like decoder layer, 20,515,200 nodes x 64 records
 
-runs the software-pipelining case study instead (Sec. 7.1, Table 4): the
-fused GEMM + SiLU persistent kernel in four pipeline organisations x five
-tile shapes x four edge-class sets (80 graphs of 270-1020 nodes), each
-simulated under 4096 seeded single-SM Hopper machines (tensor rate 0.5-4x,
-DRAM 1.5-8 TB/s, TMA 50-200 B/cycle); its line adds the case-study table
-(normalised performance and Tensor Core utilisation per organisation at
-Table 3's H100 with FP8 rate), read off GPU timelines.
+Graph images and hardware records are resident in HBM before timing.  The
+line reports simulated tile-nodes per second (value), simulations per second,
+the roofline of the simulation kernel (algorithmic bytes per step over the
+step's wall time from HIP events, against 8 TB/s HBM; the per-launch figure
+beside it) and the CPU oracle timed on a bounded sample of the same
+simulations on this host's cores, each sampled result compared with the
+GPU's.
 
-    python bench.py --workload noc
-
-runs the NoC-enabled fusion case study (Sec. 7.2): the cluster-fused
-attention block (32 heads, one cluster per head, clusters of 2-16 CTAs,
-communication over the SM-cluster NoC or through DRAM; 8 graphs of
-12K-61K nodes), each under 4096 seeded H100 machines with a 16-SM-domain
-crossbar or 4 x 4 mesh NoC (any of three placements, port bandwidth 8-64
-B/cycle, latency 60-400 cycles, DRAM 1.5-8 TB/s, tensor 0.5-4x); its line
-adds the case-study table (NoC vs DRAM cycles and mean NoC residence per
-topology and placement) read off GPU timelines.
-
-    python bench.py --workload l2lru
-
-runs eight GEMMs of the design sweep (the smallest of 40K-300K nodes) with
-tile ids (the LRU L2 of Sec. 5.2), each under 4096 seeded H100 sweep
-machines with an L2 of 4-64 MiB; its line adds the kernel cycles of one GEMM across L2 sizes
-(static first-touch flags vs LRU) read off the GPU.
+Case studies (one step = every graph of the study, each under 4096 seeded
+machines): `--workload pipelining` (Sec. 7.1, Table 4: fused GEMM + SiLU in
+four pipeline organisations x five tiles x four edge sets), `--workload noc`
+(Sec. 7.2: cluster-fused attention over an SM-cluster NoC), `--workload
+l2lru` (eight sweep GEMMs with tile ids under an LRU L2 of 4-64 MiB); each
+line adds the study's table read off GPU timelines.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
+import itertools
 import json
 import os
 import re
+import statistics
+import subprocess
 import sys
 import time
 
@@ -60,63 +54,311 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-B_PER_GRAPH = 4096
+B_STUDY = 4096
+NAMED = ("gemm_design_sweep", "gemm_1024_a100", "flash_attention_b8_h32_s4096", "splitkv_decode_b64",
+         "decoder_layer_prefill_2048")
+STUDIES = ("pipelining", "noc", "l2lru")
+KERNEL_SOURCES = ("gts_window.hip", "gts_sim.hip", "gts_common.h", "gts_dev.h")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
-def alg_bytes_per_sim(g) -> int:
-    """Bytes one simulation must read from the graph (16-byte node record per
-    node, 4 bytes per edge) plus its 16 bytes of per-simulation output."""
-    return 16 * g.n_nodes + 4 * g.n_edges + 16
+def alg_bytes_per_sim(g, out_nodes: bool) -> int:
+    """Bytes one simulation must move: its graph read once -- per node the op
+    id (2 B), warp mask (2 B), successor offset (4 B) and in-degree (2 B), 4 B
+    per edge -- its makespan, status and digest (16 B), and with per-node
+    output 8 B per node (start, finish)."""
+    return 10 * g.n_nodes + 4 * g.n_edges + 16 + (8 * g.n_nodes if out_nodes else 0)
 
 
-PROFILE = os.path.join(ROOT, "profiles", "gts_sim_window_gemm_design_sweep.md")
-KERNEL_SOURCES = ("gts_window.hip", "gts_common.h", "gts_dev.h")
-
-
-def recorded_traffic(n_launch: int):
-    """HBM bytes per launch of the simulation kernel, from the committed
-    rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE summed over the
-    timed launches, scaled by the same counters on a plain copy), or None
-    when that summary was taken on other kernel sources or other launches."""
-    try:
-        text = open(PROFILE).read()
-    except OSError:
-        return None
-    m = re.search(r"traffic-record: sha256=(\w+) launches=(\d+) fetch_kib=(\d+) write_kib=(\d+) "
-                  r"fetch_factor=([\d.]+) write_factor=([\d.]+)", text)
-    if not m:
-        return None
+def sources_hash() -> str:
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2607_11262_amd", "csrc", name), "rb") as f:
             h.update(f.read())
-    if m.group(1) != h.hexdigest() or int(m.group(2)) != n_launch:
+    return h.hexdigest()
+
+
+TRAFFIC_RE = re.compile(r"traffic-record: workload=(\S+) outputs=(\S+) sha256=(\w+) node_sims=(\d+) "
+                        r"fetch_kib=(\d+) write_kib=(\d+) fetch_factor=([\d.]+) write_factor=([\d.]+)")
+
+
+def recorded_traffic(workload: str, outputs: str, profiles=PROFILES):
+    """HBM bytes per simulated node of the simulation kernels, from a
+    committed rocprofv3 counter summary of this workload and output mode
+    (FETCH_SIZE and WRITE_SIZE summed over the profiled dispatches, each
+    scaled by what the same counter reads for a plain device copy, over the
+    node-simulations of those dispatches); None when no summary was taken on
+    the current kernel sources."""
+    sha = sources_hash()
+    try:
+        names = sorted(os.listdir(profiles))
+    except OSError:
         return None
-    fetch = int(m.group(3)) * 1024 * float(m.group(5))
-    write = int(m.group(4)) * 1024 * float(m.group(6))
-    return (fetch + write) / n_launch
+    for name in names:
+        if not name.endswith(".md"):
+            continue
+        with open(os.path.join(profiles, name)) as f:
+            for m in TRAFFIC_RE.finditer(f.read()):
+                if m.group(1) == workload and m.group(2) == outputs and m.group(3) == sha:
+                    fetch = int(m.group(5)) * 1024 * float(m.group(7))
+                    write = int(m.group(6)) * 1024 * float(m.group(8))
+                    return (fetch + write) / int(m.group(4))
+    return None
+
+
+def cpu_model() -> str:
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def workload_parts(name):
+    """(describe, make(i) -> (graph, hw records), count) of a workload's
+    graphs; one step simulates every graph under all of its records."""
+    from paper_2607_11262_amd.gen import clusterfusion as CF
+    from paper_2607_11262_amd.gen import pipelining as PL
+    from paper_2607_11262_amd.gen import workloads as W
+    if name == "gemm_design_sweep":
+        params = W.sweep_params()
+        return (lambda i: params[i],
+                lambda i: (W.sweep_graph(params[i]), W.workload_hw(name, index=i)), len(params))
+    if name in NAMED:
+        return (lambda i: name, lambda i: (W.workload_graph(name), W.workload_hw(name)), 1)
+    if name == "pipelining":
+        return (lambda i: PL.case_study_graphs()[i],
+                lambda i: (PL.case_study_graph(i), PL.sample_hopper_1sm(i, B_STUDY)), len(PL.case_study_graphs()))
+    if name == "noc":
+        graphs = [(S, comm) for S in CF.CLUSTER_SIZES for comm in CF.COMMS]
+        return (lambda i: graphs[i],
+                lambda i: (CF.cluster_attention(graphs[i][0], comm=graphs[i][1]), CF.sample_noc_machines(i, B_STUDY)),
+                len(graphs))
+    if name == "l2lru":
+        ps = [q for q in sorted(W.sweep_params(), key=W.sweep_nodes) if 40_000 <= W.sweep_nodes(q) <= 300_000][:8]
+
+        def make(i):
+            hw = W.workload_hw("gemm_design_sweep", B=B_STUDY, index=i)
+            rng = np.random.default_rng(5000 + i)
+            hw[:, 26] = (rng.integers(4, 65, size=B_STUDY) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
+            return W.gemm(*ps[i], tiles=True), hw
+        return (lambda i: ps[i], make, len(ps))
+    raise KeyError(name)
+
+
+class Plan:
+    """Every graph of the workload uploaded with its records, and the
+    launches of one step: each graph's records in equal chunks that fit the
+    per-stream scratch budget, consecutive launches alternating over the
+    streams."""
+
+    def __init__(self, api, torch, name, flags, budget, streams, dev):
+        describe, make, n = workload_parts(name)
+        self.parts = []   # (graph handle, hw set, outputs, host graph, host hw)
+        self.launches = []  # (part, first, count)
+        self.flags = flags
+        max_scratch = 0
+        for i in range(n):
+            g, hw = make(i)
+            dg = api.upload(g)
+            hs = api.upload_hw(hw)
+            B = hw.shape[0]
+            per_sim = api.scratch_bytes(dg, 2, flags) - api.scratch_bytes(dg, 1, flags)
+            most = max(1, min(B, budget // max(per_sim, 1)))
+            n_launch = -(-B // most)
+            chunk = -(-B // n_launch)  # equal launches: a short tail launch costs a whole simulation's latency
+            max_scratch = max(max_scratch, api.scratch_bytes(dg, chunk, flags))
+            outs = api.alloc_outputs(dg, B, flags, dev)
+            self.parts.append((dg, hs, outs, g, hw))
+            for first in range(0, B, chunk):
+                self.launches.append((i, first, min(chunk, B - first)))
+            print(f"[bench] graph {i} {describe(i)} N={g.n_nodes} E={g.n_edges} B={B} chunk={chunk}",
+                  file=sys.stderr, flush=True)
+        self.streams = streams
+        self.scratches = [torch.empty(max(max_scratch, 1), dtype=torch.uint8, device=dev) for _ in streams]
+
+    def step(self, api, torch, events=None, flags=None):
+        """Enqueue one step; with `events`, append (start, end) HIP events
+        around each launch on its stream."""
+        flags = self.flags if flags is None else flags
+        for k, (i, first, b) in enumerate(self.launches):
+            dg, hs, (cyc, mk, st, dgst), _, _ = self.parts[i]
+            s, scratch = self.streams[k % len(self.streams)], self.scratches[k % len(self.streams)]
+            if events is not None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+            api.simulate_hwset_into(dg, hs, first, b, flags, cyc[first:first + b] if cyc is not None else None,
+                                    mk[first:first + b], st[first:first + b],
+                                    dgst[first:first + b] if dgst is not None else None, scratch, s)
+            if events is not None:
+                e1.record(s)
+                events.append((e0, e1))
+
+    def timed(self, api, torch, steps, flags=None):
+        """Run `steps` steps, each bracketed by HIP events on the first
+        stream (the others wait for its start event, and it for their ends).
+        Returns (per-step seconds, per-launch seconds, wall seconds)."""
+        s0 = self.streams[0]
+        step_ev, launch_ev = [], []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s0)
+            for s in self.streams[1:]:
+                s.wait_event(a)
+            self.step(api, torch, launch_ev, flags)
+            for s in self.streams[1:]:
+                e = torch.cuda.Event()
+                e.record(s)
+                s0.wait_event(e)
+            z.record(s0)
+            step_ev.append((a, z))
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return ([a.elapsed_time(z) * 1e-3 for a, z in step_ev], [a.elapsed_time(z) * 1e-3 for a, z in launch_ev],
+                wall)
+
+    def feasible(self):
+        """Per graph: its feasible records (an infeasible simulation stops
+        after the residency check and simulates no node)."""
+        return [(p[2][2] == 0).cpu().numpy() for p in self.parts]
+
+    def step_totals(self, out_nodes):
+        ok = self.feasible()
+        node_sims = sum(int(f.sum()) * p[3].n_nodes for f, p in zip(ok, self.parts))
+        sims = sum(p[4].shape[0] for p in self.parts)
+        abytes = sum(int(f.sum()) * (alg_bytes_per_sim(p[3], out_nodes) - 16) + 16 * p[4].shape[0]
+                     for f, p in zip(ok, self.parts))
+        return node_sims, sims, abytes, sum(int((~f).sum()) for f in ok)
+
+
+def cpu_leg(plan, flags, seconds, out_nodes):
+    """The oracle on this host: a single-thread rate first, then every core
+    on records drawn in rounds that take one record from each launch of the
+    step (spread over the launch), each result compared with the GPU's --
+    digest, makespan and status, and every node's cycles for the first
+    records of each launch when per-node output is on."""
+    import oracle
+    from concurrent.futures import ThreadPoolExecutor
+    threads = len(os.sched_getaffinity(0))
+    rng = np.random.default_rng(7)
+    orders = [first + rng.permutation(b) for (_, first, b) in plan.launches]
+    host_out = []
+    for p in plan.parts:
+        mk, st, dg = p[2][1:]
+        host_out.append((mk.cpu().numpy().view(np.uint32), st.cpu().numpy(),
+                         dg.cpu().numpy().view(np.uint64) if dg is not None else None))
+    checked = bad = node_fail = 0
+    nodes_checked_sims = 0
+    unique = set()
+
+    def one(task):
+        i, r, want = task
+        g, hw = plan.parts[i][3], plan.parts[i][4]
+        f = flags | (oracle.F_NODES if want else 0)
+        mk, st, dg, cyc = oracle.simulate_records(g, hw[r:r + 1], f, want_nodes=want)
+        return i, r, want, mk[0], st[0], dg[0], (cyc[0] if want else None), g.n_nodes
+
+    def check(res):
+        nonlocal checked, bad, node_fail, nodes_checked_sims
+        i, r, want, mk, st, dg, cyc, n = res
+        gmk, gst, gdg = host_out[i]
+        checked += 1
+        unique.add((i, r))
+        wrong = st != gst[r] or mk != gmk[r] or (gdg is not None and dg != gdg[r])
+        bad += int(wrong)
+        if want and st == 0:
+            gc = plan.parts[i][2][0][r].cpu().numpy().view(np.uint32)
+            node_fail += int(not np.array_equal(gc, cyc))
+            nodes_checked_sims += 1
+        return n if st == 0 else 0
+
+    def rounds():
+        for k in range(max(len(o) for o in orders)):
+            yield [(plan.launches[j][0], int(o[k]), bool(out_nodes and k < 2)) for j, o in enumerate(orders)
+                   if k < len(o)]
+
+    # single thread: the first tasks in order, about a sixth of the budget;
+    # a workload with fewer simulations than the budget covers is sampled
+    # again from its start (each pass rechecks the same records)
+    it = itertools.cycle(t for rnd in rounds() for t in rnd)
+    t1 = time.perf_counter()
+    nodes1 = 0
+    done1 = 0
+    for task in it:
+        nodes1 += check(one(task))
+        done1 += 1
+        if time.perf_counter() - t1 > seconds / 6:
+            break
+    sec1 = time.perf_counter() - t1
+    # all cores: whole rounds of the remaining tasks
+    t2 = time.perf_counter()
+    nodes_all = 0
+    done_all = 0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        pending = []
+        for task in it:
+            pending.append(task)
+            if len(pending) >= threads * 4:
+                for res in ex.map(one, pending):
+                    nodes_all += check(res)
+                done_all += len(pending)
+                pending = []
+                if time.perf_counter() - t2 > seconds:
+                    break
+        if pending and time.perf_counter() - t2 <= seconds:
+            for res in ex.map(one, pending):
+                nodes_all += check(res)
+            done_all += len(pending)
+    sec_all = time.perf_counter() - t2
+    launches_touched = len({j for j, (i, first, b) in enumerate(plan.launches)
+                            if any(i == ui and first <= ur < first + b for ui, ur in unique)}) \
+        if len(plan.launches) < 512 else None
+    cpu = {"value": nodes_all / sec_all if sec_all > 0 else None, "unit": "simulated tile-nodes/s",
+           "cores": threads, "kind": "oracle",
+           "single_core": nodes1 / sec1 if sec1 > 0 else None,
+           "cores_available": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
+           "sample": f"{done1} simulations on 1 thread ({sec1:.1f} s), then {done_all} on {threads} threads "
+                     f"({sec_all:.1f} s), records drawn in rounds of one per launch of the step"}
+    parity = {"checked_sims": len(unique), "checks": checked, "mismatches": bad, "launches": len(plan.launches),
+              "launches_sampled": launches_touched, "node_cycle_sims": nodes_checked_sims,
+              "node_cycle_mismatches": node_fail}
+    return cpu, parity
 
 
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", choices=("gemm_design_sweep", "pipelining", "noc", "l2lru"),
-                    default="gemm_design_sweep")
-    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--workload", choices=NAMED + STUDIES, default="gemm_design_sweep")
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--digest-only", action="store_true",
+                    help="named workloads other than the sweep: time digest outputs only (no per-node cycles)")
+    ap.add_argument("--nodes-only", action="store_true",
+                    help="named workloads other than the sweep: skip the second, digest-only timed region")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mem-budget-gb", type=float, default=220.0,
                     help="device scratch budget, split evenly over the streams")
-    ap.add_argument("--graphs", type=str, default="", help="comma-separated sweep graph indices (default: step order)")
     ap.add_argument("--streams", type=int, default=2,
-                    help="consecutive launches alternate over this many HIP streams, so one launch "
-                         "overlaps the tail of the previous one")
+                    help="consecutive launches alternate over this many HIP streams, so one launch overlaps the "
+                         "tail of the previous one")
     ap.add_argument("--launch-log", type=str, default="", help="write one JSON line per timed launch to this file")
     ap.add_argument("--host-io", action="store_true",
                     help="after the timed region, time the same steps through host buffers: hardware records "
                          "passed from host memory per call (gts_simulate_batch) and results copied back, then "
-                         "also with each step's graph uploaded from host arrays")
+                         "also with each graph uploaded from its host arrays every step")
     ap.add_argument("--phase-stats", action="store_true",
                     help="after the timed region, report the windowed kernel's per-phase counters per graph")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
@@ -131,9 +373,6 @@ def main() -> int:
     import torch
 
     from paper_2607_11262_amd import api
-    from paper_2607_11262_amd.gen import clusterfusion as CF
-    from paper_2607_11262_amd.gen import pipelining as PL
-    from paper_2607_11262_amd.gen import workloads as W
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -152,214 +391,110 @@ def main() -> int:
     dev = torch.device("cuda:0")
     streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(max(1, args.streams) - 1)]
 
-    pipelining = args.workload == "pipelining"
-    noc = args.workload == "noc"
-    lru = args.workload == "l2lru"
-    noc_graphs = [(S, comm) for S in CF.CLUSTER_SIZES for comm in CF.COMMS]
-    if lru:
-        all_params = W.sweep_params()
-        lru_params = [q for q in sorted(all_params, key=W.sweep_nodes) if 40_000 <= W.sweep_nodes(q) <= 300_000][:8]
-        n_graphs = len(lru_params)
-
-        def make(gi):
-            g = W.gemm(*lru_params[gi], tiles=True)
-            hw = W.workload_hw("gemm_design_sweep", B=B_PER_GRAPH, index=gi)
-            rng = np.random.default_rng(5000 + gi)
-            hw[:, 26] = (rng.integers(4, 65, size=B_PER_GRAPH) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
-            return g, hw
-
-        def describe(gi):
-            return lru_params[gi]
-    elif noc:
-        n_graphs = len(noc_graphs)
-
-        def make(gi):
-            return CF.cluster_attention(noc_graphs[gi][0], comm=noc_graphs[gi][1]), CF.sample_noc_machines(gi, B_PER_GRAPH)
-
-        def describe(gi):
-            return noc_graphs[gi]
-    elif pipelining:
-        n_graphs = len(PL.case_study_graphs())
-
-        def make(gi):
-            return PL.case_study_graph(gi), PL.sample_hopper_1sm(gi, B_PER_GRAPH)
-
-        def describe(gi):
-            return PL.case_study_graphs()[gi]
-    else:
-        params = W.sweep_params()
-        n_graphs = len(params)
-
-        def make(gi):
-            return W.sweep_graph(params[gi]), W.workload_hw("gemm_design_sweep", B=B_PER_GRAPH, index=gi)
-
-        def describe(gi):
-            return params[gi]
-    if args.graphs:
-        order = [int(x) for x in args.graphs.split(",")]
-    else:
-        order = list(range(n_graphs))
-    step_graphs = [order[i % len(order)] for i in range(args.steps)]
-    warm_graphs = [order[i % len(order)] for i in range(args.warmup)]
-    needed = sorted(set(step_graphs) | set(warm_graphs))
-
-    flags = api.OUT_DIGEST
-    t_gen = time.time()
-    prepared = {}
-    host_graphs = {}
+    name = args.workload
+    sweep = name == "gemm_design_sweep"
+    per_node = name in NAMED and not sweep and not args.digest_only
+    flags = api.OUT_DIGEST | (api.OUT_NODES if per_node else 0)
+    t_setup = time.time()
     budget = int(args.mem_budget_gb * (1 << 30)) // max(1, args.streams)
-    max_scratch = 0
-    for gi in needed:
-        g, hw = make(gi)
-        dg = api.upload(g)
-        hs = api.upload_hw(hw)
-        per_sim = api.scratch_bytes(dg, 1, flags) - api.scratch_bytes(dg, 0, flags)
-        # launches of equal size (a short tail launch would cost a whole
-        # simulation's latency for a few waves)
-        most = max(1, min(B_PER_GRAPH, budget // max(per_sim, 1)))
-        n_launch = -(-B_PER_GRAPH // most)
-        chunk = -(-B_PER_GRAPH // n_launch)
-        max_scratch = max(max_scratch, api.scratch_bytes(dg, chunk, flags))
-        outs = api.alloc_outputs(dg, B_PER_GRAPH, flags, dev)
-        prepared[gi] = (dg, hs, chunk, outs, g.n_nodes, alg_bytes_per_sim(g))
-        host_graphs[gi] = (g, hw)
-        print(f"[bench] graph {gi} {describe(gi)} N={g.n_nodes} E={g.n_edges} chunk={chunk}", file=sys.stderr,
-              flush=True)
-    t_gen = time.time() - t_gen
-    # one scratch area per stream; each graph's outputs are its own
-    scratches = [torch.empty(max_scratch, dtype=torch.uint8, device=dev) for _ in streams]
-    launches = []  # (start event, end event, algorithmic bytes, node-sims)
-    launch_info = []  # (graph, first record, records)
+    plan = Plan(api, torch, name, flags, budget, streams, dev)
+    t_setup = time.time() - t_setup
 
-    n_launched = [0]
-
-    def step(k, gi, record):
-        dg, hs, chunk, (cyc, mk, st, dgst), n, abps = prepared[gi]
-        for first in range(0, B_PER_GRAPH, chunk):
-            # launches (not steps) alternate over the streams: the chunks of a
-            # graph too large for one launch then run side by side
-            stream, scratch = streams[n_launched[0] % len(streams)], scratches[n_launched[0] % len(streams)]
-            n_launched[0] += 1
-            b = min(chunk, B_PER_GRAPH - first)
-            if record:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-            api.simulate_hwset_into(dg, hs, first, b, flags, None, mk[first:first + b], st[first:first + b],
-                                    dgst[first:first + b], scratch, stream)
-            if record:
-                e1.record(stream)
-                launches.append((e0, e1, abps * b, n * b))
-                launch_info.append((gi, first, b))
-
-    for k, gi in enumerate(warm_graphs):
-        step(k, gi, False)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k, gi in enumerate(step_graphs):
-        step(k, gi, True)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
-
-    # simulated nodes count only feasible simulations (an infeasible one
-    # stops after the residency check); simulations/s counts all of them
-    ok_per_graph = {gi: int((prepared[gi][3][2] == 0).sum().item()) for gi in set(step_graphs)}
-    node_sims = sum(prepared[gi][4] * ok_per_graph[gi] for gi in step_graphs)
-    sims = B_PER_GRAPH * len(step_graphs)
-    durs = np.array([a.elapsed_time(b) * 1e-3 for a, b, _, _ in launches])
+    for _ in range(args.warmup):
+        plan.step(api, torch)
+    step_s, launch_s, wall = plan.timed(api, torch, args.steps)
+    node_sims, sims, abytes, infeasible = plan.step_totals(per_node)
+    K = args.steps
     if args.launch_log:
         with open(args.launch_log, "w") as f:
-            for (gi, first, b), d in zip(launch_info, durs):
-                f.write(json.dumps({"graph": gi, "first": first, "sims": b, "ms": float(d * 1e3)}) + "\n")
-    abytes = np.array([x for _, _, x, _ in launches], dtype=np.float64)
-    # dominant kernel: the simulation kernel (the only kernel in the step).
-    # achieved: algorithmic bytes per launch / mean launch duration; with
-    # launches overlapping on several streams the aggregate rate (all bytes
-    # over the timed region) is higher and is reported beside it.
-    achieved_gbs = float(abytes.sum() / durs.sum() / 1e9)
-    aggregate_gbs = float(abytes.sum() / elapsed / 1e9)
-    traffic = None if (pipelining or noc or lru) else recorded_traffic(len(launches))
-    statuses = np.concatenate([prepared[gi][3][2].cpu().numpy() for gi in sorted(set(step_graphs))])
+            for (i, first, b), d in zip(plan.launches * K, launch_s):
+                f.write(json.dumps({"graph": i, "first": first, "sims": b, "ms": d * 1e3,
+                                    "node_sims": int((plan.parts[i][2][2][first:first + b] == 0).sum().item())
+                                    * plan.parts[i][3].n_nodes}) + "\n")
+    mean_step = float(np.mean(step_s))
+    achieved = abytes / mean_step / 1e9
+    launches_per_step = len(plan.launches)
+    mean_launch = float(np.mean(launch_s))
+    outputs = "nodes" if per_node else "digest"
+    traffic_per_node = recorded_traffic(name, outputs)
+    traffic = traffic_per_node * node_sims if traffic_per_node else None
 
-    host_io_rates = host_io(api, torch, prepared, host_graphs, scratches, streams, step_graphs, flags) \
-        if args.host_io else None
+    digest_only = None
+    if per_node and not args.nodes_only:
+        # the same steps with digest outputs only (no per-node cycles written)
+        for _ in range(args.warmup):
+            plan.step(api, torch, flags=api.OUT_DIGEST)
+        d_step, d_launch, d_wall = plan.timed(api, torch, K, flags=api.OUT_DIGEST)
+        nb = sum(int(f.sum()) * (alg_bytes_per_sim(p[3], False) - 16) + 16 * p[4].shape[0]
+                 for f, p in zip(plan.feasible(), plan.parts))
+        d_traffic = recorded_traffic(name, "digest")
+        digest_only = {"value": node_sims * K / d_wall, "ms_per_step": float(np.mean(d_step)) * 1e3,
+                       "median_ms_per_step": float(statistics.median(d_step)) * 1e3,
+                       "achieved_gbs": nb / float(np.mean(d_step)) / 1e9,
+                       "frac": nb / float(np.mean(d_step)) / 1e9 / HBM_PEAK_GBS,
+                       "traffic": d_traffic * node_sims if d_traffic else None}
+        # the per-node outputs of the last per-node step are what the CPU leg
+        # checks: run it once more
+        plan.step(api, torch)
+        torch.cuda.synchronize()
+
+    host_io_rates = host_io(api, torch, plan, K) if args.host_io else None
 
     phases = None
     if args.phase_stats:
-        if noc or lru:  # clustered and tiled graphs run on the general kernel, which keeps no such counters
-            print("--phase-stats covers the windowed kernel only", file=sys.stderr)
-        else:
-            phases = phase_stats(api, torch, prepared, scratches[0], streams[0], sorted(set(step_graphs)), flags)
+        phases = phase_stats(api, torch, plan)
 
-    cpu = None
-    parity = None
+    cpu = parity = None
     if not args.no_cpu_baseline:
-        # the oracle on a bounded sample of the same sweep: batches of
-        # `threads` configurations, cycling through the timed graphs, each
-        # result also checked against the GPU's
-        import oracle
-        threads = min(16, len(os.sched_getaffinity(0)))
-        checked, bad, nodes_done = 0, 0, 0
-        used = []
-        c0 = time.perf_counter()
-        k = 0
-        while time.perf_counter() - c0 < args.cpu_seconds and (k // len(step_graphs) + 1) * threads <= B_PER_GRAPH:
-            gi = step_graphs[k % len(step_graphs)]
-            first = (k // len(step_graphs)) * threads
-            k += 1
-            g, hw = host_graphs[gi]
-            idx = list(range(first, min(first + threads, B_PER_GRAPH)))
-            mk_gpu = prepared[gi][3][1][idx].cpu().numpy().view(np.uint32)
-            st_gpu = prepared[gi][3][2][idx].cpu().numpy()
-            dg_gpu = prepared[gi][3][3][idx].cpu().numpy().view(np.uint64)
-            omk, ost, odg, _ = oracle.simulate_batch(g, hw[idx], flags, want_nodes=False, threads=threads)
-            checked += len(idx)
-            bad += int(np.sum((omk != mk_gpu) | (ost != st_gpu) | (odg != dg_gpu)))
-            nodes_done += g.n_nodes * int(np.sum(ost == 0))
-            used.append(gi)
-        csec = time.perf_counter() - c0
-        cpu = {"value": nodes_done / csec, "unit": "simulated tile-nodes/s", "cores": threads, "kind": "oracle",
-               "sample": f"{checked} simulations ({len(set(used))} sweep graphs, {threads} configurations each, "
-                         f"cycling in step order), {threads} threads, {csec:.1f} s"}
-        parity = {"checked_sims": checked, "mismatches": bad}
+        cpu, parity = cpu_leg(plan, flags & ~api.OUT_NODES, args.cpu_seconds, per_node)
+        cpu["value_unit_note"] = "simulated tile-nodes per second of the oracle (feasible simulations)"
 
     out = {
         "metric": "simulated tile-nodes/sec (batched) + simulations/sec; % of HBM roofline",
-        "value": node_sims / elapsed,
+        "value": node_sims * K / wall,
         "unit": "simulated tile-nodes/s",
         "n_gpus": 1,
-        "steps": len(step_graphs),
-        "warmup": len(warm_graphs),
-        "ms_per_step": elapsed / len(step_graphs) * 1e3,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": wall / K * 1e3,
+        "median_ms_per_step": float(statistics.median(step_s)) * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "graphs": step_graphs, "sims_per_graph": B_PER_GRAPH,
-                   "outputs": "makespan+status+digest", "parallelism": "one wavefront per simulation",
-                   "streams": len(streams)},
-        "simulations_per_s": sims / elapsed,
-        "node_sims": node_sims,
-        "infeasible_sims": int((statuses == 1).sum()),
-        "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "traffic_over_algorithmic": (traffic / float(abytes.mean())) if traffic else None,
-                     "kernel": "gts_sim_wave" if (noc or lru) else "gts_sim_window", "launches": len(launches),
-                     "mean_launch_ms": float(durs.mean() * 1e3),
-                     "streams": len(streams), "aggregate_gbs": aggregate_gbs,
-                     "aggregate_frac": aggregate_gbs / HBM_PEAK_GBS},
+        "config": {"workload": name, "graphs": len(plan.parts),
+                   "sims_per_step": sims,
+                   "outputs": "per-node start/finish + makespan + status + digest" if per_node
+                   else "makespan + status + digest",
+                   "parallelism": "one wavefront per simulation", "streams": len(streams),
+                   "launches_per_step": launches_per_step},
+        "simulations_per_s": sims * K / wall,
+        "node_sims_per_step": node_sims,
+        "infeasible_sims_per_step": infeasible,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_over_algorithmic": (traffic / abytes) if traffic else None,
+                     "traffic_per_node_sim": traffic_per_node,
+                     "algorithmic_bytes_per_step": abytes,
+                     "step_ms": mean_step * 1e3,
+                     "kernel": "gts_sim_wave" if name in ("noc", "l2lru") else "gts_sim_window",
+                     "launch_ms": mean_launch * 1e3,
+                     "per_launch_gbs": abytes / launches_per_step / mean_launch / 1e9,
+                     "note": "achieved = algorithmic bytes per step / mean step time (HIP events; launches of a "
+                             "step overlap on the streams); per_launch_gbs = bytes per launch / mean launch time"},
         "cpu_baseline": cpu,
         "parity_sample": parity,
-        "setup_s": t_gen,
+        "setup_s": t_setup,
     }
-    if pipelining:
-        out["case_study"] = case_study(api, torch, PL)
-    if noc:
-        out["case_study"] = noc_case_study(api, torch, CF)
-    if lru:
-        out["case_study"] = lru_case_study(api, torch, W)
+    if digest_only is not None:
+        out["digest_only"] = digest_only
+    if name == "pipelining":
+        out["case_study"] = case_study(api, torch)
+    if name == "noc":
+        out["case_study"] = noc_case_study(api, torch)
+    if name == "l2lru":
+        out["case_study"] = lru_case_study(api, torch)
     if phases is not None:
         out["phase_stats"] = phases
     if host_io_rates is not None:
@@ -368,43 +503,43 @@ def main() -> int:
     return 0
 
 
-def host_io(api, torch, prepared, host_graphs, scratches, streams, step_graphs, flags):
+def host_io(api, torch, plan, K):
     """The timed steps again, end to end from host memory (never the
     headline value): (a) each launch passes its hardware records from host
-    memory (the C ABI copies them over PCIe into scratch) and each step's
-    makespan / status / digest come back to pinned host memory; (b) as (a),
-    with each step's graph also uploaded from its host arrays (validation and
-    image construction on the CPU, then the copy)."""
-    pinned = {gi: [torch.empty(prepared[gi][3][i].shape, dtype=prepared[gi][3][i].dtype, pin_memory=True)
-                   for i in (1, 2, 3)] for gi in set(step_graphs)}
+    memory (the C ABI copies them over PCIe into scratch) and each graph's
+    makespan / status / digest come back to pinned host memory every step;
+    (b) as (a), with every graph also uploaded from its host arrays every
+    step (validation and image construction on the CPU, then the copy)."""
+    pinned = [[torch.empty(x.shape, dtype=x.dtype, pin_memory=True) for x in p[2][1:] if x is not None]
+              for p in plan.parts]
+    node_sims = plan.step_totals(False)[0]
     rates = {}
     for mode in ("records", "records+graph"):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        nodes = 0
-        keep = []  # uploaded images stay alive until every launch that reads them is done
-        for k, gi in enumerate(step_graphs):
-            stream, scratch = streams[k % len(streams)], scratches[k % len(streams)]
-            dg, hs, chunk, (cyc, mk, st, dgst), n, _ = prepared[gi]
-            g, hw = host_graphs[gi]
-            if mode == "records+graph":
-                dg = api.upload(g, stream)
-                keep.append(dg)
-            for first in range(0, B_PER_GRAPH, chunk):
-                b = min(chunk, B_PER_GRAPH - first)
-                api.simulate_into(dg, hw[first:first + b], flags, None, mk[first:first + b], st[first:first + b],
-                                  dgst[first:first + b], scratch, stream)
-            with torch.cuda.stream(stream):
-                for dst, src in zip(pinned[gi], (mk, st, dgst)):
-                    dst.copy_(src, non_blocking=True)
-        torch.cuda.synchronize()
+        for _ in range(K):
+            keep = []  # uploaded images stay alive until every launch that reads them is done
+            graphs = {}
+            for k, (i, first, b) in enumerate(plan.launches):
+                s, scratch = plan.streams[k % len(plan.streams)], plan.scratches[k % len(plan.streams)]
+                dg, hs, (cyc, mk, st, dgst), g, hw = plan.parts[i]
+                if mode == "records+graph":
+                    if i not in graphs:
+                        graphs[i] = api.upload(g, s)
+                        keep.append(graphs[i])
+                    dg = graphs[i]
+                api.simulate_into(dg, hw[first:first + b], api.OUT_DIGEST, None, mk[first:first + b],
+                                  st[first:first + b], dgst[first:first + b], scratch, s)
+                if first + b == hw.shape[0]:  # the graph's last launch: its results to the host
+                    with torch.cuda.stream(s):
+                        for dst, src in zip(pinned[i], (mk, st, dgst)):
+                            dst.copy_(src, non_blocking=True)
+            torch.cuda.synchronize()
+            keep.clear()
         dt = time.perf_counter() - t0
-        keep.clear()
-        for gi in set(step_graphs):
-            nodes_ok = prepared[gi][4] * int((pinned[gi][1] == 0).sum().item())
-            nodes += nodes_ok * step_graphs.count(gi)
-        rates[mode] = {"value": nodes / dt, "unit": "simulated tile-nodes/s", "seconds": dt}
-        print(f"[bench] host io {mode}: {nodes / dt:.4e} tile-nodes/s over {dt:.2f} s", file=sys.stderr, flush=True)
+        rates[mode] = {"value": node_sims * K / dt, "unit": "simulated tile-nodes/s", "seconds": dt}
+        print(f"[bench] host io {mode}: {node_sims * K / dt:.4e} tile-nodes/s over {dt:.2f} s", file=sys.stderr,
+              flush=True)
     return rates
 
 
@@ -412,7 +547,7 @@ PHASE_COLUMNS = ("windows", "local_steps", "local_nodes", "memory_arrivals", "re
                  "clk_scan", "clk_retire", "clk_local", "clk_gather", "clk_memory")
 
 
-def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
+def phase_stats(api, torch, plan):
     """Where a windowed-kernel simulation spends its time: one untimed launch
     of each graph's first chunk, then the per-simulation counter block the
     kernel writes at the end of each simulation's scratch slice (windows,
@@ -424,13 +559,19 @@ def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
     access, which the timed launches avoid."""
     rows = {}
     os.environ["GTS_WINDOW_CLOCKS"] = "1"  # the kernel reads its clock only when asked
-    for gi in graphs:
-        dg, hs, chunk, (cyc, mk, st, dgst), n, _ = prepared[gi]
+    scratch, stream = plan.scratches[0], plan.streams[0]
+    seen = set()
+    for (i, first, b) in plan.launches:
+        if i in seen:
+            continue
+        seen.add(i)
+        dg, hs, (cyc, mk, st, dgst), _, _ = plan.parts[i]
+        flags = api.OUT_DIGEST
         stride = api.scratch_bytes(dg, 2, flags) - api.scratch_bytes(dg, 1, flags)
-        api.simulate_hwset_into(dg, hs, 0, chunk, flags, None, mk[:chunk], st[:chunk], dgst[:chunk], scratch, stream)
+        api.simulate_hwset_into(dg, hs, 0, b, flags, None, mk[:b], st[:b], dgst[:b], scratch, stream)
         torch.cuda.synchronize()
-        blk = scratch[:chunk * stride].view(chunk, stride)[:, stride - 128:].contiguous().view(torch.int64)
-        ok = (st[:chunk] == 0).cpu().numpy()
+        blk = scratch[:b * stride].view(b, stride)[:, stride - 128:].contiguous().view(torch.int64)
+        ok = (st[:b] == 0).cpu().numpy()
         if not ok.any():
             continue
         m = blk.cpu().numpy()[ok][:, :len(PHASE_COLUMNS)].astype(np.float64).mean(axis=0)
@@ -438,20 +579,21 @@ def phase_stats(api, torch, prepared, scratch, stream, graphs, flags):
         clk = m[6:11]
         row["nodes_per_local_step"] = round(float(m[2] / max(m[1], 1)), 2)
         row["arrivals_per_window"] = round(float(m[3] / max(m[0], 1)), 2)
-        row["clk_share"] = {k[4:]: round(float(c / clk.sum()), 3) for k, c in zip(PHASE_COLUMNS[6:], clk)}
+        row["clk_share"] = {k[4:]: round(float(c / max(clk.sum(), 1)), 3) for k, c in zip(PHASE_COLUMNS[6:], clk)}
         row["clk_per_local_step"] = round(float(m[8] / max(m[1], 1)))
         row["clk_per_window_memory"] = round(float((m[9] + m[10]) / max(m[0], 1)))
-        rows[str(gi)] = row
-        print(f"[bench] phase stats graph {gi}: {json.dumps(row)}", file=sys.stderr, flush=True)
+        rows[str(i)] = row
+        print(f"[bench] phase stats graph {i}: {json.dumps(row)}", file=sys.stderr, flush=True)
     os.environ.pop("GTS_WINDOW_CLOCKS", None)
     return rows
 
 
-def lru_case_study(api, torch, W):
+def lru_case_study(api, torch):
     """One GEMM (4096 x 4096 x 2048, 128 x 128 x 64 tiles, 3 stages) on
     Table 3's H100 across L2 sizes: kernel cycles under the static
     first-touch flags (0 MiB) and under the LRU L2."""
     from paper_2607_11262_amd.gen import hw as H
+    from paper_2607_11262_amd.gen import workloads as W
     g = W.gemm(4096, 4096, 2048, 128, 128, 64, 3, tiles=True)
     sizes = (0, 0.5, 2, 8, 32, 50)
     recs = np.stack([H.preset("H100", l2_lines=H.l2_lines(m)) for m in sizes])
@@ -462,12 +604,13 @@ def lru_case_study(api, torch, W):
             "cycles_by_l2_mib": {("static" if m == 0 else str(m)): int(c) for m, c in zip(sizes, mk)}}
 
 
-def noc_case_study(api, torch, CF):
+def noc_case_study(api, torch):
     """Sec. 7.2 table from GPU timelines on Table 3's H100 with a 16-node
     crossbar or a 4 x 4 mesh of the same total bandwidth and mean latency:
     per cluster size, kernel cycles with NoC and with DRAM communication,
     and the mean NoC residence of a request per topology and placement."""
     from paper_2607_11262_amd import timeline as TL
+    from paper_2607_11262_amd.gen import clusterfusion as CF
     topos = (("crossbar", "strips"), ("mesh", "strips"), ("mesh", "blocks"), ("mesh", "strided"))
     recs = np.stack([CF.noc_h100(t, m) for t, m in topos])
     table = {}
@@ -489,12 +632,13 @@ def noc_case_study(api, torch, CF):
     return table
 
 
-def case_study(api, torch, PL):
+def case_study(api, torch):
     """Sec. 7.1 table from GPU timelines at Table 3's H100 (one SM, FP8
     tensor rate): per tile, each organisation's performance relative to naive
     2-stage and its Tensor Core utilisation (full tile graphs)."""
     from paper_2607_11262_amd import timeline as TL
     from paper_2607_11262_amd.gen import hw as H
+    from paper_2607_11262_amd.gen import pipelining as PL
     rec = H.preset("H100", n_sm=1, tensor_permille=2000)[None, :]
     table = {}
     for tile in PL.TILES:

@@ -21,6 +21,8 @@ def test_more_than_one_gpu_is_refused(monkeypatch, capsys):
 
 
 def test_algorithmic_bytes():
+    """10 B per node and 4 B per edge of graph read, 16 B of per-simulation
+    output, and 8 B per node more with per-node cycles."""
     b = GraphBuilder()
     b.kernel(4, 0)
     b.cta()
@@ -28,34 +30,39 @@ def test_algorithmic_bytes():
     s = b.node(GSTORE, 256, 1)
     b.edge(a, s, DATA)
     g = b.build("two")
-    assert bench.alg_bytes_per_sim(g) == 16 * 2 + 4 * 1 + 16
+    assert bench.alg_bytes_per_sim(g, False) == 10 * 2 + 4 * 1 + 16
+    assert bench.alg_bytes_per_sim(g, True) == 10 * 2 + 4 * 1 + 16 + 8 * 2
 
 
-def _sources_hash():
-    h = hashlib.sha256()
-    for name in bench.KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2607_11262_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()
-
-
-def _record(tmp_path, sha, launches=4):
+def _record(tmp_path, sha, workload="gemm_design_sweep", outputs="digest"):
     p = tmp_path / "summary.md"
-    p.write_text(f"text\n    traffic-record: sha256={sha} launches={launches} fetch_kib=1000 write_kib=3000 "
-                 f"fetch_factor=2.0000 write_factor=1.0000\n")
-    return str(p)
+    p.write_text(f"text\n    traffic-record: workload={workload} outputs={outputs} sha256={sha} node_sims=1000 "
+                 f"fetch_kib=1000 write_kib=3000 fetch_factor=2.0000 write_factor=1.0000\n")
+    return str(tmp_path)
 
 
-def test_traffic_record_read_while_sources_match(tmp_path, monkeypatch):
-    monkeypatch.setattr(bench, "PROFILE", _record(tmp_path, _sources_hash()))
-    assert bench.recorded_traffic(4) == pytest.approx((1000 * 1024 * 2.0 + 3000 * 1024 * 1.0) / 4)
+def test_traffic_record_read_while_sources_match(tmp_path):
+    d = _record(tmp_path, bench.sources_hash())
+    assert bench.recorded_traffic("gemm_design_sweep", "digest", d) == pytest.approx(
+        (1000 * 1024 * 2.0 + 3000 * 1024 * 1.0) / 1000)
 
 
-def test_traffic_record_ignored_for_other_sources_or_launches(tmp_path, monkeypatch):
-    monkeypatch.setattr(bench, "PROFILE", _record(tmp_path, "0" * 64))
-    assert bench.recorded_traffic(4) is None
-    monkeypatch.setattr(bench, "PROFILE", _record(tmp_path, _sources_hash()))
-    assert bench.recorded_traffic(5) is None
-    monkeypatch.setattr(bench, "PROFILE", str(tmp_path / "missing.md"))
-    assert bench.recorded_traffic(4) is None
+def test_traffic_record_ignored_for_other_sources_workloads_or_outputs(tmp_path):
+    d = _record(tmp_path, "0" * 64)
+    assert bench.recorded_traffic("gemm_design_sweep", "digest", d) is None
+    d = _record(tmp_path, bench.sources_hash())
+    assert bench.recorded_traffic("splitkv_decode_b64", "digest", d) is None
+    assert bench.recorded_traffic("gemm_design_sweep", "nodes", d) is None
+    assert bench.recorded_traffic("gemm_design_sweep", "digest", str(tmp_path / "missing")) is None
 
+
+def test_workload_parts_cover_the_named_configs():
+    """Every named workload and case study has its graphs and records; the
+    sweep is 64 graphs x 4096 records, the others one graph each with the
+    batch size of their configuration."""
+    sizes = {"gemm_design_sweep": (64, 4096), "gemm_1024_a100": (1, 16)}
+    for name, (n_graphs, B) in sizes.items():
+        describe, make, n = bench.workload_parts(name)
+        assert n == n_graphs
+        g, hw = make(0)
+        assert hw.shape == (B, 32) and g.n_nodes > 0

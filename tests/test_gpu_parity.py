@@ -224,12 +224,14 @@ def test_gemm_design_sweep_bench_launch(torch_cuda):
 
 
 def test_flash_attention_full(torch_cuda):
-    """FlashAttention forward, 2.6M nodes, all 256 records in one launch."""
+    """FlashAttention forward, 2.6M nodes, all 256 records in one launch:
+    every record against the oracle (makespan, status, digest), per-node
+    cycles on three."""
     g = W.workload_graph("flash_attention_b8_h32_s4096")
     hws = W.workload_hw("flash_attention_b8_h32_s4096")
     note(f"flash attention N={g.n_nodes} B={hws.shape[0]}")
     gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
-    compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 16))
+    compare(g, hws, api.OUT_DIGEST, gpu, threads=16)
     sub = hws[[3, 128, 255]]
     compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
 
@@ -245,12 +247,12 @@ def test_splitkv_decode_digest_all(torch_cuda):
 
 def test_decoder_layer_full(torch_cuda):
     """Decoder layer, 20.5M nodes over nine kernels, all 64 records in one
-    launch; per-node cycles on two records."""
+    launch, every record against the oracle; per-node cycles on two."""
     g = W.workload_graph("decoder_layer_prefill_2048")
     hws = W.workload_hw("decoder_layer_prefill_2048")
     note(f"decoder layer N={g.n_nodes} B={hws.shape[0]}")
     gpu = run_gpu(torch_cuda, g, hws, api.OUT_DIGEST)
-    compare(g, hws, api.OUT_DIGEST, gpu, sims=range(0, hws.shape[0], 8))
+    compare(g, hws, api.OUT_DIGEST, gpu, threads=16)
     sub = hws[[5, 63]]
     compare(g, sub, ALL, run_gpu(torch_cuda, g, sub, ALL))
 
