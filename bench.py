@@ -39,7 +39,6 @@ from __future__ import annotations
 
 import argparse
 import hashlib
-import itertools
 import json
 import os
 import re
@@ -244,13 +243,17 @@ class Plan:
 
 
 def cpu_leg(plan, flags, seconds, out_nodes):
-    """The oracle on this host: a single-thread rate first, then every core
-    on records drawn in rounds that take one record from each launch of the
-    step (spread over the launch), each result compared with the GPU's --
-    digest, makespan and status, and every node's cycles for the first
-    records of each launch when per-node output is on."""
+    """The oracle on this host: a single-thread rate first, then every core.
+    Records are drawn in rounds that take a few records from each launch of
+    the step (spread over the launch by a seeded permutation; about 50K
+    simulated nodes per task, so small graphs are not timed as Python
+    overhead), each result compared with the GPU's -- digest, makespan and
+    status, and every node's cycles for the first records of each launch
+    when per-node output is on.  A workload smaller than the budget is
+    sampled again from its start (the rate counts the repeats; the parity
+    count does not)."""
     import oracle
-    from concurrent.futures import ThreadPoolExecutor
+    from concurrent.futures import FIRST_COMPLETED, ThreadPoolExecutor, wait
     threads = len(os.sched_getaffinity(0))
     rng = np.random.default_rng(7)
     orders = [first + rng.permutation(b) for (_, first, b) in plan.launches]
@@ -264,63 +267,69 @@ def cpu_leg(plan, flags, seconds, out_nodes):
     unique = set()
 
     def one(task):
-        i, r, want = task
+        i, recs, want = task
         g, hw = plan.parts[i][3], plan.parts[i][4]
         f = flags | (oracle.F_NODES if want else 0)
-        mk, st, dg, cyc = oracle.simulate_records(g, hw[r:r + 1], f, want_nodes=want)
-        return i, r, want, mk[0], st[0], dg[0], (cyc[0] if want else None), g.n_nodes
+        return i, recs, want, oracle.simulate_records(g, hw[recs], f, want_nodes=want), g.n_nodes
 
     def check(res):
         nonlocal checked, bad, node_fail, nodes_checked_sims
-        i, r, want, mk, st, dg, cyc, n = res
+        i, recs, want, (mk, st, dg, cyc), n = res
         gmk, gst, gdg = host_out[i]
-        checked += 1
-        unique.add((i, r))
-        wrong = st != gst[r] or mk != gmk[r] or (gdg is not None and dg != gdg[r])
-        bad += int(wrong)
-        if want and st == 0:
-            gc = plan.parts[i][2][0][r].cpu().numpy().view(np.uint32)
-            node_fail += int(not np.array_equal(gc, cyc))
-            nodes_checked_sims += 1
-        return n if st == 0 else 0
+        nodes = 0
+        for k, r in enumerate(recs):
+            checked += 1
+            unique.add((i, r))
+            wrong = st[k] != gst[r] or mk[k] != gmk[r] or (gdg is not None and dg[k] != gdg[r])
+            bad += int(wrong)
+            if want and st[k] == 0:
+                gc = plan.parts[i][2][0][r].cpu().numpy().view(np.uint32)
+                node_fail += int(not np.array_equal(gc, cyc[k]))
+                nodes_checked_sims += 1
+            nodes += n if st[k] == 0 else 0
+        return nodes, len(recs)
 
-    def rounds():
-        for k in range(max(len(o) for o in orders)):
-            yield [(plan.launches[j][0], int(o[k]), bool(out_nodes and k < 2)) for j, o in enumerate(orders)
-                   if k < len(o)]
+    def tasks():
+        pos = [0] * len(orders)
+        while True:
+            for j, o in enumerate(orders):
+                i = plan.launches[j][0]
+                take = max(1, 50_000 // max(1, plan.parts[i][3].n_nodes))
+                if pos[j] >= len(o):
+                    continue
+                recs = [int(r) for r in o[pos[j]:pos[j] + take]]
+                want = bool(out_nodes and pos[j] < 2)
+                if want:
+                    recs = recs[:2 - pos[j]]
+                pos[j] += len(recs)
+                yield i, recs, want
+            if all(p >= len(o) for p, o in zip(pos, orders)):
+                pos = [0] * len(orders)  # again from the start
 
-    # single thread: the first tasks in order, about a sixth of the budget;
-    # a workload with fewer simulations than the budget covers is sampled
-    # again from its start (each pass rechecks the same records)
-    it = itertools.cycle(t for rnd in rounds() for t in rnd)
+    it = tasks()
+    # single thread, about a sixth of the budget
     t1 = time.perf_counter()
-    nodes1 = 0
-    done1 = 0
+    nodes1 = done1 = 0
     for task in it:
-        nodes1 += check(one(task))
-        done1 += 1
+        n, c = check(one(task))
+        nodes1 += n
+        done1 += c
         if time.perf_counter() - t1 > seconds / 6:
             break
     sec1 = time.perf_counter() - t1
-    # all cores: whole rounds of the remaining tasks
+    # all cores: a sliding window of tasks in flight
     t2 = time.perf_counter()
-    nodes_all = 0
-    done_all = 0
+    nodes_all = done_all = 0
     with ThreadPoolExecutor(max_workers=threads) as ex:
-        pending = []
-        for task in it:
-            pending.append(task)
-            if len(pending) >= threads * 4:
-                for res in ex.map(one, pending):
-                    nodes_all += check(res)
-                done_all += len(pending)
-                pending = []
-                if time.perf_counter() - t2 > seconds:
-                    break
-        if pending and time.perf_counter() - t2 <= seconds:
-            for res in ex.map(one, pending):
-                nodes_all += check(res)
-            done_all += len(pending)
+        live = {ex.submit(one, next(it)) for _ in range(2 * threads)}
+        while live:
+            done, live = wait(live, return_when=FIRST_COMPLETED)
+            for fu in done:
+                n, c = check(fu.result())
+                nodes_all += n
+                done_all += c
+                if time.perf_counter() - t2 < seconds:
+                    live.add(ex.submit(one, next(it)))
     sec_all = time.perf_counter() - t2
     launches_touched = len({j for j, (i, first, b) in enumerate(plan.launches)
                             if any(i == ui and first <= ur < first + b for ui, ur in unique)}) \
@@ -330,7 +339,7 @@ def cpu_leg(plan, flags, seconds, out_nodes):
            "single_core": nodes1 / sec1 if sec1 > 0 else None,
            "cores_available": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": cpu_model(),
            "sample": f"{done1} simulations on 1 thread ({sec1:.1f} s), then {done_all} on {threads} threads "
-                     f"({sec_all:.1f} s), records drawn in rounds of one per launch of the step"}
+                     f"({sec_all:.1f} s), records drawn in rounds over every launch of the step"}
     parity = {"checked_sims": len(unique), "checks": checked, "mismatches": bad, "launches": len(plan.launches),
               "launches_sampled": launches_touched, "node_cycle_sims": nodes_checked_sims,
               "node_cycle_mismatches": node_fail}

@@ -66,3 +66,39 @@ def test_workload_parts_cover_the_named_configs():
         assert n == n_graphs
         g, hw = make(0)
         assert hw.shape == (B, 32) and g.n_nodes > 0
+
+
+def test_cpu_leg_checks_every_launch_and_counts_mismatches():
+    """The CPU leg with a stand-in plan whose 'GPU' outputs are the oracle's
+    own: it samples every launch and finds no mismatch; a wrong makespan
+    planted in one record and a wrong node cycle in every record are
+    counted."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_11262_amd.gen import hw as H
+    from paper_2607_11262_amd.gen import workloads as W
+
+    class FakePlan:
+        pass
+
+    g = W.gemm(256, 256, 256, 64, 64, 32, 2)
+    hw = H.sample_h100_sweep(5, 12)
+    mk, st, dg, cyc = oracle.simulate_records(g, hw, oracle.F_NODES | oracle.F_DIGEST, want_nodes=True)
+    mk = mk.copy()
+    cyc = cyc.copy()
+    outs = (torch.from_numpy(cyc.view(np.int32)), torch.from_numpy(mk.view(np.int32)), torch.from_numpy(st),
+            torch.from_numpy(dg.view(np.int64)))
+    plan = FakePlan()
+    plan.parts = [(None, None, outs, g, hw)]
+    plan.launches = [(0, 0, 6), (0, 6, 6)]
+    cpu, parity = bench.cpu_leg(plan, oracle.F_DIGEST, 1.0, True)
+    assert parity["mismatches"] == 0 and parity["node_cycle_mismatches"] == 0
+    assert parity["launches_sampled"] == 2 and parity["checked_sims"] == 12
+    assert cpu["value"] > 0 and cpu["single_core"] > 0 and cpu["cores"] >= 1
+    # plant a wrong makespan and a wrong node cycle in every record (stand-in GPU outputs)
+    outs[1][3] += 1
+    outs[0][:, 5, 1] += 1
+    cpu, parity = bench.cpu_leg(plan, oracle.F_DIGEST, 1.0, True)
+    assert parity["mismatches"] >= 1 and parity["node_cycle_mismatches"] >= 1
