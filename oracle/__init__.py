@@ -42,7 +42,7 @@ def _open(path):
     lib = ctypes.CDLL(path)
     p = ctypes.c_void_p
     u32 = ctypes.c_uint32
-    lib.gtso_simulate.argtypes = [u32, u32, u32, u32, u32] + [p] * 13 + [p, u32] + [p] * 5
+    lib.gtso_simulate.argtypes = [u32, u32, u32, u32, u32] + [p] * 16 + [p, u32] + [p] * 5
     lib.gtso_simulate.restype = ctypes.c_int
     lib.gts_oracle_simulate.argtypes = [p, p, u32, p, p, p, p, u32]
     lib.gts_oracle_simulate.restype = ctypes.c_int
@@ -93,6 +93,15 @@ def _c(a, dt):
     return np.ascontiguousarray(a, dtype=dt)
 
 
+def _addr_arrays(g):
+    """Tile addresses and per-op tile rows / row strides (transaction-level
+    memory), or None each."""
+    def opt(name, dt):
+        a = getattr(g, name, None)
+        return _c(a, dt) if a is not None else None
+    return [opt("node_addr", np.uint64), opt("op_rows", np.uint32), opt("op_pitch", np.uint32)]
+
+
 class OracleResult:
     __slots__ = ("cycles", "makespan", "status", "digest", "cta")
 
@@ -108,7 +117,7 @@ def simulate(g, hw, flags: int = 0, want_nodes: bool = True, want_cta: bool = Fa
             _c(g.node_op, np.uint16), _c(g.succ_ptr, np.uint32), _c(g.succ, np.uint32),
             _c(g.cta_node_begin, np.uint32), _c(g.kernel_cta_begin, np.uint32), _c(g.kernel_warps, np.uint16),
             _c(g.kernel_smem, np.uint32), _c(g.kernel_cluster, np.uint8),
-            _c(g.node_tile, np.uint32) if g.node_tile is not None else None]
+            _c(g.node_tile, np.uint32) if g.node_tile is not None else None] + _addr_arrays(g)
     N = int(arrs[4].shape[0])
     C = int(arrs[7].shape[0]) - 1
     hw = _c(hw, np.uint32)
@@ -132,7 +141,8 @@ class _GraphHost(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint32) for n in ("n_nodes", "n_edges", "n_ctas", "n_kernels", "n_ops")] + \
                [(n, ctypes.c_void_p) for n in ("op_cls", "op_flags", "op_work", "op_warps", "node_op", "succ_ptr",
                                                "succ", "cta_node_begin", "kernel_cta_begin", "kernel_warps",
-                                               "kernel_smem", "kernel_cluster", "node_tile")]
+                                               "kernel_smem", "kernel_cluster", "node_tile", "node_addr",
+                                               "op_rows", "op_pitch")]
 
 
 def simulate_records(g, hws, flags: int = 0, want_nodes: bool = False):
@@ -144,7 +154,7 @@ def simulate_records(g, hws, flags: int = 0, want_nodes: bool = False):
             _c(g.node_op, np.uint16), _c(g.succ_ptr, np.uint32), _c(g.succ, np.uint32),
             _c(g.cta_node_begin, np.uint32), _c(g.kernel_cta_begin, np.uint32), _c(g.kernel_warps, np.uint16),
             _c(g.kernel_smem, np.uint32), _c(g.kernel_cluster, np.uint8),
-            _c(g.node_tile, np.uint32) if g.node_tile is not None else None]
+            _c(g.node_tile, np.uint32) if g.node_tile is not None else None] + _addr_arrays(g)
     h = _GraphHost(int(arrs[4].shape[0]), int(arrs[6].shape[0]), int(arrs[7].shape[0]) - 1, int(arrs[9].shape[0]),
                    int(arrs[0].shape[0]), *[(a.ctypes.data if a is not None and a.size else None) for a in arrs])
     hws = np.ascontiguousarray(hws, dtype=np.uint32).reshape(-1, 32)

@@ -109,6 +109,37 @@
  *      (all lines) otherwise; either way the tile becomes most recent.  A
  *      hit is served by the L2 server, a miss by the DRAM server (R7).
  *      Nodes without a tile id, or C = 0, keep the op's MISS flag.
+ *  R17 Transaction-level memory (Sec. 5.2 Memory; Sec. 5.3 memory nodes: a
+ *      tile access is expanded into transactions from the tile's shape,
+ *      coordinates and layout at the transaction granularity, the TMA front
+ *      end streams 128-B transactions at its issue rate, each transaction is
+ *      serviced on its own, and the node completes with its last one).  A
+ *      GLOAD / GSTORE node with a byte address a (node_addr; the tensor's
+ *      base, layout and the tile's coordinates folded into it) accesses its
+ *      op's tile of R = op_rows rows of W = work / R bytes, row r starting at
+ *      a + r * P (P = op_pitch, the row stride).  Its transactions are the
+ *      distinct 128-B lines floor(x / 128) of those bytes, in the order the
+ *      rows first reach them (row by row, lines in increasing address); n of
+ *      them.  At issue (engine start s, R6.3) the engine is held for
+ *      occ_e = max(1, cdiv(n*128*65536, rate_gmem)); transaction j enters at
+ *      e_j = s + cdiv(j*128*65536, rate_gmem) and has left the engine at
+ *      e'_j = s + cdiv((j+1)*128*65536, rate_gmem).  It arrives at the L2
+ *      at e_j (MEM_ARRIVE in (cycle, node id, j) order): with an L2 capacity
+ *      (l2_lines = C > 0) its line hits iff it is among the C most recently
+ *      accessed lines (then becomes the most recent), else the op's MISS
+ *      flag decides; a hit is served by the L2 server, a miss by DRAM, each
+ *      transaction for occ_t = max(1, cdiv(128*65536, rate_srv)):
+ *      m_j = max(e_j, avail), avail = m_j + occ_t (NO_CONTENTION: m_j = e_j),
+ *      finish_j = max(e'_j, m_j + occ_t) + lat_srv.  The node finishes at the
+ *      largest finish_j, decided when its last transaction arrives; then its
+ *      DATA / SYNC edges release (R8).  A one-transaction tile therefore
+ *      times exactly as R6.4 does for the same node without an address.
+ *      Readings: one transaction per distinct line of the tile (a line two
+ *      rows share is fetched once); a transaction arrives at the L2 when the
+ *      engine starts injecting it and completes no earlier than its last
+ *      byte leaves the engine (cut-through, as R6.4); conventional loads and
+ *      stores use the same engine at its rate (the A100 record's engine is
+ *      the LSU at the SRAM bandwidth), stores allocate in the LRU as loads do.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -126,6 +157,7 @@ enum {
   HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT = 24, HW_NOC_MAP = 25, HW_L2_LINES = 26
 };
 #define NO_TILE 0xFFFFFFFFu
+#define NO_ADDR 0xFFFFFFFFFFFFFFFFull
 enum { F_NODES = 1, F_DIGEST = 2, F_NOCONT = 4, F_ORDER_FIN = 8 };
 enum { ST_OK = 0, ST_INFEASIBLE = 1, ST_OVERFLOW = 2, ST_DEADLOCK = 3 };
 
@@ -143,29 +175,36 @@ static uint64_t mix64(uint64_t z) {
 static uint64_t cdiv(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 static uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
-/* ---- binary min-heap of 64-bit keys (cycle << 32 | phase << 30 | id) ----- */
-typedef struct { uint64_t *a; size_t n; } heap_t;
+/* ---- binary min-heap of events: key (cycle << 32 | phase << 30 | id), then
+ * j (the transaction index of an R17 memory arrival, else 0) ------------- */
+typedef struct { uint64_t key; uint32_t j; } ev_t;
+typedef struct { ev_t *a; size_t n; } heap_t;
 
-static void heap_push(heap_t *h, uint64_t key) {
+static int ev_less(ev_t x, ev_t y) { return x.key < y.key || (x.key == y.key && x.j < y.j); }
+
+static void heap_push_j(heap_t *h, uint64_t key, uint32_t j) {
+  ev_t e = {key, j};
   size_t i = h->n++;
   while (i > 0) {
     size_t p = (i - 1) / 2;
-    if (h->a[p] <= key) break;
+    if (!ev_less(e, h->a[p])) break;
     h->a[i] = h->a[p];
     i = p;
   }
-  h->a[i] = key;
+  h->a[i] = e;
 }
 
-static uint64_t heap_pop(heap_t *h) {
-  uint64_t top = h->a[0];
-  uint64_t last = h->a[--h->n];
+static void heap_push(heap_t *h, uint64_t key) { heap_push_j(h, key, 0); }
+
+static ev_t heap_pop(heap_t *h) {
+  ev_t top = h->a[0];
+  ev_t last = h->a[--h->n];
   size_t i = 0;
   for (;;) {
     size_t l = 2 * i + 1, r = l + 1, m = i;
-    uint64_t mv = last;
-    if (l < h->n && h->a[l] < mv) { m = l; mv = h->a[l]; }
-    if (r < h->n && h->a[r] < mv) { m = r; mv = h->a[r]; }
+    ev_t mv = last;
+    if (l < h->n && ev_less(h->a[l], mv)) { m = l; mv = h->a[l]; }
+    if (r < h->n && ev_less(h->a[r], mv)) { m = r; mv = h->a[r]; }
     if (m == i) break;
     h->a[i] = h->a[m];
     i = m;
@@ -208,11 +247,17 @@ typedef struct {
   uint64_t *noc_av;        /* per domain node: 4 link/port servers */
   /* R16: tiles in recency order (most recent first) and their lines */
   uint32_t *lru_tile, *lru_lines; uint32_t lru_n;
+  /* R17: tile addresses, shapes; per issued node its lines, transactions
+   * left and largest transaction finish; lines in recency order */
+  const uint64_t *node_addr;   /* or NULL */
+  const uint32_t *op_rows, *op_pitch;  /* or NULL */
+  uint64_t **txn_lines; uint32_t *txn_n, *txn_left; uint64_t *txn_maxf;
+  uint64_t *lru_line; uint64_t lru_line_n;
   /* control */
   heap_t heap;
   uint32_t next_cta; uint64_t retired;
   int64_t *kstart;
-  int overflow;
+  int overflow, oom;
   uint64_t nfinished;
 } sim_t;
 
@@ -336,6 +381,32 @@ static void dispatch(sim_t *S, uint64_t t) {
   }
 }
 
+/* R17: the distinct 128-B lines of node v's tile, in the order the rows
+ * first reach them; stored for the node, returns their number (0 when host
+ * memory runs out) */
+static uint32_t tile_lines(sim_t *S, uint32_t v) {
+  uint32_t p = S->node_op[v];
+  uint64_t R = S->op_rows ? S->op_rows[p] : 1;
+  uint64_t W = S->op_work[p] / R;
+  uint64_t P = S->op_pitch ? S->op_pitch[p] : W;
+  uint64_t cap = R * (W / 128 + 2);
+  uint64_t *lines = malloc(cap * sizeof *lines);
+  if (!lines) return 0;
+  uint32_t n = 0;
+  for (uint64_t r = 0; r < R; r++) {
+    uint64_t first = (S->node_addr[v] + r * P) / 128, last = (S->node_addr[v] + r * P + W - 1) / 128;
+    for (uint64_t L = first; L <= last; L++) {
+      uint32_t i = 0;
+      while (i < n && lines[i] != L) i++;
+      if (i == n) lines[n++] = L;
+    }
+  }
+  free(S->txn_lines[v]);
+  S->txn_lines[v] = lines;
+  S->txn_n[v] = n;
+  return n;
+}
+
 static void issue(sim_t *S, uint32_t v, uint64_t t) {
   uint32_t p = S->node_op[v];
   uint32_t c = S->node_cta[v];
@@ -387,6 +458,20 @@ static void issue(sim_t *S, uint32_t v, uint64_t t) {
     if (!complete(S, v, s, s + S->occ[p] + S->lat[p] * lat_mult)) return;
     release_out(S, v, 0, s + 1);
     release_out(S, v, 1, S->fin[v]);
+  } else if (S->node_addr && S->node_addr[v] != NO_ADDR) { /* R17: transactions */
+    uint32_t n = tile_lines(S, v);
+    if (n == 0) { S->oom = S->overflow = 1; return; }   /* out of host memory: stop */
+    uint64_t rate = S->hw[HW_RATE + 4];
+    uint64_t occ_e = max64(1, cdiv((uint64_t)n * 128 * 65536, rate));
+    uint64_t s = nocont ? t : max64(t, S->eng_av[sm]);
+    if (s + occ_e > MAXCYC) { S->overflow = 1; return; }
+    S->eng_av[sm] = s + occ_e;
+    S->st[v] = (uint32_t)s;
+    S->txn_left[v] = n;
+    S->txn_maxf[v] = 0;
+    release_out(S, v, 0, s + 1);
+    for (uint32_t j = 0; j < n; j++)
+      heap_push_j(&S->heap, mkkey(s + cdiv((uint64_t)j * 128 * 65536, rate), EV_MEM, v), j);
   } else { /* GLOAD / GSTORE: engine now, global server at MEM_ARRIVE */
     uint64_t s = nocont ? t : max64(t, S->eng_av[sm]);
     if (s + S->occ[p] > MAXCYC) { S->overflow = 1; return; }
@@ -427,6 +512,36 @@ static void mem_arrive(sim_t *S, uint32_t v, uint64_t t) {
   release_out(S, v, 1, f);
 }
 
+/* R17: line access to the LRU of lines; returns 1 on a hit */
+static int lru_line_access(sim_t *S, uint64_t line) {
+  uint64_t i = 0;
+  while (i < S->lru_line_n && S->lru_line[i] != line) i++;
+  int hit = i < S->lru_line_n && i < S->hw[HW_L2_LINES];
+  if (i == S->lru_line_n) S->lru_line_n++;
+  memmove(S->lru_line + 1, S->lru_line, (size_t)i * sizeof *S->lru_line);
+  S->lru_line[0] = line;
+  return hit;
+}
+
+/* R17: transaction j of node v arrives at the L2 at cycle t */
+static void mem_txn(sim_t *S, uint32_t v, uint32_t j, uint64_t t) {
+  uint32_t p = S->node_op[v];
+  int dram = S->to_dram[p];
+  if (S->hw[HW_L2_LINES]) dram = !lru_line_access(S, S->txn_lines[v][j]);
+  uint64_t rate_srv = S->hw[HW_RATE + (dram ? 6 : 5)];
+  uint64_t occ_t = max64(1, cdiv(128ull * 65536, rate_srv));
+  uint64_t lat = S->hw[HW_LAT + (dram ? 5 : 4)];
+  uint64_t *av = dram ? &S->dram_av : &S->l2_av;
+  uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);
+  *av = m + occ_t;
+  uint64_t left_engine = (uint64_t)S->st[v] + cdiv((uint64_t)(j + 1) * 128 * 65536, S->hw[HW_RATE + 4]);
+  uint64_t f = max64(left_engine, m + occ_t) + lat;
+  if (f > S->txn_maxf[v]) S->txn_maxf[v] = f;
+  if (--S->txn_left[v]) return;
+  if (!complete(S, v, S->st[v], S->txn_maxf[v])) return;
+  release_out(S, v, 1, S->fin[v]);
+}
+
 #define ALLOC(ptr, n) do { size_t cnt_ = (size_t)(n); (ptr) = calloc(cnt_ ? cnt_ : 1, sizeof(*(ptr))); if (!(ptr)) goto oom; } while (0)
 
 int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t n_kernels,
@@ -435,6 +550,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
                   const uint32_t *succ_ptr, const uint32_t *succ, const uint32_t *cta_node_begin,
                   const uint32_t *kernel_cta_begin, const uint16_t *kernel_warps,
                   const uint32_t *kernel_smem, const uint8_t *kernel_cluster, const uint32_t *node_tile,
+                  const uint64_t *node_addr, const uint32_t *op_rows, const uint32_t *op_pitch,
                   const uint32_t *hw, uint32_t flags,
                   uint32_t *out_cycles, uint32_t *out_makespan, int32_t *out_status,
                   uint64_t *out_digest, uint32_t *out_cta) {
@@ -448,6 +564,7 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   S.cta_node_begin = cta_node_begin; S.kernel_cta_begin = kernel_cta_begin;
   S.kernel_warps = kernel_warps; S.kernel_smem = kernel_smem; S.kernel_cluster = kernel_cluster;
   S.node_tile = node_tile;
+  S.node_addr = node_addr; S.op_rows = op_rows; S.op_pitch = op_pitch;
   S.hw = hw; S.nsm = hw[HW_NSM]; S.nsub = hw[HW_NSUB]; S.flags = flags;
   S.noc_d = hw[HW_NOC_NODES]; S.noc_w = hw[HW_NOC_W];
   int rc = 0;
@@ -534,26 +651,43 @@ int gtso_simulate(uint32_t n_nodes, uint32_t n_edges, uint32_t n_ctas, uint32_t 
   ALLOC(S.lru_tile, S.N); ALLOC(S.lru_lines, S.N);
   ALLOC(S.kstart, S.K);
   for (uint32_t k = 0; k < S.K; k++) S.kstart[k] = -1;
-  ALLOC(S.heap.a, (uint64_t)S.N + S.C);
+  uint64_t txn_bound = 0;  /* R17: transactions a node's tile can have */
+  if (node_addr)
+    for (uint32_t v = 0; v < S.N; v++)
+      if (node_addr[v] != NO_ADDR) {
+        uint32_t p = node_op[v];
+        uint64_t R = op_rows ? op_rows[p] : 1;
+        txn_bound += R * (op_work[p] / R / 128 + 2);
+      }
+  ALLOC(S.heap.a, (uint64_t)S.N + S.C + txn_bound);
+  ALLOC(S.txn_lines, S.N); ALLOC(S.txn_n, S.N); ALLOC(S.txn_left, S.N); ALLOC(S.txn_maxf, S.N);
+  ALLOC(S.lru_line, txn_bound);
 
   /* R6 event loop */
   dispatch(&S, 0);
   while (S.heap.n && !S.overflow) {
-    uint64_t t = S.heap.a[0] >> 32;
+    uint64_t t = S.heap.a[0].key >> 32;
     int any_retire = 0;
-    while (S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_RETIRE) {
-      uint32_t c = (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu);
+    while (S.heap.n && (S.heap.a[0].key >> 32) == t && ((S.heap.a[0].key >> 30) & 3) == EV_RETIRE) {
+      uint32_t c = (uint32_t)(heap_pop(&S.heap).key & 0x3FFFFFFFu);
       S.resident[S.cta_sm[c]]--;
       S.retired++;
       any_retire = 1;
     }
     if (any_retire) dispatch(&S, t);
-    while (!S.overflow && S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_READY)
-      issue(&S, (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu), t);
-    while (!S.overflow && S.heap.n && (S.heap.a[0] >> 32) == t && ((S.heap.a[0] >> 30) & 3) == EV_MEM)
-      mem_arrive(&S, (uint32_t)(heap_pop(&S.heap) & 0x3FFFFFFFu), t);
+    while (!S.overflow && S.heap.n && (S.heap.a[0].key >> 32) == t && ((S.heap.a[0].key >> 30) & 3) == EV_READY)
+      issue(&S, (uint32_t)(heap_pop(&S.heap).key & 0x3FFFFFFFu), t);
+    while (!S.overflow && S.heap.n && (S.heap.a[0].key >> 32) == t && ((S.heap.a[0].key >> 30) & 3) == EV_MEM) {
+      ev_t e = heap_pop(&S.heap);
+      uint32_t v = (uint32_t)(e.key & 0x3FFFFFFFu);
+      if (S.node_addr && S.node_addr[v] != NO_ADDR)
+        mem_txn(&S, v, e.j, t);
+      else
+        mem_arrive(&S, v, t);
+    }
   }
 
+  if (S.oom) goto oom;
   if (S.overflow) {
     *out_status = ST_OVERFLOW; *out_makespan = 0xFFFFFFFFu;
     if (out_digest) *out_digest = 0;
@@ -586,6 +720,9 @@ done:
   free(S.resident); free(S.lane_av); free(S.smem_av); free(S.eng_av); free(S.kstart); free(S.heap.a);
   free(S.noc_av); free(S.lru_tile); free(S.lru_lines);
   free(S.occ_l2); free(S.occ_d); free(S.lat_l2); free(S.lat_d);
+  if (S.txn_lines)
+    for (uint32_t v = 0; v < S.N; v++) free(S.txn_lines[v]);
+  free(S.txn_lines); free(S.txn_n); free(S.txn_left); free(S.txn_maxf); free(S.lru_line);
   return rc;
 }
 
@@ -606,6 +743,8 @@ typedef struct gtso_graph_host {
   const uint32_t *kernel_smem;
   const uint8_t *kernel_cluster; /* NULL: one CTA per cluster everywhere */
   const uint32_t *node_tile;     /* NULL: no node names a tile */
+  const uint64_t *node_addr;     /* NULL: no node has a tile address */
+  const uint32_t *op_rows, *op_pitch;  /* NULL: one row; pitch = row bytes */
 } gtso_graph_host;
 
 int gts_oracle_simulate(const gtso_graph_host *h, const uint32_t *hw, uint32_t B, uint32_t *out_cycles,
@@ -624,7 +763,7 @@ int gts_oracle_simulate(const gtso_graph_host *h, const uint32_t *hw, uint32_t B
     rc = gtso_simulate(h->n_nodes, h->n_edges, h->n_ctas, h->n_kernels, h->n_ops, h->op_cls, h->op_flags,
                        h->op_work, h->op_warps, h->node_op, h->succ_ptr, h->succ, h->cta_node_begin,
                        h->kernel_cta_begin, h->kernel_warps, h->kernel_smem, cluster, h->node_tile,
-                       hw + 32 * (uint64_t)b, flags,
+                       h->node_addr, h->op_rows, h->op_pitch, hw + 32 * (uint64_t)b, flags,
                        out_cycles ? out_cycles + 2 * (uint64_t)h->n_nodes * b : NULL, out_makespan + b,
                        out_status + b, out_digest ? out_digest + b : NULL, NULL);
   free(ones);

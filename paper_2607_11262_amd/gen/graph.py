@@ -31,7 +31,9 @@ MISS = 1
 RANK_SHIFT = 4      # REMOTE ops: target rank = flags >> RANK_SHIFT
 MAX_CLUSTER = 16
 NO_TILE = 0xFFFFFFFF
+NO_ADDR = 0xFFFFFFFFFFFFFFFF
 LINE_BYTES = 128
+MAX_NODE_TXN = 1 << 21  # transactions one addressed node may have (bound: rows * (row bytes / 128 + 2))
 
 
 def remote_flags(rank: int) -> int:
@@ -63,6 +65,12 @@ class TileGraph:
     meta: dict = field(default_factory=dict)
     kernel_cluster: np.ndarray = None  # u8 [K] CTAs per cluster (None: all 1)
     node_tile: np.ndarray = None       # u32 [N] tile of a load / store, NO_TILE otherwise (None: no tiles)
+    # transaction-level memory: byte address of a load / store's tile (NO_ADDR
+    # otherwise; None: no addresses), and per op the tile's rows and row
+    # stride in bytes (None: one row, stride = row bytes)
+    node_addr: np.ndarray = None       # u64 [N]
+    op_rows: np.ndarray = None         # u32 [P]
+    op_pitch: np.ndarray = None        # u32 [P]
 
     def __post_init__(self):
         if self.kernel_cluster is None:
@@ -70,6 +78,12 @@ class TileGraph:
         self.kernel_cluster = np.asarray(self.kernel_cluster, dtype=np.uint8)
         if self.node_tile is not None:
             self.node_tile = np.asarray(self.node_tile, dtype=np.uint32)
+        if self.node_addr is not None:
+            self.node_addr = np.asarray(self.node_addr, dtype=np.uint64)
+        if self.op_rows is not None:
+            self.op_rows = np.asarray(self.op_rows, dtype=np.uint32)
+        if self.op_pitch is not None:
+            self.op_pitch = np.asarray(self.op_pitch, dtype=np.uint32)
 
     @property
     def n_nodes(self) -> int:
@@ -136,10 +150,10 @@ class OpTable:
         self.index: dict = {}
         self.rows: list = []
 
-    def get(self, cls: int, work: int, warps: int, flags: int = 0) -> int:
-        if cls not in COMPUTE_CLASSES and cls != SMEM:
-            pass  # the warp mask of memory / sync ops is descriptive only
-        key = (int(cls), int(flags), int(work), int(warps))
+    def get(self, cls: int, work: int, warps: int, flags: int = 0, rows: int = 1, pitch: int = 0) -> int:
+        """Op id of the tuple; rows / pitch: the tile shape of an addressed
+        load / store (pitch 0: rows packed, stride = row bytes)."""
+        key = (int(cls), int(flags), int(work), int(warps), int(rows), int(pitch))
         if key not in self.index:
             self.index[key] = len(self.rows)
             self.rows.append(key)
@@ -152,6 +166,15 @@ class OpTable:
         work = np.array([r[2] for r in rows], dtype=np.uint32)
         warps = np.array([r[3] for r in rows], dtype=np.uint32)
         return cls, flags, work, warps
+
+    def shapes(self):
+        """(op_rows, op_pitch) arrays, or (None, None) when every op has the
+        default shape (one row)."""
+        if all(r[4] == 1 and r[5] == 0 for r in self.rows):
+            return None, None
+        nrows = np.array([r[4] for r in self.rows], dtype=np.uint32)
+        pitch = np.array([r[5] if r[5] else r[2] // max(r[4], 1) for r in self.rows], dtype=np.uint32)
+        return nrows, pitch
 
 
 def csr_from_edges(n_nodes: int, src: np.ndarray, dst: np.ndarray, kind: np.ndarray):
@@ -186,6 +209,7 @@ class GraphBuilder:
         self.drop = frozenset(int(k) for k in drop)
         self.ops = OpTable()
         self.node_op: list = []
+        self.node_addr: list = []
         self.cta_begin: list = [0]
         self.kernel_begin: list = [0]
         self.kernel_warps: list = []
@@ -215,9 +239,13 @@ class GraphBuilder:
             self.cta_begin.append(len(self.node_op))
             self._open_cta = False
 
-    def node(self, cls: int, work: int = 0, warps: int = 1, flags: int = 0) -> int:
+    def node(self, cls: int, work: int = 0, warps: int = 1, flags: int = 0, addr: int | None = None,
+             rows: int = 1, pitch: int = 0) -> int:
+        """A node; addr (loads / stores): the byte address of its tile of
+        `rows` rows of work / rows bytes, `pitch` bytes apart (0: packed)."""
         assert self._open_cta, "open a CTA first"
-        self.node_op.append(self.ops.get(cls, work, warps, flags))
+        self.node_op.append(self.ops.get(cls, work, warps, flags, rows, pitch))
+        self.node_addr.append(NO_ADDR if addr is None else int(addr))
         return len(self.node_op) - 1
 
     def edge(self, u: int, v: int, kind: int = DATA):
@@ -241,7 +269,10 @@ class GraphBuilder:
                          kernel_cta_begin=np.array(kb, dtype=np.uint32),
                          kernel_warps=np.array(self.kernel_warps, dtype=np.uint16),
                          kernel_smem=np.array(self.kernel_smem, dtype=np.uint32), name=name,
-                         kernel_cluster=np.array(self.kernel_cluster, dtype=np.uint8))
+                         kernel_cluster=np.array(self.kernel_cluster, dtype=np.uint8),
+                         node_addr=(np.array(self.node_addr, dtype=np.uint64)
+                                    if any(a != NO_ADDR for a in self.node_addr) else None),
+                         op_rows=self.ops.shapes()[0], op_pitch=self.ops.shapes()[1])
 
 
 def empty_graph() -> TileGraph:
@@ -300,6 +331,42 @@ def validate(g: TileGraph) -> None:
             for a, b in zip(t.tolist(), l.tolist()):
                 if first.setdefault(a, b) != b:
                     raise ValidationError("a tile is accessed with different sizes")
+    P = int(g.op_cls.shape[0])
+    if g.op_rows is not None and (g.op_rows.shape[0] != P or np.any(g.op_rows == 0)):
+        raise ValidationError("op rows must be given for every op and be at least 1")
+    if g.op_pitch is not None and g.op_pitch.shape[0] != P:
+        raise ValidationError("op pitch must be given for every op")
+    if g.node_addr is not None:
+        addr = g.node_addr.astype(np.uint64)
+        ops_n = g.node_op.astype(np.int64)
+        mem_node = np.isin(g.op_cls, (GLOAD, GSTORE))[ops_n]
+        has = addr != np.uint64(NO_ADDR)
+        if addr.shape[0] != N or np.any(~mem_node & has):
+            raise ValidationError("only loads and stores carry tile addresses")
+        if has.any() and g.node_tile is not None and np.any(g.node_tile != NO_TILE):
+            raise ValidationError("a graph names its tiles by id or by address, not both")
+        rows = (g.op_rows.astype(np.int64) if g.op_rows is not None else np.ones(P, np.int64))
+        work = g.op_work.astype(np.int64)
+        used = np.zeros(P, dtype=bool)
+        used[ops_n[has]] = True
+        for p in np.flatnonzero(used).tolist():
+            R = int(rows[p])
+            if work[p] == 0 or work[p] % R:
+                raise ValidationError("an addressed tile's bytes must be a positive multiple of its rows")
+            W = int(work[p]) // R
+            pitch = int(g.op_pitch[p]) if g.op_pitch is not None else W
+            if pitch < W:
+                raise ValidationError("an addressed tile's row stride is below its row bytes")
+            if R * (W // LINE_BYTES + 2) > MAX_NODE_TXN:
+                raise ValidationError("an addressed tile has too many transactions")
+        if has.any():
+            pv = ops_n[has]
+            R = rows[pv]
+            W = work[pv] // R
+            pitch = (g.op_pitch.astype(np.int64)[pv] if g.op_pitch is not None else W)
+            span = (R - 1) * pitch + W  # bytes from the tile's first to its last byte + 1
+            if np.any(addr[has] > np.uint64(NO_ADDR - 1) - span.astype(np.uint64)):
+                raise ValidationError("an addressed tile wraps the address space")
     nrem = remote[g.node_op.astype(np.int64)]
     rank = (g.op_flags.astype(np.int64) >> RANK_SHIFT)[g.node_op.astype(np.int64)]
     if np.any(nrem & (rank >= cl[node_kernel])):

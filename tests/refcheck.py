@@ -118,6 +118,7 @@ def verify_schedule(g, rec, flags, cycles, cta):
     order = np.lexsort((np.arange(N), ready))  # FIFO (ready, id)
     lane_av, smem_av, eng_av, noc_av = {}, {}, {}, {}
     gstart = {}
+    txn = tile_transactions(g)
     D, W = H.get(rec, "noc_nodes"), H.get(rec, "noc_width")
     for v in order:
         d = dur[ops[v]]
@@ -145,17 +146,49 @@ def verify_schedule(g, rec, flags, cycles, cta):
             assert st[v] == s and fi[v] == s + d["occ"] + d["lat"] * hops, f"remote node {v}: {st[v], fi[v]} != {s}"
         else:
             s = r if nocont else max(r, eng_av.get(sm, 0))
-            eng_av[sm] = s + d["occ"]
+            if v in txn:  # transaction-level tile: the engine streams all its lines
+                eng_av[sm] = s + max(1, cdiv(len(txn[v]) * LINE_BYTES * 65536, H.get(rec, "rate_gmem")))
+            else:
+                eng_av[sm] = s + d["occ"]
             assert st[v] == s, f"gmem node {v} start {st[v]} != {s}"
             gstart[v] = s
-    # global L2 / DRAM servers in FIFO order of (arrival = engine start, id);
-    # with an L2 capacity, tracked tiles replay an explicit LRU of 128-B lines
+    # global L2 / DRAM servers in FIFO order of (arrival, id, transaction):
+    # a node without an address arrives once, at its engine start; an
+    # addressed node's transaction j when the engine starts injecting it.
+    # With an L2 capacity, tracked tiles and addressed lines replay an
+    # explicit LRU of 128-B lines.
     av = {False: 0, True: 0}
     cap = H.get(rec, "l2_lines")
-    lines = OrderedDict()  # (tile, line) -> None, least recent first
-    for v in sorted(gstart, key=lambda x: (gstart[x], x)):
+    lines = OrderedDict()  # (tile, line) or ("addr", line) -> None, least recent first
+    rg = H.get(rec, "rate_gmem")
+    arrivals = []
+    for v, s in gstart.items():
+        if v in txn:
+            arrivals += [(s + cdiv(j * LINE_BYTES * 65536, rg), v, j) for j in range(len(txn[v]))]
+        else:
+            arrivals.append((s, v, 0))
+    tx_fin = {}
+    for a, v, j in sorted(arrivals):
         d = dur[ops[v]]
         s = gstart[v]
+        if v in txn:
+            miss = bool(d["dram"])
+            if cap:
+                key = ("addr", txn[v][j])
+                miss = key not in lines
+                lines[key] = None
+                lines.move_to_end(key)
+                while len(lines) > cap:
+                    lines.popitem(last=False)
+            occ_t = max(1, cdiv(LINE_BYTES * 65536, H.get(rec, "rate_dram" if miss else "rate_l2")))
+            m = a if nocont else max(a, av[miss])
+            av[miss] = m + occ_t
+            left = s + cdiv((j + 1) * LINE_BYTES * 65536, rg)
+            f = max(left, m + occ_t) + H.get(rec, "lat_dram" if miss else "lat_l2")
+            tx_fin[v] = max(tx_fin.get(v, 0), f)
+            if j == len(txn[v]) - 1:
+                assert fi[v] == tx_fin[v], f"addressed node {v} finish {fi[v]} != {tx_fin[v]}"
+            continue
         dram, occ_m, lat = d["dram"], d["occ_m"], d["lat"]
         tile = int(g.node_tile[v]) if g.node_tile is not None else NO_TILE
         if cap and tile != NO_TILE:
@@ -177,6 +210,29 @@ def verify_schedule(g, rec, flags, cycles, cta):
     exp_sm, exp_launch = dispatch_from_retires(g, rec, fi)
     assert np.array_equal(exp_sm, cta_sm), "CTA -> SM mapping"
     assert np.array_equal(exp_launch, launch), "CTA launch cycles"
+
+
+def tile_transactions(g):
+    """Per addressed load / store: the 128-B lines its tile covers, in the
+    order its rows first reach them (a set of lines seen, rows in order)."""
+    out = {}
+    if getattr(g, "node_addr", None) is None:
+        return out
+    for v in np.flatnonzero(g.node_addr != np.uint64(0xFFFFFFFFFFFFFFFF)).tolist():
+        p = int(g.node_op[v])
+        R = int(g.op_rows[p]) if g.op_rows is not None else 1
+        W = int(g.op_work[p]) // R
+        P = int(g.op_pitch[p]) if g.op_pitch is not None else W
+        a = int(g.node_addr[v])
+        seen, order = set(), []
+        for r in range(R):
+            lo, hi = (a + r * P) // LINE_BYTES, (a + r * P + W - 1) // LINE_BYTES
+            for line in range(lo, hi + 1):
+                if line not in seen:
+                    seen.add(line)
+                    order.append(line)
+        out[v] = order
+    return out
 
 
 def cluster_first(g, c: int) -> int:
@@ -343,10 +399,17 @@ def load_golden():
                 b.cta()
                 for cls, work, warps, extra, *tile in cta:
                     # fourth field: the L2-miss flag, or a REMOTE node's target rank;
-                    # optional fifth: the tile a load / store touches
+                    # optional fifth: the tile a load / store touches, as an id or
+                    # as {"addr", "rows", "pitch"} (transaction-level memory)
                     flags = remote_flags(extra) if cls == "REMOTE" else (1 if extra else 0)
-                    b.node(CLASS[cls], work, warps, flags)
-                    tiles.append(tile[0] if tile else NO_TILE)
+                    if tile and isinstance(tile[0], dict):
+                        t = tile[0]
+                        b.node(CLASS[cls], work, warps, flags, addr=t["addr"], rows=t.get("rows", 1),
+                               pitch=t.get("pitch", 0))
+                        tiles.append(NO_TILE)
+                    else:
+                        b.node(CLASS[cls], work, warps, flags)
+                        tiles.append(tile[0] if tile else NO_TILE)
         for u, v, kd in src["edges"]:
             b.edge(u, v, KIND[kd])
         g = b.build(c["name"])

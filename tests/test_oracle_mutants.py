@@ -66,6 +66,22 @@ MUTANTS = [
      "if (!complete(S, v, s, s + S->occ[p])) return;\n    release_out(S, v, 0, s + 1);\n    release_out(S, v, 1, S->fin[v]);\n  } else if (cls == K_SYNC)", False),
     ("sync_node_zero_latency_allowed", "S.lat[p] = max64(1, hw[HW_LAT + 6]);", "S.lat[p] = hw[HW_LAT + 6];", False),
     ("cta_launch_latency_dropped", "uint64_t launch = t + S->hw[HW_CTALAT];", "uint64_t launch = t;", True),
+    # transaction-level memory (R17)
+    ("txn_lines_not_deduplicated", "      while (i < n && lines[i] != L) i++;\n      if (i == n) lines[n++] = L;",
+     "      lines[n++] = L;", False),
+    ("txn_engine_from_tile_bytes", "uint64_t occ_e = max64(1, cdiv((uint64_t)n * 128 * 65536, rate));",
+     "uint64_t occ_e = S->occ[p];", False),
+    ("txn_leaves_engine_at_entry", "cdiv((uint64_t)(j + 1) * 128 * 65536, S->hw[HW_RATE + 4])",
+     "cdiv((uint64_t)j * 128 * 65536, S->hw[HW_RATE + 4])", False),
+    ("txn_all_enter_at_issue", "heap_push_j(&S->heap, mkkey(s + cdiv((uint64_t)j * 128 * 65536, rate), EV_MEM, v), j);",
+     "heap_push_j(&S->heap, mkkey(s, EV_MEM, v), j);", False),
+    ("txn_node_finish_is_last_transaction", "if (f > S->txn_maxf[v]) S->txn_maxf[v] = f;", "S->txn_maxf[v] = f;",
+     False),
+    ("line_lru_one_extra_line", "int hit = i < S->lru_line_n && i < S->hw[HW_L2_LINES];",
+     "int hit = i < S->lru_line_n && i <= S->hw[HW_L2_LINES];", False),
+    ("line_lru_ignored", "if (S->hw[HW_L2_LINES]) dram = !lru_line_access(S, S->txn_lines[v][j]);", ";", False),
+    ("txn_occupancy_of_tile_bytes", "uint64_t occ_t = max64(1, cdiv(128ull * 65536, rate_srv));",
+     "uint64_t occ_t = max64(1, cdiv((uint64_t)S->op_work[p] * 65536, rate_srv));", False),
 ]
 
 
@@ -96,6 +112,19 @@ def _checks(lib):
         g = W.random_graph(rng, n_nodes_max=rng.choice([6, 20, 60]), n_kernels_max=3, ctas_max=4)
         rec = H.sample_random(rng)
         flags = rng.choice([0, 0, 0, 4, 8])
+        r = oracle.simulate(g, rec, flags, want_cta=True, lib_path=lib)
+        if min(refcheck.slots_per_kernel(g, rec)) == 0:
+            assert r.status == 1
+            continue
+        assert r.status == 0
+        refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+    from addressed import with_addresses
+    for seed in range(30):
+        rng = SplitMix64(seed, 17)
+        g = with_addresses(W.random_graph(rng, n_nodes_max=rng.choice([10, 40]), n_kernels_max=2, ctas_max=4), rng)
+        rec = H.sample_random(rng)
+        rec[H.FIELDS["l2_lines"]] = rng.choice([0, 1, 2, 8, 40])
+        flags = rng.choice([0, 0, 4, 8])
         r = oracle.simulate(g, rec, flags, want_cta=True, lib_path=lib)
         if min(refcheck.slots_per_kernel(g, rec)) == 0:
             assert r.status == 1

@@ -326,3 +326,79 @@ def test_batched_call_equals_one_record_calls():
             r = oracle.simulate(g, hws[b], oracle.F_NODES | oracle.F_DIGEST)
             assert (mk[b], st[b], dg[b]) == (r.makespan, r.status, r.digest)
             assert np.array_equal(cyc[b], r.cycles)
+
+
+# ---- transaction-level memory (R17) -------------------------------------
+
+@pytest.mark.parametrize("seed", range(100))
+def test_verifier_transactions(seed):
+    """R17: every addressed load / store expanded into its tile's lines
+    (rows, stride, address), the transactions replayed through the L2 / DRAM
+    FIFO servers in (arrival, node, transaction) order with an explicit LRU
+    of lines, and each node's finish rederived as its last transaction's."""
+    from addressed import with_addresses
+    rng = SplitMix64(seed, 17)
+    g = with_addresses(W.random_graph(rng, n_nodes_max=rng.choice([10, 40, 120]), n_kernels_max=2, ctas_max=4), rng)
+    validate(g)
+    rec = H.sample_random(rng)
+    rec[H.FIELDS["l2_lines"]] = rng.choice([0, 0, 1, 2, 8, 40, 200, 4096])
+    flags = rng.choice([0, 0, 4, 8])
+    r = oracle.simulate(g, rec, flags, want_cta=True)
+    if r.status == 1:
+        return
+    assert r.status == 0
+    refcheck.verify_schedule(g, rec, flags, r.cycles, r.cta)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_one_line_tiles_equal_aggregate_rule(seed):
+    """R17 reduces to R6.4: when every addressed tile is one aligned
+    128-B line (one transaction) and the L2 model is the static flag, a
+    graph with addresses times exactly as the same graph without them."""
+    rng = SplitMix64(seed, 18)
+    g = W.random_graph(rng, n_nodes_max=rng.choice([10, 60, 200]), n_kernels_max=2, ctas_max=5)
+    g.op_work = np.where(np.isin(g.op_cls, (GLOAD, GSTORE)), 128, g.op_work).astype(np.uint32)
+    ops = g.node_op.astype(np.int64)
+    mem = np.isin(g.op_cls, (GLOAD, GSTORE))[ops]
+    if not mem.any():
+        return
+    rec = H.sample_random(rng)
+    flags = rng.choice([0, 4, 8])
+    base = oracle.simulate(g, rec, flags)
+    from paper_2607_11262_amd.gen.graph import NO_ADDR
+    addr = np.full(g.n_nodes, NO_ADDR, dtype=np.uint64)
+    addr[mem] = (np.arange(int(mem.sum()), dtype=np.uint64) * 128 + 4096) * rng.randint(1, 3)
+    g.node_addr = addr
+    r = oracle.simulate(g, rec, flags)
+    assert (r.status, r.makespan) == (base.status, base.makespan)
+    if r.status == 0:
+        assert np.array_equal(r.cycles, base.cycles)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_lone_stream_closed_form(seed):
+    """A lone addressed load of n lines on an idle machine: transaction j
+    enters at e_j = cdiv(j*128*2^16, r_e) and leaves the engine at e_(j+1);
+    the FIFO server of occupancy o then finishes the last one at
+    max_i (e_i + (n - i) o) (the latest arrival plus the work queued behind
+    it, a closed form without the recurrence), so the node finishes at
+    max(e_n, max_i (e_i + (n - i) o)) + latency."""
+    rng = SplitMix64(seed, 19)
+    n = rng.randint(1, 40)
+    rows = rng.choice([1, n]) if n > 1 else 1
+    W_ = 128 * n // rows
+    b = GraphBuilder()
+    b.kernel(1, 0)
+    b.cta()
+    miss = rng.randint(0, 1)
+    b.node(GLOAD, 128 * n, 1, miss, addr=128 * rng.randint(0, 1000), rows=rows, pitch=W_)
+    g = b.build("lone")
+    rec = H.toy(rate_gmem=rng.randint(H.Q16 // 4, 400 * H.Q16), rate_l2=rng.randint(H.Q16 // 2, 300 * H.Q16),
+                rate_dram=rng.randint(H.Q16 // 2, 300 * H.Q16), lat_l2=rng.randint(0, 300), lat_dram=rng.randint(0, 900))
+    re = H.get(rec, "rate_gmem")
+    o = max(1, -(-128 * 65536 // H.get(rec, "rate_dram" if miss else "rate_l2")))
+    e = [-(-j * 128 * 65536 // re) for j in range(n + 1)]
+    last = max(e[i] + (n - i) * o for i in range(n))
+    expect = max(e[n], last) + H.get(rec, "lat_dram" if miss else "lat_l2")
+    r = oracle.simulate(g, rec, 0)
+    assert r.status == 0 and r.cycles.tolist() == [[0, expect]]
