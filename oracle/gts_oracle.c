@@ -127,15 +127,23 @@
  *      at e_j (MEM_ARRIVE in (cycle, node id, j) order): with an L2 capacity
  *      (l2_lines = C > 0) its line hits iff it is among the C most recently
  *      accessed lines (then becomes the most recent), else the op's MISS
- *      flag decides; a hit is served by the L2 server, a miss by DRAM, each
- *      transaction for occ_t = max(1, cdiv(128*65536, rate_srv)):
- *      m_j = max(e_j, avail), avail = m_j + occ_t (NO_CONTENTION: m_j = e_j),
- *      finish_j = max(e'_j, m_j + occ_t) + lat_srv.  The node finishes at the
+ *      flag decides; a hit is served by the L2 server, a miss by DRAM.  A
+ *      server holds one 128-B transaction for q = cdiv(128*2^32, rate_srv)
+ *      units of 2^-16 cycle (rate_srv in Q16.16 B/cycle), so it sustains its
+ *      rate even when a line takes less than a cycle: with avail in those
+ *      units, m_j = max(e_j * 2^16, avail), avail = m_j + q (NO_CONTENTION:
+ *      m_j = e_j * 2^16), done_j = ceil((m_j + q) / 2^16) and
+ *      finish_j = max(e'_j, done_j) + lat_srv.  The node finishes at the
  *      largest finish_j, decided when its last transaction arrives; then its
- *      DATA / SYNC edges release (R8).  A one-transaction tile therefore
- *      times exactly as R6.4 does for the same node without an address.
+ *      DATA / SYNC edges release (R8).  A whole-cycle node of R6.4 sharing the
+ *      server starts at the first whole cycle at or after avail and leaves
+ *      avail on a whole cycle (so graphs without addresses time as before).
+ *      A lone one-transaction tile times exactly as R6.4 does for the same
+ *      node without an address.
  *      Readings: one transaction per distinct line of the tile (a line two
- *      rows share is fetched once); a transaction arrives at the L2 when the
+ *      rows share is fetched once); servers account transactions in 2^-16
+ *      cycles (whole-cycle occupancy would cap an L2 of thousands of bytes
+ *      per cycle at 128); a transaction arrives at the L2 when the
  *      engine starts injecting it and completes no earlier than its last
  *      byte leaves the engine (cut-through, as R6.4); conventional loads and
  *      stores use the same engine at its rate (the A100 record's engine is
@@ -243,7 +251,7 @@ typedef struct {
   int64_t *cta_sm; uint32_t *cta_launch, *cta_left, *cta_maxfin, *cta_kernel;
   /* per SM */
   uint64_t *resident, *lane_av, *smem_av, *eng_av;
-  uint64_t l2_av, dram_av;
+  uint64_t l2_av, dram_av;   /* in 2^-16 cycles (R17) */
   uint64_t *noc_av;        /* per domain node: 4 link/port servers */
   /* R16: tiles in recency order (most recent first) and their lines */
   uint32_t *lru_tile, *lru_lines; uint32_t lru_n;
@@ -504,8 +512,8 @@ static void mem_arrive(sim_t *S, uint32_t v, uint64_t t) {
     dram = !lru_access(S, S->node_tile[v], (uint32_t)cdiv(S->op_work[p], 128));
   uint64_t *av = dram ? &S->dram_av : &S->l2_av;
   uint64_t occm = dram ? S->occ_d[p] : S->occ_l2[p];
-  uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);
-  *av = m + occm;
+  uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, (*av + 65535) >> 16);
+  *av = (m + occm) << 16;
   uint64_t s = S->st[v];
   uint64_t f = max64(s + S->occ[p], m + occm) + (dram ? S->lat_d[p] : S->lat_l2[p]);
   if (!complete(S, v, s, f)) return;
@@ -529,13 +537,14 @@ static void mem_txn(sim_t *S, uint32_t v, uint32_t j, uint64_t t) {
   int dram = S->to_dram[p];
   if (S->hw[HW_L2_LINES]) dram = !lru_line_access(S, S->txn_lines[v][j]);
   uint64_t rate_srv = S->hw[HW_RATE + (dram ? 6 : 5)];
-  uint64_t occ_t = max64(1, cdiv(128ull * 65536, rate_srv));
+  uint64_t q = cdiv(128ull << 32, rate_srv);   /* 2^-16 cycles per transaction */
   uint64_t lat = S->hw[HW_LAT + (dram ? 5 : 4)];
   uint64_t *av = dram ? &S->dram_av : &S->l2_av;
-  uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);
-  *av = m + occ_t;
+  uint64_t m = (S->flags & F_NOCONT) ? t << 16 : max64(t << 16, *av);
+  *av = m + q;
+  uint64_t done = (m + q + 65535) >> 16;
   uint64_t left_engine = (uint64_t)S->st[v] + cdiv((uint64_t)(j + 1) * 128 * 65536, S->hw[HW_RATE + 4]);
-  uint64_t f = max64(left_engine, m + occ_t) + lat;
+  uint64_t f = max64(left_engine, done) + lat;
   if (f > S->txn_maxf[v]) S->txn_maxf[v] = f;
   if (--S->txn_left[v]) return;
   if (!complete(S, v, S->st[v], S->txn_maxf[v])) return;

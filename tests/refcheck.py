@@ -180,11 +180,12 @@ def verify_schedule(g, rec, flags, cycles, cta):
                 lines.move_to_end(key)
                 while len(lines) > cap:
                     lines.popitem(last=False)
-            occ_t = max(1, cdiv(LINE_BYTES * 65536, H.get(rec, "rate_dram" if miss else "rate_l2")))
-            m = a if nocont else max(a, av[miss])
-            av[miss] = m + occ_t
+            # the server's time in 2^-16 cycles: a line may take less than a cycle
+            q = cdiv(LINE_BYTES << 32, H.get(rec, "rate_dram" if miss else "rate_l2"))
+            m = a * 65536 if nocont else max(a * 65536, av[miss])
+            av[miss] = m + q
             left = s + cdiv((j + 1) * LINE_BYTES * 65536, rg)
-            f = max(left, m + occ_t) + H.get(rec, "lat_dram" if miss else "lat_l2")
+            f = max(left, cdiv(m + q, 65536)) + H.get(rec, "lat_dram" if miss else "lat_l2")
             tx_fin[v] = max(tx_fin.get(v, 0), f)
             if j == len(txn[v]) - 1:
                 assert fi[v] == tx_fin[v], f"addressed node {v} finish {fi[v]} != {tx_fin[v]}"
@@ -203,8 +204,8 @@ def verify_schedule(g, rec, flags, cycles, cta):
             assert all(hits) or not any(hits), f"node {v}: a whole-tile access hits all its lines or none"
             dram = not all(hits)
             occ_m, lat = (d["occ_dram"], d["lat_dram"]) if dram else (d["occ_l2"], d["lat_l2"])
-        m = s if nocont else max(s, av[dram])
-        av[dram] = m + occ_m
+        m = s if nocont else max(s, cdiv(av[dram], 65536))  # whole cycles, after any transaction
+        av[dram] = (m + occ_m) * 65536
         assert fi[v] == max(s + d["occ"], m + occ_m) + lat, f"gmem node {v} finish"
     # CTA dispatch re-simulated from retire cycles
     exp_sm, exp_launch = dispatch_from_retires(g, rec, fi)

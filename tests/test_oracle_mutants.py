@@ -45,8 +45,10 @@ MUTANTS = [
      "int is_order_now = (kind != E_DATA) && !order_at_fin;", False),
     ("occupancy_floor", "static uint64_t cdiv(uint64_t a, uint64_t b) { return (a + b - 1) / b; }",
      "static uint64_t cdiv(uint64_t a, uint64_t b) { return a / b; }", False),
-    ("no_contention_ignored_on_l2_dram", "uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, *av);",
-     "uint64_t m = max64(t, *av);", False),
+    ("no_contention_ignored_on_l2_dram", "uint64_t m = (S->flags & F_NOCONT) ? t : max64(t, (*av + 65535) >> 16);",
+     "uint64_t m = max64(t, (*av + 65535) >> 16);", False),
+    ("no_contention_ignored_on_transactions", "uint64_t m = (S->flags & F_NOCONT) ? t << 16 : max64(t << 16, *av);",
+     "uint64_t m = max64(t << 16, *av);", False),
     ("residency_ignores_warps", "s = s < wl ? s : wl;", ";", False),
     ("residency_ignores_smem", "if (kernel_smem[k]) s =", "if (0) s =", False),
     ("compute_classes_share_lanes", "uint64_t *lanes = S->lane_av + (sm * 3 + cls) * S->nsub;",
@@ -80,8 +82,10 @@ MUTANTS = [
     ("line_lru_one_extra_line", "int hit = i < S->lru_line_n && i < S->hw[HW_L2_LINES];",
      "int hit = i < S->lru_line_n && i <= S->hw[HW_L2_LINES];", False),
     ("line_lru_ignored", "if (S->hw[HW_L2_LINES]) dram = !lru_line_access(S, S->txn_lines[v][j]);", ";", False),
-    ("txn_occupancy_of_tile_bytes", "uint64_t occ_t = max64(1, cdiv(128ull * 65536, rate_srv));",
-     "uint64_t occ_t = max64(1, cdiv((uint64_t)S->op_work[p] * 65536, rate_srv));", False),
+    ("txn_occupancy_of_tile_bytes", "uint64_t q = cdiv(128ull << 32, rate_srv);",
+     "uint64_t q = cdiv((uint64_t)S->op_work[p] << 32, rate_srv);", False),
+    ("txn_occupancy_whole_cycles", "uint64_t q = cdiv(128ull << 32, rate_srv);",
+     "uint64_t q = max64(1, cdiv(128ull * 65536, rate_srv)) << 16;", False),
 ]
 
 

@@ -353,8 +353,9 @@ def test_verifier_transactions(seed):
 @pytest.mark.parametrize("seed", range(40))
 def test_one_line_tiles_equal_aggregate_rule(seed):
     """R17 reduces to R6.4: when every addressed tile is one aligned
-    128-B line (one transaction) and the L2 model is the static flag, a
-    graph with addresses times exactly as the same graph without them."""
+    128-B line (one transaction), the L2 model is the static flag and the
+    L2 / DRAM rates divide 128 B into whole cycles, a graph with addresses
+    times exactly as the same graph without them."""
     rng = SplitMix64(seed, 18)
     g = W.random_graph(rng, n_nodes_max=rng.choice([10, 60, 200]), n_kernels_max=2, ctas_max=5)
     g.op_work = np.where(np.isin(g.op_cls, (GLOAD, GSTORE)), 128, g.op_work).astype(np.uint32)
@@ -363,6 +364,8 @@ def test_one_line_tiles_equal_aggregate_rule(seed):
     if not mem.any():
         return
     rec = H.sample_random(rng)
+    rec[H.FIELDS["rate_l2"]] = rng.choice([1, 2, 4, 8, 16, 32, 64, 128]) * H.Q16
+    rec[H.FIELDS["rate_dram"]] = rng.choice([1, 2, 4, 8, 16, 32, 64, 128]) * H.Q16
     flags = rng.choice([0, 4, 8])
     base = oracle.simulate(g, rec, flags)
     from paper_2607_11262_amd.gen.graph import NO_ADDR
@@ -379,10 +382,12 @@ def test_one_line_tiles_equal_aggregate_rule(seed):
 def test_lone_stream_closed_form(seed):
     """A lone addressed load of n lines on an idle machine: transaction j
     enters at e_j = cdiv(j*128*2^16, r_e) and leaves the engine at e_(j+1);
-    the FIFO server of occupancy o then finishes the last one at
-    max_i (e_i + (n - i) o) (the latest arrival plus the work queued behind
-    it, a closed form without the recurrence), so the node finishes at
-    max(e_n, max_i (e_i + (n - i) o)) + latency."""
+    a FIFO server taking q = cdiv(128*2^32, r) units of 2^-16 cycle per line
+    then finishes the last one at max_i (e_i*2^16 + (n - i) q) (the latest
+    arrival plus the work queued behind it, a closed form without the
+    recurrence), so the node finishes at
+    max(e_n, ceil(max_i (e_i*2^16 + (n - i) q) / 2^16)) + latency.  Server
+    rates reach 300 B/cycle, more than a line per cycle."""
     rng = SplitMix64(seed, 19)
     n = rng.randint(1, 40)
     rows = rng.choice([1, n]) if n > 1 else 1
@@ -396,9 +401,9 @@ def test_lone_stream_closed_form(seed):
     rec = H.toy(rate_gmem=rng.randint(H.Q16 // 4, 400 * H.Q16), rate_l2=rng.randint(H.Q16 // 2, 300 * H.Q16),
                 rate_dram=rng.randint(H.Q16 // 2, 300 * H.Q16), lat_l2=rng.randint(0, 300), lat_dram=rng.randint(0, 900))
     re = H.get(rec, "rate_gmem")
-    o = max(1, -(-128 * 65536 // H.get(rec, "rate_dram" if miss else "rate_l2")))
+    q = -(-(128 << 32) // H.get(rec, "rate_dram" if miss else "rate_l2"))
     e = [-(-j * 128 * 65536 // re) for j in range(n + 1)]
-    last = max(e[i] + (n - i) * o for i in range(n))
-    expect = max(e[n], last) + H.get(rec, "lat_dram" if miss else "lat_l2")
+    last = max(e[i] * 65536 + (n - i) * q for i in range(n))
+    expect = max(e[n], -(-last // 65536)) + H.get(rec, "lat_dram" if miss else "lat_l2")
     r = oracle.simulate(g, rec, 0)
     assert r.status == 0 and r.cycles.tolist() == [[0, expect]]
