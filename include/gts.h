@@ -82,7 +82,13 @@ extern "C" {
  * (flags >> GTS_OPF_RANK_SHIFT); no other flag bit is set. */
 #define GTS_OPF_RANK_SHIFT 4
 #define GTS_NO_TILE 0xFFFFFFFFu  /* node_tile entry of an untracked node    */
-#define GTS_LINE_BYTES 128u      /* L2 line of the LRU model                */
+#define GTS_LINE_BYTES 128u      /* L2 line of the LRU model, and the memory
+                                    transaction of transaction-level tiles  */
+#define GTS_NO_ADDR 0xFFFFFFFFFFFFFFFFull  /* node_addr entry of a node
+                                              without a tile address      */
+#define GTS_MAX_NODE_TXN (1u << 21)  /* bound on one addressed tile's
+                                        transactions: rows * (row bytes / 128
+                                        + 2) may not exceed it             */
 
 /* ---- edge kinds (Sec. 4.1 edge semantics) ------------------------------ */
 /* succ[] entries are  target | (kind << GTS_EDGE_KIND_SHIFT).              */
@@ -179,8 +185,11 @@ typedef struct gts_hw_params {
  * kernel's CTA count; kernel_cluster = NULL means 1 for every kernel), and a
  * REMOTE op's target rank is below the cluster size of every kernel that
  * uses it; only GLOAD / GSTORE nodes carry a tile, and every node of one
- * tile has the same cdiv(work, 128) lines.  An empty graph has all counts
- * zero. */
+ * tile has the same cdiv(work, 128) lines; only GLOAD / GSTORE nodes carry
+ * an address, never in a graph whose nodes name tiles by id, and an
+ * addressed node's op has work > 0 divisible by its rows, a row stride of at
+ * least the row bytes, at most GTS_MAX_NODE_TXN transactions, and its bytes
+ * below GTS_NO_ADDR.  An empty graph has all counts zero. */
 typedef struct gts_graph_host {
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops;
   const uint8_t  *op_cls;           /* [n_ops]  GTS_TENSOR .. GTS_REMOTE     */
@@ -197,6 +206,21 @@ typedef struct gts_graph_host {
   const uint8_t  *kernel_cluster;   /* [n_kernels] CTAs per cluster, or NULL */
   const uint32_t *node_tile;        /* [n_nodes] tile of a GLOAD / GSTORE, or
                                        GTS_NO_TILE; NULL: no node has one    */
+  /* Transaction-level memory (Sec. 5.2 Memory, Sec. 5.3 memory nodes): a
+   * GLOAD / GSTORE node with an address accesses its op's tile of op_rows
+   * rows of op_work / op_rows bytes, row r at node_addr + r * op_pitch; the
+   * tile's distinct 128-B lines (in the order the rows first reach them)
+   * are its transactions, streamed by the SM's engine at its rate and
+   * served one by one by the L2 / DRAM servers (an LRU of lines decides
+   * which when l2_lines > 0, else the op's MISS flag); the node completes
+   * with its last transaction. */
+  const uint64_t *node_addr;        /* [n_nodes] tile address or GTS_NO_ADDR;
+                                       NULL: no node has one                 */
+  const uint32_t *op_rows;          /* [n_ops] rows of the tile, >= 1;
+                                       NULL: one row                         */
+  const uint32_t *op_pitch;         /* [n_ops] bytes between rows, >= row
+                                       bytes for ops of addressed nodes;
+                                       NULL: row bytes (rows packed)         */
 } gts_graph_host;
 
 typedef struct gts_graph gts_graph;  /* opaque handle to an uploaded graph */

@@ -46,7 +46,8 @@ class _GraphHost(ctypes.Structure):
                 ("succ", ctypes.c_void_p), ("cta_node_begin", ctypes.c_void_p),
                 ("kernel_cta_begin", ctypes.c_void_p), ("kernel_warps", ctypes.c_void_p),
                 ("kernel_smem", ctypes.c_void_p), ("kernel_cluster", ctypes.c_void_p),
-                ("node_tile", ctypes.c_void_p)]
+                ("node_tile", ctypes.c_void_p), ("node_addr", ctypes.c_void_p), ("op_rows", ctypes.c_void_p),
+                ("op_pitch", ctypes.c_void_p)]
 
 
 _lib = None
@@ -115,6 +116,9 @@ def _host_struct(g):
                 kernel_cluster=np.ascontiguousarray(g.kernel_cluster, np.uint8),
                 node_tile=(np.ascontiguousarray(g.node_tile, np.uint32) if g.node_tile is not None
                            else np.zeros(0, np.uint32)))
+    for name, dt in (("node_addr", np.uint64), ("op_rows", np.uint32), ("op_pitch", np.uint32)):
+        a = getattr(g, name, None)
+        arrs[name] = np.ascontiguousarray(a, dt) if a is not None else np.zeros(0, dt)
     h = _GraphHost(n_nodes=arrs["node_op"].shape[0], n_edges=arrs["succ"].shape[0],
                    n_ctas=arrs["cta_node_begin"].shape[0] - 1, n_kernels=arrs["kernel_warps"].shape[0],
                    n_ops=arrs["op_cls"].shape[0],

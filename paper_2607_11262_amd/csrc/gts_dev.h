@@ -25,6 +25,8 @@ constexpr uint32_t kGraphClassShift = 5u;         // bits 5-7: the op table has 
 constexpr uint32_t kGraphClusters = 256u;         // some kernel has clusters of more than
                                                   // one CTA or REMOTE nodes
 constexpr uint32_t kGraphTiles = 512u;            // some load / store names its tile
+constexpr uint32_t kGraphTxn = 1024u;             // some load / store has a tile address
+                                                  // (transaction-level memory)
 
 // Compute pipelines: every subpartition of an SM has one lane per compute
 // class.  Server state holds lanes only for the classes a graph uses, class
@@ -39,7 +41,7 @@ __host__ __device__ inline uint32_t compute_slot(uint32_t props, uint32_t cls) {
 struct ImageHeader {            // at offset 0 of the device image
   uint32_t magic, n_nodes, n_edges, n_ctas, n_kernels, n_ops, n_roots, props;
   uint64_t off_ops, off_nodes, off_succ, off_ctas, off_kernels, off_roots, off_indeg;
-  uint64_t off_tnodes, off_tsucc, off_tindeg, off_cclass, off_tops, off_tile;
+  uint64_t off_tnodes, off_tsucc, off_tindeg, off_cclass, off_tops, off_tile, off_txn_ptr, off_txn_line;
   uint32_t max_cta_nodes, max_outdeg, n_tnodes, n_tsucc, n_tops, pad;
 };
 
@@ -104,8 +106,14 @@ struct Image {
   const uint8_t* cclass;        // class of each CTA of a templated kernel
   const uint16_t* tops;         // [n_tops] class x slot -> op id
   const uint32_t* tile;         // [N] tile of each load / store, numbered 0..n_tiles-1 (kGraphTiles), else null
+  // transaction-level memory (kGraphTxn, else null): node v's transactions
+  // are the lines txn_line[txn_ptr[v] .. txn_ptr[v + 1]) (none: the node has
+  // no address), lines numbered densely 0..n_lines-1 in order of first use
+  const uint32_t* txn_ptr;      // [N + 1]
+  const uint32_t* txn_line;     // [n_txn]
   uint32_t n_nodes, n_edges, n_ctas, n_kernels, n_ops, props, n_tops;
   uint32_t n_tiles;             // distinct tiles
+  uint32_t n_txn, n_lines;      // transactions of all addressed nodes, distinct lines
 };
 
 // Hardware record word indices (gts_hw_params field order).
@@ -140,8 +148,8 @@ struct SimLayout {
   uint64_t off_rp;      // windowed kernel: later ready entries beyond LDS, [kPoolSpill][64] u64
   uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
   uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
-  uint64_t off_lru;     // general kernel: LRU L2, latest access stamp per tile ([n_tiles] u32)
-  uint64_t off_lru_bit; // general kernel: LRU L2, Fenwick tree of lines over stamps ([N + 1] u64)
+  uint64_t off_lru;     // general kernel: LRU L2, latest access stamp per tile or line ([keys] u32)
+  uint64_t off_lru_bit; // general kernel: LRU L2, Fenwick tree of lines over stamps ([accesses + 1] u64)
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };

@@ -73,6 +73,10 @@ struct Derived {
   std::vector<uint16_t> tops;    // class x slot -> op
   uint32_t n_tnodes = 0, n_tsucc = 0;
   uint32_t n_tiles = 0;          // distinct tiles named by loads / stores
+  // transaction-level memory: node v's lines txn_line[txn_ptr[v] ..
+  // txn_ptr[v + 1]), numbered densely in order of first use
+  std::vector<uint32_t> txn_ptr, txn_line;
+  uint32_t n_lines = 0;
 };
 
 // Template sharing: find the kernels whose CTAs run isomorphic tile graphs
@@ -246,6 +250,42 @@ int check_graph(const gts_graph_host* h, Derived* d) {
     }
     n_tiles = (uint32_t)lines.size();
   }
+  // tile addresses: only loads / stores, never beside tile ids; each
+  // addressed op's shape (rows dividing its bytes, a stride of at least a
+  // row, a bounded transaction count) and each tile's bytes below NO_ADDR
+  uint64_t n_txn_bound = 0;
+  if (h->op_rows)
+    for (uint32_t p = 0; p < P; ++p)
+      if (h->op_rows[p] == 0) return fail(GTS_E_RANGE, "op %u has 0 rows", p);
+  if (h->node_addr) {
+    for (uint32_t v = 0; v < N; ++v) {
+      const uint64_t a = h->node_addr[v];
+      if (a == GTS_NO_ADDR) continue;
+      const uint32_t p = h->node_op[v];
+      if (!is_memory(h->op_cls[p])) return fail(GTS_E_RANGE, "node %u is not a load or store but has a tile address", v);
+      if (h->node_tile && h->node_tile[v] != GTS_NO_TILE)
+        return fail(GTS_E_RANGE, "node %u names a tile both by id and by address", v);
+      const uint64_t R = h->op_rows ? h->op_rows[p] : 1u, work = h->op_work[p];
+      if (work == 0 || work % R) return fail(GTS_E_RANGE, "op %u: %llu bytes in %llu rows (node %u)", p,
+                                               (unsigned long long)work, (unsigned long long)R, v);
+      const uint64_t W = work / R, pitch = h->op_pitch ? h->op_pitch[p] : W;
+      if (pitch < W) return fail(GTS_E_RANGE, "op %u: row stride %llu below the row's %llu bytes", p,
+                                 (unsigned long long)pitch, (unsigned long long)W);
+      const uint64_t bound = R * (W / GTS_LINE_BYTES + 2);
+      if (bound > GTS_MAX_NODE_TXN) return fail(GTS_E_RANGE, "op %u: tile of up to %llu transactions (at most %u)",
+                                                p, (unsigned long long)bound, GTS_MAX_NODE_TXN);
+      const uint64_t span = (R - 1) * pitch + W;  // <= 2^32 * 2^32: no wrap in 64 bits for R, W, pitch < 2^32
+      if (a > GTS_NO_ADDR - 1 - span) return fail(GTS_E_RANGE, "node %u: tile at 0x%llx wraps the address space", v,
+                                                  (unsigned long long)a);
+      n_txn_bound += bound;
+    }
+    if (n_txn_bound && h->node_tile)
+      for (uint32_t v = 0; v < N; ++v)
+        if (h->node_tile[v] != GTS_NO_TILE)
+          return fail(GTS_E_RANGE, "node %u names a tile by id in a graph whose tiles have addresses", v);
+    if (n_txn_bound >= (1ull << 31)) return fail(GTS_E_RANGE, "addressed tiles of up to %llu transactions in all",
+                                                 (unsigned long long)n_txn_bound);
+  }
   // first CTA of each CTA's cluster (clusters are dispatched together, so
   // edges between their CTAs may go either way)
   std::vector<uint32_t> cluster_first(C);
@@ -331,10 +371,43 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   }
   for (uint32_t k = 0; k < K; ++k) clusters |= cluster_of(h, k) > 1;
   d->n_tiles = n_tiles;
+  d->txn_ptr.clear();
+  d->txn_line.clear();
+  d->n_lines = 0;
+  if (n_txn_bound) {
+    // each addressed tile's distinct lines in the order its rows reach them
+    // (a line two rows share is one transaction), lines numbered densely
+    std::unordered_map<uint64_t, uint32_t> dense;
+    std::vector<uint64_t> mine;
+    d->txn_ptr.assign((size_t)N + 1, 0);
+    for (uint32_t v = 0; v < N; ++v) {
+      d->txn_ptr[v] = (uint32_t)d->txn_line.size();
+      const uint64_t a = h->node_addr[v];
+      if (a == GTS_NO_ADDR) continue;
+      const uint32_t p = h->node_op[v];
+      const uint64_t R = h->op_rows ? h->op_rows[p] : 1u, W = h->op_work[p] / R;
+      const uint64_t pitch = h->op_pitch ? h->op_pitch[p] : W;
+      mine.clear();
+      for (uint64_t r = 0; r < R; ++r) {
+        const uint64_t lo = (a + r * pitch) / GTS_LINE_BYTES, hi = (a + r * pitch + W - 1) / GTS_LINE_BYTES;
+        for (uint64_t line = lo; line <= hi; ++line) {
+          // rows reach lines in increasing order unless the stride is below
+          // a line: only the last few lines can repeat
+          bool seen = false;
+          for (size_t i = mine.size(); i-- > 0 && !seen && mine[i] >= lo;) seen = mine[i] == line;
+          if (!seen) mine.push_back(line);
+        }
+      }
+      for (uint64_t line : mine) d->txn_line.push_back(dense.emplace(line, (uint32_t)dense.size()).first->second);
+    }
+    d->txn_ptr[N] = (uint32_t)d->txn_line.size();
+    d->n_lines = (uint32_t)dense.size();
+  }
   d->props = (sinks_memory ? gts::kGraphSinksAreMemory : 0u) | (cross_from_memory ? gts::kGraphCrossFromMemory : 0u) |
              (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
              (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift |
-             (clusters ? gts::kGraphClusters : 0u) | (n_tiles ? gts::kGraphTiles : 0u);
+             (clusters ? gts::kGraphClusters : 0u) | (n_tiles ? gts::kGraphTiles : 0u) |
+             (d->txn_line.empty() ? 0u : gts::kGraphTxn);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
   find_templates(h, d);
@@ -342,7 +415,8 @@ int check_graph(const gts_graph_host* h, Derived* d) {
 }
 
 struct ImageLayout {
-  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, tnodes, tsucc, tindeg, cclass, tops, tile, total;
+  uint64_t ops, nodes, succ, ctas, kernels, roots, indeg, tnodes, tsucc, tindeg, cclass, tops, tile, txn_ptr, txn_line,
+      total;
 };
 
 ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
@@ -375,11 +449,17 @@ ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
   off = align_up(off + d.tops.size() * 2, gts::kAlign);
   L.tile = off;
   off = align_up(off + (d.n_tiles ? (uint64_t)h->n_nodes * 4 : 0u), gts::kAlign);
+  L.txn_ptr = off;
+  off = align_up(off + d.txn_ptr.size() * 4, gts::kAlign);
+  L.txn_line = off;
+  off = align_up(off + d.txn_line.size() * 4, gts::kAlign);
   L.total = off;
   return L;
 }
 
-gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t n_tiles) {
+// keys: tiles or lines the LRU L2 tracks (0: no LRU state); accesses: a
+// bound on the LRU accesses of one simulation (the stamps of its tree)
+gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t keys, uint32_t accesses) {
   gts::SimLayout s;
   uint64_t off = 0;
   s.off_state = off;
@@ -392,9 +472,9 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t n_tiles) 
   s.off_optab = off;
   off = align_up(off + (uint64_t)P * 16, gts::kAlign);
   s.off_lru = off;
-  off = align_up(off + (uint64_t)n_tiles * 4, gts::kAlign);
+  off = align_up(off + (uint64_t)keys * 4, gts::kAlign);
   s.off_lru_bit = off;
-  off = align_up(off + (n_tiles ? ((uint64_t)N + 1) * 8 : 0u), gts::kAlign);
+  off = align_up(off + (keys ? ((uint64_t)accesses + 1) * 8 : 0u), gts::kAlign);
   // The windowed kernel's per-SM queues overlay the general kernel's pending
   // list (a simulation the windowed kernel hands back is restarted from
   // scratch by the general kernel).
@@ -435,8 +515,14 @@ int check_hw(const gts_hw_params* hw, uint32_t index) {
   return GTS_OK;
 }
 
+gts::SimLayout layout_of(const gts_graph* g) {
+  const gts::Image& m = g->img;
+  return m.n_txn ? sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_lines, m.n_txn)
+                 : sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_tiles, m.n_nodes);
+}
+
 uint64_t sim_scratch_bytes(const gts_graph* g, uint32_t B) {
-  return (uint64_t)B * sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops, g->img.n_tiles).stride;
+  return (uint64_t)B * layout_of(g).stride;
 }
 
 int check_sim_args(const gts_graph* g, uint32_t B, const uint32_t* out_cycles, const uint32_t* out_makespan,
@@ -502,7 +588,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   L.img = g->img;
   L.hw = hw_dev;
   L.sims = sims;
-  L.layout = sim_layout(g->img.n_nodes, g->img.n_ctas, g->img.n_ops, g->img.n_tiles);
+  L.layout = layout_of(g);
   L.out_cycles = (flags & GTS_OUT_NODES) ? out_cycles : nullptr;
   L.out_makespan = out_makespan;
   L.out_status = out_status;
@@ -522,7 +608,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
   bool windowed = (g->img.props & need_props) == need_props &&
-                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTiles)) &&
+                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTiles | gts::kGraphTxn)) &&
                   g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
@@ -681,6 +767,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   hdr->off_cclass = L.cclass;
   hdr->off_tops = L.tops;
   hdr->off_tile = L.tile;
+  hdr->off_txn_ptr = L.txn_ptr;
+  hdr->off_txn_line = L.txn_line;
   hdr->max_cta_nodes = d.max_cta_nodes;
   hdr->max_outdeg = d.max_outdeg;
   hdr->n_tnodes = d.n_tnodes;
@@ -787,6 +875,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
       out[v] = x == GTS_NO_TILE ? GTS_NO_TILE : dense.emplace(x, (uint32_t)dense.size()).first->second;
     }
   }
+  if (!d.txn_ptr.empty()) std::memcpy(img.data() + L.txn_ptr, d.txn_ptr.data(), d.txn_ptr.size() * 4);
+  if (!d.txn_line.empty()) std::memcpy(img.data() + L.txn_line, d.txn_line.data(), d.txn_line.size() * 4);
   if (!d.tops.empty()) std::memcpy(img.data() + L.tops, d.tops.data(), d.tops.size() * 2);
   if (!d.roots.empty()) std::memcpy(img.data() + L.roots, d.roots.data(), d.roots.size() * 4);
 
@@ -813,6 +903,11 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.n_tops = (uint32_t)d.tops.size();
   g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
   g->img.n_tiles = d.n_tiles;
+  const bool txn = !d.txn_line.empty();
+  g->img.txn_ptr = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_ptr) : nullptr;
+  g->img.txn_line = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_line) : nullptr;
+  g->img.n_txn = (uint32_t)d.txn_line.size();
+  g->img.n_lines = d.n_lines;
   g->img.n_nodes = h->n_nodes;
   g->img.n_edges = h->n_edges;
   g->img.n_ctas = h->n_ctas;

@@ -40,7 +40,17 @@
 //  * LRU L2 (tiles): a load / store that names its tile, on a machine with
 //    an L2 capacity, hits iff the tile was touched before and its lines plus
 //    the distinct lines of other tiles touched since fit, else goes to DRAM;
-//    the tile then becomes the most recent.
+//    the tile then becomes the most recent;
+//  * transaction-level memory (Sec. 5.2, 5.3): a load / store with a tile
+//    address holds its engine for its n distinct 128-B lines; transaction j
+//    enters at e_j = s + ceil(j * 128 * 2^16 / rate_gmem), arrives at the L2
+//    then (memory events in (cycle, node id, j) order), is a hit iff its line
+//    is among the l2_lines most recent (an LRU of lines; without a capacity
+//    the op's MISS flag decides) and is served FIFO for ceil(128 * 2^32 /
+//    rate) units of 2^-16 cycle (server time is kept in those units; a
+//    whole-cycle node starts at the first whole cycle after): finish_j =
+//    max(e_(j+1), ceil((m_j + q) / 2^16)) + latency; the node completes at
+//    its largest finish_j, when its last transaction arrives.
 #include <hip/hip_runtime.h>
 
 #include "../../include/gts.h"
@@ -66,9 +76,9 @@ struct Sim {
   // LRU L2 state (scratch): each tile's latest access stamp (1-based count
   // of tile accesses, 0 = never) and a Fenwick tree over stamps holding, at
   // each tile's latest stamp, that tile's line count
-  uint32_t* lru_last;   // [n_tiles], tiles numbered densely at upload
-  uint64_t* lru_bit;    // [N + 1], entry 0 unused
-  uint32_t lru_now, l2_lines;
+  uint32_t* lru_last;   // [keys]: tiles, or the lines of addressed tiles, numbered densely at upload
+  uint64_t* lru_bit;    // [accesses + 1], entry 0 unused
+  uint32_t lru_now, l2_lines, lru_acc;  // lru_acc: bound on this simulation's accesses
   uint64_t lru_total;   // lines of all distinct tiles touched so far
   uint64_t* state;      // [N]
   CtaState* cst;        // [C]
@@ -78,7 +88,8 @@ struct Sim {
   // uniform control state
   uint32_t npend, next_cta, retired, cur_k, kstart_k, kstart_t, kstart_valid;
   uint32_t run_kb, run_cl;  // first CTA and cluster size of the kernel whose CTAs are live
-  uint64_t l2_av, dram_av, digest;
+  uint64_t l2_av, dram_av;  // chip-wide servers' availability, in 2^-16 cycles
+  uint64_t digest;
   uint32_t makespan, nfin, overflow;
 
   __device__ void push_one(uint64_t key, uint32_t aux) {
@@ -385,14 +396,59 @@ struct Sim {
     } else {
       const uint32_t a = S[smem_w + 1];
       const uint64_t s = nocont ? (uint64_t)t : (a > t ? a : t);
-      if (s + od.x > kMaxCycle) {
+      // a tile with an address streams its n lines through the engine
+      const uint32_t n = G.txn_ptr ? G.txn_ptr[v + 1] - G.txn_ptr[v] : 0u;
+      const uint64_t occ_e =
+          n ? clamp_occ(cdiv64((uint64_t)n * GTS_LINE_BYTES * 65536ull, hw[HW_RATE + R_GMEM])) : (uint64_t)od.x;
+      if (s + occ_e > kMaxCycle) {
         overflow = 1;
         return;
       }
-      if (lane == 0) S[smem_w + 1] = (uint32_t)(s + od.x);
+      if (lane == 0) S[smem_w + 1] = (uint32_t)(s + occ_e);
+      // the node's state word is free once it issues: an addressed node keeps
+      // its start (high) and the largest finish of its transactions so far
+      if (n && lane == 0) pst(&state[v], s << 32);
       release(v, rec, 0, s + 1, rec.cta, sm);
-      push_one(mkkey(s, kEvMem, v), sm);
+      push_one(mkkey(s, kEvMem, v), sm);  // transaction 0 (aux: SM | transaction << 10)
     }
+  }
+
+  // Transaction j of addressed node v arrives at the L2 at cycle t.
+  __device__ void mem_txn(uint32_t v, const NodeDev& rec, uint32_t t, uint32_t sm, uint32_t j) {
+    const uint32_t first = G.txn_ptr[v], n = G.txn_ptr[v + 1] - first;
+    const uint4 od = optab[rec.op_nsucc & 0xFFFFu];
+    bool dram = (od.w >> 3) & 1u;
+    if (l2_lines) dram = !lru_access(G.txn_line[first + j], 1u, l2_lines);
+    // the servers' time is kept in 2^-16 cycles: a line may take less than a
+    // cycle on an L2 or DRAM of more than 128 B per cycle
+    const uint64_t q = cdiv64((uint64_t)GTS_LINE_BYTES << 32, hw[HW_RATE + (dram ? R_DRAM : R_L2)]);
+    const uint64_t lat = hw[HW_LAT + (dram ? L_DRAM : L_L2)];
+    const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
+    const uint64_t av = dram ? dram_av : l2_av;
+    const uint64_t tq = (uint64_t)t << 16;
+    const uint64_t m = nocont ? tq : (av > tq ? av : tq);
+    if (dram)
+      dram_av = m + q;
+    else
+      l2_av = m + q;
+    const uint64_t done = (m + q + 65535u) >> 16;
+    const uint64_t sw = uni64(pld(&state[v]));
+    const uint64_t s = sw >> 32;
+    const uint64_t rg = hw[HW_RATE + R_GMEM];
+    const uint64_t left = s + cdiv64((uint64_t)(j + 1) * GTS_LINE_BYTES * 65536ull, rg);
+    uint64_t f = (left > done ? left : done) + lat;
+    if (f > kMaxCycle) {
+      overflow = 1;
+      return;
+    }
+    f = f > (uint32_t)sw ? f : (uint32_t)sw;
+    if (j + 1 < n) {
+      if (lane == 0) pst(&state[v], (s << 32) | f);
+      push_one(mkkey(s + cdiv64((uint64_t)(j + 1) * GTS_LINE_BYTES * 65536ull, rg), kEvMem, v), sm | (j + 1) << 10);
+      return;
+    }
+    if (!complete(v, rec, s, f, sm)) return;
+    release(v, rec, 1, f, rec.cta, sm);
   }
 
   // Inclusive prefix sum across the wave.
@@ -405,7 +461,7 @@ struct Sim {
   // old stamp; lanes 32-63 add them on the nodes covering the new one; a node
   // covering both keeps its value.  Three dependent round trips per access.
   __device__ bool lru_access(uint32_t x, uint32_t n, uint32_t cap) {
-    const uint32_t N = G.n_nodes;  // at most N tile accesses, so stamps stay <= N < 2^30
+    const uint32_t N = lru_acc;  // at most this many accesses, so stamps stay <= N < 2^31
     const uint32_t t = uni(pld(&lru_last[x]));
     const uint32_t now = ++lru_now;
     const uint32_t k = lane & 31u;
@@ -437,8 +493,13 @@ struct Sim {
     return hit;
   }
 
-  __device__ void mem_arrive(uint32_t v, uint32_t t, uint32_t sm) {
+  __device__ void mem_arrive(uint32_t v, uint32_t t, uint32_t aux) {
     const NodeDev rec = G.nodes[v];
+    const uint32_t sm = aux & 1023u;
+    if (G.txn_ptr && G.txn_ptr[v + 1] != G.txn_ptr[v]) {
+      mem_txn(v, rec, t, sm, aux >> 10);
+      return;
+    }
     const uint4 od = optab[rec.op_nsucc & 0xFFFFu];
     bool dram = (od.w >> 3) & 1u;
     uint64_t occm = od.y, lat = od.z;
@@ -452,13 +513,14 @@ struct Sim {
       }
     }
     const bool nocont = (flags & GTS_NO_CONTENTION) != 0;
-    const uint64_t av = dram ? dram_av : l2_av;
+    // whole-cycle service: from the first whole cycle the server is free
+    const uint64_t av = ((dram ? dram_av : l2_av) + 65535u) >> 16;
     const uint64_t m = nocont ? (uint64_t)t : (av > t ? av : (uint64_t)t);
     const uint64_t mend = m + occm;
     if (dram)
-      dram_av = mend;
+      dram_av = mend << 16;
     else
-      l2_av = mend;
+      l2_av = mend << 16;
     const uint64_t e = (uint64_t)t + od.x;
     const uint64_t f = (e > mend ? e : mend) + lat;
     if (!complete(v, rec, t, f, sm)) return;
@@ -500,6 +562,7 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.lru_now = 0;
   S.lru_total = 0;
   S.l2_lines = S.hw[HW_L2_LINES];
+  S.lru_acc = S.G.n_txn ? S.G.n_txn : S.G.n_nodes;
   S.out_cycles = (L.flags & GTS_OUT_NODES) ? L.out_cycles : nullptr;
   const uint32_t lane = S.lane;
 
@@ -528,9 +591,10 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   const uint32_t nsrv = S.nsm * S.sstride + S.nsm + L.noc_words;
   for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
   for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);
-  if (S.G.tile && S.l2_lines) {
-    for (uint32_t x = lane; x < S.G.n_tiles; x += 64) pst(&S.lru_last[x], 0u);
-    for (uint32_t i = lane; i <= S.G.n_nodes; i += 64) pst(&S.lru_bit[i], (uint64_t)0);
+  if ((S.G.tile || S.G.txn_ptr) && S.l2_lines) {
+    const uint32_t keys = S.G.txn_ptr ? S.G.n_lines : S.G.n_tiles;
+    for (uint32_t x = lane; x < keys; x += 64) pst(&S.lru_last[x], 0u);
+    for (uint32_t i = lane; i <= S.lru_acc; i += 64) pst(&S.lru_bit[i], (uint64_t)0);
   }
   for (uint32_t c = lane; c < S.G.n_ctas; c += 64) {
     pst(&S.cst[c].sm, 0u);

@@ -140,7 +140,7 @@ class TileGraph:
                     node_op=self.node_op, succ_ptr=self.succ_ptr, succ=self.succ,
                     cta_node_begin=self.cta_node_begin, kernel_cta_begin=self.kernel_cta_begin,
                     kernel_warps=self.kernel_warps, kernel_smem=self.kernel_smem, kernel_cluster=self.kernel_cluster,
-                    node_tile=self.node_tile)
+                    node_tile=self.node_tile, node_addr=self.node_addr, op_rows=self.op_rows, op_pitch=self.op_pitch)
 
 
 class OpTable:

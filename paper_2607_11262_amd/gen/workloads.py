@@ -18,7 +18,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import hw as hwmod
-from .graph import (NO_TILE, ALU, DATA, GLOAD, GSTORE, MISS, ORDER, SFU, SYNC, SYNC_EDGE, TENSOR, GraphBuilder,
+from .graph import (NO_ADDR, NO_TILE, ALU, DATA, GLOAD, GSTORE, MISS, ORDER, SFU, SYNC, SYNC_EDGE, TENSOR, GraphBuilder,
                     OpTable, TileGraph, csr_from_edges, empty_graph)
 from .rng import SplitMix64
 
@@ -227,6 +227,73 @@ def gemm(M=1024, N=1024, K=1024, BM=128, BN=128, BK=32, S=2, per_warp=False, til
                   dict(M=M, N=N, K=K, BM=BM, BN=BN, BK=BK, S=S, per_warp=per_warp))
     if tiles:
         g.node_tile = gemm_tile_ids(M, N, K, BM, BN, BK, S, per_warp)
+    return g
+
+
+def gemm_addressed(M=1024, N=1024, K=1024, BM=128, BN=128, BK=32, S=2, per_warp=False, pad=0,
+                   b_layout="kn", elem=FP16) -> TileGraph:
+    """gemm(...) with transaction-level memory: every load and store carries
+    the byte address of its tile in its tensor, and its op the tile's rows
+    and row stride (Sec. 4.1 tile descriptor: storage, shape, layout,
+    coordinates).  A is M x K row-major, C is M x N row-major, B is K x N
+    row-major ("kn") or N x K row-major ("nk", i.e. column-major K x N);
+    each leading dimension is padded by `pad` elements.  Tensors are placed
+    one after another from address 0, each starting on a 4 KiB boundary.
+    A tile (m, k) of A is BM rows of BK elements at A + (m*BM*lda + k*BK)*elem
+    with stride lda*elem; a B tile is BK rows of BN elements ("kn") or BN
+    rows of BK ("nk"); a C tile BM rows of BN."""
+    g = gemm(M, N, K, BM, BN, BK, S, per_warp)
+    lda, ldc = K + pad, N + pad
+    ldb = (N if b_layout == "kn" else K) + pad
+    A0 = 0
+    B0 = -(-(M * lda * elem) // 4096) * 4096
+    C0 = B0 + -(-((K if b_layout == "kn" else N) * ldb * elem) // 4096) * 4096
+    T = K // BK
+    gm, gn = M // BM, N // BN
+    roles = gemm_template(T, S, per_warp)[0]
+    kind = np.zeros(len(roles), dtype=np.int64)  # 1 A, 2 B, 3 C
+    kstep = np.zeros(len(roles), dtype=np.int64)
+    for i, r in enumerate(roles):
+        if r[0] == "lA":
+            kind[i], kstep[i] = 1, r[1]
+        elif r[0] == "lB":
+            kind[i], kstep[i] = 2, r[1]
+        elif r[0] == "st":
+            kind[i] = 3
+    c = np.arange(gm * gn, dtype=np.int64)[:, None]
+    mi, ni = c // gn, c % gn
+    a_addr = A0 + (mi * BM * lda + kstep * BK) * elem
+    if b_layout == "kn":
+        b_addr = B0 + (kstep * BK * ldb + ni * BN) * elem
+        b_rows, b_pitch = BK, ldb * elem
+    else:
+        b_addr = B0 + (ni * BN * ldb + kstep * BK) * elem
+        b_rows, b_pitch = BN, ldb * elem
+    c_addr = C0 + (mi * BM * ldc + ni * BN) * elem
+    addr = np.where(kind == 1, a_addr, np.where(kind == 2, b_addr, np.where(kind == 3, c_addr, -1)))
+    addr = addr.ravel()
+    node_kind = np.tile(kind, gm * gn)
+    # ops: one per (op, tensor) so each carries its tensor's tile shape
+    shape = {1: (BM, lda * elem), 2: (b_rows, b_pitch), 3: (BM, ldc * elem)}
+    ops = OpTable()
+    for p in range(g.n_ops):
+        ops.get(int(g.op_cls[p]), int(g.op_work[p]), int(g.op_warps[p]), int(g.op_flags[p]))
+    new_op = g.node_op.astype(np.int64).copy()
+    for t in (1, 2, 3):
+        sel = node_kind == t
+        for p in np.unique(new_op[sel]).tolist():
+            rows, pitch = shape[t]
+            q = ops.get(int(g.op_cls[p]), int(g.op_work[p]), int(g.op_warps[p]), int(g.op_flags[p]), rows, pitch)
+            new_op[sel & (g.node_op == p)] = q
+    cls, flags, work, warps = ops.arrays()
+    rows, pitch = ops.shapes()
+    g.op_cls, g.op_flags, g.op_work, g.op_warps = cls, flags, work, warps
+    g.op_rows, g.op_pitch = rows, pitch
+    g.node_op = new_op.astype(np.uint16)
+    g.node_addr = np.where(addr >= 0, addr, 0).astype(np.uint64)
+    g.node_addr[addr < 0] = np.uint64(NO_ADDR)
+    g.name = g.name + f"_addr_{b_layout}_pad{pad}"
+    g.meta.update(pad=pad, b_layout=b_layout)
     return g
 
 

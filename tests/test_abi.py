@@ -207,3 +207,56 @@ def test_tile_validation_codes():
     # tiles go to the device image; sharing is unaffected
     assert api.device_bytes(g) > api.device_bytes(_mutate(g, node_tile=None))
     assert api.templates(g)["templated_kernels"] == 1
+
+
+def test_address_validation_codes():
+    """Transaction-level tiles: the library and the Python statement of the
+    rules agree on every case -- addresses only on loads / stores, never
+    beside tile ids, rows dividing the bytes, a stride of at least a row, a
+    bounded transaction count, no wrap past the address space."""
+    from paper_2607_11262_amd.gen.graph import MAX_NODE_TXN, NO_ADDR
+    g = W.gemm_addressed(256, 256, 256, 64, 64, 32, 2, pad=8)
+    assert api.validate_code(g) == 0
+    validate(g)
+    # the device image holds each node's lines
+    assert api.device_bytes(g) > api.device_bytes(_mutate(g, node_addr=None, op_rows=None, op_pitch=None))
+    mma = int(np.flatnonzero(g.op_cls[g.node_op] == TENSOR)[0])
+    load = int(np.flatnonzero(g.op_cls[g.node_op] == GLOAD)[0])
+    lop = int(g.node_op[load])
+
+    def check(g2):
+        assert api.validate_code(g2) == -4
+        with pytest.raises(ValidationError):
+            validate(g2)
+
+    bad = g.node_addr.copy()
+    bad[mma] = 4096  # a compute node with an address
+    check(_mutate(g, node_addr=bad))
+    rows = g.op_rows.copy()
+    rows[lop] = 0
+    check(_mutate(g, op_rows=rows))
+    rows = g.op_rows.copy()
+    rows[lop] = 3  # does not divide the tile's bytes
+    check(_mutate(g, op_rows=rows))
+    pitch = g.op_pitch.copy()
+    pitch[lop] = int(g.op_work[lop]) // int(g.op_rows[lop]) - 1  # rows overlap
+    check(_mutate(g, op_pitch=pitch))
+    bad = g.node_addr.copy()
+    bad[load] = np.uint64(NO_ADDR - 100)  # wraps
+    check(_mutate(g, node_addr=bad))
+    tiles = np.full(g.n_nodes, 0xFFFFFFFF, np.uint32)
+    tiles[load] = 3  # ids beside addresses
+    check(_mutate(g, node_tile=tiles))
+    # too many transactions on one tile
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    b.cta()
+    b.node(GLOAD, 128 * MAX_NODE_TXN, 1, addr=0)
+    check(b.build())
+    b = GraphBuilder()
+    b.kernel(4, 0)
+    b.cta()
+    b.node(GLOAD, 128 * (MAX_NODE_TXN - 2), 1, addr=0)
+    g3 = b.build()
+    assert api.validate_code(g3) == 0
+    validate(g3)
