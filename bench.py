@@ -32,7 +32,10 @@ Case studies (one step = every graph of the study, each under 4096 seeded
 machines): `--workload pipelining` (Sec. 7.1, Table 4: fused GEMM + SiLU in
 four pipeline organisations x five tiles x four edge sets), `--workload noc`
 (Sec. 7.2: cluster-fused attention over an SM-cluster NoC), `--workload
-l2lru` (eight sweep GEMMs with tile ids under an LRU L2 of 4-64 MiB); each
+l2lru` (eight sweep GEMMs with tile ids under an LRU L2 of 4-64 MiB),
+`--workload txn` (Sec. 5.2 transaction-level memory: eight GEMMs whose tiles
+carry addresses in row- or column-major tensors, with and without padding,
+expanded into 128-B transactions under an LRU of lines of 4-64 MiB); each
 line adds the study's table read off GPU timelines.
 """
 from __future__ import annotations
@@ -56,7 +59,7 @@ HBM_PEAK_GBS = 8000.0
 B_STUDY = 4096
 NAMED = ("gemm_design_sweep", "gemm_1024_a100", "flash_attention_b8_h32_s4096", "splitkv_decode_b64",
          "decoder_layer_prefill_2048")
-STUDIES = ("pipelining", "noc", "l2lru")
+STUDIES = ("pipelining", "noc", "l2lru", "txn")
 KERNEL_SOURCES = ("gts_window.hip", "gts_sim.hip", "gts_common.h", "gts_dev.h")
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -152,6 +155,19 @@ def workload_parts(name):
             hw[:, 26] = (rng.integers(4, 65, size=B_STUDY) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
             return W.gemm(*ps[i], tiles=True), hw
         return (lambda i: ps[i], make, len(ps))
+    if name == "txn":
+        designs = [(M, N, K, BM, BN, BK, S, var) for (M, N, K, BM, BN, BK, S) in
+                   ((512, 512, 1024, 128, 128, 32, 2), (1024, 512, 512, 128, 64, 32, 3),
+                    (512, 1024, 512, 64, 128, 64, 2), (1024, 1024, 256, 128, 128, 64, 3))
+                   for var in ("kn", "nk")]
+
+        def make(i):
+            M, N, K, BM, BN, BK, S, var = designs[i]
+            hw = W.workload_hw("gemm_design_sweep", B=B_STUDY, index=i)
+            rng = np.random.default_rng(6000 + i)
+            hw[:, 26] = (rng.integers(4, 65, size=B_STUDY) * (1 << 20)) // 128  # L2 lines, 4-64 MiB
+            return W.gemm_addressed(M, N, K, BM, BN, BK, S, b_layout=var, pad=8 * (i % 2)), hw
+        return (lambda i: designs[i], make, len(designs))
     raise KeyError(name)
 
 
@@ -487,7 +503,7 @@ def main() -> int:
                      "traffic_per_node_sim": traffic_per_node,
                      "algorithmic_bytes_per_step": abytes,
                      "step_ms": mean_step * 1e3,
-                     "kernel": "gts_sim_wave" if name in ("noc", "l2lru") else "gts_sim_window",
+                     "kernel": "gts_sim_wave" if name in ("noc", "l2lru", "txn") else "gts_sim_window",
                      "launch_ms": mean_launch * 1e3,
                      "per_launch_gbs": abytes / launches_per_step / mean_launch / 1e9,
                      "note": "achieved = algorithmic bytes per step / mean step time (HIP events; launches of a "
@@ -504,6 +520,10 @@ def main() -> int:
         out["case_study"] = noc_case_study(api, torch)
     if name == "l2lru":
         out["case_study"] = lru_case_study(api, torch)
+    if name == "txn":
+        out["case_study"] = txn_case_study(api, torch)
+        out["transactions_per_s"] = sum(int((p[2][2] == 0).sum().item()) * _transactions(p[3])
+                                        for p in plan.parts) * K / wall
     if phases is not None:
         out["phase_stats"] = phases
     if host_io_rates is not None:
@@ -595,6 +615,53 @@ def phase_stats(api, torch, plan):
         print(f"[bench] phase stats graph {i}: {json.dumps(row)}", file=sys.stderr, flush=True)
     os.environ.pop("GTS_WINDOW_CLOCKS", None)
     return rows
+
+
+def _transactions(g) -> int:
+    """Transactions of one simulation of an addressed graph: its tiles'
+    distinct 128-B lines (as the library expands them at upload)."""
+    ops = g.node_op.astype(np.int64)
+    has = g.node_addr != np.uint64(0xFFFFFFFFFFFFFFFF)
+    total = 0
+    for v in np.flatnonzero(has).tolist():
+        p = ops[v]
+        R = int(g.op_rows[p]) if g.op_rows is not None else 1
+        W_ = int(g.op_work[p]) // R
+        P = int(g.op_pitch[p]) if g.op_pitch is not None else W_
+        a = int(g.node_addr[v])
+        lines = set()
+        for r in range(R):
+            lines.update(range((a + r * P) // 128, (a + r * P + W_ - 1) // 128 + 1))
+        total += len(lines)
+    return total
+
+
+def txn_case_study(api, torch):
+    """Sec. 5.2's transaction-level memory on one GEMM (1024 x 1024 x 1024,
+    128 x 128 x 32 tiles, 3 stages) at Table 3's H100 with its 50 MiB L2:
+    kernel cycles under the whole-tile model (static first-touch flags, and
+    the LRU of tiles) and with tiles expanded into 128-B transactions for
+    row-major and column-major B, unpadded and with the leading dimensions
+    padded by 8 elements (rows then straddle lines), and BK = 64 (128-B
+    rows); transactions per simulation beside each."""
+    from paper_2607_11262_amd.gen import hw as H
+    from paper_2607_11262_amd.gen import workloads as W
+    rec = H.preset("H100", l2_lines=H.l2_lines(H.L2_MIB["H100"]))
+    static = H.preset("H100")
+    cases = [("whole tiles, static flags", W.gemm(1024, 1024, 1024, 128, 128, 32, 3), static),
+             ("whole tiles, LRU of tiles", W.gemm(1024, 1024, 1024, 128, 128, 32, 3, tiles=True), rec)]
+    for var in ("kn", "nk"):
+        for pad in (0, 8):
+            cases.append((f"transactions, B {var}, pad {pad}",
+                          W.gemm_addressed(1024, 1024, 1024, 128, 128, 32, 3, b_layout=var, pad=pad), rec))
+    cases.append(("transactions, B kn, BK 64", W.gemm_addressed(1024, 1024, 1024, 128, 128, 64, 3), rec))
+    out = {}
+    for label, g, r in cases:
+        res = api.simulate(api.upload(g), r[None, :], api.OUT_DIGEST)
+        torch.cuda.synchronize()
+        _, mk, st, _ = api.to_numpy(res)
+        out[label] = {"cycles": int(mk[0]), "transactions": _transactions(g) if g.node_addr is not None else None}
+    return out
 
 
 def lru_case_study(api, torch):
