@@ -70,6 +70,13 @@ constexpr uint32_t kSmallBatch = 16;  // batches this small are ordered by count
 __device__ __forceinline__ uint32_t* st_acc(uint64_t* st) { return reinterpret_cast<uint32_t*>(st); }
 __device__ __forceinline__ uint32_t* st_cnt(uint64_t* st) { return reinterpret_cast<uint32_t*>(st) + 1; }
 
+// A pointer into global memory (address space 1).
+template <typename T>
+using gmem = __attribute__((address_space(1))) T;
+
+// Four consecutive words of global memory (one 16-B load).
+__device__ __forceinline__ uint4 ld4(const gmem<const uint32_t>* p) { return make_uint4(p[0], p[1], p[2], p[3]); }
+
 // Loads of words that global atomics may change bypass the L1.
 template <typename T>
 __device__ __forceinline__ T gld(const T* p) {
@@ -279,9 +286,12 @@ struct WSim {
   // (near was full), which the local phase then scans as well.
   // rarely used pointers, from LDS (kWinPtrs)
   enum : uint32_t { kPSucc, kPIndeg, kPRoots, kPCtas, kPKernels, kPTsucc, kPTindeg, kPFrG, kPRetG, kPHw };
+  // The pointers are global-memory ones: typed so, their accesses compile to
+  // global instructions rather than flat ones (a flat access also counts
+  // against the LDS wait counter, so every later LDS wait would wait for it).
   template <typename T>
-  __device__ __forceinline__ T* cold(uint32_t i) const {
-    return reinterpret_cast<T*>(uni64(reinterpret_cast<const uint64_t*>(lds_base() + kWinPtrs)[i]));
+  __device__ __forceinline__ gmem<T>* cold(uint32_t i) const {
+    return (gmem<T>*)(uni64(reinterpret_cast<const uint64_t*>(lds_base() + kWinPtrs)[i]));
   }
 
   __device__ __forceinline__ uint64_t fr_get(uint32_t l, uint32_t i) const {
@@ -390,7 +400,10 @@ struct WSim {
               ++nn;
             } else {
               hot |= cyc < H;
-              fr_set(lane, kp, kk[q]);
+              // an entry that keeps its place is not written back: most
+              // windows move nothing, and rewriting unchanged entries
+              // dirtied the far list's lines in the L2 on every window
+              if (kp != i0 + q) fr_set(lane, kp, kk[q]);
               ++kp;
               mn = cyc < mn ? cyc : mn;
             }
@@ -539,7 +552,7 @@ struct WSim {
     return cold<const uint16_t>(kPTindeg)[t_base + (w - t_node0 - (r.cta() - t_kc0) * t_n)];
   }
   __device__ __forceinline__ void load_template(uint32_t k) {
-    const KernelDev kd = cold<const KernelDev>(kPKernels)[k];
+    const KernelDev kd = kernel_rec(k);
     run_k = k;
     t_n = uni(kd.t_n);
     t_node0 = uni(kd.node_begin);
@@ -550,12 +563,23 @@ struct WSim {
     t_nslot = uni(kd.t_ops >> 16);
   }
 
+  // kernel k's record, read as words from global memory
+  __device__ __forceinline__ KernelDev kernel_rec(uint32_t k) const {
+    static_assert(sizeof(KernelDev) == 48, "three 16-B words");
+    const gmem<const uint32_t>* p = (const gmem<const uint32_t>*)(cold<const KernelDev>(kPKernels) + k);
+    KernelDev kd;
+    uint4* d = reinterpret_cast<uint4*>(&kd);
+    d[0] = ld4(p);
+    d[1] = ld4(p + 4);
+    d[2] = ld4(p + 8);
+    return kd;
+  }
   // first and end CTA and CTA slots per SM of kernel k
   __device__ __forceinline__ void load_kernel(uint32_t k, uint32_t& k_begin, uint32_t& k_end, uint64_t& slots) const {
-    const KernelDev kd = cold<const KernelDev>(kPKernels)[k];
+    const KernelDev kd = kernel_rec(k);
     k_begin = uni(kd.cta_begin);
     k_end = uni(kd.cta_end);
-    slots = uni64(kernel_slots(kd, cold<const uint32_t>(kPHw)));
+    slots = uni64(kernel_slots(kd, (const uint32_t*)cold<const uint32_t>(kPHw)));
   }
 
   // ---- wave-cooperative dispatch at cycle t (after the retirements at t):
@@ -614,7 +638,7 @@ struct WSim {
         kstart_k = cur_k;
         kstart_t = t;
       }
-      const uint32_t* const hwc = cold<const uint32_t>(kPHw);
+      const gmem<const uint32_t>* const hwc = cold<const uint32_t>(kPHw);
       const uint64_t launch = (uint64_t)t + hwc[HW_CTALAT] + (kstart_t == t ? hwc[HW_KLAT] : 0u);
       if (launch > kMaxCycle) {
         bad |= kBadOverflow;
@@ -623,9 +647,9 @@ struct WSim {
       const uint32_t c = next_cta + lane;
       uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
       if (lane < k) {
-        const uint4* p = reinterpret_cast<const uint4*>(cold<const CtaDev>(kPCtas) + c);
-        c0 = p[0];  // node_begin, node_count, root_begin, root_count
-        c1 = p[1];  // memory nodes, first three roots
+        const gmem<const uint32_t>* p = (const gmem<const uint32_t>*)(cold<const CtaDev>(kPCtas) + c);
+        c0 = ld4(p);      // node_begin, node_count, root_begin, root_count
+        c1 = ld4(p + 4);  // memory nodes, first three roots
         *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
       }
       // zero the node state of unshared CTAs (shared ones were zeroed at start)
