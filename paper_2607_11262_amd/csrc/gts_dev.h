@@ -58,8 +58,12 @@ struct NodeDev {                // 32 B, one per node and a sentinel after the l
   uint32_t succ_begin;          // successors: succ[succ_begin, next record's succ_begin)
   uint32_t succ[kInlineSucc];   // copies of the first three successors
   uint16_t sindeg[kInlineSucc]; // and their in-degrees
-  uint16_t pad;
+  uint16_t pad;                 // template records: kRecSink on the retiring sink
 };
+// Template record flag: the CTA's retiring sink (its kernel has pad[0] = 1:
+// every node reaches this load / store over DATA / SYNC edges, so the CTA
+// retires at its finish).
+constexpr uint16_t kRecSink = 1;
 
 constexpr uint32_t kInlineRoots = 3;
 struct CtaDev {                 // 32 B, one per CTA
@@ -86,7 +90,7 @@ struct KernelDev {              // 48 B, one per kernel
   uint32_t t_base;              // first template record (and in-degree) of the kernel
   uint32_t t_ops;               // tops offset (low 16) | slots per class (high 16)
   uint32_t cluster;             // CTAs per cluster | kKernelRemote
-  uint32_t pad[3];
+  uint32_t pad[3];              // pad[0]: 1 if the template's CTAs retire with their sink
 };
 constexpr uint32_t kKernelRemote = 0x10000u;  // the kernel has REMOTE nodes
 constexpr uint32_t kMaxTops = 128;   // class x slot op entries per graph (held in LDS)

@@ -60,6 +60,7 @@ struct KTemplate {
   uint32_t t_ops = 0;   // first class x slot entry
   uint32_t nslot = 0;
   uint32_t tsucc = 0;   // first template successor
+  int32_t sink = -1;    // local index of the template's retiring sink, or -1
 };
 
 // Everything the image needs that is derived from a valid host graph.
@@ -158,6 +159,46 @@ void find_templates(const gts_graph_host* h, Derived* d) {
       for (uint32_t s = 0; s < nslot; ++s) d->tops.push_back(slot_cols[s][q]);
     for (uint32_t c = c0; c < c1; ++c) d->cclass[c] = (uint8_t)cls[c - c0];
     d->tslot.insert(d->tslot.end(), slot_of.begin(), slot_of.end());
+    // A CTA whose only node without a successor is a load / store that every
+    // other node reaches over DATA / SYNC edges retires exactly when that
+    // node finishes (each such edge starts its target no earlier than the
+    // source's finish, so the sink finishes last): the kernel then needs no
+    // per-CTA count of finished nodes.
+    {
+      const uint32_t u0 = nb[c0];
+      int32_t sink = -1;
+      bool single = true;
+      for (uint32_t i = 0; i < n; ++i)
+        if (h->succ_ptr[u0 + i + 1] == h->succ_ptr[u0 + i]) {
+          if (sink >= 0) single = false;
+          sink = (int32_t)i;
+        }
+      bool memory_sink = single && sink >= 0;
+      for (uint32_t q = 0; q < nclass && memory_sink; ++q) memory_sink = is_memory(h->op_cls[class_ops[q][sink]]);
+      if (memory_sink) {
+        // reverse reachability from the sink over DATA / SYNC edges
+        std::vector<std::vector<uint32_t>> pred(n);
+        for (uint32_t i = 0; i < n; ++i)
+          for (uint32_t e = h->succ_ptr[u0 + i]; e < h->succ_ptr[u0 + i + 1]; ++e)
+            if ((h->succ[e] >> GTS_EDGE_KIND_SHIFT) != GTS_EDGE_ORDER)
+              pred[(h->succ[e] & GTS_EDGE_TARGET_MASK) - u0].push_back(i);
+        std::vector<uint8_t> seen(n, 0);
+        std::vector<uint32_t> stack{(uint32_t)sink};
+        seen[sink] = 1;
+        uint32_t reached = 1;
+        while (!stack.empty()) {
+          const uint32_t v = stack.back();
+          stack.pop_back();
+          for (uint32_t u : pred[v])
+            if (!seen[u]) {
+              seen[u] = 1;
+              ++reached;
+              stack.push_back(u);
+            }
+        }
+        if (reached == n) t.sink = sink;
+      }
+    }
     d->n_tnodes += n;
     d->n_tsucc += h->succ_ptr[nb[c0] + n] - h->succ_ptr[nb[c0]];
   }
@@ -831,6 +872,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
     ks[k].t_n = t.t_n;
     ks[k].t_base = t.t_base;
     ks[k].t_ops = t.t_ops | t.nslot << 16;
+    ks[k].pad[0] = t.sink >= 0 ? 1u : 0u;  // retires with its sink (kKernelSinkRetire)
     bool remote = false;
     for (uint32_t v = h->cta_node_begin[ks[k].cta_begin]; v < h->cta_node_begin[ks[k].cta_end] && !remote; ++v)
       remote = h->op_cls[h->node_op[v]] == GTS_REMOTE;
@@ -861,6 +903,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
         r.succ[j] = j < deg ? ts[r.succ_begin + j] : 0u;
         r.sindeg[j] = j < deg ? nodes[u].sindeg[j] : (uint16_t)0;
       }
+      r.pad = (uint16_t)(t.sink == (int32_t)i ? gts::kRecSink : 0u);
       ti[t.t_base + i] = (uint16_t)d.indeg[u];
     }
   }

@@ -233,6 +233,7 @@ struct WSim {
   uint32_t b, lane, flags, nsm, nsub, sstride, smem_w, nslot, QF;
   bool nocont, ofin;
   bool mem_only;  // CTA bookkeeping on memory nodes only (compute nodes always feed a later memory node)
+  bool sink_ret;  // the running kernel's CTAs retire with their sink: no CTA bookkeeping at all
   // LDS
   uint4* optab;
   uint16_t* tops;  // template class x slot -> op
@@ -561,6 +562,7 @@ struct WSim {
     t_base = uni(kd.t_base);
     t_ops = uni(kd.t_ops & 0xFFFFu);
     t_nslot = uni(kd.t_ops >> 16);
+    sink_ret = uni(kd.pad[0]) != 0;
   }
 
   // kernel k's record, read as words from global memory
@@ -650,7 +652,8 @@ struct WSim {
         const gmem<const uint32_t>* p = (const gmem<const uint32_t>*)(cold<const CtaDev>(kPCtas) + c);
         c0 = ld4(p);      // node_begin, node_count, root_begin, root_count
         c1 = ld4(p + 4);  // memory nodes, first three roots
-        *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
+        if (!sink_ret)  // a CTA that retires with its sink keeps no state
+          *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
       }
       // zero the node state of unshared CTAs (shared ones were zeroed at start)
       for (uint32_t j = 0; j < k; ++j) {
@@ -848,7 +851,7 @@ struct WSim {
         }
       }
       cs[j] = make_uint4(0, 0, 0, 0);
-      if (ok[j] && !is_mem[j] && !mem_only) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
+      if (ok[j] && !is_mem[j] && !mem_only && !sink_ret) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
     }
 #pragma unroll
     for (uint32_t j = 0; j < W; ++j) {
@@ -869,7 +872,7 @@ struct WSim {
       }
       rq_push_n(ev_s[j], rdy, racc, rw);
       if (ok[j]) {
-        if (!is_mem[j] && !mem_only) {  // a compute node never completes its CTA
+        if (!is_mem[j] && !mem_only && !sink_ret) {  // a compute node never completes its CTA
           const uint32_t mf = (uint32_t)rel_f[j] > cs[j].w ? (uint32_t)rel_f[j] : cs[j].w;
           *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(cs[j].z - 1u, mf);
         }
@@ -1101,7 +1104,7 @@ struct WSim {
         }
       }
       cs[j] = make_uint4(0, 0, 0, 0);
-      if (ok[j]) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
+      if (ok[j] && !sink_ret) cs[j] = *reinterpret_cast<const uint4*>(&cst[rec[j].cta()]);
     }
 #pragma unroll
     for (uint32_t j = 0; j < W; ++j) {
@@ -1122,10 +1125,14 @@ struct WSim {
       rq_push_n(ss[j], rdy, racc, rw);
       if (ok[j]) {
         record(vv[j], tt[j], f);
-        const uint32_t left = cs[j].z - 1u;
-        const uint32_t mf = f > cs[j].w ? f : cs[j].w;
-        *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(left, mf);
-        if (left == 0) ret_push(mf, ss[j]);  // the CTA retires at its largest finish
+        if (sink_ret) {
+          if ((rec[j].b.w >> 16) & kRecSink) ret_push(f, ss[j]);  // the sink finishes last
+        } else {
+          const uint32_t left = cs[j].z - 1u;
+          const uint32_t mf = f > cs[j].w ? f : cs[j].w;
+          *reinterpret_cast<uint2*>(&cst[rec[j].cta()].left) = make_uint2(left, mf);
+          if (left == 0) ret_push(mf, ss[j]);  // the CTA retires at its largest finish
+        }
         if (needs_slow(rec[j])) release_slow(rec[j], 1u, 0, f, ss[j]);
       }
     }
@@ -1261,6 +1268,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   }
   S.run_k = 0xFFFFFFFFu;  // no CTA dispatched yet
   S.t_n = 0;
+  S.sink_ret = false;
   S.l2_av = 0;
   S.dram_av = 0;
   S.digest = 0;
