@@ -126,16 +126,17 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def workload_parts(name):
+def workload_parts(name, records=0):
     """(describe, make(i) -> (graph, hw records), count) of a workload's
-    graphs; one step simulates every graph under all of its records."""
+    graphs; one step simulates every graph under all of its records
+    (records: another record count per graph of the GEMM sweep)."""
     from paper_2607_11262_amd.gen import clusterfusion as CF
     from paper_2607_11262_amd.gen import pipelining as PL
     from paper_2607_11262_amd.gen import workloads as W
     if name == "gemm_design_sweep":
         params = W.sweep_params()
         return (lambda i: params[i],
-                lambda i: (W.sweep_graph(params[i]), W.workload_hw(name, index=i)), len(params))
+                lambda i: (W.sweep_graph(params[i]), W.workload_hw(name, B=records or None, index=i)), len(params))
     if name in NAMED:
         return (lambda i: name, lambda i: (W.workload_graph(name), W.workload_hw(name)), 1)
     if name == "pipelining":
@@ -177,13 +178,13 @@ class Plan:
     per-stream scratch budget, consecutive launches alternating over the
     streams."""
 
-    def __init__(self, api, torch, name, flags, budget, streams, dev):
-        describe, make, n = workload_parts(name)
+    def __init__(self, api, torch, name, flags, budget, streams, dev, only=-1, records=0):
+        describe, make, n = workload_parts(name, records)
         self.parts = []   # (graph handle, hw set, outputs, host graph, host hw)
         self.launches = []  # (part, first, count)
         self.flags = flags
         max_scratch = 0
-        for i in range(n):
+        for i in (range(n) if only < 0 else [only]):
             g, hw = make(i)
             dg = api.upload(g)
             hs = api.upload_hw(hw)
@@ -196,7 +197,7 @@ class Plan:
             outs = api.alloc_outputs(dg, B, flags, dev)
             self.parts.append((dg, hs, outs, g, hw))
             for first in range(0, B, chunk):
-                self.launches.append((i, first, min(chunk, B - first)))
+                self.launches.append((len(self.parts) - 1, first, min(chunk, B - first)))
             print(f"[bench] graph {i} {describe(i)} N={g.n_nodes} E={g.n_edges} B={B} chunk={chunk}",
                   file=sys.stderr, flush=True)
         self.streams = streams
@@ -386,6 +387,10 @@ def main() -> int:
                          "also with each graph uploaded from its host arrays every step")
     ap.add_argument("--phase-stats", action="store_true",
                     help="after the timed region, report the windowed kernel's per-phase counters per graph")
+    ap.add_argument("--only-graph", type=int, default=-1,
+                    help="diagnostics: simulate only this graph of the workload (index into its graphs)")
+    ap.add_argument("--records", type=int, default=0,
+                    help="diagnostics: hardware records per graph of the GEMM sweep (default 4096)")
     ap.add_argument("--calibrate-copy-gib", type=float, default=0.0,
                     help="only run a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -422,7 +427,7 @@ def main() -> int:
     flags = api.OUT_DIGEST | (api.OUT_NODES if per_node else 0)
     t_setup = time.time()
     budget = int(args.mem_budget_gb * (1 << 30)) // max(1, args.streams)
-    plan = Plan(api, torch, name, flags, budget, streams, dev)
+    plan = Plan(api, torch, name, flags, budget, streams, dev, only=args.only_graph, records=args.records)
     t_setup = time.time() - t_setup
 
     for _ in range(args.warmup):
