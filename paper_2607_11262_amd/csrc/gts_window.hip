@@ -517,7 +517,7 @@ struct WSim {
         const uint32_t cnt = (uint32_t)(sv >> 32) + 1u;
         uint32_t acc = (uint32_t)sv;
         acc = r > acc ? (uint32_t)r : acc;
-        if (ind != 1) state[w] = ((uint64_t)cnt << 32) | acc;
+        if (ind != 1 && cnt != ind) state[w] = ((uint64_t)cnt << 32) | acc;  // a readied node's state is not read again
         if (cnt == ind) rq_push(s, acc, w);
       }
     }
@@ -865,7 +865,8 @@ struct WSim {
         const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
         uint32_t acc = (uint32_t)sv[j][k];
         acc = r > acc ? (uint32_t)r : acc;
-        if (sel[j][k] && rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
+        // the release that readies a node is its last: its state is not read again
+        if (sel[j][k] && rec[j].sindeg(k) != 1 && cnt != rec[j].sindeg(k)) state[w] = ((uint64_t)cnt << 32) | acc;
         rdy[k] = sel[j][k] && cnt == rec[j].sindeg(k);
         racc[k] = acc;
         rw[k] = w;
@@ -1117,7 +1118,8 @@ struct WSim {
         const uint32_t cnt = (uint32_t)(sv[j][k] >> 32) + 1u;
         uint32_t acc = (uint32_t)sv[j][k];
         acc = f > acc ? f : acc;
-        if (sel[j][k] && rec[j].sindeg(k) != 1) state[w] = ((uint64_t)cnt << 32) | acc;
+        // the release that readies a node is its last: its state is not read again
+        if (sel[j][k] && rec[j].sindeg(k) != 1 && cnt != rec[j].sindeg(k)) state[w] = ((uint64_t)cnt << 32) | acc;
         rdy[k] = sel[j][k] && cnt == rec[j].sindeg(k);
         racc[k] = acc;
         rw[k] = w;
@@ -1342,7 +1344,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
             S.w_key[dp + lanes_below(bd, lane)] = k;
         }
         if (keep) {
-          S.ret_set(kp + lanes_below(bk, lane), k);
+          const uint32_t dst = kp + lanes_below(bk, lane);
+          if (dst != i) S.ret_set(dst, k);  // an entry that keeps its place is not rewritten
           kmin = (uint32_t)(k >> 32) < kmin ? (uint32_t)(k >> 32) : kmin;
         }
         dp += (uint32_t)__popcll(bd);
