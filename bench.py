@@ -240,6 +240,13 @@ class Plan:
                 s0.wait_event(e)
             z.record(s0)
             step_ev.append((a, z))
+        # every step is enqueued; wait for them one by one so that a long
+        # region still reports progress (the host only waits: the GPU's
+        # timing is unaffected)
+        for k, (_, z) in enumerate(step_ev):
+            z.synchronize()
+            print(f"[bench] step {k + 1}/{steps} done at {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+                  flush=True)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         return ([a.elapsed_time(z) * 1e-3 for a, z in step_ev], [a.elapsed_time(z) * 1e-3 for a, z in launch_ev],
@@ -430,8 +437,10 @@ def main() -> int:
     plan = Plan(api, torch, name, flags, budget, streams, dev, only=args.only_graph, records=args.records)
     t_setup = time.time() - t_setup
 
-    for _ in range(args.warmup):
+    for k in range(args.warmup):
         plan.step(api, torch)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup step {k + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     step_s, launch_s, wall = plan.timed(api, torch, args.steps)
     node_sims, sims, abytes, infeasible = plan.step_totals(per_node)
     K = args.steps
@@ -454,6 +463,8 @@ def main() -> int:
         # the same steps with digest outputs only (no per-node cycles written)
         for _ in range(args.warmup):
             plan.step(api, torch, flags=api.OUT_DIGEST)
+        torch.cuda.synchronize()
+        print("[bench] digest-only pass", file=sys.stderr, flush=True)
         d_step, d_launch, d_wall = plan.timed(api, torch, K, flags=api.OUT_DIGEST)
         nb = sum(int(f.sum()) * (alg_bytes_per_sim(p[3], False) - 16) + 16 * p[4].shape[0]
                  for f, p in zip(plan.feasible(), plan.parts))
