@@ -152,8 +152,8 @@ struct SimLayout {
   uint64_t off_rp;      // windowed kernel: later ready entries beyond LDS, [kPoolSpill][64] u64
   uint64_t off_mq;      // windowed kernel: memory-arrival rings, [kWinMaxSm][kRing] x 3 u32
   uint64_t off_ret;     // windowed kernel: pending retirements beyond LDS (u64 each)
-  uint64_t off_lru;     // general kernel: LRU L2, latest access stamp per tile or line ([keys] u32)
-  uint64_t off_lru_bit; // general kernel: LRU L2, Fenwick tree of lines over stamps ([accesses + 1] u64)
+  uint64_t off_lru;     // LRU L2: latest access stamp per tile or line ([keys] u32)
+  uint64_t off_lru_bit; // LRU L2: Fenwick tree of lines over stamps ([accesses + 1] u64)
   uint64_t pend_cap;
   uint64_t stride;      // bytes per simulation (multiple of kAlign)
 };
@@ -171,6 +171,7 @@ constexpr uint32_t kRetireLds = 0;     // pending CTA retirements held in LDS (n
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
 constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
 constexpr uint32_t kWindowMax = 1024;  // longest window, in cycles
+constexpr uint64_t kWinMaxTileLines = 1ull << 22;  // LRU L2: lines of a tile the windowed kernel takes (below)
 constexpr int32_t kStatusRetry = 0x52455452;  // rerun this simulation on the general kernel
 constexpr uint64_t kStatsBytes = 128;          // windowed-kernel counters at the end of a slice
 
@@ -199,7 +200,8 @@ struct Launch {
 // kernel addresses without registers; then the parts sized by the batch.
 // NS: largest n_sm of the batch; SS: server words per SM (server_stride at
 // the largest n_subpart); QP: later ready entries per lane held in LDS; NT:
-// template class x slot op entries (u16).
+// template class x slot op entries (u16); LRU: the graph's loads / stores name
+// tiles (one word per memory-batch position for the LRU decisions).
 constexpr uint32_t kWinNrCnt = 0, kWinFrCnt = 64, kWinFrMin = 128, kWinFrHot = 192;
 constexpr uint32_t kWinRetCnt = 256, kWinRetMin = 257;
 constexpr uint32_t kWinNr = 258;
@@ -226,10 +228,11 @@ static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinS
               "64-bit arrays on even words");
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
 struct WinLds {
-  uint32_t optab, tops, srv, mq_head, mq_pos, fr;
+  uint32_t optab, tops, srv, mq_head, mq_pos, fr, lru;
   uint32_t total;
 };
-__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP, uint32_t NT) {
+__host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP, uint32_t NT,
+                                          bool LRU) {
   WinLds L;
   uint32_t o = kWinFixed;
   auto take = [&o](uint32_t words, bool wide) {
@@ -244,6 +247,7 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, 
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
   L.fr = take(2u * 64u * QP, true);
+  L.lru = take(LRU ? kWinCap : 0u, false);
   L.total = o;
   return L;
 }

@@ -26,6 +26,7 @@ struct gts_graph {
   gts::Image img;
   uint64_t bytes;
   uint32_t max_cta_nodes, max_outdeg;
+  uint64_t max_tile_lines;
 };
 
 struct gts_hwset {
@@ -74,6 +75,7 @@ struct Derived {
   std::vector<uint16_t> tops;    // class x slot -> op
   uint32_t n_tnodes = 0, n_tsucc = 0;
   uint32_t n_tiles = 0;          // distinct tiles named by loads / stores
+  uint64_t max_tile_lines = 0;   // the most lines of any of them
   // transaction-level memory: node v's lines txn_line[txn_ptr[v] ..
   // txn_ptr[v + 1]), numbered densely in order of first use
   std::vector<uint32_t> txn_ptr, txn_line;
@@ -275,6 +277,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   }
   // tiles: only loads / stores, one line count per tile
   uint32_t n_tiles = 0;
+  uint64_t max_tile_lines = 0;
   if (h->node_tile) {
     std::unordered_map<uint32_t, uint64_t> lines;
     for (uint32_t v = 0; v < N; ++v) {
@@ -284,6 +287,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
       if (!is_memory(h->op_cls[p])) return fail(GTS_E_RANGE, "node %u is not a load or store but names tile %u", v, t);
       // 64-bit, as in the kernels and the oracle: work near 2^32 must not wrap
       const uint64_t n = ((uint64_t)h->op_work[p] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES;
+      max_tile_lines = std::max(max_tile_lines, n);
       auto it = lines.emplace(t, n).first;
       if (it->second != n)
         return fail(GTS_E_RANGE, "tile %u is touched with %llu and with %llu lines (node %u)", t,
@@ -412,6 +416,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   }
   for (uint32_t k = 0; k < K; ++k) clusters |= cluster_of(h, k) > 1;
   d->n_tiles = n_tiles;
+  d->max_tile_lines = max_tile_lines;
   d->txn_ptr.clear();
   d->txn_line.clear();
   d->n_lines = 0;
@@ -512,18 +517,19 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t keys, uin
   off = align_up(off + s.pend_cap * 12, gts::kAlign);
   s.off_optab = off;
   off = align_up(off + (uint64_t)P * 16, gts::kAlign);
+  // The windowed kernel's per-SM queues overlay the general kernel's pending
+  // list and op table (a simulation the windowed kernel hands back is
+  // restarted from scratch by the general kernel); both kernels use the LRU
+  // state, which follows.
+  s.off_rp = s.off_pend;
+  s.off_mq = align_up(s.off_rp + 8ull * gts::kPoolSpill * 64, gts::kAlign);
+  s.off_ret = align_up(s.off_mq + 12ull * gts::kRing * gts::kWinMaxSm, gts::kAlign);
+  off = std::max(off, align_up(s.off_ret + 8ull * (gts::kRetireCap - gts::kRetireLds), gts::kAlign));
   s.off_lru = off;
   off = align_up(off + (uint64_t)keys * 4, gts::kAlign);
   s.off_lru_bit = off;
   off = align_up(off + (keys ? ((uint64_t)accesses + 1) * 8 : 0u), gts::kAlign);
-  // The windowed kernel's per-SM queues overlay the general kernel's pending
-  // list (a simulation the windowed kernel hands back is restarted from
-  // scratch by the general kernel).
-  s.off_rp = s.off_pend;
-  s.off_mq = align_up(s.off_rp + 8ull * gts::kPoolSpill * 64, gts::kAlign);
-  s.off_ret = align_up(s.off_mq + 12ull * gts::kRing * gts::kWinMaxSm, gts::kAlign);
-  const uint64_t ret_end = align_up(s.off_ret + 8ull * (gts::kRetireCap - gts::kRetireLds), gts::kAlign);
-  s.stride = std::max(off, ret_end) + gts::kStatsBytes;
+  s.stride = off + gts::kStatsBytes;
   return s;
 }
 
@@ -648,8 +654,11 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
+  // tiles (LRU L2): the memory phase packs a tile's line count into 22 bits
+  const bool lru = (g->img.props & gts::kGraphTiles) != 0;
   bool windowed = (g->img.props & need_props) == need_props &&
-                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTiles | gts::kGraphTxn)) &&
+                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTxn)) &&
+                  (!lru || g->max_tile_lines < gts::kWinMaxTileLines) &&
                   g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
@@ -660,7 +669,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // slower even for batches that fill only part of the chip.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) {
-      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops).total;
+      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops, lru).total;
     };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
     uint32_t want = kWavesPerCu;
@@ -946,6 +955,7 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.n_tops = (uint32_t)d.tops.size();
   g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
   g->img.n_tiles = d.n_tiles;
+  g->max_tile_lines = d.max_tile_lines;
   const bool txn = !d.txn_line.empty();
   g->img.txn_ptr = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_ptr) : nullptr;
   g->img.txn_line = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_line) : nullptr;

@@ -8,7 +8,8 @@
 //   T = a lower bound of the earliest pending event;  H = T + min(Lm, 1024),
 //       where Lm is the smallest possible delay from a memory arrival to its
 //       completion (min over the graph's memory ops of L2/DRAM occupancy +
-//       latency);
+//       latency, over both servers for graphs whose tiles go through the LRU
+//       L2);
 //   retirement phase: every CTA retirement with cycle < H, in cycle order,
 //       each distinct cycle followed by dispatch (wave-cooperative);
 //   local phase: every lane issues its SMs' ready nodes with cycle < H in
@@ -17,9 +18,12 @@
 //       engine and queue an arrival at their engine start;
 //   memory phase: the arrivals with cycle < H from all SMs are sorted by
 //       (cycle, node id) (a bitonic network across the wave; a few keys by
-//       counting ranks), served by the chip-wide L2 and DRAM FIFO servers through a max-plus
-//       prefix scan, and completed by the lane that owns their SM (CTA
-//       bookkeeping, release of out-edges).
+//       counting ranks), sent to the L2 or DRAM by their op's flag or, for a
+//       tile access on a machine with an LRU L2, by LRU decisions taken for
+//       the whole batch in that order (LRU kernels), served by the chip-wide
+//       L2 and DRAM FIFO servers through a max-plus prefix scan, and
+//       completed by the lane that owns their SM (CTA bookkeeping, release of
+//       out-edges).
 //
 // Why this equals the one-event-at-a-time order of the general kernel and of
 // the CPU oracle: an arrival at s >= T completes no earlier than s + Lm >= H,
@@ -226,7 +230,7 @@ __device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][kGq<NB>]
 extern __shared__ uint32_t win_lds_words[];
 __device__ __forceinline__ uint32_t* lds_base() { return win_lds_words; }
 
-template <uint32_t NB>
+template <uint32_t NB, bool LRU>
 struct WSim {
   Image G;
   const uint32_t* hw;
@@ -258,6 +262,16 @@ struct WSim {
   // first template record, class x slot table offset and slots per class
   uint32_t run_k, t_n, t_node0, t_kc0, t_nc, t_base, t_ops, t_nslot;
   uint64_t l2_av, dram_av, Lm, Hnear;
+  // LRU L2 (LRU only): each tile's latest access stamp (a count of tile
+  // accesses, 0 = never; scratch), a Fenwick tree over stamps holding at each
+  // tile's latest stamp its line count (scratch, entry 0 unused), one LDS
+  // word per memory-batch position; the stamps handed out so far, the lines
+  // of every tile touched so far, the L2's lines, the bound on stamps
+  gmem<uint32_t>* lru_last;
+  gmem<uint64_t>* lru_bit;
+  uint32_t* lw;
+  uint32_t lru_now, l2_lines, lru_acc;
+  uint64_t lru_total;
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
@@ -892,7 +906,6 @@ struct WSim {
   template <uint32_t E>
   __device__ __forceinline__ void sort_batch(uint32_t M, uint64_t (&k)[E], uint32_t (&sl)[E]) {
     static_assert(E == 1 || E == 2 || E == 4, "64, 128 or 256 positions");
-    constexpr uint32_t n = 64u * E;
     if (M <= kSmallBatch) {
       // few keys (one SM's arrivals, say): count each key's rank across the
       // lanes and pick, for each position, the key of that rank
@@ -925,6 +938,14 @@ struct WSim {
       k[r] = s < M ? w_key[s] : kNoKey;
       sl[r] = s;  // distinct, so every comparison is strict
     }
+    bitonic<E>(k, sl);
+  }
+  // Bitonic network over the wave's 64 * E (key, tag) pairs, ordered by key,
+  // then tag (distinct tags make every comparison strict): position
+  // lane * E + r ends with the pair of that rank.
+  template <uint32_t E, bool kTags = true>
+  __device__ __forceinline__ void bitonic(uint64_t (&k)[E], uint32_t (&sl)[E]) const {
+    constexpr uint32_t n = 64u * E;
 #pragma unroll
     for (uint32_t kk = 2; kk <= n; kk <<= 1) {
 #pragma unroll
@@ -935,13 +956,13 @@ struct WSim {
             const int lj = (int)(j / E);
             const uint64_t pk = ((uint64_t)(uint32_t)__shfl_xor((int)(uint32_t)(k[r] >> 32), lj, 64) << 32) |
                                 (uint32_t)__shfl_xor((int)(uint32_t)k[r], lj, 64);
-            const uint32_t ps = (uint32_t)__shfl_xor((int)sl[r], lj, 64);
+            const uint32_t ps = kTags ? (uint32_t)__shfl_xor((int)sl[r], lj, 64) : 0u;
             const uint32_t i = lane * E + r;
             const bool keep_min = ((i & j) == 0) == ((i & kk) == 0);
-            const bool pless = pk < k[r] || (pk == k[r] && ps < sl[r]);
+            const bool pless = pk < k[r] || (kTags && pk == k[r] && ps < sl[r]);
             const bool take = keep_min == pless;
             k[r] = take ? pk : k[r];
-            sl[r] = take ? ps : sl[r];
+            if (kTags) sl[r] = take ? ps : sl[r];
           }
         } else {
 #pragma unroll
@@ -949,14 +970,16 @@ struct WSim {
             if ((r & j) != 0) continue;  // r is the lower position of its pair
             const uint32_t q = r | j, i = lane * E + r;
             const bool up = (i & kk) == 0;
-            const bool qless = k[q] < k[r] || (k[q] == k[r] && sl[q] < sl[r]);
+            const bool qless = k[q] < k[r] || (kTags && k[q] == k[r] && sl[q] < sl[r]);
             const bool sw = up == qless;
             const uint64_t tk = k[r];
             const uint32_t ts = sl[r];
             k[r] = sw ? k[q] : k[r];
-            sl[r] = sw ? sl[q] : sl[r];
             k[q] = sw ? tk : k[q];
-            sl[q] = sw ? ts : sl[q];
+            if (kTags) {
+              sl[r] = sw ? sl[q] : sl[r];
+              sl[q] = sw ? ts : sl[q];
+            }
           }
         }
       }
@@ -974,6 +997,151 @@ struct WSim {
     wsync();
   }
 
+  // ---- LRU L2 (tiles): a load / store that names a tile hits iff the tile
+  // was touched before and its lines plus those of the distinct tiles touched
+  // since fit the L2 (then the L2 server takes it, else DRAM); the tile
+  // becomes the most recent.  Decided here for the whole memory batch, in its
+  // (cycle, id) order, from the state before the batch and the batch itself.
+  // For the arrival at sorted position i, of tile x with stamp q before the
+  // batch, the distinct tiles touched since x's last access are
+  //  * x also at earlier positions, the latest j: the tiles at positions
+  //    (j, i), each counted at its first position after j;
+  //  * else (q = 0: never touched, a miss): the tiles whose stamp before the
+  //    batch follows q -- the tree's total minus its prefix sum to q -- and
+  //    the tiles at positions before i (counted at their first position in
+  //    the batch) whose stamp before it was at most q (the others are in the
+  //    tree's part already).
+  // The batch's tiles then move to stamps following every earlier one, in
+  // position order: each tile's entry moves from its old stamp to the stamp
+  // of its last position.  The positions' tiles sort by (tile, position) to
+  // find each one's previous and next position of the same tile.  LDS per
+  // position i: w_fin[i] = stamp before the batch, lw[i] = lines | (previous
+  // position + 1) << 22 | (a later position follows) << 31.
+  __device__ __forceinline__ uint64_t fen_prefix(uint32_t q) const {
+    uint64_t s = 0;
+    while (q) {  // up to eight tree nodes per round trip; entry 0 holds 0
+      uint64_t v[8];
+#pragma unroll
+      for (uint32_t u = 0; u < 8; ++u) {
+        v[u] = __hip_atomic_load(lru_bit + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        q &= q - 1u;
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < 8; ++u) s += v[u];
+    }
+    return s;
+  }
+  __device__ __forceinline__ void fen_add(uint32_t u, uint64_t d) const {
+    for (; u != 0u && u <= lru_acc; u += u & (0u - u))
+      __hip_atomic_fetch_add(lru_bit + u, d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  template <uint32_t E>
+  __device__ __forceinline__ void lru_batch(const uint64_t (&k)[E], const uint32_t (&p)[E], uint4 (&od)[E]) {
+    constexpr uint32_t kLines = (1u << 22) - 1u, kLater = 1u << 31;
+    const gmem<const uint32_t>* tile = (const gmem<const uint32_t>*)G.tile;
+    const gmem<const OpDev>* ops = (const gmem<const OpDev>*)G.ops;
+    uint32_t x[E], n[E], q[E], wk[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      x[r] = GTS_NO_TILE;
+      wk[r] = 0;
+      if (k[r] != kNoKey) {
+        x[r] = tile[(uint32_t)k[r] & GTS_EDGE_TARGET_MASK];
+        wk[r] = ops[w_aux[p[r]] & 0xFFFFu].work;
+      }
+    }
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      const bool t = x[r] != GTS_NO_TILE;
+      q[r] = t ? lru_last[x[r]] : 0u;
+      n[r] = t ? (uint32_t)(((uint64_t)wk[r] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES) : 0u;
+    }
+    uint64_t tk[E];
+    uint32_t unused[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      const uint32_t i = lane * E + r;
+      w_fin[i] = q[r];
+      lw[i] = n[r];
+      tk[r] = ((uint64_t)x[r] << 32) | i;  // distinct keys: no tags
+    }
+    bitonic<E, false>(tk, unused);
+    wsync();
+    // previous / next position of the same tile: the neighbours in (tile,
+    // position) order (untracked positions sort last and are skipped)
+    {
+      const uint64_t before = __shfl_up(tk[E - 1], 1, 64), after = __shfl_down(tk[0], 1, 64);
+#pragma unroll
+      for (uint32_t r = 0; r < E; ++r) {
+        const uint32_t xt = (uint32_t)(tk[r] >> 32);
+        const uint64_t pk = r > 0 ? tk[r - 1] : before, nk = r + 1 < E ? tk[r + 1] : after;
+        const bool has_prev = (lane > 0 || r > 0) && (uint32_t)(pk >> 32) == xt;
+        const bool has_next = (lane < 63 || r + 1 < E) && (uint32_t)(nk >> 32) == xt;
+        if (xt != GTS_NO_TILE)
+          atomicOr(&lw[(uint32_t)tk[r]], (has_prev ? ((uint32_t)pk + 1u) << 22 : 0u) | (has_next ? kLater : 0u));
+      }
+    }
+    wsync();
+    uint64_t above[E];
+    bool seen[E];
+    uint32_t word[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      const uint32_t i = lane * E + r;
+      word[r] = lw[i];
+      const uint32_t j1 = (word[r] >> 22) & 511u;  // previous position + 1
+      uint64_t a = 0;
+      seen[r] = x[r] != GTS_NO_TILE && (j1 != 0u || q[r] != 0u);
+      if (x[r] != GTS_NO_TILE && j1 != 0u) {
+#pragma unroll 8
+        for (uint32_t t = j1; t < i; ++t) {
+          const uint32_t wt = lw[t];
+          a += ((wt >> 22) & 511u) <= j1 ? (wt & kLines) : 0u;
+        }
+      } else if (x[r] != GTS_NO_TILE && q[r] != 0u) {
+#pragma unroll 8
+        for (uint32_t t = 0; t < i; ++t) {
+          const uint32_t wt = lw[t];
+          a += ((wt >> 22) & 511u) == 0u && w_fin[t] <= q[r] ? (wt & kLines) : 0u;
+        }
+      }
+      above[r] = a;
+    }
+    mem_wait();  // the previous batch's tree updates are done
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r)
+      if (x[r] != GTS_NO_TILE && ((word[r] >> 22) & 511u) == 0u && q[r] != 0u)
+        above[r] += lru_total - fen_prefix(q[r]);
+    // stamps in position order; a tile's last position moves its tree entry
+    uint32_t c = 0;
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) c += x[r] != GTS_NO_TILE ? 1u : 0u;
+    const uint32_t incl = wave_incl_sum_u32(c);
+    uint32_t st = lru_now + incl - c;
+    uint32_t fresh = 0;
+    const gmem<const uint32_t>* hw_w = cold<const uint32_t>(kPHw);
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      if (x[r] == GTS_NO_TILE) continue;
+      ++st;
+      if (!(word[r] & kLater)) {
+        if (q[r] != 0u)
+          fen_add(q[r], (uint64_t)0 - n[r]);
+        else
+          fresh += n[r];
+        fen_add(st, n[r]);
+        lru_last[x[r]] = st;
+      }
+      const bool dram = !(seen[r] && above[r] + n[r] <= (uint64_t)l2_lines);
+      od[r].y = clamp_occ(cdiv64((uint64_t)wk[r] * 65536ull, hw_w[HW_RATE + (dram ? R_DRAM : R_L2)]));
+      od[r].z = hw_w[HW_LAT + (dram ? L_DRAM : L_L2)];
+      od[r].w = (od[r].w & ~8u) | (dram ? 8u : 0u);
+    }
+    lru_now += lane_u32(incl, 63);
+    lru_total += wave_sum_u32(fresh);
+    wsync();
+  }
+
   // ---- memory phase, E arrivals per lane: sort w_key[0, M) by (cycle, id),
   // serve them in that order, then complete them on their SMs' lanes.
   template <uint32_t E>
@@ -983,13 +1151,16 @@ struct WSim {
     uint64_t k[E];
     uint32_t p[E];
     sort_batch<E>(M, k, p);
-    Compose fl2{kNegCycle, 0}, fdr{kNegCycle, 0};
     uint4 od[E];
 #pragma unroll
+    for (uint32_t r = 0; r < E; ++r) od[r] = k[r] != kNoKey ? optab[w_aux[p[r]] & 0xFFFFu] : make_uint4(0, 0, 0, 0);
+    if constexpr (LRU) {
+      if (l2_lines) lru_batch<E>(k, p, od);
+    }
+    Compose fl2{kNegCycle, 0}, fdr{kNegCycle, 0};
+#pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
-      od[r] = make_uint4(0, 0, 0, 0);
       if (k[r] != kNoKey) {
-        od[r] = optab[w_aux[p[r]] & 0xFFFFu];
         const Compose g{(int64_t)(k[r] >> 32), (int64_t)od[r].y};
         if ((od[r].w >> 3) & 1u)
           fdr = compose(fdr, g);
@@ -1143,12 +1314,12 @@ struct WSim {
 };
 
 
-template <uint32_t NB>
+template <uint32_t NB, bool LRU>
 __device__ __forceinline__ void window_body(const Launch& L) {
   const uint32_t b = blockIdx.x;
   if (b >= L.B) return;
   uint32_t* const lds = lds_base();
-  WSim<NB> S;
+  WSim<NB, LRU> S;
   S.G = L.img;
   S.hw = L.hw + (uint64_t)b * HW_WORDS;
   S.b = b;
@@ -1168,7 +1339,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
-  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops);
+  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops, LRU);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.tops = reinterpret_cast<uint16_t*>(lds + W.tops);
   S.srv = lds + W.srv;
@@ -1224,6 +1395,13 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (cls == C_GLOAD || cls == C_GSTORE) {
       const uint64_t d = (uint64_t)e.y + e.z;
       lm = d < lm ? d : lm;
+      if constexpr (LRU) {  // a tile access may take either server
+        const bool other_dram = ((e.w >> 3) & 1u) == 0u;
+        const uint64_t d2 = (uint64_t)clamp_occ(cdiv64((uint64_t)S.G.ops[q].work * 65536ull,
+                                                        S.hw[HW_RATE + (other_dram ? R_DRAM : R_L2)])) +
+                            S.hw[HW_LAT + (other_dram ? L_DRAM : L_L2)];
+        lm = d2 < lm ? d2 : lm;
+      }
     }
   }
   lm = wmin64(lm);
@@ -1242,6 +1420,19 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   if (lane == 0) {
     *S.ret_cnt = 0;
     *S.ret_min = 0xFFFFFFFFu;
+  }
+  if constexpr (LRU) {
+    S.l2_lines = S.hw[HW_L2_LINES];
+    S.lru_last = (gmem<uint32_t>*)(sim + L.layout.off_lru);
+    S.lru_bit = (gmem<uint64_t>*)(sim + L.layout.off_lru_bit);
+    S.lw = lds + W.lru;
+    S.lru_acc = S.G.n_nodes;  // at most one tile access per node
+    S.lru_now = 0;
+    S.lru_total = 0;
+    if (S.l2_lines) {
+      for (uint32_t x = lane; x < S.G.n_tiles; x += 64) S.lru_last[x] = 0u;
+      for (uint32_t i = lane; i <= S.lru_acc; i += 64) S.lru_bit[i] = 0ull;
+    }
   }
   if (S.G.props & kGraphHasShared) {
     for (uint32_t c = lane; c < S.G.n_ctas; c += 64) {
@@ -1283,6 +1474,9 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   // phase clocks only on request: reading the clock waits for every
   // outstanding scalar and LDS access
   const bool clk = L.clocks != 0;
+  // memory arrivals per window: the LRU decisions keep registers for half
+  // the batch positions
+  constexpr uint32_t kMemCap = LRU ? kWinCap / 2 : kWinCap;
   S.dispatch(0);
   wsync();
   while (!__ballot(S.bad != 0)) {
@@ -1409,7 +1603,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     constexpr uint32_t GQ = kGq<NB>;
     // Up to GQ head entries of each SM whose head may be below H0 are loaded;
     // K is lowered so that every due arrival is among them, and so that at
-    // most kWinCap are due -- the rest, possibly of the same cycle, wait for
+    // most kMemCap are due -- the rest, possibly of the same cycle, wait for
     // the next window (they complete after it starts, and no arrival of a
     // cycle below H0 can still appear).
     uint32_t M = 0;
@@ -1443,18 +1637,18 @@ __device__ __forceinline__ void window_body(const Launch& L) {
       }
       uint64_t K = wmin64(Kl);
       M = wave_sum_u32(due_count(ehi, elo, K));
-      if (M > kWinCap) {
-        // keep at most kWinCap: the largest cycle boundary that does (a
+      if (M > kMemCap) {
+        // keep at most kMemCap: the largest cycle boundary that does (a
         // window spans at most 1024 cycles: a few halvings), or, when cycle T
         // alone holds more, a boundary between the keys of cycle T
-        const uint64_t Kmax = K;  // count(< Kmax) > kWinCap
+        const uint64_t Kmax = K;  // count(< Kmax) > kMemCap
         uint64_t lo = T, hi = Kmax >> 32;  // cycles; count(< T << 32) = 0
-        if (wave_sum_u32(due_count(ehi, elo, hi << 32)) <= kWinCap) {
+        if (wave_sum_u32(due_count(ehi, elo, hi << 32)) <= kMemCap) {
           lo = hi;
         } else {
           while (hi - lo > 1) {
             const uint64_t mid = lo + (hi - lo) / 2;
-            if (wave_sum_u32(due_count(ehi, elo, mid << 32)) <= kWinCap)
+            if (wave_sum_u32(due_count(ehi, elo, mid << 32)) <= kMemCap)
               lo = mid;
             else
               hi = mid;
@@ -1462,11 +1656,11 @@ __device__ __forceinline__ void window_body(const Launch& L) {
         }
         K = lo << 32;
         if (lo == T) {
-          uint64_t klo = T << 32, khi = (T + 1) << 32;  // count(< khi) > kWinCap
+          uint64_t klo = T << 32, khi = (T + 1) << 32;  // count(< khi) > kMemCap
           khi = Kmax < khi ? Kmax : khi;
           while (khi - klo > 1) {
             const uint64_t mid = klo + (khi - klo) / 2;
-            if (wave_sum_u32(due_count(ehi, elo, mid)) <= kWinCap)
+            if (wave_sum_u32(due_count(ehi, elo, mid)) <= kMemCap)
               klo = mid;
             else
               khi = mid;
@@ -1513,7 +1707,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (M) {
       if (M <= 64)
         S.template memory_phase<1>(M);
-      else if (M <= 128)
+      else if (LRU || M <= 128)
         S.template memory_phase<2>(M);
       else
         S.template memory_phase<4>(M);
@@ -1583,22 +1777,27 @@ __device__ __forceinline__ void window_body(const Launch& L) {
 
 }  // namespace
 
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window1(Launch L) { window_body<1>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window2(Launch L) { window_body<2>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window3(Launch L) { window_body<3>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window4(Launch L) { window_body<4>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window1(Launch L) { window_body<1, false>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window2(Launch L) { window_body<2, false>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window3(Launch L) { window_body<3, false>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window4(Launch L) { window_body<4, false>(L); }
+// graphs whose loads / stores name tiles (LRU L2): held to three waves per
+// SIMD, as the others (a few registers spill at three and four SMs per
+// lane; measured faster than two waves per SIMD without spills)
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_lru(Launch L) { window_body<1, true>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_lru(Launch L) { window_body<2, true>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L) { window_body<3, true>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L) { window_body<4, true>(L); }
 
 hipError_t launch_window(const Launch& L, uint32_t lds_bytes, hipStream_t stream) {
   if (L.B == 0) return hipSuccess;
   const uint32_t nb = (L.max_nsm + 63) / 64;
-  if (nb <= 1)
-    hipLaunchKernelGGL(gts_sim_window1, dim3(L.B), dim3(64), lds_bytes, stream, L);
-  else if (nb == 2)
-    hipLaunchKernelGGL(gts_sim_window2, dim3(L.B), dim3(64), lds_bytes, stream, L);
-  else if (nb == 3)
-    hipLaunchKernelGGL(gts_sim_window3, dim3(L.B), dim3(64), lds_bytes, stream, L);
-  else
-    hipLaunchKernelGGL(gts_sim_window4, dim3(L.B), dim3(64), lds_bytes, stream, L);
+  const bool lru = (L.img.props & kGraphTiles) != 0;
+  void (*const plain[4])(Launch) = {gts_sim_window1, gts_sim_window2, gts_sim_window3, gts_sim_window4};
+  void (*const tiled[4])(Launch) = {gts_sim_window1_lru, gts_sim_window2_lru, gts_sim_window3_lru,
+                                    gts_sim_window4_lru};
+  const uint32_t i = nb <= 1 ? 0u : nb >= 4 ? 3u : nb - 1u;
+  hipLaunchKernelGGL(lru ? tiled[i] : plain[i], dim3(L.B), dim3(64), lds_bytes, stream, L);
   return hipGetLastError();
 }
 

@@ -2,8 +2,9 @@
 
 The windowed kernel takes a graph when every node without a successor in its
 own CTA is a global load or store, every edge between CTAs leaves a load or
-store and is a DATA or SYNC edge, out-degrees stay below 0xFFFF, and no
-kernel has clusters or tiles.  These graphs meet that and otherwise vary what
+store and is a DATA or SYNC edge, out-degrees stay below 0xFFFF, no kernel
+has clusters, no load / store has a byte address, and every named tile
+(LRU L2) has fewer than 2^22 lines.  These graphs meet that and otherwise vary what
 the kernel has to get right: 1-4 kernels of 1-32 warps, CTAs of a few to
 several dozen nodes of every class (zero-work nodes included), all three
 edge kinds inside a CTA, fan-outs beyond the three successors a node record
@@ -14,8 +15,8 @@ a later kernel), whose targets then have in-edges from several CTAs.
 the generator without the library's internals."""
 import numpy as np
 
-from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, MISS, ORDER, SFU, SMEM, SYNC, SYNC_EDGE, TENSOR,
-                                             GraphBuilder)
+from paper_2607_11262_amd.gen.graph import (ALU, DATA, GLOAD, GSTORE, LINE_BYTES, MISS, NO_ADDR, NO_TILE, ORDER, SFU,
+                                             SMEM, SYNC, SYNC_EDGE, TENSOR, GraphBuilder)
 from paper_2607_11262_amd.gen import hw as H
 
 MEM = (GLOAD, GSTORE)
@@ -83,9 +84,16 @@ def windowed_graph(rng, n_kernels=(1, 4), ctas=(1, 12), nodes=(1, 40), cross_p=8
 
 def window_eligible(g) -> bool:
     """The windowed kernel's graph conditions, written out."""
-    if g.n_nodes == 0 or g.node_tile is not None or np.any(np.asarray(g.kernel_cluster) > 1):
+    if g.n_nodes == 0 or np.any(np.asarray(g.kernel_cluster) > 1):
+        return False
+    if getattr(g, "node_addr", None) is not None and np.any(np.asarray(g.node_addr) != NO_ADDR):
         return False
     cls = np.asarray(g.op_cls)[np.asarray(g.node_op, np.int64)]
+    if g.node_tile is not None:
+        named = np.asarray(g.node_tile) != NO_TILE
+        work = np.asarray(g.op_work, np.int64)[np.asarray(g.node_op, np.int64)]
+        if np.any(named & (-(-work // LINE_BYTES) >= 1 << 22)):
+            return False
     if np.any(cls == 7):  # REMOTE
         return False
     cta = np.repeat(np.arange(len(g.cta_node_begin) - 1), np.diff(np.asarray(g.cta_node_begin, np.int64)))
