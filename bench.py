@@ -382,6 +382,8 @@ def main() -> int:
                     help="named workloads other than the sweep: skip the second, digest-only timed region")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="bounded CPU-oracle sample length")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-case-study", action="store_true",
+                    help="skip a study workload's case-study table (its launches would join a counter profile)")
     ap.add_argument("--mem-budget-gb", type=float, default=220.0,
                     help="device scratch budget, split evenly over the streams")
     ap.add_argument("--streams", type=int, default=2,
@@ -531,16 +533,17 @@ def main() -> int:
     }
     if digest_only is not None:
         out["digest_only"] = digest_only
-    if name == "pipelining":
+    if name == "pipelining" and not args.no_case_study:
         out["case_study"] = case_study(api, torch)
-    if name == "noc":
+    if name == "noc" and not args.no_case_study:
         out["case_study"] = noc_case_study(api, torch)
-    if name == "l2lru":
+    if name == "l2lru" and not args.no_case_study:
         out["case_study"] = lru_case_study(api, torch)
     if name == "txn":
-        out["case_study"] = txn_case_study(api, torch)
         out["transactions_per_s"] = sum(int((p[2][2] == 0).sum().item()) * _transactions(p[3])
                                         for p in plan.parts) * K / wall
+        if not args.no_case_study:
+            out["case_study"] = txn_case_study(api, torch)
     if phases is not None:
         out["phase_stats"] = phases
     if host_io_rates is not None:
