@@ -521,7 +521,7 @@ def main() -> int:
                      "traffic_per_node_sim": traffic_per_node,
                      "algorithmic_bytes_per_step": abytes,
                      "step_ms": mean_step * 1e3,
-                     "kernel": {"noc": "gts_sim_wave", "txn": "gts_sim_wave",
+                     "kernel": {"noc": "gts_sim_wave", "txn": "gts_sim_window_txn",
                                 "l2lru": "gts_sim_window_lru"}.get(name, "gts_sim_window"),
                      "launch_ms": mean_launch * 1e3,
                      "per_launch_gbs": abytes / launches_per_step / mean_launch / 1e9,

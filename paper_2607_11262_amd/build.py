@@ -21,7 +21,13 @@ ARCH = os.environ.get("GTS_OFFLOAD_ARCH", "gfx950")
 # Packed FP32 instructions are kept out of generated code (-packed-fp32-ops).
 DEVICE_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
                 "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
-KERNELS = ("gts_sim.hip", "gts_window.hip", "gts_noalloc.hip")
+# (source, extra flags, object): the windowed kernel's three modes compile
+# as parts of their own, side by side
+KERNELS = (("gts_sim.hip", (), "gts_sim.o"),
+           ("gts_window.hip", ("-DGTS_WINDOW_PART=0",), "gts_window0.o"),
+           ("gts_window.hip", ("-DGTS_WINDOW_PART=1",), "gts_window1.o"),
+           ("gts_window.hip", ("-DGTS_WINDOW_PART=2",), "gts_window2.o"),
+           ("gts_noalloc.hip", (), "gts_noalloc.o"))
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 
 
@@ -34,9 +40,9 @@ def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
     jobs = []
     objs = []
-    for src in KERNELS:
-        o = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        jobs.append([HIPCC, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", o])
+    for src, extra, obj in KERNELS:
+        o = os.path.join(BUILD, obj)
+        jobs.append([HIPCC, *DEVICE_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", o])
         objs.append(o)
     host_o = os.path.join(BUILD, "gts_host.o")
     jobs.append([HIPCC, *HOST_FLAGS, "-x", "c++", "-c", os.path.join(CSRC, "gts_host.cpp"), "-o", host_o])

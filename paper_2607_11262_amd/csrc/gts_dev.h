@@ -167,6 +167,8 @@ constexpr uint32_t kWinMaxSm = 256;    // largest n_sm it simulates (four SMs pe
 constexpr uint32_t kNear = 4;          // ready entries per lane due in the current window (LDS)
 constexpr uint32_t kPoolSpill = 240;   // later ready entries per lane beyond the LDS part
 constexpr uint32_t kRing = 64;         // memory-arrival FIFO entries per SM
+constexpr uint32_t kRingWords = 3;     // words per entry: key low, key high, op
+constexpr uint32_t kRingWordsTxn = 8;  // transaction-level memory: node, entry cycle, remainder, line index, lines left
 constexpr uint32_t kRetireLds = 0;     // pending CTA retirements held in LDS (none: the room went to kWinCap) ...
 constexpr uint32_t kRetireCap = 8192;  // ... and in all (the rest spilled to scratch)
 constexpr uint32_t kWinCap = 256;      // memory arrivals (or retirements) per window
@@ -200,8 +202,11 @@ struct Launch {
 // kernel addresses without registers; then the parts sized by the batch.
 // NS: largest n_sm of the batch; SS: server words per SM (server_stride at
 // the largest n_subpart); QP: later ready entries per lane held in LDS; NT:
-// template class x slot op entries (u16); LRU: the graph's loads / stores name
-// tiles (one word per memory-batch position for the LRU decisions).
+// template class x slot op entries (u16); mode: kWinPlain, kWinTiles (loads /
+// stores name tiles: one word per memory-batch position for the LRU
+// decisions) or kWinTxn (transaction-level memory: that word, and per
+// batch slot a line index, the next line's entry cycle, a node's largest
+// finish so far and its start).
 constexpr uint32_t kWinNrCnt = 0, kWinFrCnt = 64, kWinFrMin = 128, kWinFrHot = 192;
 constexpr uint32_t kWinRetCnt = 256, kWinRetMin = 257;
 constexpr uint32_t kWinNr = 258;
@@ -227,12 +232,13 @@ static_assert(kWinNr % 2 == 0 && kWinRetL % 2 == 0 && kWinWKey % 2 == 0 && kWinS
                   kWinPtrs % 2 == 0,
               "64-bit arrays on even words");
 static_assert(2 * 64 * kNear >= kWinMaxSm + kWinCap, "near lists hold the memory phase's split");
+constexpr uint32_t kWinPlain = 0, kWinTiles = 1, kWinTxn = 2;
 struct WinLds {
-  uint32_t optab, tops, srv, mq_head, mq_pos, fr, lru;
+  uint32_t optab, tops, srv, mq_head, mq_pos, fr, lru, t_idx, t_next, t_max, t_start;
   uint32_t total;
 };
 __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, uint32_t QP, uint32_t NT,
-                                          bool LRU) {
+                                          uint32_t mode) {
   WinLds L;
   uint32_t o = kWinFixed;
   auto take = [&o](uint32_t words, bool wide) {
@@ -247,7 +253,12 @@ __host__ __device__ inline WinLds win_lds(uint32_t P, uint32_t NS, uint32_t SS, 
   L.mq_head = take(NS, false);
   L.mq_pos = take(NS, false);
   L.fr = take(2u * 64u * QP, true);
-  L.lru = take(LRU ? kWinCap : 0u, false);
+  L.lru = take(mode != kWinPlain ? kWinCap : 0u, false);
+  const bool txn = mode == kWinTxn;
+  L.t_idx = take(txn ? kWinCap : 0u, false);
+  L.t_next = take(txn ? kWinCap : 0u, false);
+  L.t_max = take(txn ? kWinCap : 0u, false);
+  L.t_start = take(txn ? kWinCap : 0u, false);
   L.total = o;
   return L;
 }

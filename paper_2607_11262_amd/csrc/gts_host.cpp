@@ -27,6 +27,7 @@ struct gts_graph {
   uint64_t bytes;
   uint32_t max_cta_nodes, max_outdeg;
   uint64_t max_tile_lines;
+  bool all_mem_txn;  // every load / store streams at least one line (transaction-level memory)
 };
 
 struct gts_hwset {
@@ -505,7 +506,7 @@ ImageLayout image_layout(const gts_graph_host* h, const Derived& d) {
 
 // keys: tiles or lines the LRU L2 tracks (0: no LRU state); accesses: a
 // bound on the LRU accesses of one simulation (the stamps of its tree)
-gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t keys, uint32_t accesses) {
+gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t keys, uint32_t accesses, uint32_t ring_words) {
   gts::SimLayout s;
   uint64_t off = 0;
   s.off_state = off;
@@ -523,7 +524,7 @@ gts::SimLayout sim_layout(uint32_t N, uint32_t C, uint32_t P, uint32_t keys, uin
   // state, which follows.
   s.off_rp = s.off_pend;
   s.off_mq = align_up(s.off_rp + 8ull * gts::kPoolSpill * 64, gts::kAlign);
-  s.off_ret = align_up(s.off_mq + 12ull * gts::kRing * gts::kWinMaxSm, gts::kAlign);
+  s.off_ret = align_up(s.off_mq + 4ull * ring_words * gts::kRing * gts::kWinMaxSm, gts::kAlign);
   off = std::max(off, align_up(s.off_ret + 8ull * (gts::kRetireCap - gts::kRetireLds), gts::kAlign));
   s.off_lru = off;
   off = align_up(off + (uint64_t)keys * 4, gts::kAlign);
@@ -564,8 +565,8 @@ int check_hw(const gts_hw_params* hw, uint32_t index) {
 
 gts::SimLayout layout_of(const gts_graph* g) {
   const gts::Image& m = g->img;
-  return m.n_txn ? sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_lines, m.n_txn)
-                 : sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_tiles, m.n_nodes);
+  return m.n_txn ? sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_lines, m.n_txn, gts::kRingWordsTxn)
+                 : sim_layout(m.n_nodes, m.n_ctas, m.n_ops, m.n_tiles, m.n_nodes, gts::kRingWords);
 }
 
 uint64_t sim_scratch_bytes(const gts_graph* g, uint32_t B) {
@@ -654,11 +655,14 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
 
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
-  // tiles (LRU L2): the memory phase packs a tile's line count into 22 bits
+  // tiles (LRU L2): the memory phase packs a tile's line count into 22 bits;
+  // transaction-level memory: every load / store streams lines (no node on
+  // the whole-cycle servers of R6.4 beside them)
   const bool lru = (g->img.props & gts::kGraphTiles) != 0;
-  bool windowed = (g->img.props & need_props) == need_props &&
-                  !(g->img.props & (gts::kGraphClusters | gts::kGraphTxn)) &&
-                  (!lru || g->max_tile_lines < gts::kWinMaxTileLines) &&
+  const bool txn = (g->img.props & gts::kGraphTxn) != 0;
+  const uint32_t mode = txn ? gts::kWinTxn : lru ? gts::kWinTiles : gts::kWinPlain;
+  bool windowed = (g->img.props & need_props) == need_props && !(g->img.props & gts::kGraphClusters) &&
+                  (!lru || g->max_tile_lines < gts::kWinMaxTileLines) && (!txn || g->all_mem_txn) &&
                   g->img.n_nodes > 0 && max_nsm <= gts::kWinMaxSm &&
                   !(force && std::strcmp(force, "general") == 0);
   uint32_t lds_window = 0;
@@ -669,7 +673,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // slower even for batches that fill only part of the chip.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) {
-      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops, lru).total;
+      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops, mode).total;
     };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
     uint32_t want = kWavesPerCu;
@@ -956,6 +960,12 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
   g->img.n_tiles = d.n_tiles;
   g->max_tile_lines = d.max_tile_lines;
+  g->all_mem_txn = false;
+  if (!d.txn_line.empty()) {
+    g->all_mem_txn = true;
+    for (uint32_t v = 0; v < h->n_nodes && g->all_mem_txn; ++v)
+      if (is_memory(h->op_cls[h->node_op[v]]) && d.txn_ptr[v + 1] == d.txn_ptr[v]) g->all_mem_txn = false;
+  }
   const bool txn = !d.txn_line.empty();
   g->img.txn_ptr = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_ptr) : nullptr;
   g->img.txn_line = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_line) : nullptr;

@@ -230,8 +230,11 @@ __device__ __forceinline__ uint32_t due_count(const uint32_t (&ehi)[NB][kGq<NB>]
 extern __shared__ uint32_t win_lds_words[];
 __device__ __forceinline__ uint32_t* lds_base() { return win_lds_words; }
 
-template <uint32_t NB, bool LRU>
+template <uint32_t NB, uint32_t MODE>
 struct WSim {
+  // LRU decisions in the memory phase (tiles, or the lines of transaction-
+  // level memory); transaction-level memory
+  static constexpr bool LRU = MODE != kWinPlain, TXN = MODE == kWinTxn;
   Image G;
   const uint32_t* hw;
   uint32_t b, lane, flags, nsm, nsub, sstride, smem_w, nslot, QF;
@@ -272,6 +275,13 @@ struct WSim {
   uint32_t* lw;
   uint32_t lru_now, l2_lines, lru_acc;
   uint64_t lru_total;
+  // transaction-level memory (TXN only): per batch slot the index of its
+  // line in txn_line, the next transaction's entry cycle, and for the first
+  // slot of a node the node's largest finish so far and its start (LDS); the
+  // engine rate, the L2 / DRAM line occupancy in 2^-16 cycles, latencies
+  uint32_t *t_idx, *t_next, *t_max, *t_start;
+  uint32_t r_gmem, lat_l2, lat_dr;
+  uint64_t q_l2, q_dr;
   // per lane
   uint64_t digest;
   uint32_t makespan, nfin, bad;
@@ -450,6 +460,57 @@ struct WSim {
     if (c == 0) mq_head[s] = (uint32_t)(key >> 32);
     mq_pos[s] = (pos & 0xFFFF0000u) | h | ((c + 1) << 8);
     st_maxmq = c + 1 > st_maxmq ? c + 1 : st_maxmq;
+  }
+
+  // ---- transaction-level memory: a load / store streams its lines through
+  // the SM's engine, line k entering at e_k = s + ceil(k L / r) (L = 128 B in
+  // 2^-16 cycles, r the engine rate).  Its ring entry (kRingWordsTxn words):
+  // {node | MISS << 31, entry cycle e of its next line, remainder rem, index
+  // of that line in txn_line, lines left, largest finish so far, start s}
+  // with e = s + c and rem = c r - k L for the next line k; from there line
+  // k + i enters at e + ceil((i L - rem) / r), so the lines entering below a
+  // cycle X number min(left, floor(((X - e - 1) r + rem) / L) + 1) for X > e.
+  static constexpr uint32_t kLineShift = 23;  // L = 2^23
+  static constexpr uint32_t kTxnMiss = 1u, kTxnLast = 2u, kTxnHead = 4u;  // slot flags (w_aux bits 0-7)
+  __device__ __forceinline__ void mq_push_txn(uint32_t s, uint32_t v, uint32_t st, uint32_t idx, uint32_t n,
+                                              uint32_t miss) {
+    const uint32_t pos = mq_pos[s];
+    const uint32_t h = pos & 0xFFu, c = (pos >> 8) & 0xFFu;
+    if (c >= kRing) {
+      bad |= kBadMemQ;
+      return;
+    }
+    uint32_t* e = mq_g + ((uint64_t)s * kRing + (h + c) % kRing) * kRingWordsTxn;
+    *reinterpret_cast<uint4*>(e) = make_uint4(v | (miss << 31), st, 0u, idx);
+    *reinterpret_cast<uint4*>(e + 4) = make_uint4(n, 0u, st, 0u);
+    if (c == 0) mq_head[s] = st;
+    mq_pos[s] = (pos & 0xFFFF0000u) | h | ((c + 1) << 8);
+    st_maxmq = c + 1 > st_maxmq ? c + 1 : st_maxmq;
+  }
+  // lines of an entry whose key (e << 32 | kEvMem << 30 | node) is below K
+  __device__ __forceinline__ uint32_t txn_due(uint32_t w0, uint32_t e, uint32_t rem, uint32_t left,
+                                              uint64_t K) const {
+    const uint32_t low = (kEvMem << 30) | (w0 & GTS_EDGE_TARGET_MASK);
+    const uint64_t X = (K >> 32) + (low < (uint32_t)K ? 1u : 0u);
+    if (left == 0u || X <= e) return 0u;
+    const uint64_t k = ((((X - e - 1u) * (uint64_t)r_gmem) + rem) >> kLineShift) + 1u;
+    return k < left ? (uint32_t)k : left;
+  }
+  // the engine's end for the entry: the entry cycle after its last line
+  __device__ __forceinline__ uint64_t txn_end(uint32_t e, uint32_t rem, uint32_t left) const {
+    const uint64_t a = (uint64_t)left << kLineShift;
+    return a > rem ? e + cdiv64(a - rem, r_gmem) : e;
+  }
+  // the next line's entry cycle and remainder
+  __device__ __forceinline__ void txn_step(uint32_t& e, uint32_t& rem) const {
+    constexpr uint32_t Lb = 1u << kLineShift;
+    if (rem >= Lb) {
+      rem -= Lb;
+      return;
+    }
+    const uint64_t d = cdiv64(Lb - rem, r_gmem);
+    e += (uint32_t)d;
+    rem = (uint32_t)((uint64_t)rem + d * r_gmem - Lb);
   }
 
   // ---- pending CTA retirements, (cycle << 32 | SM) each, unordered: entries
@@ -790,6 +851,7 @@ struct WSim {
     uint32_t ev_t[W], ev_v[W], ev_s[W];
     bool ok[W];
     Rec rec[W];
+    uint32_t tb[W], tn[W];  // TXN: the node's first line index and line count
 #pragma unroll
     for (uint32_t w = 0; w < W; ++w) {
       const uint32_t i = i0 + w * 64u + lane;
@@ -799,6 +861,14 @@ struct WSim {
       ev_v[w] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
       ev_s[w] = ok[w] ? w_aux[i] : 0u;
       rec[w] = rec_of(ev_v[w]);
+      tb[w] = tn[w] = 0u;
+      if constexpr (TXN) {
+        if (ok[w]) {
+          const gmem<const uint32_t>* tp = (const gmem<const uint32_t>*)G.txn_ptr;
+          tb[w] = tp[ev_v[w]];
+          tn[w] = tp[ev_v[w] + 1u] - tb[w];
+        }
+      }
     }
     // timing on the SM's servers: the node holds its class's subpartition
     // lanes (compute), the shared-memory pipe, or the global-memory engine
@@ -829,16 +899,25 @@ struct WSim {
             }
           st = busy > st ? busy : st;
         }
-        const uint64_t f = st + od.x + (is_mem[j] ? 0u : od.z);
+        // a load / store of transaction-level memory holds the engine while
+        // its lines stream through
+        const uint64_t occ = TXN && is_mem[j] ? (uint64_t)clamp_occ(cdiv64((uint64_t)tn[j] << kLineShift, r_gmem))
+                                              : (uint64_t)od.x;
+        const uint64_t f = st + occ + (is_mem[j] ? 0u : od.z);
         if (f > kMaxCycle) {
           bad |= kBadOverflow;
           ok[j] = false;
         } else {
-          const uint32_t free_at = (uint32_t)(st + od.x);
+          const uint32_t free_at = (uint32_t)(st + occ);
 #pragma unroll
           for (uint32_t l = 0; l < kMaxSubpart; ++l)
             if (l < nsub && ((held >> l) & 1u)) Sv[comp ? l : 0u] = free_at;
-          if (is_mem[j]) mq_push(ev_s[j], mkkey(st, kEvMem, ev_v[j]), rec[j].op());
+          if (is_mem[j]) {
+            if constexpr (TXN)
+              mq_push_txn(ev_s[j], ev_v[j], (uint32_t)st, tb[j], tn[j], (od.w >> 3) & 1u);
+            else
+              mq_push(ev_s[j], mkkey(st, kEvMem, ev_v[j]), rec[j].op());
+          }
           rel_i[j] = st + 1;
           rel_f[j] = f;
           if (!is_mem[j]) record(ev_v[j], st, f);
@@ -1035,12 +1114,13 @@ struct WSim {
     for (; u != 0u && u <= lru_acc; u += u & (0u - u))
       __hip_atomic_fetch_add(lru_bit + u, d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+  // Tile accesses: tile and lines of each arrival, the decisions, and the
+  // chosen server's occupancy and latency.
   template <uint32_t E>
   __device__ __forceinline__ void lru_batch(const uint64_t (&k)[E], const uint32_t (&p)[E], uint4 (&od)[E]) {
-    constexpr uint32_t kLines = (1u << 22) - 1u, kLater = 1u << 31;
     const gmem<const uint32_t>* tile = (const gmem<const uint32_t>*)G.tile;
     const gmem<const OpDev>* ops = (const gmem<const OpDev>*)G.ops;
-    uint32_t x[E], n[E], q[E], wk[E];
+    uint32_t x[E], n[E], wk[E];
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
       x[r] = GTS_NO_TILE;
@@ -1051,11 +1131,28 @@ struct WSim {
       }
     }
 #pragma unroll
+    for (uint32_t r = 0; r < E; ++r)
+      n[r] = x[r] != GTS_NO_TILE ? (uint32_t)(((uint64_t)wk[r] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES) : 0u;
+    bool hit[E];
+    lru_core<E>(x, n, hit);
+    const gmem<const uint32_t>* hw_w = cold<const uint32_t>(kPHw);
+#pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
-      const bool t = x[r] != GTS_NO_TILE;
-      q[r] = t ? lru_last[x[r]] : 0u;
-      n[r] = t ? (uint32_t)(((uint64_t)wk[r] + GTS_LINE_BYTES - 1) / GTS_LINE_BYTES) : 0u;
+      if (x[r] == GTS_NO_TILE) continue;
+      const bool dram = !hit[r];
+      od[r].y = clamp_occ(cdiv64((uint64_t)wk[r] * 65536ull, hw_w[HW_RATE + (dram ? R_DRAM : R_L2)]));
+      od[r].z = hw_w[HW_LAT + (dram ? L_DRAM : L_L2)];
+      od[r].w = (od[r].w & ~8u) | (dram ? 8u : 0u);
     }
+  }
+  // The decisions for keys x (GTS_NO_TILE: none) of n lines at batch
+  // positions lane * E + r.
+  template <uint32_t E>
+  __device__ __forceinline__ void lru_core(const uint32_t (&x)[E], const uint32_t (&n)[E], bool (&hit)[E]) {
+    constexpr uint32_t kLines = (1u << 22) - 1u, kLater = 1u << 31;
+    uint32_t q[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) q[r] = x[r] != GTS_NO_TILE ? lru_last[x[r]] : 0u;
     uint64_t tk[E];
     uint32_t unused[E];
 #pragma unroll
@@ -1119,9 +1216,9 @@ struct WSim {
     const uint32_t incl = wave_incl_sum_u32(c);
     uint32_t st = lru_now + incl - c;
     uint32_t fresh = 0;
-    const gmem<const uint32_t>* hw_w = cold<const uint32_t>(kPHw);
 #pragma unroll
     for (uint32_t r = 0; r < E; ++r) {
+      hit[r] = false;
       if (x[r] == GTS_NO_TILE) continue;
       ++st;
       if (!(word[r] & kLater)) {
@@ -1132,13 +1229,277 @@ struct WSim {
         fen_add(st, n[r]);
         lru_last[x[r]] = st;
       }
-      const bool dram = !(seen[r] && above[r] + n[r] <= (uint64_t)l2_lines);
-      od[r].y = clamp_occ(cdiv64((uint64_t)wk[r] * 65536ull, hw_w[HW_RATE + (dram ? R_DRAM : R_L2)]));
-      od[r].z = hw_w[HW_LAT + (dram ? L_DRAM : L_L2)];
-      od[r].w = (od[r].w & ~8u) | (dram ? 8u : 0u);
+      hit[r] = seen[r] && above[r] + n[r] <= (uint64_t)l2_lines;
     }
     lru_now += lane_u32(incl, 63);
     lru_total += wave_sum_u32(fresh);
+    wsync();
+  }
+
+  // ---- transaction-level memory: the window's due lines.  Up to two ring
+  // entries of each SM whose head may be below H0 are loaded; the entries
+  // after them start no earlier than the last loaded one's engine end, so K
+  // stays at or below the smallest key any of them can have.  At most `cap`
+  // lines are due (the largest cycle boundary that keeps them, or a key
+  // boundary inside cycle T: one node's lines of one cycle share a key, and
+  // the host keeps them within the cap).  The due lines fill slots SM by SM,
+  // each SM's in ring order, an entry's lines consecutive: w_key = entry
+  // cycle << 32 | kEvMem << 30 | node, w_aux = SM << 16 | ring position << 8
+  // | flags, t_idx = line index, t_next = the next line's entry cycle (after
+  // the last line, the engine's end); an entry's first slot also carries its
+  // largest finish so far and its start.  Entries keep their progress in the
+  // ring, and the head moves past the front entries with no line left.  (An
+  // entry's lines can be due while an earlier one still has lines: the last
+  // line of a node and the first of the next can enter in one cycle, and the
+  // order between them is by node.)
+  __device__ __forceinline__ uint32_t txn_select(uint64_t T, uint64_t H0, uint32_t cap) {
+    constexpr uint32_t GQ = 2;
+    uint32_t ew[NB][GQ], ee[NB][GQ], er[NB][GQ], ei[NB][GQ], el[NB][GQ], em[NB][GQ], es[NB][GQ];
+    uint32_t cnt[NB], hd[NB];
+    bool ld[NB];
+    uint64_t Kl = H0 << 32;
+#pragma unroll
+    for (uint32_t j = 0; j < NB; ++j) {
+      const uint32_t s = lane + 64u * j;
+      const bool valid = j < nslot && s < nsm;
+      const uint32_t pos = valid ? mq_pos[s] : 0u;
+      hd[j] = pos & 0xFFu;
+      cnt[j] = (pos >> 8) & 0xFFu;
+      ld[j] = valid && cnt[j] > 0 && mq_head[s] < H0;
+#pragma unroll
+      for (uint32_t q = 0; q < GQ; ++q) {
+        ew[j][q] = ee[j][q] = er[j][q] = ei[j][q] = el[j][q] = em[j][q] = es[j][q] = 0u;
+        if (ld[j] && q < cnt[j]) {
+          const gmem<const uint32_t>* e =
+              (const gmem<const uint32_t>*)(mq_g + ((uint64_t)s * kRing + (hd[j] + q) % kRing) * kRingWordsTxn);
+          const uint4 a = ld4(e), c = ld4(e + 4);
+          ew[j][q] = a.x;
+          ee[j][q] = a.y;
+          er[j][q] = a.z;
+          ei[j][q] = a.w;
+          el[j][q] = c.x;
+          em[j][q] = c.y;
+          es[j][q] = c.z;
+        }
+      }
+      if (ld[j] && cnt[j] > GQ) {
+        const uint64_t x = (txn_end(ee[j][GQ - 1], er[j][GQ - 1], el[j][GQ - 1]) << 32) | ((uint64_t)kEvMem << 30);
+        Kl = x < Kl ? x : Kl;
+      }
+    }
+    auto due = [&](uint64_t K) -> uint32_t {
+      uint32_t c = 0;
+#pragma unroll
+      for (uint32_t j = 0; j < NB; ++j)
+#pragma unroll
+        for (uint32_t q = 0; q < GQ; ++q)
+          if (ld[j] && q < cnt[j]) c += txn_due(ew[j][q], ee[j][q], er[j][q], el[j][q], K);
+      return c;
+    };
+    uint64_t K = wmin64(Kl);
+    uint32_t M = wave_sum_u32(due(K));
+    if (M > cap) {
+      const uint64_t Kmax = K;  // due(Kmax) > cap
+      uint64_t lo = T, hi = Kmax >> 32;  // cycles; due(T << 32) = 0
+      if (wave_sum_u32(due(hi << 32)) <= cap) {
+        lo = hi;
+      } else {
+        while (hi - lo > 1) {
+          const uint64_t mid = lo + (hi - lo) / 2;
+          if (wave_sum_u32(due(mid << 32)) <= cap)
+            lo = mid;
+          else
+            hi = mid;
+        }
+      }
+      K = lo << 32;
+      if (lo == T) {
+        uint64_t klo = T << 32, khi = (T + 1) << 32;
+        khi = Kmax < khi ? Kmax : khi;
+        while (khi - klo > 1) {
+          const uint64_t mid = klo + (khi - klo) / 2;
+          if (wave_sum_u32(due(mid)) <= cap)
+            klo = mid;
+          else
+            khi = mid;
+        }
+        K = klo;
+      }
+      M = wave_sum_u32(due(K));
+    }
+    uint32_t p = wave_excl_scan_u32(due(K));
+#pragma unroll
+    for (uint32_t j = 0; j < NB; ++j) {
+      const uint32_t s = lane + 64u * j;
+      if (!(j < nslot && s < nsm)) continue;
+      uint32_t d = 0, gone = 0;
+      bool front = true;
+      uint64_t nh = kNoKey;  // lower bound of the next line's entry cycle among the entries that stay
+#pragma unroll
+      for (uint32_t q = 0; q < GQ; ++q) {
+        if (!(ld[j] && q < cnt[j])) continue;
+        const uint32_t c = txn_due(ew[j][q], ee[j][q], er[j][q], el[j][q], K);
+        const uint32_t rp = (hd[j] + q) % kRing;
+        const uint32_t v = ew[j][q] & GTS_EDGE_TARGET_MASK;
+        const uint32_t fl = (ew[j][q] >> 31) ? kTxnMiss : 0u;
+        uint32_t e = ee[j][q], rem = er[j][q];
+        for (uint32_t k = 0; k < c; ++k) {
+          const uint32_t slot = p + d + k;
+          w_key[slot] = ((uint64_t)e << 32) | ((uint64_t)kEvMem << 30) | v;
+          txn_step(e, rem);
+          t_next[slot] = e;
+          t_idx[slot] = ei[j][q] + k;
+          w_aux[slot] = (s << 16) | (rp << 8) | fl | (k + 1u == el[j][q] ? kTxnLast : 0u) | (k == 0u ? kTxnHead : 0u);
+          if (k == 0u) {
+            t_max[slot] = em[j][q];
+            t_start[slot] = es[j][q];
+          }
+        }
+        d += c;
+        const uint32_t left = el[j][q] - c;
+        if (c) {  // progress stays in the ring (the largest finish is written after the batch)
+          gmem<uint32_t>* g = (gmem<uint32_t>*)(mq_g + ((uint64_t)s * kRing + rp) * kRingWordsTxn);
+          g[1] = e;
+          g[2] = rem;
+          g[3] = ei[j][q] + c;
+          g[4] = left;
+        }
+        if (front && left == 0u)
+          ++gone;
+        else
+          front = false;
+        if (left) nh = e < nh ? e : nh;
+      }
+      dsc[s] = p | (d << 16);
+      p += d;
+      if (ld[j]) {
+        const uint32_t rest = cnt[j] - gone;
+        mq_pos[s] = (mq_pos[s] & 0xFFFF0000u) | ((hd[j] + gone) % kRing) | (rest << 8);
+        if (rest) {
+          if (cnt[j] > GQ) {
+            const uint64_t x = txn_end(ee[j][GQ - 1], er[j][GQ - 1], el[j][GQ - 1]);
+            nh = x < nh ? x : nh;
+          }
+          mq_head[s] = (uint32_t)nh;
+        }
+      }
+    }
+    return M;
+  }
+
+  // Memory phase of transaction-level memory: each due line, in (cycle,
+  // node, line) order, hits iff it is among the L2's most recent lines (an
+  // LRU of lines; without a capacity the op's MISS flag decides) and is
+  // served FIFO by the L2 or DRAM server, which keeps time in 2^-16 cycles
+  // and holds a line for q of them: m = max(e << 16, avail), avail = m + q,
+  // finish = max(next entry cycle, ceil((m + q) / 2^16)) + latency.
+  template <uint32_t E>
+  __device__ __forceinline__ void memory_phase_txn(uint32_t M) {
+    uint64_t k[E];
+    uint32_t p[E];
+    sort_batch<E>(M, k, p);
+    const gmem<const uint32_t>* tl = (const gmem<const uint32_t>*)G.txn_line;
+    uint32_t x[E], one[E], nxt[E];
+    bool dram[E];
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      x[r] = GTS_NO_TILE;
+      one[r] = nxt[r] = 0u;
+      dram[r] = false;
+      if (k[r] != kNoKey) {
+        dram[r] = (w_aux[p[r]] & kTxnMiss) != 0u;
+        nxt[r] = t_next[p[r]];
+        if (l2_lines) {
+          x[r] = tl[t_idx[p[r]]];
+          one[r] = 1u;
+        }
+      }
+    }
+    if (l2_lines) {
+      bool hit[E];
+      lru_core<E>(x, one, hit);
+#pragma unroll
+      for (uint32_t r = 0; r < E; ++r)
+        if (x[r] != GTS_NO_TILE) dram[r] = !hit[r];
+    }
+    Compose fl2{kNegCycle, 0}, fdr{kNegCycle, 0};
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      if (k[r] != kNoKey) {
+        const Compose g{(int64_t)((k[r] >> 32) << 16), (int64_t)(dram[r] ? q_dr : q_l2)};
+        if (dram[r])
+          fdr = compose(fdr, g);
+        else
+          fl2 = compose(fl2, g);
+      }
+    }
+    const Compose il2 = wave_incl_compose(fl2), idr = wave_incl_compose(fdr);
+    Compose el2 = Compose{__shfl_up(il2.a, 1, 64), __shfl_up(il2.o, 1, 64)};
+    Compose edr = Compose{__shfl_up(idr.a, 1, 64), __shfl_up(idr.o, 1, 64)};
+    if (lane == 0) el2 = edr = Compose{kNegCycle, 0};
+    const Compose tl2 = lane_c(il2, 63), tdr = lane_c(idr, 63);
+    int64_t xl2 = ((int64_t)l2_av > el2.a ? (int64_t)l2_av : el2.a) + el2.o;
+    int64_t xdr = ((int64_t)dram_av > edr.a ? (int64_t)dram_av : edr.a) + edr.o;
+    if (!nocont) {
+      l2_av = (uint64_t)(((int64_t)l2_av > tl2.a ? (int64_t)l2_av : tl2.a) + tl2.o);
+      dram_av = (uint64_t)(((int64_t)dram_av > tdr.a ? (int64_t)dram_av : tdr.a) + tdr.o);
+    }
+#pragma unroll
+    for (uint32_t r = 0; r < E; ++r) {
+      if (k[r] != kNoKey) {
+        const int64_t st = (int64_t)((k[r] >> 32) << 16);
+        const int64_t q = (int64_t)(dram[r] ? q_dr : q_l2);
+        const int64_t xs = dram[r] ? xdr : xl2;
+        const int64_t m = nocont ? st : (xs > st ? xs : st);
+        if (dram[r])
+          xdr = m + q;
+        else
+          xl2 = m + q;
+        const uint64_t done = ((uint64_t)(m + q) + 65535u) >> 16;
+        const uint64_t f = (nxt[r] > done ? (uint64_t)nxt[r] : done) + (dram[r] ? lat_dr : lat_l2);
+        if (f > kMaxCycle) bad |= kBadOverflow;
+        w_fin[p[r]] = f > kMaxCycle ? 0xFFFFFFFFu : (uint32_t)f;
+      }
+    }
+    wsync();
+    if (__ballot(bad != 0)) return;
+    txn_fold();
+    complete_arrivals();
+  }
+
+  // Each SM's lines of the batch, in ring order (an entry's lines are
+  // consecutive slots, led by its first): the node's largest finish folds
+  // over them; a node whose last line is here completes (the slot then
+  // holds the node's finish and, in t_next, its start); an entry with lines
+  // left keeps its largest finish in the ring.  The completing slots are
+  // listed from each SM's first slot on (lw), for the completion rounds.
+  __device__ __forceinline__ void txn_fold() {
+#pragma unroll
+    for (uint32_t j = 0; j < NB; ++j) {
+      const uint32_t s = lane + 64u * j;
+      if (!(j < nslot && s < nsm)) continue;
+      const uint32_t sp = dsc[s], first = sp & 0xFFFFu, d = sp >> 16;
+      uint32_t m = 0, st = 0, c = 0;
+      for (uint32_t i = first; i < first + d; ++i) {
+        const uint32_t a = w_aux[i];
+        if (a & kTxnHead) {
+          m = t_max[i];
+          st = t_start[i];
+        }
+        const uint32_t f = w_fin[i];
+        m = f > m ? f : m;
+        if (a & kTxnLast) {
+          w_fin[i] = m;
+          t_next[i] = st;
+          lw[first + c] = i;
+          ++c;
+        } else if (i + 1u == first + d || (w_aux[i + 1u] & kTxnHead)) {
+          gmem<uint32_t>* g = (gmem<uint32_t>*)(mq_g + ((uint64_t)s * kRing + ((a >> 8) & 0xFFu)) * kRingWordsTxn);
+          g[5] = m;
+        }
+      }
+      dsc[s] = first | (c << 16);
+    }
     wsync();
   }
 
@@ -1227,7 +1588,7 @@ struct WSim {
       uint32_t p = incl - cnt;
 #pragma unroll
       for (uint32_t j = 0; j < NB; ++j)
-        if (r < (sp[j] >> 16)) stage[p++] = (sp[j] & 0xFFFFu) + r;
+        if (r < (sp[j] >> 16)) stage[p++] = TXN ? lw[(sp[j] & 0xFFFFu) + r] : (sp[j] & 0xFFFFu) + r;
       wsync();
       if (E <= 64) {
         complete_events<1>(0, E);
@@ -1253,7 +1614,7 @@ struct WSim {
       const uint32_t slot = ok[j] ? stage[i] : 0u;
       const uint64_t key = ok[j] ? w_key[slot] : 0ull;
       vv[j] = (uint32_t)key & GTS_EDGE_TARGET_MASK;
-      tt[j] = (uint32_t)(key >> 32);
+      tt[j] = TXN ? (ok[j] ? t_next[slot] : 0u) : (uint32_t)(key >> 32);  // the node's start
       ff[j] = ok[j] ? w_fin[slot] : 0u;
       ss[j] = ok[j] ? w_aux[slot] >> 16 : 0u;
       rec[j] = rec_of(vv[j]);
@@ -1314,12 +1675,13 @@ struct WSim {
 };
 
 
-template <uint32_t NB, bool LRU>
+template <uint32_t NB, uint32_t MODE>
 __device__ __forceinline__ void window_body(const Launch& L) {
+  constexpr bool LRU = MODE != kWinPlain, TXN = MODE == kWinTxn;
   const uint32_t b = blockIdx.x;
   if (b >= L.B) return;
   uint32_t* const lds = lds_base();
-  WSim<NB, LRU> S;
+  WSim<NB, MODE> S;
   S.G = L.img;
   S.hw = L.hw + (uint64_t)b * HW_WORDS;
   S.b = b;
@@ -1339,7 +1701,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
-  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops, LRU);
+  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops, MODE);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.tops = reinterpret_cast<uint16_t*>(lds + W.tops);
   S.srv = lds + W.srv;
@@ -1405,6 +1767,29 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     }
   }
   lm = wmin64(lm);
+  if constexpr (TXN) {
+    // a node completes with its last line, no earlier than a cycle after the
+    // line enters plus the faster server's latency
+    S.t_idx = lds + W.t_idx;
+    S.t_next = lds + W.t_next;
+    S.t_max = lds + W.t_max;
+    S.t_start = lds + W.t_start;
+    S.r_gmem = S.hw[HW_RATE + R_GMEM];
+    S.q_l2 = cdiv64((uint64_t)GTS_LINE_BYTES << 32, S.hw[HW_RATE + R_L2]);
+    S.q_dr = cdiv64((uint64_t)GTS_LINE_BYTES << 32, S.hw[HW_RATE + R_DRAM]);
+    S.lat_l2 = S.hw[HW_LAT + L_L2];
+    S.lat_dr = S.hw[HW_LAT + L_DRAM];
+    lm = 1ull + (S.lat_l2 < S.lat_dr ? S.lat_l2 : S.lat_dr);
+    // one node's lines of one cycle share a key and must fit one batch: at
+    // most ceil(rate / 128 B) of them; faster engines go to the general
+    // kernel.  So does NO_CONTENTION: without the engine's order the lines
+    // of the nodes queued on an SM interleave, and looking ahead a bounded
+    // number of ring entries no longer finds every due line.
+    if (S.r_gmem > (kWinCap / 2) << S.kLineShift || S.nocont) {
+      if (lane == 0) L.out_status[b] = kStatusRetry;
+      return;
+    }
+  }
   S.Lm = lm < kWindowMax ? lm : kWindowMax;
   for (uint32_t i = lane; i < S.G.n_tops; i += 64) S.tops[i] = S.G.tops[i];
   for (uint32_t i = lane; i < S.nsm * S.sstride; i += 64) S.srv[i] = 0;
@@ -1426,11 +1811,12 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     S.lru_last = (gmem<uint32_t>*)(sim + L.layout.off_lru);
     S.lru_bit = (gmem<uint64_t>*)(sim + L.layout.off_lru_bit);
     S.lw = lds + W.lru;
-    S.lru_acc = S.G.n_nodes;  // at most one tile access per node
+    S.lru_acc = TXN ? S.G.n_txn : S.G.n_nodes;  // at most one access per node, or per line of a node
     S.lru_now = 0;
     S.lru_total = 0;
     if (S.l2_lines) {
-      for (uint32_t x = lane; x < S.G.n_tiles; x += 64) S.lru_last[x] = 0u;
+      const uint32_t keys = TXN ? S.G.n_lines : S.G.n_tiles;
+      for (uint32_t x = lane; x < keys; x += 64) S.lru_last[x] = 0u;
       for (uint32_t i = lane; i <= S.lru_acc; i += 64) S.lru_bit[i] = 0ull;
     }
   }
@@ -1479,6 +1865,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   constexpr uint32_t kMemCap = LRU ? kWinCap / 2 : kWinCap;
   S.dispatch(0);
   wsync();
+  uint64_t last_T = kNoKey;  // TXN: windows in a row that start at one cycle (a bound, never reached)
+  uint32_t same_T = 0;
   while (!__ballot(S.bad != 0)) {
     const uint64_t c0 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
     // T: lower bound of the earliest pending event
@@ -1499,6 +1887,17 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (uni(*S.ret_cnt)) tmin = rmin < tmin ? rmin : tmin;
     const uint64_t T = wmin64(tmin);
     if (T == kNoKey) break;
+    if constexpr (TXN) {
+      // every window processes an event or raises a lower bound; should one
+      // cycle ever open 2^20 windows in a row, the simulation goes back to
+      // the general kernel rather than spinning
+      same_T = T == last_T ? same_T + 1u : 0u;
+      last_T = T;
+      if (same_T > (1u << 20)) {
+        S.bad |= kBadMemQ;
+        break;
+      }
+    }
     uint64_t H0 = T + S.Lm;
     H0 = H0 < 0xFFFFFFFFull ? H0 : 0xFFFFFFFFull;  // cycles never exceed kMaxCycle
     const uint64_t c1 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
@@ -1600,101 +1999,105 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     if (__ballot(S.bad != 0)) break;
 
     // Memory phase: the arrivals whose key (cycle, id) is below K <= H0 << 32.
-    constexpr uint32_t GQ = kGq<NB>;
-    // Up to GQ head entries of each SM whose head may be below H0 are loaded;
-    // K is lowered so that every due arrival is among them, and so that at
-    // most kMemCap are due -- the rest, possibly of the same cycle, wait for
-    // the next window (they complete after it starts, and no arrival of a
-    // cycle below H0 can still appear).
     uint32_t M = 0;
-    {
-      uint32_t elo[NB][GQ], ehi[NB][GQ], eop[NB][GQ], cnt[NB], hd[NB];
-      bool ld[NB];
-      uint64_t Kl = H0 << 32;
-#pragma unroll
-      for (uint32_t j = 0; j < NB; ++j) {
-        const uint32_t s = lane + 64u * j;
-        const bool valid = j < S.nslot && s < S.nsm;
-        const uint32_t pos = valid ? S.mq_pos[s] : 0u;
-        hd[j] = pos & 0xFFu;
-        cnt[j] = (pos >> 8) & 0xFFu;
-        ld[j] = valid && cnt[j] > 0 && S.mq_head[s] < H0;
-#pragma unroll
-        for (uint32_t q = 0; q < GQ; ++q) {
-          eop[j][q] = 0;
-          elo[j][q] = ehi[j][q] = 0xFFFFFFFFu;
-          if (ld[j] && q < cnt[j]) {
-            const uint32_t* e = S.mq_g + ((uint64_t)s * kRing + (hd[j] + q) % kRing) * 3u;
-            elo[j][q] = e[0];
-            ehi[j][q] = e[1];
-            eop[j][q] = e[2];
-          }
-        }
-        if (ld[j] && cnt[j] > GQ) {
-          const uint64_t x = (((uint64_t)ehi[j][GQ - 1] << 32) | elo[j][GQ - 1]) + 1;
-          Kl = x < Kl ? x : Kl;
-        }
-      }
-      uint64_t K = wmin64(Kl);
-      M = wave_sum_u32(due_count(ehi, elo, K));
-      if (M > kMemCap) {
-        // keep at most kMemCap: the largest cycle boundary that does (a
-        // window spans at most 1024 cycles: a few halvings), or, when cycle T
-        // alone holds more, a boundary between the keys of cycle T
-        const uint64_t Kmax = K;  // count(< Kmax) > kMemCap
-        uint64_t lo = T, hi = Kmax >> 32;  // cycles; count(< T << 32) = 0
-        if (wave_sum_u32(due_count(ehi, elo, hi << 32)) <= kMemCap) {
-          lo = hi;
-        } else {
-          while (hi - lo > 1) {
-            const uint64_t mid = lo + (hi - lo) / 2;
-            if (wave_sum_u32(due_count(ehi, elo, mid << 32)) <= kMemCap)
-              lo = mid;
-            else
-              hi = mid;
-          }
-        }
-        K = lo << 32;
-        if (lo == T) {
-          uint64_t klo = T << 32, khi = (T + 1) << 32;  // count(< khi) > kMemCap
-          khi = Kmax < khi ? Kmax : khi;
-          while (khi - klo > 1) {
-            const uint64_t mid = klo + (khi - klo) / 2;
-            if (wave_sum_u32(due_count(ehi, elo, mid)) <= kMemCap)
-              klo = mid;
-            else
-              khi = mid;
-          }
-          K = klo;
-        }
-        M = wave_sum_u32(due_count(ehi, elo, K));
-      }
+    if constexpr (TXN) {
+      M = S.txn_select(T, H0, kMemCap);
+    } else {
+      constexpr uint32_t GQ = kGq<NB>;
+      // Up to GQ head entries of each SM whose head may be below H0 are loaded;
+      // K is lowered so that every due arrival is among them, and so that at
+      // most kMemCap are due -- the rest, possibly of the same cycle, wait for
+      // the next window (they complete after it starts, and no arrival of a
+      // cycle below H0 can still appear).
       {
-        uint32_t p = wave_excl_scan_u32(due_count(ehi, elo, K));
-#pragma unroll
+        uint32_t elo[NB][GQ], ehi[NB][GQ], eop[NB][GQ], cnt[NB], hd[NB];
+        bool ld[NB];
+        uint64_t Kl = H0 << 32;
+  #pragma unroll
         for (uint32_t j = 0; j < NB; ++j) {
           const uint32_t s = lane + 64u * j;
-          if (j < S.nslot && s < S.nsm) {
-            uint32_t d = 0;
-#pragma unroll
-            for (uint32_t q = 0; q < GQ; ++q) {
-              if ((((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K) {
-                S.w_key[p + d] = ((uint64_t)ehi[j][q] << 32) | elo[j][q];
-                S.w_aux[p + d] = eop[j][q] | (s << 16);
-                ++d;
-              }
+          const bool valid = j < S.nslot && s < S.nsm;
+          const uint32_t pos = valid ? S.mq_pos[s] : 0u;
+          hd[j] = pos & 0xFFu;
+          cnt[j] = (pos >> 8) & 0xFFu;
+          ld[j] = valid && cnt[j] > 0 && S.mq_head[s] < H0;
+  #pragma unroll
+          for (uint32_t q = 0; q < GQ; ++q) {
+            eop[j][q] = 0;
+            elo[j][q] = ehi[j][q] = 0xFFFFFFFFu;
+            if (ld[j] && q < cnt[j]) {
+              const uint32_t* e = S.mq_g + ((uint64_t)s * kRing + (hd[j] + q) % kRing) * 3u;
+              elo[j][q] = e[0];
+              ehi[j][q] = e[1];
+              eop[j][q] = e[2];
             }
-            S.dsc[s] = p | (d << 16);
-            p += d;
-            if (ld[j]) {
-              const uint32_t left = cnt[j] - d;
-              S.mq_pos[s] = (S.mq_pos[s] & 0xFFFF0000u) | ((hd[j] + d) % kRing) | (left << 8);
-              if (left) {
-                uint32_t nh = ehi[j][GQ - 1] + 1;  // lower bound when the next entry was not loaded
-#pragma unroll
-                for (uint32_t q = 0; q < GQ; ++q)
-                  if (q == d) nh = ehi[j][q];
-                S.mq_head[s] = nh;
+          }
+          if (ld[j] && cnt[j] > GQ) {
+            const uint64_t x = (((uint64_t)ehi[j][GQ - 1] << 32) | elo[j][GQ - 1]) + 1;
+            Kl = x < Kl ? x : Kl;
+          }
+        }
+        uint64_t K = wmin64(Kl);
+        M = wave_sum_u32(due_count(ehi, elo, K));
+        if (M > kMemCap) {
+          // keep at most kMemCap: the largest cycle boundary that does (a
+          // window spans at most 1024 cycles: a few halvings), or, when cycle T
+          // alone holds more, a boundary between the keys of cycle T
+          const uint64_t Kmax = K;  // count(< Kmax) > kMemCap
+          uint64_t lo = T, hi = Kmax >> 32;  // cycles; count(< T << 32) = 0
+          if (wave_sum_u32(due_count(ehi, elo, hi << 32)) <= kMemCap) {
+            lo = hi;
+          } else {
+            while (hi - lo > 1) {
+              const uint64_t mid = lo + (hi - lo) / 2;
+              if (wave_sum_u32(due_count(ehi, elo, mid << 32)) <= kMemCap)
+                lo = mid;
+              else
+                hi = mid;
+            }
+          }
+          K = lo << 32;
+          if (lo == T) {
+            uint64_t klo = T << 32, khi = (T + 1) << 32;  // count(< khi) > kMemCap
+            khi = Kmax < khi ? Kmax : khi;
+            while (khi - klo > 1) {
+              const uint64_t mid = klo + (khi - klo) / 2;
+              if (wave_sum_u32(due_count(ehi, elo, mid)) <= kMemCap)
+                klo = mid;
+              else
+                khi = mid;
+            }
+            K = klo;
+          }
+          M = wave_sum_u32(due_count(ehi, elo, K));
+        }
+        {
+          uint32_t p = wave_excl_scan_u32(due_count(ehi, elo, K));
+  #pragma unroll
+          for (uint32_t j = 0; j < NB; ++j) {
+            const uint32_t s = lane + 64u * j;
+            if (j < S.nslot && s < S.nsm) {
+              uint32_t d = 0;
+  #pragma unroll
+              for (uint32_t q = 0; q < GQ; ++q) {
+                if ((((uint64_t)ehi[j][q] << 32) | elo[j][q]) < K) {
+                  S.w_key[p + d] = ((uint64_t)ehi[j][q] << 32) | elo[j][q];
+                  S.w_aux[p + d] = eop[j][q] | (s << 16);
+                  ++d;
+                }
+              }
+              S.dsc[s] = p | (d << 16);
+              p += d;
+              if (ld[j]) {
+                const uint32_t left = cnt[j] - d;
+                S.mq_pos[s] = (S.mq_pos[s] & 0xFFFF0000u) | ((hd[j] + d) % kRing) | (left << 8);
+                if (left) {
+                  uint32_t nh = ehi[j][GQ - 1] + 1;  // lower bound when the next entry was not loaded
+  #pragma unroll
+                  for (uint32_t q = 0; q < GQ; ++q)
+                    if (q == d) nh = ehi[j][q];
+                  S.mq_head[s] = nh;
+                }
               }
             }
           }
@@ -1704,12 +2107,17 @@ __device__ __forceinline__ void window_body(const Launch& L) {
     wsync();
     if (__ballot(S.bad != 0)) break;
     const uint64_t c4 = clk ? __builtin_amdgcn_s_memtime() : 0ull;
-    if (M) {
-      if (M <= 64)
+    if constexpr (TXN) {
+      if (M && M <= 64)
+        S.template memory_phase_txn<1>(M);
+      else if (M)
+        S.template memory_phase_txn<2>(M);
+    } else {
+      if (M && M <= 64)
         S.template memory_phase<1>(M);
-      else if (LRU || M <= 128)
+      else if (M && (LRU || M <= 128))
         S.template memory_phase<2>(M);
-      else
+      else if (M)
         S.template memory_phase<4>(M);
     }
     wsync();
@@ -1777,28 +2185,55 @@ __device__ __forceinline__ void window_body(const Launch& L) {
 
 }  // namespace
 
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window1(Launch L) { window_body<1, false>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window2(Launch L) { window_body<2, false>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window3(Launch L) { window_body<3, false>(L); }
-extern "C" __global__ __launch_bounds__(64) void gts_sim_window4(Launch L) { window_body<4, false>(L); }
+// The kernels of each mode are compiled in a part of their own (the same
+// source built with GTS_WINDOW_PART = 0, 1, 2, in parallel); the launch
+// lives in part 0 and names the others by declaration.
+#ifndef GTS_WINDOW_PART
+#define GTS_WINDOW_PART 0
+#endif
+#if GTS_WINDOW_PART == 0
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window1(Launch L) { window_body<1, kWinPlain>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window2(Launch L) { window_body<2, kWinPlain>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window3(Launch L) { window_body<3, kWinPlain>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window4(Launch L) { window_body<4, kWinPlain>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_lru(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_lru(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_txn(Launch L);
+#elif GTS_WINDOW_PART == 1
 // graphs whose loads / stores name tiles (LRU L2): held to three waves per
 // SIMD, as the others (a few registers spill at three and four SMs per
 // lane; measured faster than two waves per SIMD without spills)
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_lru(Launch L) { window_body<1, true>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_lru(Launch L) { window_body<2, true>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L) { window_body<3, true>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L) { window_body<4, true>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_lru(Launch L) { window_body<1, kWinTiles>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_lru(Launch L) { window_body<2, kWinTiles>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L) { window_body<3, kWinTiles>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L) { window_body<4, kWinTiles>(L); }
+#else
+// graphs whose loads / stores stream 128-B lines (transaction-level memory)
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_txn(Launch L) { window_body<1, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_txn(Launch L) { window_body<2, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_txn(Launch L) { window_body<3, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_txn(Launch L) { window_body<4, kWinTxn>(L); }
+#endif
 
+#if GTS_WINDOW_PART == 0
 hipError_t launch_window(const Launch& L, uint32_t lds_bytes, hipStream_t stream) {
   if (L.B == 0) return hipSuccess;
   const uint32_t nb = (L.max_nsm + 63) / 64;
-  const bool lru = (L.img.props & kGraphTiles) != 0;
   void (*const plain[4])(Launch) = {gts_sim_window1, gts_sim_window2, gts_sim_window3, gts_sim_window4};
   void (*const tiled[4])(Launch) = {gts_sim_window1_lru, gts_sim_window2_lru, gts_sim_window3_lru,
                                     gts_sim_window4_lru};
+  void (*const txn[4])(Launch) = {gts_sim_window1_txn, gts_sim_window2_txn, gts_sim_window3_txn,
+                                  gts_sim_window4_txn};
   const uint32_t i = nb <= 1 ? 0u : nb >= 4 ? 3u : nb - 1u;
-  hipLaunchKernelGGL(lru ? tiled[i] : plain[i], dim3(L.B), dim3(64), lds_bytes, stream, L);
+  void (*const k)(Launch) = (L.img.props & kGraphTxn) ? txn[i] : (L.img.props & kGraphTiles) ? tiled[i] : plain[i];
+  hipLaunchKernelGGL(k, dim3(L.B), dim3(64), lds_bytes, stream, L);
   return hipGetLastError();
 }
+#endif
 
 }  // namespace gts

@@ -3,8 +3,9 @@
 The windowed kernel takes a graph when every node without a successor in its
 own CTA is a global load or store, every edge between CTAs leaves a load or
 store and is a DATA or SYNC edge, out-degrees stay below 0xFFFF, no kernel
-has clusters, no load / store has a byte address, and every named tile
-(LRU L2) has fewer than 2^22 lines.  These graphs meet that and otherwise vary what
+has clusters, every named tile (LRU L2) has fewer than 2^22 lines, and
+byte addresses (transaction-level memory), if any, sit on every load and
+store, each of at least one byte.  These graphs meet that and otherwise vary what
 the kernel has to get right: 1-4 kernels of 1-32 warps, CTAs of a few to
 several dozen nodes of every class (zero-work nodes included), all three
 edge kinds inside a CTA, fan-outs beyond the three successors a node record
@@ -86,9 +87,12 @@ def window_eligible(g) -> bool:
     """The windowed kernel's graph conditions, written out."""
     if g.n_nodes == 0 or np.any(np.asarray(g.kernel_cluster) > 1):
         return False
-    if getattr(g, "node_addr", None) is not None and np.any(np.asarray(g.node_addr) != NO_ADDR):
-        return False
     cls = np.asarray(g.op_cls)[np.asarray(g.node_op, np.int64)]
+    if getattr(g, "node_addr", None) is not None and np.any(np.asarray(g.node_addr) != NO_ADDR):
+        mem = np.isin(cls, MEM)
+        work = np.asarray(g.op_work, np.int64)[np.asarray(g.node_op, np.int64)]
+        if np.any(mem & ((np.asarray(g.node_addr) == NO_ADDR) | (work == 0))):
+            return False
     if g.node_tile is not None:
         named = np.asarray(g.node_tile) != NO_TILE
         work = np.asarray(g.op_work, np.int64)[np.asarray(g.node_op, np.int64)]
