@@ -2200,10 +2200,10 @@ extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3
 extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_lru(Launch L);
 extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L);
 extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L);
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_txn(Launch L);
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_txn(Launch L);
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_txn(Launch L);
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window1_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window2_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window3_txn(Launch L);
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window4_txn(Launch L);
 #elif GTS_WINDOW_PART == 1
 // graphs whose loads / stores name tiles (LRU L2): held to three waves per
 // SIMD, as the others (a few registers spill at three and four SMs per
@@ -2213,11 +2213,13 @@ extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3
 extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_lru(Launch L) { window_body<3, kWinTiles>(L); }
 extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_lru(Launch L) { window_body<4, kWinTiles>(L); }
 #else
-// graphs whose loads / stores stream 128-B lines (transaction-level memory)
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window1_txn(Launch L) { window_body<1, kWinTxn>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window2_txn(Launch L) { window_body<2, kWinTxn>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window3_txn(Launch L) { window_body<3, kWinTxn>(L); }
-extern "C" __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void gts_sim_window4_txn(Launch L) { window_body<4, kWinTxn>(L); }
+// graphs whose loads / stores stream 128-B lines (transaction-level memory):
+// the register allocator's own occupancy (measured 15 % faster than three
+// waves per SIMD with spills)
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window1_txn(Launch L) { window_body<1, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window2_txn(Launch L) { window_body<2, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window3_txn(Launch L) { window_body<3, kWinTxn>(L); }
+extern "C" __global__ __launch_bounds__(64) void gts_sim_window4_txn(Launch L) { window_body<4, kWinTxn>(L); }
 #endif
 
 #if GTS_WINDOW_PART == 0
