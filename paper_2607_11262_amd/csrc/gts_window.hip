@@ -342,6 +342,22 @@ struct WSim {
       bad |= kBadReady;
     }
   }
+  // m (<= 8) entries of one cycle onto SM s's far list, their slots
+  // reserved at once (as m single pushes would take them)
+  __device__ __forceinline__ void far_push_n(uint32_t s, uint32_t cyc, const uint32_t (&v)[8], uint32_t m) {
+    const uint32_t l = s & 63u;
+    const uint32_t slot = atomicAdd(&fr_cnt[l], m);
+    st_maxrq = slot + m > st_maxrq ? slot + m : st_maxrq;
+#pragma unroll
+    for (uint32_t u = 0; u < 8; ++u) {
+      if (u >= m) continue;
+      if (slot + u < QF + kPoolSpill)
+        fr_set(l, slot + u, ((uint64_t)cyc << 32) | ((uint64_t)(s >> 6) << 30) | v[u]);
+      else
+        bad |= kBadReady;
+    }
+    atomicMin(&fr_min[l], cyc);
+  }
   __device__ __forceinline__ void rq_push(uint32_t s, uint32_t cyc, uint32_t v) {
     const uint32_t l = s & 63u;
     const uint64_t key = ((uint64_t)cyc << 32) | ((uint64_t)(s >> 6) << 30) | v;
@@ -691,7 +707,13 @@ struct WSim {
         load_kernel(cur_k, k_begin, k_end, slots);
       }
       if (retired < k_begin) return;  // the previous kernel is still running
-      const uint32_t lim = k_end - next_cta < 64u ? k_end - next_cta : 64u;
+      // every CTA before next_cta is dispatched and `retired` of them have
+      // retired, all of the running kernel: its free slots are known, and
+      // the placement takes exactly that many (no search that finds none)
+      const uint64_t cap = (uint64_t)nsm * slots, busy = next_cta - retired;
+      const uint64_t room = cap > busy ? cap - busy : 0u;
+      uint32_t lim = k_end - next_cta < 64u ? k_end - next_cta : 64u;
+      lim = room < lim ? (uint32_t)room : lim;
       uint32_t k = 0, mysm = 0;
       while (k < lim) {
         uint64_t best = 0;
@@ -736,7 +758,21 @@ struct WSim {
         if (!(rc & kCtaShared))
           for (uint32_t i = lane; i < nc; i += 64) state[nb + i] = 0ull;
       }
-      if (lane < k) {
+      if (lane < k && !(c0.w & kCtaShared) && launch >= Hnear) {
+        // no in-edges at all: every root is ready at launch; up to eight
+        // root ids read together, their far-list slots reserved at once
+        const uint32_t nroots = c0.w;
+        for (uint32_t r0 = 0; r0 < nroots; r0 += 8) {
+          const uint32_t m = nroots - r0 < 8u ? nroots - r0 : 8u;
+          uint32_t v[8];
+#pragma unroll
+          for (uint32_t u = 0; u < 8; ++u) {
+            const uint32_t r = r0 + u;
+            v[u] = r == 0 ? c1.y : r == 1 ? c1.z : r == 2 ? c1.w : u < m ? cold<const uint32_t>(kPRoots)[c0.z + r] : 0u;
+          }
+          far_push_n(mysm, (uint32_t)launch, v, m);
+        }
+      } else if (lane < k) {
         const bool shared = (c0.w & kCtaShared) != 0;
         const uint32_t nroots = c0.w & ~kCtaShared;
         for (uint32_t r = 0; r < nroots; ++r) {
