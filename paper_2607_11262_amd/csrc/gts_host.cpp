@@ -28,6 +28,7 @@ struct gts_graph {
   uint32_t max_cta_nodes, max_outdeg;
   uint64_t max_tile_lines;
   bool all_mem_txn;  // every load / store streams at least one line (transaction-level memory)
+  uint32_t full_lanes;  // bit n: at n_subpart = n every compute op holds every subpartition lane
 };
 
 struct gts_hwset {
@@ -653,6 +654,14 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   const char* clocks = std::getenv("GTS_WINDOW_CLOCKS");  // diagnostics: per-phase shader clocks
   L.clocks = clocks && std::strcmp(clocks, "0") != 0 ? 1u : 0u;
 
+  // When every compute op holds every subpartition lane at each n_subpart up
+  // to the batch's largest, a class's lanes are always busy together: the
+  // windowed kernel keeps one server word per class instead of one per lane
+  // (less LDS per simulation: more simulations per CU, more of the ready
+  // lists in LDS).
+  const uint32_t upto = max_nsub < 31u ? ((2u << max_nsub) - 2u) : 0xFFFFFFFEu;  // bits 1..max_nsub
+  L.srv_one = (g->full_lanes & upto) == upto ? 1u : 0u;
+  const uint32_t wstride = gts::server_stride(g->img.props, L.srv_one ? 1u : max_nsub);
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel
   // tiles (LRU L2): the memory phase packs a tile's line count into 22 bits;
@@ -673,7 +682,7 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
     // slower even for batches that fill only part of the chip.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) {
-      return 4u * gts::win_lds(g->img.n_ops, max_nsm, sstride, qp, g->img.n_tops, mode).total;
+      return 4u * gts::win_lds(g->img.n_ops, max_nsm, wstride, qp, g->img.n_tops, mode).total;
     };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
     uint32_t want = kWavesPerCu;
@@ -960,6 +969,18 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
   g->img.n_tiles = d.n_tiles;
   g->max_tile_lines = d.max_tile_lines;
+  g->full_lanes = 0;
+  for (uint32_t ns = 1; ns <= GTS_MAX_SUBPART && ns < 32; ++ns) {
+    bool full = true;
+    for (uint32_t p = 0; p < h->n_ops && full; ++p) {
+      if (h->op_cls[p] > gts::C_SFU) continue;
+      uint32_t lanes = 0;
+      for (uint32_t w = 0; w < 32; ++w)
+        if ((h->op_warps[p] >> w) & 1u) lanes |= 1u << (w % ns);
+      full = lanes == (1u << ns) - 1u;
+    }
+    if (full) g->full_lanes |= 1u << ns;
+  }
   g->all_mem_txn = false;
   if (!d.txn_line.empty()) {
     g->all_mem_txn = true;

@@ -1727,7 +1727,7 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.ofin = (L.flags & GTS_ORDER_AT_FINISH) != 0;
   S.mem_only = (L.img.props & kGraphComputeFeedsData) != 0;
   S.nsm = S.hw[HW_NSM];
-  S.nsub = S.hw[HW_NSUB];
+  S.nsub = L.srv_one ? 1u : S.hw[HW_NSUB];  // server words per compute class (one when the lanes move together)
   S.sstride = server_stride(S.G.props, S.nsub);
   S.smem_w = S.sstride - 2;
   S.nslot = (S.nsm + 63) / 64;
@@ -1737,7 +1737,8 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   S.state = reinterpret_cast<uint64_t*>(sim + L.layout.off_state);
   S.cst = reinterpret_cast<CtaState*>(sim + L.layout.off_cta);
   S.mq_g = reinterpret_cast<uint32_t*>(sim + L.layout.off_mq);
-  const WinLds W = win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.max_nsub), L.qp, S.G.n_tops, MODE);
+  const WinLds W =
+      win_lds(S.G.n_ops, L.max_nsm, server_stride(S.G.props, L.srv_one ? 1u : L.max_nsub), L.qp, S.G.n_tops, MODE);
   S.optab = reinterpret_cast<uint4*>(lds + W.optab);
   S.tops = reinterpret_cast<uint16_t*>(lds + W.tops);
   S.srv = lds + W.srv;
@@ -1787,9 +1788,11 @@ __device__ __forceinline__ void window_body(const Launch& L) {
   // CTAs that receive cross-CTA edges (the others are zeroed at dispatch).
   uint64_t lm = ~0ull;
   for (uint32_t q = lane; q < S.G.n_ops; q += 64) {
-    const uint4 e = op_entry(S.G.ops[q], S.hw, S.G.props);
-    S.optab[q] = e;
+    uint4 e = op_entry(S.G.ops[q], S.hw, S.G.props);
     const uint32_t cls = e.w & 7u;
+    if (L.srv_one && cls <= C_SFU)  // the class's single word: lane 0 of its slot
+      e.w = (e.w & 0xFFu) | (1u << 8) | (compute_slot(S.G.props, cls) << 16);
+    S.optab[q] = e;
     if (cls == C_GLOAD || cls == C_GSTORE) {
       const uint64_t d = (uint64_t)e.y + e.z;
       lm = d < lm ? d : lm;
