@@ -27,6 +27,7 @@ constexpr uint32_t kGraphClusters = 256u;         // some kernel has clusters of
 constexpr uint32_t kGraphTiles = 512u;            // some load / store names its tile
 constexpr uint32_t kGraphTxn = 1024u;             // some load / store has a tile address
                                                   // (transaction-level memory)
+constexpr uint32_t kGraphSmem = 2048u;            // the op table has shared-memory ops
 
 // Compute pipelines: every subpartition of an SM has one lane per compute
 // class.  Server state holds lanes only for the classes a graph uses, class
@@ -138,9 +139,12 @@ enum : uint32_t { HW_NOC_NODES = 21, HW_NOC_W = 22, HW_NOC_RATE = 23, HW_NOC_LAT
 constexpr uint32_t kDevOrder = 1u, kDevShared = 2u;
 
 // Per-SM server words: compute lanes (slots x n_subpart), then the shared-
-// memory pipe and the global-memory engine.
+// memory pipe (only for graphs with shared-memory ops, or without compute
+// ops) and the global-memory engine; the pipe's index is stride - 2, the
+// engine's stride - 1.
 __host__ __device__ inline uint32_t server_stride(uint32_t props, uint32_t nsub) {
-  return compute_slots(props) * nsub + 2u;
+  const uint32_t slots = compute_slots(props);
+  return slots * nsub + ((props & kGraphSmem) || slots == 0u ? 2u : 1u);
 }
 
 // Per-simulation scratch regions (byte offsets within one simulation's slice).

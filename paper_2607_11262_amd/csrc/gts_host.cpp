@@ -411,9 +411,10 @@ int check_graph(const gts_graph_host* h, Derived* d) {
   bool any_shared = false;
   for (uint32_t v = 0; v < N && !any_shared; ++v) any_shared = d->shared[v] != 0;
   uint32_t classes = 0;
-  bool clusters = false;
+  bool clusters = false, has_smem = false;
   for (uint32_t p = 0; p < P; ++p) {
     if (is_compute(h->op_cls[p])) classes |= 1u << h->op_cls[p];
+    if (h->op_cls[p] == GTS_SMEM) has_smem = true;
     if (h->op_cls[p] == GTS_REMOTE) clusters = true;
   }
   for (uint32_t k = 0; k < K; ++k) clusters |= cluster_of(h, k) > 1;
@@ -455,6 +456,7 @@ int check_graph(const gts_graph_host* h, Derived* d) {
              (max_outdeg < 0xFFFFu ? gts::kGraphSmallOutdeg : 0u) | (any_shared ? gts::kGraphHasShared : 0u) |
              (compute_feeds_data ? gts::kGraphComputeFeedsData : 0u) | classes << gts::kGraphClassShift |
              (clusters ? gts::kGraphClusters : 0u) | (n_tiles ? gts::kGraphTiles : 0u) |
+             (has_smem ? gts::kGraphSmem : 0u) |
              (d->txn_line.empty() ? 0u : gts::kGraphTxn);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
