@@ -199,8 +199,8 @@ struct Launch {
   uint32_t qp;                 // windowed kernel: later ready entries per lane held in LDS
   uint32_t noc_words;          // general kernel: NoC server words after the per-SM servers
   uint32_t clocks;             // windowed kernel: time its phases with the shader clock
-  uint32_t srv_one;            // windowed kernel: one server word per compute class (every compute op holds every
-                               // subpartition lane of every record, so their lanes' times stay equal)
+  uint32_t srv_one;            // one server word per compute class (every compute op holds every subpartition
+                               // lane of every record, so their lanes' times stay equal)
 };
 
 // LDS carve-up of the windowed kernel (32-bit words; 64-bit arrays start on

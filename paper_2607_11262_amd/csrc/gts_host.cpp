@@ -601,9 +601,17 @@ struct GeneralLds {
   uint32_t server_bytes, noc_words, total;
   bool optab;
 };
+// Every compute op holds every subpartition lane at each n_subpart up to
+// max_nsub: a class's lanes are always busy together, and both kernels keep
+// one server word per class instead of one per lane.
+bool one_word_per_class(const gts_graph* g, uint32_t max_nsub) {
+  const uint32_t upto = max_nsub < 31u ? ((2u << max_nsub) - 2u) : 0xFFFFFFFEu;  // bits 1..max_nsub
+  return (g->full_lanes & upto) == upto;
+}
+
 GeneralLds general_lds(const gts_graph* g, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc) {
   GeneralLds r;
-  const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
+  const uint32_t sstride = gts::server_stride(g->img.props, one_word_per_class(g, max_nsub) ? 1u : max_nsub);
   r.noc_words = (g->img.props & gts::kGraphClusters) && max_noc ? 4u * (max_nsm + max_noc) : 0u;
   r.server_bytes = 4u * (max_nsm * sstride + max_nsm + r.noc_words);
   const uint64_t optab_bytes = (uint64_t)g->img.n_ops * 16;
@@ -656,13 +664,10 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   const char* clocks = std::getenv("GTS_WINDOW_CLOCKS");  // diagnostics: per-phase shader clocks
   L.clocks = clocks && std::strcmp(clocks, "0") != 0 ? 1u : 0u;
 
-  // When every compute op holds every subpartition lane at each n_subpart up
-  // to the batch's largest, a class's lanes are always busy together: the
-  // windowed kernel keeps one server word per class instead of one per lane
-  // (less LDS per simulation: more simulations per CU, more of the ready
-  // lists in LDS).
-  const uint32_t upto = max_nsub < 31u ? ((2u << max_nsub) - 2u) : 0xFFFFFFFEu;  // bits 1..max_nsub
-  L.srv_one = (g->full_lanes & upto) == upto ? 1u : 0u;
+  // one server word per compute class when the lanes move together (less
+  // LDS per simulation: more simulations per CU, and in the windowed kernel
+  // more of the ready lists in LDS)
+  L.srv_one = one_word_per_class(g, max_nsub) ? 1u : 0u;
   const uint32_t wstride = gts::server_stride(g->img.props, L.srv_one ? 1u : max_nsub);
   const uint32_t need_props = gts::kGraphSinksAreMemory | gts::kGraphCrossFromMemory | gts::kGraphSmallOutdeg;
   const char* force = std::getenv("GTS_KERNEL");  // "general": skip the windowed kernel

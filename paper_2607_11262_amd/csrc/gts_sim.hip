@@ -542,7 +542,7 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   S.lane = threadIdx.x;
   S.flags = L.flags;
   S.nsm = S.hw[HW_NSM];
-  S.nsub = S.hw[HW_NSUB];
+  S.nsub = L.srv_one ? 1u : S.hw[HW_NSUB];  // server words per compute class (one when the lanes move together)
   S.sstride = server_stride(S.G.props, S.nsub);
   S.smem_w = S.sstride - 2;
   uint8_t* sim = L.sims + (uint64_t)b * L.layout.stride;
@@ -587,7 +587,13 @@ extern "C" __global__ __launch_bounds__(64) void gts_sim_wave(Launch L) {
   }
 
   // Setup: duration table, idle servers, zeroed node / CTA state.
-  for (uint32_t p = lane; p < S.G.n_ops; p += 64) S.optab[p] = op_entry(S.G.ops[p], S.hw, S.G.props);
+  for (uint32_t p = lane; p < S.G.n_ops; p += 64) {
+    uint4 e = op_entry(S.G.ops[p], S.hw, S.G.props);
+    const uint32_t cls = e.w & 7u;
+    if (L.srv_one && cls <= C_SFU)  // the class's single word: lane 0 of its slot
+      e.w = (e.w & 0xFFu) | (1u << 8) | (compute_slot(S.G.props, cls) << 16);
+    S.optab[p] = e;
+  }
   const uint32_t nsrv = S.nsm * S.sstride + S.nsm + L.noc_words;
   for (uint32_t i = lane; i < nsrv; i += 64) S.srv[i] = 0;
   for (uint32_t v = lane; v < S.G.n_nodes; v += 64) pst(&S.state[v], (uint64_t)0);
