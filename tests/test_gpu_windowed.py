@@ -186,3 +186,24 @@ def test_side_stream_lifetime(torch_cuda):
     torch.cuda.synchronize()
     compare(g, hws, ALL, api.to_numpy(res))
     del junk
+
+
+def test_server_word_per_class(torch_cuda):
+    """The one-server-word-per-class layout (every compute op holds every
+    subpartition lane of every record of the batch): a GEMM on warp group
+    0-3 takes it for records of at most four subpartitions; adding a record
+    of eight turns it off for the whole batch.  Both batches give the same
+    cycles for the shared records, equal to the oracle node by node."""
+    g = W.gemm(1024, 1024, 512, 128, 128, 32, 3)
+    base = H.sample_h100_sweep(77, 12)
+    base[:, H.FIELDS["n_subpart"]] = [1, 2, 3, 4] * 3
+    eight = H.preset("H100", n_sm=132)
+    eight[H.FIELDS["n_subpart"]] = 8
+    mixed = np.concatenate([base, eight[None, :]])
+    dg = api.upload(g)
+    a = api.to_numpy(api.simulate(dg, base, ALL))
+    b = api.to_numpy(api.simulate(dg, mixed, ALL))
+    torch_cuda.cuda.synchronize()
+    n = base.shape[0]
+    assert np.array_equal(a[0], b[0][:n]) and np.array_equal(a[1], b[1][:n]) and np.array_equal(a[3], b[3][:n])
+    compare(g, mixed, ALL, b)
