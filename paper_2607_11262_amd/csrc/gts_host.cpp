@@ -78,6 +78,8 @@ struct Derived {
   uint32_t n_tnodes = 0, n_tsucc = 0;
   uint32_t n_tiles = 0;          // distinct tiles named by loads / stores
   uint64_t max_tile_lines = 0;   // the most lines of any of them
+  bool all_mem_txn = false;      // every load / store streams at least one line (transaction-level memory)
+  uint32_t full_lanes = 0;       // bit n: at n_subpart = n every compute op holds every subpartition lane
   // transaction-level memory: node v's lines txn_line[txn_ptr[v] ..
   // txn_ptr[v + 1]), numbered densely in order of first use
   std::vector<uint32_t> txn_ptr, txn_line;
@@ -460,6 +462,21 @@ int check_graph(const gts_graph_host* h, Derived* d) {
              (d->txn_line.empty() ? 0u : gts::kGraphTxn);
   d->max_cta_nodes = max_cta_nodes;
   d->max_outdeg = max_outdeg;
+  d->full_lanes = 0;
+  for (uint32_t ns = 1; ns <= GTS_MAX_SUBPART && ns < 32; ++ns) {
+    bool full = true;
+    for (uint32_t p = 0; p < P && full; ++p) {
+      if (!is_compute(h->op_cls[p])) continue;
+      uint32_t lanes = 0;
+      for (uint32_t w = 0; w < 32; ++w)
+        if ((h->op_warps[p] >> w) & 1u) lanes |= 1u << (w % ns);
+      full = lanes == (1u << ns) - 1u;
+    }
+    if (full) d->full_lanes |= 1u << ns;
+  }
+  d->all_mem_txn = !d->txn_line.empty();
+  for (uint32_t v = 0; v < N && d->all_mem_txn; ++v)
+    if (is_memory(h->op_cls[h->node_op[v]]) && d->txn_ptr[v + 1] == d->txn_ptr[v]) d->all_mem_txn = false;
   find_templates(h, d);
   return GTS_OK;
 }
@@ -976,24 +993,8 @@ int gts_graph_upload(const gts_graph_host* h, void* dev_image, uint64_t dev_byte
   g->img.tile = d.n_tiles ? reinterpret_cast<const uint32_t*>(base + L.tile) : nullptr;
   g->img.n_tiles = d.n_tiles;
   g->max_tile_lines = d.max_tile_lines;
-  g->full_lanes = 0;
-  for (uint32_t ns = 1; ns <= GTS_MAX_SUBPART && ns < 32; ++ns) {
-    bool full = true;
-    for (uint32_t p = 0; p < h->n_ops && full; ++p) {
-      if (h->op_cls[p] > gts::C_SFU) continue;
-      uint32_t lanes = 0;
-      for (uint32_t w = 0; w < 32; ++w)
-        if ((h->op_warps[p] >> w) & 1u) lanes |= 1u << (w % ns);
-      full = lanes == (1u << ns) - 1u;
-    }
-    if (full) g->full_lanes |= 1u << ns;
-  }
-  g->all_mem_txn = false;
-  if (!d.txn_line.empty()) {
-    g->all_mem_txn = true;
-    for (uint32_t v = 0; v < h->n_nodes && g->all_mem_txn; ++v)
-      if (is_memory(h->op_cls[h->node_op[v]]) && d.txn_ptr[v + 1] == d.txn_ptr[v]) g->all_mem_txn = false;
-  }
+  g->full_lanes = d.full_lanes;
+  g->all_mem_txn = d.all_mem_txn;
   const bool txn = !d.txn_line.empty();
   g->img.txn_ptr = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_ptr) : nullptr;
   g->img.txn_line = txn ? reinterpret_cast<const uint32_t*>(base + L.txn_line) : nullptr;
