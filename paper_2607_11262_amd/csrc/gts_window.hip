@@ -9,7 +9,8 @@
 //       where Lm is the smallest possible delay from a memory arrival to its
 //       completion (min over the graph's memory ops of L2/DRAM occupancy +
 //       latency, over both servers for graphs whose tiles go through the LRU
-//       L2);
+//       L2; one cycle plus the smaller latency for transaction-level
+//       memory);
 //   retirement phase: every CTA retirement with cycle < H, in cycle order,
 //       each distinct cycle followed by dispatch (wave-cooperative);
 //   local phase: every lane issues its SMs' ready nodes with cycle < H in
@@ -20,10 +21,16 @@
 //       (cycle, node id) (a bitonic network across the wave; a few keys by
 //       counting ranks), sent to the L2 or DRAM by their op's flag or, for a
 //       tile access on a machine with an LRU L2, by LRU decisions taken for
-//       the whole batch in that order (LRU kernels), served by the chip-wide
+//       the whole batch in that order (tile kernels), served by the chip-wide
 //       L2 and DRAM FIFO servers through a max-plus prefix scan, and
 //       completed by the lane that owns their SM (CTA bookkeeping, release of
 //       out-edges).
+//
+// The transaction-level kernels queue one ring entry per load / store that
+// streams its 128-B lines through the engine; the memory phase takes the
+// lines due in the window from those entries (each line an arrival, the
+// servers keeping time in 2^-16 cycles, an LRU of lines), and a node
+// completes with its last line.
 //
 // Why this equals the one-event-at-a-time order of the general kernel and of
 // the CPU oracle: an arrival at s >= T completes no earlier than s + Lm >= H,
