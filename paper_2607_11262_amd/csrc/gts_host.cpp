@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -653,10 +654,25 @@ int check_lds(const gts_graph* g, uint32_t max_nsm, uint32_t max_nsub, uint32_t 
   return GTS_OK;
 }
 
+// Compute units of the current device (0 if it cannot be queried), once per
+// device.
+uint32_t device_cus() {
+  static std::atomic<uint32_t> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  uint32_t c = cached[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+    c = (uint32_t)n;
+    cached[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
 int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_nsm, uint32_t max_nsub, uint32_t max_noc,
            uint32_t* out_cycles, uint32_t* out_makespan, int32_t* out_status, uint64_t* out_digest, uint8_t* sims,
            uint32_t flags, hipStream_t st) {
-  const uint32_t sstride = gts::server_stride(g->img.props, max_nsub);
   const GeneralLds gl = general_lds(g, max_nsm, max_nsub, max_noc);
   const uint32_t noc_words = gl.noc_words, server_bytes = gl.server_bytes, lds_general = gl.total;
   const bool lds_optab = gl.optab;
@@ -702,14 +718,22 @@ int launch(const gts_graph* g, const uint32_t* hw_dev, uint32_t B, uint32_t max_
   if (windowed) {
     // LDS per simulation: fixed tables plus qp later-ready entries per lane;
     // take the largest qp that keeps twelve simulations per CU (the register
-    // limit of the kernel).  Measured: fewer, larger simulations per CU are
-    // slower even for batches that fill only part of the chip.
+    // limit of the kernel), or one per CU for a batch of at most one
+    // simulation per CU, whose simulations then hold more of their
+    // later-ready entries in LDS rather than in scratch.  Measured: a
+    // 64-simulation decoder layer (long later-ready lists) 1.22x faster at
+    // one per CU than at twelve, 16 and 256 simulations unchanged; a
+    // 1024-simulation launch 3 % faster at four per CU than at twelve, but
+    // launches of 1364 - 2048 simulations beside another stream's launches
+    // (the GEMM design sweep) 15 % slower overall at six or eight per CU,
+    // whose LDS keeps the other launch's simulations off the CU.
     constexpr uint32_t kLdsPerCu = 160 * 1024, kWavesPerCu = 12, kMaxQp = 160;
     auto bytes = [&](uint32_t qp) {
       return 4u * gts::win_lds(g->img.n_ops, max_nsm, wstride, qp, g->img.n_tops, mode).total;
     };
     auto per_cu = [&](uint32_t qp) { return std::min(kWavesPerCu, kLdsPerCu / bytes(qp)); };
-    uint32_t want = kWavesPerCu;
+    const uint32_t cus = device_cus();
+    uint32_t want = cus && B <= cus ? 1u : kWavesPerCu;
     if (const char* w = std::getenv("GTS_WINDOW_WAVES"))  // tuning: target simulations per CU
       want = std::min<uint32_t>(kWavesPerCu, std::max<uint32_t>(1u, (uint32_t)std::strtoul(w, nullptr, 10)));
     constexpr uint32_t kMinQp = 0;

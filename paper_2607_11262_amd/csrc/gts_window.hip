@@ -418,14 +418,30 @@ struct WSim {
       bi[jj] = t ? i : bi[jj];
     }
   }
+  // The far list's LDS part and its scratch part are read in loops of their
+  // own, eight reads in flight, past the end clamped to the last entry: a
+  // choice between the two per entry made every LDS read wait for all
+  // outstanding global accesses.
   __device__ __forceinline__ void scan_far(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
-    for (uint32_t i0 = 0; i0 < n; i0 += 8) {
+    const uint32_t nl = n < QF ? n : QF;
+    for (uint32_t i0 = 0; i0 < nl; i0 += 8) {
       uint64_t kk[8];
 #pragma unroll
-      for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? fr_get(lane, i0 + q) : kNoKey;
+      for (uint32_t q = 0; q < 8; ++q) kk[q] = fr[(i0 + q < nl ? i0 + q : nl - 1u) * 64u + lane];
 #pragma unroll
       for (uint32_t q = 0; q < 8; ++q)
-        if (i0 + q < n) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
+        if (i0 + q < nl) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
+    }
+    if (n > QF) {
+      const gmem<uint64_t>* g = cold<uint64_t>(kPFrG);
+      for (uint32_t i0 = QF; i0 < n; i0 += 8) {
+        uint64_t kk[8];
+#pragma unroll
+        for (uint32_t q = 0; q < 8; ++q) kk[q] = g[((i0 + q < n ? i0 + q : n - 1u) - QF) * 64u + lane];
+#pragma unroll
+        for (uint32_t q = 0; q < 8; ++q)
+          if (i0 + q < n) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
+      }
     }
   }
 
@@ -435,13 +451,12 @@ struct WSim {
     if (fr_min[lane] < H) {
       const uint32_t n = fr_n(lane);
       uint32_t nn = nr_cnt[lane], kp = 0, mn = 0xFFFFFFFFu;
-      for (uint32_t i0 = 0; i0 < n; i0 += 8) {  // in place: writes stay below the reads
-        uint64_t kk[8];
-#pragma unroll
-        for (uint32_t q = 0; q < 8; ++q) kk[q] = i0 + q < n ? fr_get(lane, i0 + q) : kNoKey;
+      // in place (writes stay below the reads); the LDS part, then the
+      // scratch part, as in scan_far
+      auto take = [&](const uint64_t (&kk)[8], uint32_t i0, uint32_t m) {
 #pragma unroll
         for (uint32_t q = 0; q < 8; ++q) {
-          if (i0 + q < n) {
+          if (i0 + q < m) {
             const uint32_t cyc = (uint32_t)(kk[q] >> 32);
             if (cyc < H && nn < kNear) {
               nr[nn * 64u + lane] = kk[q];
@@ -456,6 +471,22 @@ struct WSim {
               mn = cyc < mn ? cyc : mn;
             }
           }
+        }
+      };
+      const uint32_t nl = n < QF ? n : QF;
+      for (uint32_t i0 = 0; i0 < nl; i0 += 8) {
+        uint64_t kk[8];
+#pragma unroll
+        for (uint32_t q = 0; q < 8; ++q) kk[q] = fr[(i0 + q < nl ? i0 + q : nl - 1u) * 64u + lane];
+        take(kk, i0, nl);
+      }
+      if (n > QF) {
+        const gmem<uint64_t>* g = cold<uint64_t>(kPFrG);
+        for (uint32_t i0 = QF; i0 < n; i0 += 8) {
+          uint64_t kk[8];
+#pragma unroll
+          for (uint32_t q = 0; q < 8; ++q) kk[q] = g[((i0 + q < n ? i0 + q : n - 1u) - QF) * 64u + lane];
+          take(kk, i0, n);
         }
       }
       fr_cnt[lane] = kp;
