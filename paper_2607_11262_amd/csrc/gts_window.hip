@@ -60,6 +60,8 @@
 // lane handles one node of each of its SMs per round trip.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "../../include/gts.h"
 #include "gts_common.h"
 #include "gts_dev.h"
@@ -69,6 +71,8 @@ namespace gts {
 namespace {
 
 constexpr uint64_t kNoKey = ~0ull;
+// far-list word: a due entry was pushed since the window start
+constexpr uint32_t kFrPushedDue = 0x80000000u;
 constexpr uint32_t kBadOverflow = 1u, kBadReady = 2u, kBadMemQ = 4u, kBadRetire = 8u;
 // ring entries loaded per SM and window: as many as the registers allow
 // at three waves per SIMD (fewer cut windows short)
@@ -314,8 +318,11 @@ struct WSim {
   // below the current window end (kNear per lane, LDS), "far" the rest ([0,
   // QF) in LDS, [QF, QF + kPoolSpill) in scratch) with a lower bound of its
   // cycles in fr_min.  At each window start the far entries below the window
-  // end move to near; fr_hot marks a far list that still holds such entries
-  // (near was full), which the local phase then scans as well.
+  // end move to near; those that do not fit (near is full) are put first, so
+  // a far list is [due | later | pushed since the window start].  fr_hot
+  // holds the end of the due part (bits 0-15), the start of the pushed part
+  // (bits 16-30) and whether a due entry was pushed (bit 31); the local
+  // phase scans the due part, and the pushed part once that bit is set.
   // rarely used pointers, from LDS (kWinPtrs)
   enum : uint32_t { kPSucc, kPIndeg, kPRoots, kPCtas, kPKernels, kPTsucc, kPTindeg, kPFrG, kPRetG, kPHw };
   // The pointers are global-memory ones: typed so, their accesses compile to
@@ -375,7 +382,7 @@ struct WSim {
         return;
       }
       atomicSub(&nr_cnt[l], 1u);
-      fr_hot[l] = 1u;
+      atomicOr(&fr_hot[l], kFrPushedDue);
     }
     far_push(l, key);
   }
@@ -399,7 +406,7 @@ struct WSim {
       } else {
         if (cyc[k] < Hnear) {
           atomicSub(&nr_cnt[l], 1u);
-          fr_hot[l] = 1u;
+          atomicOr(&fr_hot[l], kFrPushedDue);
         }
         far_push(l, key);
       }
@@ -418,58 +425,71 @@ struct WSim {
       bi[jj] = t ? i : bi[jj];
     }
   }
-  // The far list's LDS part and its scratch part are read in loops of their
-  // own, eight reads in flight, past the end clamped to the last entry: a
-  // choice between the two per entry made every LDS read wait for all
-  // outstanding global accesses.
-  __device__ __forceinline__ void scan_far(uint32_t n, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
-    const uint32_t nl = n < QF ? n : QF;
-    for (uint32_t i0 = 0; i0 < nl; i0 += 8) {
+  // Far entries [b, e): the LDS part and the scratch part are read in loops
+  // of their own, eight reads in flight, past the end clamped to the last
+  // entry (a choice between the two per entry made every LDS read wait for
+  // all outstanding global accesses).
+  __device__ __forceinline__ void scan_far(uint32_t b, uint32_t e, uint64_t (&best)[NB], uint32_t (&bi)[NB]) const {
+    const uint32_t el = e < QF ? e : QF;
+    for (uint32_t i0 = b; i0 < el; i0 += 8) {
       uint64_t kk[8];
 #pragma unroll
-      for (uint32_t q = 0; q < 8; ++q) kk[q] = fr[(i0 + q < nl ? i0 + q : nl - 1u) * 64u + lane];
+      for (uint32_t q = 0; q < 8; ++q) kk[q] = fr[(i0 + q < el ? i0 + q : el - 1u) * 64u + lane];
 #pragma unroll
       for (uint32_t q = 0; q < 8; ++q)
-        if (i0 + q < nl) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
+        if (i0 + q < el) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
     }
-    if (n > QF) {
+    if (e > QF) {
       const gmem<uint64_t>* g = cold<uint64_t>(kPFrG);
-      for (uint32_t i0 = QF; i0 < n; i0 += 8) {
+      for (uint32_t i0 = b > QF ? b : QF; i0 < e; i0 += 8) {
         uint64_t kk[8];
 #pragma unroll
-        for (uint32_t q = 0; q < 8; ++q) kk[q] = g[((i0 + q < n ? i0 + q : n - 1u) - QF) * 64u + lane];
+        for (uint32_t q = 0; q < 8; ++q) kk[q] = g[((i0 + q < e ? i0 + q : e - 1u) - QF) * 64u + lane];
 #pragma unroll
         for (uint32_t q = 0; q < 8; ++q)
-          if (i0 + q < n) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
+          if (i0 + q < e) consider(kk[q], (i0 + q) | 0x80000000u, best, bi);
       }
     }
   }
 
-  // Window start: move this lane's far entries below H to near.
+  // Window start: move this lane's far entries below H to near, and put
+  // those that do not fit first.
   __device__ __forceinline__ void pool_rebuild(uint64_t H) {
-    uint32_t hot = 0;
     if (fr_min[lane] < H) {
       const uint32_t n = fr_n(lane);
-      uint32_t nn = nr_cnt[lane], kp = 0, mn = 0xFFFFFFFFu;
-      // in place (writes stay below the reads); the LDS part, then the
-      // scratch part, as in scan_far
-      auto take = [&](const uint64_t (&kk)[8], uint32_t i0, uint32_t m) {
+      uint32_t nn = nr_cnt[lane], kp = 0, h = 0, mn = 0xFFFFFFFFu;
+      // in place, writes at or below the entry at hand (the kept entries
+      // [0, h) due, [h, kp) later); the LDS part, then the scratch part, as
+      // in scan_far (inside the LDS part every position written is in LDS)
+      auto take = [&](auto in_lds, const uint64_t(&kk)[8], uint32_t i0, uint32_t m) {
+        constexpr bool kLds = decltype(in_lds)::value;
+        auto get = [&](uint32_t p) -> uint64_t {
+          if constexpr (kLds) return fr[p * 64u + lane]; else return fr_get(lane, p);
+        };
+        auto set = [&](uint32_t p, uint64_t k) {
+          if constexpr (kLds) fr[p * 64u + lane] = k; else fr_set(lane, p, k);
+        };
 #pragma unroll
         for (uint32_t q = 0; q < 8; ++q) {
           if (i0 + q < m) {
-            const uint32_t cyc = (uint32_t)(kk[q] >> 32);
+            const uint32_t i = i0 + q, cyc = (uint32_t)(kk[q] >> 32);
             if (cyc < H && nn < kNear) {
               nr[nn * 64u + lane] = kk[q];
               ++nn;
-            } else {
-              hot |= cyc < H;
+              continue;
+            }
+            if (cyc < H) {  // due: the first later entry moves to the end
+              if (h != kp) set(kp, get(h));
+              if (h != i) set(h, kk[q]);
+              ++h;
+            } else if (kp != i) {
               // an entry that keeps its place is not written back: most
               // windows move nothing, and rewriting unchanged entries
               // dirtied the far list's lines in the L2 on every window
-              if (kp != i0 + q) fr_set(lane, kp, kk[q]);
-              ++kp;
-              mn = cyc < mn ? cyc : mn;
+              set(kp, kk[q]);
             }
+            ++kp;
+            mn = cyc < mn ? cyc : mn;
           }
         }
       };
@@ -478,7 +498,7 @@ struct WSim {
         uint64_t kk[8];
 #pragma unroll
         for (uint32_t q = 0; q < 8; ++q) kk[q] = fr[(i0 + q < nl ? i0 + q : nl - 1u) * 64u + lane];
-        take(kk, i0, nl);
+        take(std::true_type{}, kk, i0, nl);
       }
       if (n > QF) {
         const gmem<uint64_t>* g = cold<uint64_t>(kPFrG);
@@ -486,14 +506,16 @@ struct WSim {
           uint64_t kk[8];
 #pragma unroll
           for (uint32_t q = 0; q < 8; ++q) kk[q] = g[((i0 + q < n ? i0 + q : n - 1u) - QF) * 64u + lane];
-          take(kk, i0, n);
+          take(std::false_type{}, kk, i0, n);
         }
       }
       fr_cnt[lane] = kp;
       fr_min[lane] = mn;
       nr_cnt[lane] = nn;
+      fr_hot[lane] = h | (kp << 16);
+    } else {
+      fr_hot[lane] = fr_n(lane) << 16;  // nothing due; pushes go after the present entries
     }
-    fr_hot[lane] = hot;
   }
 
   // ---- per-SM memory-arrival FIFO (strictly increasing cycles): a ring of
@@ -838,7 +860,9 @@ struct WSim {
   __device__ __forceinline__ bool local_step(uint64_t H) {
     uint32_t nn = nr_cnt[lane];
     nn = nn < kNear ? nn : kNear;
-    const bool hot = fr_hot[lane] != 0;
+    const uint32_t fw = fr_hot[lane];
+    uint32_t fh = fw & 0xFFFFu, fa = (fw >> 16) & 0x7FFFu;
+    const bool pushed_due = (fw & kFrPushedDue) != 0, hot = fh != 0 || pushed_due;
     uint32_t fn = hot ? fr_n(lane) : 0u;
     uint64_t best[NB];
     uint32_t bi[NB];
@@ -856,7 +880,10 @@ struct WSim {
         for (uint32_t q = 0; q < 4; ++q)
           if (i0 + q < nn) consider(kk[q], i0 + q, best, bi);
       }
-      if (hot) scan_far(fn, best, bi);
+      if (hot) {
+        scan_far(0, fh, best, bi);
+        if (pushed_due) scan_far(fa, fn, best, bi);
+      }
     }
     uint32_t taken = 0, cnt = 0;
 #pragma unroll
@@ -897,7 +924,16 @@ struct WSim {
         taken &= ~(1u << sel);
         if (mx & 0x80000000u) {
           const uint32_t i = mx & 0x7FFFFFFFu;
-          if (i != fn - 1) fr_set(lane, i, fr_get(lane, fn - 1));
+          if (i >= fa) {  // pushed since the window start: the last entry fills its place
+            if (i != fn - 1) fr_set(lane, i, fr_get(lane, fn - 1));
+          } else {  // in the due part: the last due, later and pushed entries each move down one place
+            const uint64_t v1 = fr_get(lane, fh - 1), v2 = fr_get(lane, fa - 1), v3 = fr_get(lane, fn - 1);
+            if (i != fh - 1) fr_set(lane, i, v1);
+            if (fh != fa) fr_set(lane, fh - 1, v2);
+            if (fa != fn) fr_set(lane, fa - 1, v3);
+            --fh;
+            --fa;
+          }
           --fn;
         } else {
           if (mx != nn - 1) nr[mx * 64u + lane] = nr[(nn - 1) * 64u + lane];
@@ -906,7 +942,10 @@ struct WSim {
       }
     }
     nr_cnt[lane] = nn;
-    if (hot) fr_cnt[lane] = fn;
+    if (hot) {
+      fr_cnt[lane] = fn;
+      fr_hot[lane] = fh | (fa << 16) | (pushed_due ? kFrPushedDue : 0u);
+    }
     wsync();
     if (E <= 64) {
       issue_events<1>(0, E);
