@@ -98,6 +98,28 @@ def test_window_random_graphs(torch_cuda, chunk, monkeypatch):
     assert ran > 0
 
 
+@pytest.mark.parametrize("waves", [1, 12])
+def test_far_list_in_lds_and_in_scratch(torch_cuda, waves, monkeypatch):
+    """Per-warp MMA GEMM CTAs (64x64x32 tiles, 3 stages, the decoder layer's
+    GEMM shape) release five or eight successors per MMA node, so a lane's
+    near list overflows and due entries wait at the front of its far list.
+    The same records run with the LDS sized for one simulation per CU (the
+    far lists nearly all in LDS) and for twelve (a few entries per lane in
+    LDS, the rest in scratch): each simulation ran on the windowed kernel to
+    the end, and every node's cycles equal the oracle's, both times."""
+    monkeypatch.setenv("GTS_WINDOW_WAVES", str(waves))
+    g = W.gemm(2048, 1024, 512, 64, 64, 32, 3, per_warp=True)
+    assert window_eligible(g)
+    hws = np.stack([H.preset("H100", n_sm=s, max_cta_per_sm=c)
+                    for s, c in ((16, 8), (64, 4), (100, 2), (132, 2), (160, 4), (192, 3))])
+    note(f"far list waves={waves} N={g.n_nodes} E={g.n_edges} B={hws.shape[0]}")
+    gpu, windows = run_window_only(torch_cuda, g, hws, ALL, monkeypatch)
+    st = gpu[2]
+    assert not np.any(st == STATUS_RETRY), f"windowed kernel handed back sims {np.flatnonzero(st == STATUS_RETRY)}"
+    assert np.all(windows > 0)
+    compare(g, hws, ALL, gpu)
+
+
 def _wide_roots_graph(n_loads=150):
     """Two CTAs of 150 independent loads feeding one store: more ready nodes
     on one SM than the windowed kernel's per-lane lists hold."""
