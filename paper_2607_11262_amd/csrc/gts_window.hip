@@ -774,6 +774,17 @@ struct WSim {
       const uint64_t room = cap > busy ? cap - busy : 0u;
       uint32_t lim = k_end - next_cta < 64u ? k_end - next_cta : 64u;
       lim = room < lim ? (uint32_t)room : lim;
+      // the hardware record's launch latencies and the records of the CTAs
+      // that may be placed (k <= lim of them), in flight during the placement
+      const gmem<const uint32_t>* const hwc = cold<const uint32_t>(kPHw);
+      const uint32_t cta_lat = hwc[HW_CTALAT], k_lat = hwc[HW_KLAT];
+      const uint32_t c = next_cta + lane;
+      uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
+      if (lane < lim) {
+        const gmem<const uint32_t>* p = (const gmem<const uint32_t>*)(cold<const CtaDev>(kPCtas) + c);
+        c0 = ld4(p);      // node_begin, node_count, root_begin, root_count
+        c1 = ld4(p + 4);  // memory nodes, first three roots
+      }
       uint32_t k = 0, mysm = 0;
       while (k < lim) {
         uint64_t best = 0;
@@ -797,21 +808,13 @@ struct WSim {
         kstart_k = cur_k;
         kstart_t = t;
       }
-      const gmem<const uint32_t>* const hwc = cold<const uint32_t>(kPHw);
-      const uint64_t launch = (uint64_t)t + hwc[HW_CTALAT] + (kstart_t == t ? hwc[HW_KLAT] : 0u);
+      const uint64_t launch = (uint64_t)t + cta_lat + (kstart_t == t ? k_lat : 0u);
       if (launch > kMaxCycle) {
         bad |= kBadOverflow;
         return;
       }
-      const uint32_t c = next_cta + lane;
-      uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
-      if (lane < k) {
-        const gmem<const uint32_t>* p = (const gmem<const uint32_t>*)(cold<const CtaDev>(kPCtas) + c);
-        c0 = ld4(p);      // node_begin, node_count, root_begin, root_count
-        c1 = ld4(p + 4);  // memory nodes, first three roots
-        if (!sink_ret)  // a CTA that retires with its sink keeps no state
-          *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
-      }
+      if (lane < k && !sink_ret)  // a CTA that retires with its sink keeps no state
+        *reinterpret_cast<uint4*>(&cst[c]) = make_uint4(mysm, (uint32_t)launch, mem_only ? c1.x : c0.y, 0u);
       // zero the node state of unshared CTAs (shared ones were zeroed at start)
       for (uint32_t j = 0; j < k; ++j) {
         const uint32_t nb = __shfl(c0.x, j, 64), nc = __shfl(c0.y, j, 64), rc = __shfl(c0.w, j, 64);
